@@ -1,0 +1,68 @@
+"""Synthetic input generator: reproducibility, shapes and distributions."""
+import numpy as np
+import pytest
+
+import workloads as W
+
+
+def test_config_shapes():
+    assert W.CONFIGS[1].shapes == ((64, 64),)
+    assert W.CONFIGS[2].n_layers == 72
+    assert W.CONFIGS[3].n_layers == 144 and W.CONFIGS[3].grad_dtype == "bf16"
+    assert W.CONFIGS[4].shapes == ((8192, 8192),) and W.CONFIGS[4].gamma == 0.95
+    assert W.CONFIGS[5].n_layers == 192
+    # algorithmic sizes used for the roofline (factor elements, precondition flops)
+    assert W.CONFIGS[3].factor_elems == 1_056_964_608
+    assert abs(W.CONFIGS[3].precond_flops - 2.474e12) / 2.474e12 < 1e-3
+    assert abs(W.CONFIGS[5].precond_flops - 21.23e12) / 21.23e12 < 1e-3
+
+
+def test_reproducible_and_independent():
+    w = W.CONFIGS[2]
+    a1, g1 = W.rank1_vectors(w, 5, 3)
+    a2, g2 = W.rank1_vectors(w, 5, 3)
+    np.testing.assert_array_equal(a1, a2)
+    np.testing.assert_array_equal(g1, g2)
+    a3, _ = W.rank1_vectors(w, 5, 4)
+    assert not np.array_equal(a1, a3)
+    G1, G2 = W.gradient(w, 0, 0), W.gradient(w, 0, 0)
+    np.testing.assert_array_equal(G1, G2)
+    assert G1.dtype == np.float32 and G1.shape == (768, 768)
+
+
+def test_mean_distribution_explicit_vs_shortcut():
+    w = W.custom([(512, 512)], rows=256, cid=900)
+    ae, ge = W.rank1_vectors(w, 0, 0, explicit=True)
+    a, g = W.rank1_vectors(w, 0, 0, explicit=False)
+    # std of the mean of 256 N(0,1) rows is 1/16; grads 1e-3/16
+    for v, s in ((ae, 1 / 16), (a, 1 / 16), (ge, 1e-3 / 16), (g, 1e-3 / 16)):
+        assert abs(v.std() / s - 1) < 0.15
+
+
+def test_student_t_rows_heavier_tail():
+    w = W.custom([(256, 256)], rows=64, cid=901, act_dist="student_t4")
+    a, _ = W.rank1_vectors(w, 0, 0, explicit=True)
+    assert abs(a.std() / np.sqrt(2 / 64) - 1) < 0.2
+
+
+def test_bf16_rounding():
+    x = np.array([1.0, 1.00390625, 1.005859375, -3.3, np.float32(2 ** -130)], dtype=np.float32)
+    r = W.round_to_bf16(x)
+    assert (r.view(np.uint32) & 0xFFFF == 0).all()
+    assert r[0] == 1.0
+    assert r[1] == 1.0        # tie -> even
+    assert r[2] == 1.0078125  # rounds up
+    torch = pytest.importorskip("torch")
+    t = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    np.testing.assert_array_equal(r, t)
+    G = W.gradient(W.CONFIGS[3], 0, 0)
+    assert (G.view(np.uint32) & 0xFFFF == 0).all()
+
+
+def test_perturbed_init_spd_symmetric():
+    w = W.custom([(96, 80)], cid=902, init="perturbed")
+    L, R = W.initial_factors(w, 0)
+    assert L.shape == (96, 96) and R.shape == (80, 80)
+    np.testing.assert_array_equal(L, L.T)
+    np.linalg.cholesky(L.astype(np.float64))
+    assert abs(np.trace(L) / 96 - 1.0 - 0.01 * 64 / 96) < 0.01
