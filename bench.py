@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Benchmark of MKOR's per-step hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+
+A step is one full pass of the hot path (stabiliser + SM update of both
+factors of every layer, preconditioning, rescale) over the whole grouped layer
+list, launched through the C ABI (mkor_step).  The default workload is the
+BERT-Large-shaped set: 24 blocks x {4 x 1024x1024, 1024x4096, 4096x1024},
+fp32 factors, bf16 gradients.  Inputs are synthetic, seeded, and resident in
+HBM before the timed region starts.
+
+Prints one JSON line: layer-updates/s, per-kernel times measured with HIP
+events on the launch stream, the roofline of the dominant kernel, and the
+float64 CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "layer-updates/sec (SM update + precondition), BERT-Large set; % HBM / % MFMA peak"
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+FP32_MFMA_PEAK_TF = 157.3   # MI355X dense fp32 matrix
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--eps", type=float, default=100.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stage-timing", action="store_true")
+    return ap.parse_args()
+
+
+def workload_desc(w):
+    counts = {}
+    for s in w.block_shapes:
+        counts[s] = counts.get(s, 0) + 1
+    inner = ", ".join(f"{c}x {i}x{o}" if c > 1 else f"{i}x{o}" for (i, o), c in counts.items())
+    return f"{w.name}: {w.blocks} x {{{inner}}}, fp32 factors, {w.grad_dtype} G"
+
+
+def fill_inputs(layers, w, seed=2306):
+    """Seeded synthetic inputs drawn on the GPU with the workload's distributions:
+    a ~ N(0, v/rows) (v = 1, or 2 for Student-t(4) rows), g ~ N(0, 1e-6/rows),
+    G ~ N(0, 1e-6) (bf16-rounded for bf16 workloads)."""
+    import torch
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    va = 2.0 if w.act_dist == "student_t4" else 1.0
+    for L in layers:
+        L["a"].normal_(0.0, math.sqrt(va / w.rows), generator=gen)
+        L["g"].normal_(0.0, w.grad_row_std / math.sqrt(w.rows), generator=gen)
+        if L["G"].dtype == torch.float32:
+            L["G"].normal_(0.0, w.G_std, generator=gen)
+        else:
+            tmp = torch.empty(L["G"].shape, dtype=torch.float32, device="cuda")
+            tmp.normal_(0.0, w.G_std, generator=gen)
+            L["G"].copy_(tmp)
+            del tmp
+
+
+def cpu_baseline(w, budget_s):
+    """The float64 oracle (as is) on a bounded sample: the first block of the
+    workload (one layer of each shape), full steps from the initial factors,
+    repeated until the time budget is used."""
+    import numpy as np
+
+    import oracle as O
+    import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    nb = len(w.block_shapes)
+    inputs = []
+    for i in range(nb):
+        a, g = W.rank1_vectors(w, i, 0)
+        G = W.gradient(w, i, 0)
+        L0, R0 = W.initial_factors(w, i)
+        inputs.append(dict(Linv=L0.astype(np.float64), Rinv=R0.astype(np.float64), a=a, g=g, G=G))
+    p = O.Params(gamma=w.gamma, eps=100.0)
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        out = O.oracle_step(inputs, p)
+        for L, o in zip(inputs, out):
+            L["Linv"], L["Rinv"] = o["Linv"], o["Rinv"]
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return dict(value=nb * steps / el, unit="layer-updates/s", cores=int(threads), kind="oracle",
+                sample=f"first block of the workload ({nb} layers, one of each shape), {steps} full "
+                       f"float64 steps in {el:.1f} s; host has {len(os.sched_getaffinity(0))} cpus")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the hot path runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads as W
+    from paper_2306_01685_amd import NUM_STAGES, STAGE_NAMES, Params, harness as H
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = W.CONFIGS[args.config]
+    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False)
+    if w.init != "identity":
+        for i, L in enumerate(layers):
+            H.set_factors(L, *W.initial_factors(w, i))
+    fill_inputs(layers, w)
+    plan = H.make_plan(layers)
+    params = Params(gamma=w.gamma, zeta=0.5, eps=args.eps)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        plan.step(params)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(args.steps):
+        plan.step(params)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    value = w.n_layers / (ms_step / 1e3)
+
+    # per-kernel times: the same steps launched stage by stage with HIP events
+    # between consecutive kernels on the launch stream
+    kernels = {}
+    if not args.no_stage_timing:
+        acc = [0.0] * NUM_STAGES
+        for _ in range(args.steps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(NUM_STAGES + 1)]
+            ev[0].record(stream)
+            for s in range(NUM_STAGES):
+                plan.run_stage(params, s)
+                ev[s + 1].record(stream)
+            torch.cuda.synchronize()
+            for s in range(NUM_STAGES):
+                acc[s] += ev[s].elapsed_time(ev[s + 1])
+        ms = [a / args.steps for a in acc]
+        sq = w.factor_elems
+        f1 = sum(2 * i * o * i for i, o in w.shapes)
+        f2 = sum(2 * i * o * o for i, o in w.shapes)
+        nel = sum(i * o for i, o in w.shapes)
+        gb = 1e-9
+        gbytes_G = nel * (2 if w.grad_dtype == "bf16" else 4)
+        kernels = {
+            "sm_matvec": dict(ms=ms[0], alg_bytes=4 * sq, gbs=4 * sq * gb / (ms[0] / 1e3)),
+            "sm_update": dict(ms=ms[1], alg_bytes=8 * sq, gbs=8 * sq * gb / (ms[1] / 1e3)),
+            "gemm_xt": dict(ms=ms[2], flops=f1, tflops=f1 / (ms[2] / 1e3) / 1e12),
+            "gemm_dw": dict(ms=ms[3], flops=f2, tflops=f2 / (ms[3] / 1e3) / 1e12),
+            "rescale": dict(ms=ms[4], alg_bytes=8 * nel, gbs=8 * nel * gb / (ms[4] / 1e3)),
+        }
+        sm_ms = ms[0] + ms[1]
+        kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=8 * sq, gbs=8 * sq * gb / (sm_ms / 1e3),
+                                   frac_hbm=8 * sq * gb / (sm_ms / 1e3) / HBM_PEAK_GBS,
+                                   eager_bytes=12 * sq)
+        pre_ms = ms[2] + ms[3]
+        kernels["gemm_total"] = dict(ms=pre_ms, flops=f1 + f2,
+                                     tflops=(f1 + f2) / (pre_ms / 1e3) / 1e12,
+                                     frac_mfma=(f1 + f2) / (pre_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TF)
+        for k in ("sm_matvec", "sm_update", "rescale"):
+            kernels[k]["frac_hbm"] = kernels[k]["gbs"] / HBM_PEAK_GBS
+        for k in ("gemm_xt", "gemm_dw"):
+            kernels[k]["frac_mfma"] = kernels[k]["tflops"] / FP32_MFMA_PEAK_TF
+        dom = max(range(NUM_STAGES), key=lambda s: ms[s])
+        name = STAGE_NAMES[dom]
+        k = kernels[name]
+        if "flops" in k:
+            roof = dict(kernel=name, bound="mfma", achieved=k["tflops"], peak=FP32_MFMA_PEAK_TF,
+                        unit="TFLOP/s", frac=k["tflops"] / FP32_MFMA_PEAK_TF, traffic=None,
+                        per_launch=f"{k['flops']:.4e} flop (sum of 2*M*N*K over the layers)")
+        else:
+            roof = dict(kernel=name, bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
+                        frac=k["gbs"] / HBM_PEAK_GBS, traffic=None,
+                        per_launch=f"{k['alg_bytes']:.4e} B")
+    else:
+        roof = None
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "layer-updates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded; layer shapes only)",
+        "config": {"workload": workload_desc(w), "n_layers": w.n_layers,
+                   "factor_elems": w.factor_elems, "precond_flops": w.precond_flops,
+                   "gamma": w.gamma, "zeta": 0.5, "eps": args.eps, "grad_dtype": w.grad_dtype},
+        "roofline": roof,
+        "kernels": kernels,
+        "device": torch.cuda.get_device_name(0),
+    }
+    del plan, layers
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,192 @@
+/*
+ * mkor.h - C ABI of the MI355X (gfx950) implementation of MKOR's per-step
+ * hot path (arXiv 2306.01685, "MKOR: Momentum-Enabled Kronecker-Factor-Based
+ * Optimizer Using Rank-1 Updates").
+ *
+ * For every layer of a grouped list the library runs, on the caller's HIP
+ * stream, the second-order branch of Algorithm 1 with the rank-1 means handed
+ * in as inputs:
+ *
+ *   1. norm-based stabiliser of each inverse factor   (Algorithm 1, the two
+ *      stabilisation lines; Eq. 9-11; "Exploding Gradients Problem")
+ *   2. momentum rank-1 Sherman-Morrison update of each inverse factor
+ *      (Algorithm 1, SM-based factor inversion; Eq. 4-7)
+ *   3. preconditioning dW_hat = Linv * G * Rinv with the updated factors
+ *      (Algorithm 1, precondition line; Eq. 2)
+ *   4. rescaling dW = (||G||_F / ||dW_hat||_F) * dW_hat
+ *      (Algorithm 1, rescale line; "Rescaling Gradients")
+ *   5. first-order layers: dW = G (Algorithm 1, else-branch)
+ *
+ * Orientation.  The gradient G of a layer is stored d_in x d_out, row-major.
+ * Linv is d_in x d_in and is driven by the mean activation a (length d_in);
+ * Rinv is d_out x d_out and is driven by the mean output gradient g (length
+ * d_out).  The paper writes the transposed gradient; since both factors are
+ * symmetric the two forms are the same update.
+ *
+ * Update of one factor P with vector x (both sides use the same rule):
+ *   nu    = ||P||              (induced infinity norm = max abs row sum, or
+ *                               max |entry|, see mkor_params.norm_kind)
+ *   P_hat = zeta P + (1 - zeta) I   if nu > eps (strict),  else P
+ *   u     = P_hat x,  s = x^T u
+ *   MKOR_SM_EXACT:     P <- (1/gamma) (P_hat - k u u^T),
+ *                      k = (1 - gamma) / (gamma + (1 - gamma) s)
+ *                      (the Sherman-Morrison inverse of the momentum
+ *                      accumulation M_t = gamma M_hat_{t-1} + (1 - gamma) x x^T
+ *                      of Eq. 4/5; the default)
+ *   MKOR_SM_PAPER_EQ6: P <- gamma P_hat
+ *                            + (1 - gamma) / (gamma^2 (1 + gamma (1 - gamma) s)) u u^T
+ *                      (Eq. 6/7 exactly as printed, which is not the inverse
+ *                      of Eq. 4/5; kept as an option)
+ *
+ * Memory and ownership.
+ *   - Every buffer named in mkor_layer, and the workspace, is device memory
+ *     owned by the caller.  The library never allocates or frees device
+ *     memory; its only allocation is the host-side mkor_plan object.
+ *   - Matrices are dense, row-major, contiguous (leading dimension = row
+ *     length).  Every pointer must be 16-byte aligned; the workspace must be
+ *     256-byte aligned.
+ *   - Pointers are captured by mkor_plan_create.  Before each step the
+ *     caller refills a, g and G in place; Linv and Rinv are updated in place
+ *     and must hold symmetric matrices (initially I in the paper).
+ *   - Writable buffers (Linv, Rinv, dW, stats) must not overlap any other
+ *     buffer of any layer or the workspace.  Read-only inputs may be shared.
+ *
+ * Errors.  Every int-returning call returns MKOR_OK (0) or a negative status.
+ * All argument checks run on the host before the first HIP call of a call.
+ * Execution is asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ * is the default stream); device-side faults surface at the caller's next
+ * synchronisation.  No call blocks on the device, and none prints.
+ * mkor_last_error() returns a thread-local text describing the last failure.
+ *
+ * Calls that share a plan (or a workspace) must not run concurrently.
+ */
+#ifndef MKOR_H
+#define MKOR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MKOR_ABI_VERSION 1
+
+/* status codes */
+#define MKOR_OK                   0
+#define MKOR_INVALID_ARG         -1  /* null pointer, bad size, bad parameter, aliasing, misalignment */
+#define MKOR_WORKSPACE_TOO_SMALL -2
+#define MKOR_UNSUPPORTED         -3  /* e.g. an unknown gradient dtype */
+#define MKOR_HIP_ERROR           -4  /* a HIP runtime call or kernel launch failed */
+
+/* mkor_params.sm_variant */
+#define MKOR_SM_EXACT      0
+#define MKOR_SM_PAPER_EQ6  1
+/* mkor_params.norm_kind */
+#define MKOR_NORM_INF      0   /* max_i sum_j |P_ij| */
+#define MKOR_NORM_MAXABS   1   /* max_ij |P_ij| */
+/* mkor_layer.grad_dtype */
+#define MKOR_DTYPE_F32     0
+#define MKOR_DTYPE_BF16    1
+
+/* kernels of one step, in launch order (mkor_run_stage) */
+#define MKOR_STAGE_SM_MATVEC  0   /* u_raw = P x, norm and s partials, all factors */
+#define MKOR_STAGE_SM_UPDATE  1   /* stabiliser decision + in-place rank-1 update */
+#define MKOR_STAGE_GEMM_XT    2   /* X^T = (Linv G)^T, ||G||^2 partials */
+#define MKOR_STAGE_GEMM_DW    3   /* dW_hat = X Rinv, ||dW_hat||^2 partials */
+#define MKOR_STAGE_RESCALE    4   /* rescale / first-order pass-through */
+#define MKOR_NUM_STAGES       5
+
+/* largest supported d_in / d_out */
+#define MKOR_MAX_DIM       32768
+
+typedef struct mkor_params {
+    float   gamma;            /* momentum of Eq. 4/5, 0 < gamma < 1 */
+    float   zeta;             /* stabiliser blend of Eq. 9/10, 0 < zeta <= 1 */
+    float   stab_eps;         /* stabiliser threshold, >= 0; +INFINITY turns it off */
+    int32_t norm_kind;        /* MKOR_NORM_INF or MKOR_NORM_MAXABS */
+    int32_t sm_variant;       /* MKOR_SM_EXACT (default) or MKOR_SM_PAPER_EQ6 */
+    int32_t rescale;          /* 1: rescale line of Algorithm 1 on; 0: dW = dW_hat */
+    int32_t guard_nonfinite;  /* 1: a factor whose norm, s or update coefficient is
+                                 not finite is left unchanged (and flagged in stats);
+                                 0: non-finite values propagate */
+} mkor_params;
+
+typedef struct mkor_layer {
+    int32_t      d_in, d_out;   /* 1 .. MKOR_MAX_DIM */
+    int32_t      second_order;  /* 1: MKOR branch; 0: dW = G (first-order layer) */
+    int32_t      grad_dtype;    /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (element type of G) */
+    float*       Linv;          /* d_in x d_in, in/out (unused if second_order = 0) */
+    float*       Rinv;          /* d_out x d_out, in/out (unused if second_order = 0) */
+    const float* a;             /* d_in, mean activation (unused if second_order = 0) */
+    const float* g;             /* d_out, mean output gradient (unused if second_order = 0) */
+    const void*  G;             /* d_in x d_out gradient, grad_dtype elements */
+    float*       dW;            /* d_in x d_out fp32 output */
+    void*        stats;         /* optional device mkor_layer_stats*, may be NULL */
+} mkor_layer;
+
+/* Per-layer observability record, written on the device when
+ * mkor_layer.stats is not NULL.  Fields of a half that did not run keep their
+ * previous contents. */
+typedef struct mkor_layer_stats {
+    float   nu_L, nu_R;        /* factor norms before this step's update */
+    float   s_L, s_R;          /* x^T P_hat x */
+    float   norm_G;            /* ||G||_F */
+    float   norm_dW_hat;       /* ||Linv G Rinv||_F */
+    float   scale;             /* rescale factor applied (1 when rescale = 0) */
+    int32_t stab_L, stab_R;    /* 1 if the stabiliser fired */
+    int32_t skip_L, skip_R;    /* 1 if nu, s or the coefficient was not finite */
+    int32_t nonfinite_scale;   /* 1 if a rescale norm was not finite */
+} mkor_layer_stats;
+
+typedef struct mkor_plan mkor_plan;
+
+/* MKOR_ABI_VERSION of the loaded library. */
+int mkor_abi_version(void);
+
+/* Static text for a status code. */
+const char* mkor_status_string(int status);
+
+/* Thread-local description of the last failure in this thread ("" if none). */
+const char* mkor_last_error(void);
+
+/* Checks a parameter block without touching the device. */
+int mkor_params_check(const mkor_params* params);
+
+/* Bytes of device workspace a plan over `layers[0..n)` needs (written to
+ * *bytes).  Host-only. */
+int mkor_workspace_size(const mkor_layer* layers, int32_t n, size_t* bytes);
+
+/* Validates the layer list (sizes, pointers, alignment, aliasing), lays out
+ * the workspace and uploads the grouped launch descriptors into it (one
+ * synchronous host-to-device copy).  `layers` is copied; the caller may free
+ * it afterwards.  n = 0 gives an empty plan whose calls are no-ops. */
+int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace,
+                     size_t ws_bytes, mkor_plan** out);
+
+/* Stabiliser + SM update of Linv and Rinv of every second-order layer
+ * (Algorithm 1, stabilisation and SM lines), in one grouped pass. */
+int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream);
+
+/* Preconditioning with the current factors, rescale, and the first-order
+ * pass-through (Algorithm 1, precondition, rescale and else lines). */
+int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream);
+
+/* mkor_update_factors followed by mkor_precondition: one full step. */
+int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream);
+
+/* Launches one kernel of a step (MKOR_STAGE_*), for profiling and per-kernel
+ * timing.  Launching stages 0..MKOR_NUM_STAGES-1 in order on one stream is
+ * exactly mkor_step; a stage launched out of that order reads whatever the
+ * workspace holds from earlier launches. */
+int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, void* stream);
+
+/* Frees the host-side plan (NULL is allowed).  The workspace stays the
+ * caller's. */
+void mkor_plan_destroy(mkor_plan* plan);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MKOR_H */

@@ -1,0 +1,264 @@
+"""Thin ctypes binding of libmkor's C ABI (include/mkor.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP
+kernels of libmkor.so.  PyTorch supplies device memory and streams.  There is
+no fallback: if the library is missing or fails to load, every entry point
+raises.
+
+torch is imported before the library is loaded so that libmkor resolves to
+the HIP runtime torch already loaded (one runtime per process; streams and
+device pointers are shared).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch  # noqa: F401  (must precede loading libmkor, see module docstring)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmkor.so")
+
+MKOR_OK = 0
+MKOR_INVALID_ARG = -1
+MKOR_WORKSPACE_TOO_SMALL = -2
+MKOR_UNSUPPORTED = -3
+MKOR_HIP_ERROR = -4
+
+SM_EXACT = 0
+SM_PAPER_EQ6 = 1
+NORM_INF = 0
+NORM_MAXABS = 1
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+MAX_DIM = 32768
+ABI_VERSION = 1
+
+
+class mkor_params(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_float), ("zeta", ctypes.c_float), ("stab_eps", ctypes.c_float),
+                ("norm_kind", ctypes.c_int32), ("sm_variant", ctypes.c_int32),
+                ("rescale", ctypes.c_int32), ("guard_nonfinite", ctypes.c_int32)]
+
+
+class mkor_layer(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("second_order", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
+                ("Linv", ctypes.c_void_p), ("Rinv", ctypes.c_void_p),
+                ("a", ctypes.c_void_p), ("g", ctypes.c_void_p),
+                ("G", ctypes.c_void_p), ("dW", ctypes.c_void_p), ("stats", ctypes.c_void_p)]
+
+
+class mkor_layer_stats(ctypes.Structure):
+    _fields_ = [("nu_L", ctypes.c_float), ("nu_R", ctypes.c_float),
+                ("s_L", ctypes.c_float), ("s_R", ctypes.c_float),
+                ("norm_G", ctypes.c_float), ("norm_dW_hat", ctypes.c_float), ("scale", ctypes.c_float),
+                ("stab_L", ctypes.c_int32), ("stab_R", ctypes.c_int32),
+                ("skip_L", ctypes.c_int32), ("skip_R", ctypes.c_int32),
+                ("nonfinite_scale", ctypes.c_int32)]
+
+
+STATS_BYTES = ctypes.sizeof(mkor_layer_stats)
+STATS_FIELDS = [f for f, _ in mkor_layer_stats._fields_]
+
+EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_params_check",
+            "mkor_workspace_size", "mkor_plan_create", "mkor_update_factors",
+            "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_plan_destroy"]
+
+STAGE_SM_MATVEC, STAGE_SM_UPDATE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(5)
+NUM_STAGES = 5
+STAGE_NAMES = ["sm_matvec", "sm_update", "gemm_xt", "gemm_dw", "rescale"]
+
+
+class MkorError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: {status_string(status)} ({status}): {detail}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libmkor.so once; raises if it is absent (no fallback path)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libmkor.so not found at {path}: build it with "
+                           "`python -m paper_2306_01685_amd.build` (or __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.mkor_abi_version.restype = ctypes.c_int
+    lib.mkor_abi_version.argtypes = []
+    lib.mkor_status_string.restype = ctypes.c_char_p
+    lib.mkor_status_string.argtypes = [ctypes.c_int]
+    lib.mkor_last_error.restype = ctypes.c_char_p
+    lib.mkor_last_error.argtypes = []
+    lib.mkor_params_check.restype = ctypes.c_int
+    lib.mkor_params_check.argtypes = [ctypes.POINTER(mkor_params)]
+    lib.mkor_workspace_size.restype = ctypes.c_int
+    lib.mkor_workspace_size.argtypes = [ctypes.POINTER(mkor_layer), I32, ctypes.POINTER(SZ)]
+    lib.mkor_plan_create.restype = ctypes.c_int
+    lib.mkor_plan_create.argtypes = [ctypes.POINTER(mkor_layer), I32, P, SZ, ctypes.POINTER(P)]
+    for name in ("mkor_update_factors", "mkor_precondition", "mkor_step"):
+        fn = getattr(lib, name)
+        fn.restype = ctypes.c_int
+        fn.argtypes = [P, ctypes.POINTER(mkor_params), P]
+    lib.mkor_run_stage.restype = ctypes.c_int
+    lib.mkor_run_stage.argtypes = [P, ctypes.POINTER(mkor_params), I32, P]
+    lib.mkor_plan_destroy.restype = None
+    lib.mkor_plan_destroy.argtypes = [P]
+    if lib.mkor_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"libmkor ABI {lib.mkor_abi_version()} != binding ABI {ABI_VERSION}")
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().mkor_status_string(status).decode()
+
+
+def last_error() -> str:
+    return load_library().mkor_last_error().decode()
+
+
+def _check(status: int, where: str):
+    if status != MKOR_OK:
+        raise MkorError(status, where, last_error())
+
+
+@dataclass
+class Params:
+    gamma: float = 0.9
+    zeta: float = 0.5
+    eps: float = 100.0
+    norm_kind: int = NORM_INF
+    variant: int = SM_EXACT
+    rescale: bool = True
+    guard_nonfinite: bool = True
+
+    def to_c(self) -> mkor_params:
+        return mkor_params(self.gamma, self.zeta, self.eps,
+                           int(self.norm_kind), int(self.variant), int(bool(self.rescale)),
+                           int(bool(self.guard_nonfinite)))
+
+
+def params_check(p) -> int:
+    c = p.to_c() if isinstance(p, Params) else p
+    return load_library().mkor_params_check(ctypes.byref(c))
+
+
+def make_layer_array(descs):
+    """descs: list of dicts with integer fields and raw pointer values."""
+    arr = (mkor_layer * max(1, len(descs)))()
+    for i, d in enumerate(descs):
+        arr[i] = mkor_layer(d["d_in"], d["d_out"], d.get("second_order", 1), d.get("grad_dtype", 0),
+                            d.get("Linv") or None, d.get("Rinv") or None, d.get("a") or None,
+                            d.get("g") or None, d.get("G") or None, d.get("dW") or None,
+                            d.get("stats") or None)
+    return arr
+
+
+def workspace_size_raw(descs) -> int:
+    arr = make_layer_array(descs)
+    out = ctypes.c_size_t(0)
+    _check(load_library().mkor_workspace_size(arr, len(descs), ctypes.byref(out)), "mkor_workspace_size")
+    return out.value
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class MkorPlan:
+    """A plan over a grouped list of layers, holding torch device tensors.
+
+    Each layer is a dict with d_in, d_out and tensors Linv, Rinv (fp32,
+    symmetric), a, g (fp32 vectors), G (fp32 or bf16, d_in x d_out), dW (fp32,
+    d_in x d_out), optional second_order (default True) and optional stats
+    (a uint8 device tensor of STATS_BYTES bytes).  The plan owns its workspace
+    (a torch uint8 tensor) and keeps references to every tensor it was given.
+    """
+
+    def __init__(self, layers, device=None):
+        self._lib = load_library()
+        self.layers = layers
+        descs = []
+        for L in layers:
+            so = int(bool(L.get("second_order", True)))
+            G = L["G"]
+            if G.dtype == torch.bfloat16:
+                gdt = DTYPE_BF16
+            elif G.dtype == torch.float32:
+                gdt = DTYPE_F32
+            else:
+                raise TypeError(f"unsupported gradient dtype {G.dtype}")
+            for k in ("Linv", "Rinv", "a", "g", "G", "dW"):
+                t = L.get(k)
+                if t is not None and not t.is_contiguous():
+                    raise ValueError(f"{k} must be contiguous")
+            descs.append(dict(d_in=int(L["d_in"]), d_out=int(L["d_out"]), second_order=so,
+                              grad_dtype=gdt, Linv=_ptr(L.get("Linv")), Rinv=_ptr(L.get("Rinv")),
+                              a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
+                              stats=_ptr(L.get("stats"))))
+        self._arr = make_layer_array(descs)
+        n = len(descs)
+        size = ctypes.c_size_t(0)
+        _check(self._lib.mkor_workspace_size(self._arr, n, ctypes.byref(size)), "mkor_workspace_size")
+        self.ws_bytes = size.value
+        if device is None:
+            device = layers[0]["dW"].device if layers else torch.device("cuda")
+        # over-allocate by 256 bytes and align the base to 256
+        self._ws_raw = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
+        base = self._ws_raw.data_ptr()
+        off = (-base) % 256
+        self.workspace = self._ws_raw[off:off + self.ws_bytes]
+        plan = ctypes.c_void_p(None)
+        _check(self._lib.mkor_plan_create(self._arr, n, ctypes.c_void_p(base + off), self.ws_bytes,
+                                          ctypes.byref(plan)), "mkor_plan_create")
+        self._plan = plan
+
+    def _call(self, name, params, stream):
+        p = params.to_c() if isinstance(params, Params) else params
+        fn = getattr(self._lib, name)
+        _check(fn(self._plan, ctypes.byref(p), _stream_handle(stream)), name)
+
+    def update_factors(self, params: Params, stream=None):
+        self._call("mkor_update_factors", params, stream)
+
+    def precondition(self, params: Params, stream=None):
+        self._call("mkor_precondition", params, stream)
+
+    def step(self, params: Params, stream=None):
+        self._call("mkor_step", params, stream)
+
+    def run_stage(self, params: Params, stage: int, stream=None):
+        p = params.to_c() if isinstance(params, Params) else params
+        _check(self._lib.mkor_run_stage(self._plan, ctypes.byref(p), int(stage), _stream_handle(stream)),
+               "mkor_run_stage")
+
+    def close(self):
+        if getattr(self, "_plan", None) is not None and self._plan.value:
+            self._lib.mkor_plan_destroy(self._plan)
+            self._plan = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def read_stats(stats_tensor) -> dict:
+    """Decodes one mkor_layer_stats record from a uint8 tensor (any device)."""
+    raw = bytes(stats_tensor.detach().cpu().numpy().tobytes())
+    s = mkor_layer_stats.from_buffer_copy(raw[:STATS_BYTES])
+    return {f: getattr(s, f) for f in STATS_FIELDS}

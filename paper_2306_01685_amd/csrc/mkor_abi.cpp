@@ -1,0 +1,433 @@
+// C ABI of libmkor: argument validation, plan / workspace layout, launches.
+//
+// All validation runs on the host before the first HIP call of an entry
+// point, so every error path can be exercised without a GPU.
+#include "mkor_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace mkor;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(MKOR_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Interval {
+    uintptr_t lo, hi;
+    bool writable;
+    int layer;
+    const char* what;
+};
+
+int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_bytes) {
+    if (n < 0) return fail(MKOR_INVALID_ARG, "n = %d is negative", n);
+    if (n > 0 && layers == nullptr) return fail(MKOR_INVALID_ARG, "layers is NULL with n = %d", n);
+    std::vector<Interval> iv;
+    iv.reserve((size_t)n * 7 + 1);
+    for (int32_t i = 0; i < n; ++i) {
+        const mkor_layer& L = layers[i];
+        if (L.d_in < 1 || L.d_in > MKOR_MAX_DIM || L.d_out < 1 || L.d_out > MKOR_MAX_DIM)
+            return fail(MKOR_INVALID_ARG, "layer %d: d_in = %d, d_out = %d outside 1..%d", i, L.d_in,
+                        L.d_out, MKOR_MAX_DIM);
+        if (L.second_order != 0 && L.second_order != 1)
+            return fail(MKOR_INVALID_ARG, "layer %d: second_order = %d is not 0 or 1", i, L.second_order);
+        if (L.grad_dtype != MKOR_DTYPE_F32 && L.grad_dtype != MKOR_DTYPE_BF16)
+            return fail(MKOR_UNSUPPORTED, "layer %d: grad_dtype = %d is not supported", i, L.grad_dtype);
+        const size_t din = (size_t)L.d_in, dout = (size_t)L.d_out;
+        const size_t gsz = din * dout * (L.grad_dtype == MKOR_DTYPE_BF16 ? 2 : 4);
+        struct { const void* p; size_t bytes; bool w; const char* what; bool used; } bufs[] = {
+            {L.G, gsz, false, "G", true},
+            {L.dW, din * dout * 4, true, "dW", true},
+            {L.Linv, din * din * 4, true, "Linv", L.second_order == 1},
+            {L.Rinv, dout * dout * 4, true, "Rinv", L.second_order == 1},
+            {L.a, din * 4, false, "a", L.second_order == 1},
+            {L.g, dout * 4, false, "g", L.second_order == 1},
+            {L.stats, sizeof(mkor_layer_stats), true, "stats", L.stats != nullptr},
+        };
+        for (auto& b : bufs) {
+            if (!b.used) continue;
+            if (b.p == nullptr) return fail(MKOR_INVALID_ARG, "layer %d: %s is NULL", i, b.what);
+            if (!aligned(b.p, 16))
+                return fail(MKOR_INVALID_ARG, "layer %d: %s is not 16-byte aligned", i, b.what);
+            const uintptr_t lo = reinterpret_cast<uintptr_t>(b.p);
+            if (lo + b.bytes < lo) return fail(MKOR_INVALID_ARG, "layer %d: %s wraps the address space", i, b.what);
+            iv.push_back({lo, lo + b.bytes, b.w, i, b.what});
+        }
+    }
+    if (ws != nullptr && ws_bytes > 0) {
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(ws);
+        iv.push_back({lo, lo + ws_bytes, true, -1, "workspace"});
+    }
+    // Any overlap that involves a writable buffer is an error.  After sorting
+    // by start, an interval overlaps an earlier one iff its start lies below
+    // the largest end seen so far; tracking that maximum separately for
+    // writable intervals and for all intervals catches every such pair.
+    std::sort(iv.begin(), iv.end(), [](const Interval& x, const Interval& y) { return x.lo < y.lo; });
+    uintptr_t max_all = 0, max_w = 0;
+    const Interval *arg_all = nullptr, *arg_w = nullptr;
+    for (const Interval& c : iv) {
+        if (arg_w && c.lo < max_w)
+            return fail(MKOR_INVALID_ARG, "%s of layer %d overlaps writable %s of layer %d", c.what,
+                        c.layer, arg_w->what, arg_w->layer);
+        if (c.writable && arg_all && c.lo < max_all)
+            return fail(MKOR_INVALID_ARG, "writable %s of layer %d overlaps %s of layer %d", c.what,
+                        c.layer, arg_all->what, arg_all->layer);
+        if (c.hi > max_all) { max_all = c.hi; arg_all = &c; }
+        if (c.writable && c.hi > max_w) { max_w = c.hi; arg_w = &c; }
+    }
+    return MKOR_OK;
+}
+
+// ------------------------------------------------------------------ layout
+struct Layout {
+    size_t off_factors = 0, off_rowblocks = 0, off_u = 0, off_smpart = 0;
+    size_t off_g1l = 0, off_g1t = 0, off_g2l = 0, off_g2t = 0, off_gpart = 0, off_dpart = 0;
+    size_t off_rsl = 0, off_rsb = 0, off_x = 0;
+    size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
+    size_t total = 0;
+    int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
+    int32_t nsecond = 0;
+    std::vector<size_t> u_off, x_off;   // per factor / per layer offsets (bytes)
+};
+
+int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
+
+int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
+    int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const mkor_layer& L = layers[i];
+        rsb += ceil_div((int64_t)L.d_in * L.d_out, RS_ELEMS);
+        if (!L.second_order) continue;
+        Lo.nsecond++;
+        rowblocks += ceil_div(L.d_in, SM_ROWS) + ceil_div(L.d_out, SM_ROWS);
+        const int64_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
+        g1 += tm * tn;
+        gpart += tn;
+        usum += L.d_in + L.d_out;
+    }
+    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX)
+        return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
+    Lo.nfactors = 2 * Lo.nsecond;
+    Lo.nrowblocks = (int32_t)rowblocks;
+    Lo.ng1 = Lo.ng2 = (int32_t)g1;
+    Lo.ngpart = (int32_t)gpart;
+    Lo.ndpart = (int32_t)g1;
+    Lo.nrsblocks = (int32_t)rsb;
+
+    size_t o = 0;
+    auto take = [&](size_t bytes) { o = align_up(o, 256); size_t r = o; o += bytes; return r; };
+    Lo.off_factors = take(sizeof(FactorDesc) * Lo.nfactors);
+    Lo.off_rowblocks = take(sizeof(RowBlock) * Lo.nrowblocks);
+    Lo.off_g1l = take(sizeof(GemmLayer) * n);
+    Lo.off_g1t = take(sizeof(GemmTile) * Lo.ng1);
+    Lo.off_g2l = take(sizeof(GemmLayer) * n);
+    Lo.off_g2t = take(sizeof(GemmTile) * Lo.ng2);
+    Lo.off_rsl = take(sizeof(RescaleLayer) * n);
+    Lo.off_rsb = take(sizeof(RescaleBlock) * Lo.nrsblocks);
+    Lo.table_bytes = align_up(o, 256);
+    Lo.off_smpart = take(sizeof(float4) * Lo.nrowblocks);
+    Lo.off_gpart = take(sizeof(float) * Lo.ngpart);
+    Lo.off_dpart = take(sizeof(float) * Lo.ndpart);
+    Lo.u_off.clear();
+    Lo.x_off.assign(n, 0);
+    for (int32_t i = 0; i < n; ++i) {
+        if (!layers[i].second_order) continue;
+        Lo.u_off.push_back(take(sizeof(float) * layers[i].d_in));
+        Lo.u_off.push_back(take(sizeof(float) * layers[i].d_out));
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        if (!layers[i].second_order) continue;
+        Lo.x_off[i] = take(sizeof(float) * (size_t)layers[i].d_in * layers[i].d_out);
+    }
+    Lo.total = align_up(o, 256);
+    (void)usum;
+    return MKOR_OK;
+}
+
+int check_params(const mkor_params* p) {
+    if (p == nullptr) return fail(MKOR_INVALID_ARG, "params is NULL");
+    if (!(p->gamma > 0.f && p->gamma < 1.f))
+        return fail(MKOR_INVALID_ARG, "gamma = %g outside (0, 1)", (double)p->gamma);
+    if (!(p->zeta > 0.f && p->zeta <= 1.f))
+        return fail(MKOR_INVALID_ARG, "zeta = %g outside (0, 1]", (double)p->zeta);
+    if (std::isnan(p->stab_eps) || p->stab_eps < 0.f)
+        return fail(MKOR_INVALID_ARG, "stab_eps = %g must be >= 0 or +inf", (double)p->stab_eps);
+    if (p->norm_kind != MKOR_NORM_INF && p->norm_kind != MKOR_NORM_MAXABS)
+        return fail(MKOR_INVALID_ARG, "norm_kind = %d unknown", p->norm_kind);
+    if (p->sm_variant != MKOR_SM_EXACT && p->sm_variant != MKOR_SM_PAPER_EQ6)
+        return fail(MKOR_INVALID_ARG, "sm_variant = %d unknown", p->sm_variant);
+    if (p->rescale != 0 && p->rescale != 1)
+        return fail(MKOR_INVALID_ARG, "rescale = %d is not 0 or 1", p->rescale);
+    if (p->guard_nonfinite != 0 && p->guard_nonfinite != 1)
+        return fail(MKOR_INVALID_ARG, "guard_nonfinite = %d is not 0 or 1", p->guard_nonfinite);
+    return MKOR_OK;
+}
+
+}  // namespace
+
+struct mkor_plan {
+    int32_t n = 0;
+    char* ws = nullptr;
+    Layout lo;
+};
+
+extern "C" {
+
+int mkor_abi_version(void) { return MKOR_ABI_VERSION; }
+
+const char* mkor_status_string(int status) {
+    switch (status) {
+        case MKOR_OK: return "MKOR_OK";
+        case MKOR_INVALID_ARG: return "MKOR_INVALID_ARG";
+        case MKOR_WORKSPACE_TOO_SMALL: return "MKOR_WORKSPACE_TOO_SMALL";
+        case MKOR_UNSUPPORTED: return "MKOR_UNSUPPORTED";
+        case MKOR_HIP_ERROR: return "MKOR_HIP_ERROR";
+        default: return "MKOR_UNKNOWN_STATUS";
+    }
+}
+
+const char* mkor_last_error(void) { return g_err; }
+
+int mkor_params_check(const mkor_params* params) {
+    g_err[0] = 0;
+    return check_params(params);
+}
+
+int mkor_workspace_size(const mkor_layer* layers, int32_t n, size_t* bytes) {
+    g_err[0] = 0;
+    if (bytes == nullptr) return fail(MKOR_INVALID_ARG, "bytes is NULL");
+    int st = check_layers(layers, n, nullptr, 0);
+    if (st != MKOR_OK) return st;
+    Layout lo;
+    st = compute_layout(layers, n, lo);
+    if (st != MKOR_OK) return st;
+    *bytes = lo.total;
+    return MKOR_OK;
+}
+
+int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, size_t ws_bytes,
+                     mkor_plan** out) {
+    g_err[0] = 0;
+    if (out == nullptr) return fail(MKOR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    int st = check_layers(layers, n, nullptr, 0);
+    if (st != MKOR_OK) return st;
+    Layout lo;
+    st = compute_layout(layers, n, lo);
+    if (st != MKOR_OK) return st;
+    if (lo.total > 0) {
+        if (d_workspace == nullptr) return fail(MKOR_INVALID_ARG, "workspace is NULL");
+        if (!aligned(d_workspace, 256)) return fail(MKOR_INVALID_ARG, "workspace is not 256-byte aligned");
+        if (ws_bytes < lo.total)
+            return fail(MKOR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, the plan needs %zu", ws_bytes,
+                        lo.total);
+        st = check_layers(layers, n, d_workspace, lo.total);
+        if (st != MKOR_OK) return st;
+    }
+
+    // ---- host-side descriptor tables
+    char* base = static_cast<char*>(d_workspace);
+    std::vector<char> host(lo.table_bytes, 0);
+    FactorDesc* fd = reinterpret_cast<FactorDesc*>(host.data() + lo.off_factors);
+    RowBlock* rb = reinterpret_cast<RowBlock*>(host.data() + lo.off_rowblocks);
+    GemmLayer* g1l = reinterpret_cast<GemmLayer*>(host.data() + lo.off_g1l);
+    GemmLayer* g2l = reinterpret_cast<GemmLayer*>(host.data() + lo.off_g2l);
+    GemmTile* g1t = reinterpret_cast<GemmTile*>(host.data() + lo.off_g1t);
+    GemmTile* g2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_g2t);
+    RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
+    RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
+
+    int32_t fi = 0, bi = 0, gp = 0, dp = 0, rbi = 0;
+    std::vector<GemmTile> t1, t2;
+    t1.reserve(lo.ng1);
+    t2.reserve(lo.ng2);
+    for (int32_t i = 0; i < n; ++i) {
+        const mkor_layer& L = layers[i];
+        mkor_layer_stats* stats = static_cast<mkor_layer_stats*>(L.stats);
+        RescaleLayer& R = rsl[i];
+        R.G = L.G;
+        R.dW = L.dW;
+        R.stats = stats;
+        R.numel = (int64_t)L.d_in * L.d_out;
+        R.second_order = L.second_order;
+        R.g_bf16 = L.grad_dtype == MKOR_DTYPE_BF16;
+        R.first_blk = rbi;
+        for (int64_t s = 0; s < R.numel; s += RS_ELEMS) rsb[rbi++] = RescaleBlock{i, 0, s};
+        if (!L.second_order) continue;
+        for (int side = 0; side < 2; ++side) {
+            FactorDesc& f = fd[fi];
+            f.P = side == 0 ? L.Linv : L.Rinv;
+            f.x = side == 0 ? L.a : L.g;
+            f.u = reinterpret_cast<float*>(base + lo.u_off[fi]);
+            f.stats = stats;
+            f.d = side == 0 ? L.d_in : L.d_out;
+            f.blk0 = bi;
+            f.nblk = ceil_div(f.d, SM_ROWS);
+            f.side = side;
+            for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * SM_ROWS};
+            ++fi;
+        }
+        float* X = reinterpret_cast<float*>(base + lo.x_off[i]);
+        const int32_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
+        const bool bf16 = L.grad_dtype == MKOR_DTYPE_BF16;
+        GemmLayer& A = g1l[i];
+        A.At = L.Linv; A.B = L.G; A.C = X;
+        A.M = L.d_in; A.N = L.d_out; A.K = L.d_in;
+        A.b_bf16 = bf16;
+        A.vec = (L.d_in % 4 == 0) && (L.d_out % (bf16 ? 8 : 4) == 0);
+        A.part0 = gp; A.ntn = tn;
+        GemmLayer& B = g2l[i];
+        B.At = X; B.B = L.Rinv; B.C = L.dW;
+        B.M = L.d_in; B.N = L.d_out; B.K = L.d_out;
+        B.b_bf16 = 0;
+        B.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
+        B.part0 = dp; B.ntn = tn;
+        R.gpart0 = gp; R.ngpart = tn;
+        R.dpart0 = dp; R.ndpart = tm * tn;
+        gp += tn;
+        dp += tm * tn;
+        for (int32_t a = 0; a < tm; ++a)
+            for (int32_t b = 0; b < tn; ++b) {
+                t1.push_back(GemmTile{i, a, b, 0});
+                t2.push_back(GemmTile{i, a, b, 0});
+            }
+    }
+    // longest K first, so the long tiles do not form the tail of the launch
+    std::stable_sort(t1.begin(), t1.end(), [&](const GemmTile& x, const GemmTile& y) {
+        return layers[x.layer].d_in > layers[y.layer].d_in;
+    });
+    std::stable_sort(t2.begin(), t2.end(), [&](const GemmTile& x, const GemmTile& y) {
+        return layers[x.layer].d_out > layers[y.layer].d_out;
+    });
+    std::copy(t1.begin(), t1.end(), g1t);
+    std::copy(t2.begin(), t2.end(), g2t);
+
+    mkor_plan* plan = new (std::nothrow) mkor_plan;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "out of host memory");
+    plan->n = n;
+    plan->ws = base;
+    plan->lo = lo;
+    if (lo.table_bytes > 0) {
+        hipError_t e = hipMemcpy(base, host.data(), lo.table_bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            delete plan;
+            return hip_fail(e, "uploading plan descriptors");
+        }
+    }
+    *out = plan;
+    return MKOR_OK;
+}
+
+static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStream_t s) {
+    const Layout& lo = p->lo;
+    char* ws = p->ws;
+    const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(ws + lo.off_factors);
+    const RowBlock* rb = reinterpret_cast<const RowBlock*>(ws + lo.off_rowblocks);
+    float4* smpart = reinterpret_cast<float4*>(ws + lo.off_smpart);
+    float* gpart = reinterpret_cast<float*>(ws + lo.off_gpart);
+    float* dpart = reinterpret_cast<float*>(ws + lo.off_dpart);
+    hipError_t e = hipSuccess;
+    switch (stage) {
+        case MKOR_STAGE_SM_MATVEC:
+            if (lo.nrowblocks == 0) return MKOR_OK;
+            e = launch_sm_matvec(fd, rb, lo.nrowblocks, smpart, prm->norm_kind, s);
+            if (e != hipSuccess) return hip_fail(e, "sm_matvec launch");
+            return MKOR_OK;
+        case MKOR_STAGE_SM_UPDATE:
+            if (lo.nrowblocks == 0) return MKOR_OK;
+            e = launch_sm_update(fd, rb, lo.nrowblocks, smpart, *prm, s);
+            if (e != hipSuccess) return hip_fail(e, "sm_update launch");
+            return MKOR_OK;
+        case MKOR_STAGE_GEMM_XT:
+            e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
+                               reinterpret_cast<const GemmTile*>(ws + lo.off_g1t), lo.ng1, gpart, s);
+            if (e != hipSuccess) return hip_fail(e, "gemm_xt launch");
+            return MKOR_OK;
+        case MKOR_STAGE_GEMM_DW:
+            e = launch_gemm_dw(reinterpret_cast<const GemmLayer*>(ws + lo.off_g2l),
+                               reinterpret_cast<const GemmTile*>(ws + lo.off_g2t), lo.ng2, dpart, s);
+            if (e != hipSuccess) return hip_fail(e, "gemm_dw launch");
+            return MKOR_OK;
+        case MKOR_STAGE_RESCALE:
+            e = launch_rescale(reinterpret_cast<const RescaleLayer*>(ws + lo.off_rsl),
+                               reinterpret_cast<const RescaleBlock*>(ws + lo.off_rsb), lo.nrsblocks, gpart,
+                               dpart, prm->rescale, s);
+            if (e != hipSuccess) return hip_fail(e, "rescale launch");
+            return MKOR_OK;
+        default:
+            return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
+    }
+}
+
+static int run_range(mkor_plan* p, const mkor_params* prm, int32_t first, int32_t last, hipStream_t s) {
+    if (p->n == 0) return MKOR_OK;
+    for (int32_t st = first; st <= last; ++st) {
+        const int r = run_stage(p, prm, st, s);
+        if (r != MKOR_OK) return r;
+    }
+    return MKOR_OK;
+}
+
+int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    int st = check_params(params);
+    if (st != MKOR_OK) return st;
+    return run_range(plan, params, MKOR_STAGE_SM_MATVEC, MKOR_STAGE_SM_UPDATE,
+                     static_cast<hipStream_t>(stream));
+}
+
+int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    int st = check_params(params);
+    if (st != MKOR_OK) return st;
+    return run_range(plan, params, MKOR_STAGE_GEMM_XT, MKOR_STAGE_RESCALE,
+                     static_cast<hipStream_t>(stream));
+}
+
+int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    int st = check_params(params);
+    if (st != MKOR_OK) return st;
+    return run_range(plan, params, MKOR_STAGE_SM_MATVEC, MKOR_STAGE_RESCALE,
+                     static_cast<hipStream_t>(stream));
+}
+
+int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    int st = check_params(params);
+    if (st != MKOR_OK) return st;
+    if (stage < 0 || stage >= MKOR_NUM_STAGES) return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
+    if (plan->n == 0) return MKOR_OK;
+    return run_stage(plan, params, stage, static_cast<hipStream_t>(stream));
+}
+
+void mkor_plan_destroy(mkor_plan* plan) { delete plan; }
+
+}  // extern "C"

@@ -1,0 +1,68 @@
+"""Device-memory plumbing for a grouped layer list (torch tensors on the GPU).
+
+Allocates the per-layer buffers that the C ABI consumes and moves host arrays
+in and out of them.  No arithmetic of the method happens here.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from .binding import STATS_BYTES, MkorPlan, read_stats
+
+
+def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True):
+    """One dict of device tensors per (d_in, d_out); factors start as I."""
+    gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
+    layers = []
+    for i, (d_in, d_out) in enumerate(shapes):
+        so = True if second_order is None else bool(second_order[i])
+        L = dict(d_in=d_in, d_out=d_out, second_order=so,
+                 G=torch.zeros((d_in, d_out), dtype=gdt, device=device),
+                 dW=torch.zeros((d_in, d_out), dtype=torch.float32, device=device))
+        if so:
+            L["Linv"] = torch.eye(d_in, dtype=torch.float32, device=device)
+            L["Rinv"] = torch.eye(d_out, dtype=torch.float32, device=device)
+            L["a"] = torch.zeros(d_in, dtype=torch.float32, device=device)
+            L["g"] = torch.zeros(d_out, dtype=torch.float32, device=device)
+        if stats:
+            L["stats"] = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=device)
+        layers.append(L)
+    return layers
+
+
+def _put(dst: torch.Tensor, src: np.ndarray):
+    t = torch.from_numpy(np.ascontiguousarray(src))
+    dst.copy_(t.to(dst.dtype) if dst.dtype != t.dtype else t, non_blocking=False)
+
+
+def set_inputs(L, a=None, g=None, G=None):
+    """Copies host arrays into the layer's a, g and G (G given as float32; for
+    a bf16 layer the values must already be bf16-representable)."""
+    if a is not None:
+        _put(L["a"], a)
+    if g is not None:
+        _put(L["g"], g)
+    if G is not None:
+        _put(L["G"], G)
+
+
+def set_factors(L, Linv, Rinv):
+    _put(L["Linv"], np.asarray(Linv, dtype=np.float32))
+    _put(L["Rinv"], np.asarray(Rinv, dtype=np.float32))
+
+
+def get_factors(L):
+    return L["Linv"].cpu().numpy(), L["Rinv"].cpu().numpy()
+
+
+def get_dW(L):
+    return L["dW"].cpu().numpy()
+
+
+def get_stats(L):
+    return read_stats(L["stats"])
+
+
+def make_plan(layers) -> MkorPlan:
+    return MkorPlan(layers)

@@ -1,0 +1,151 @@
+"""Shared helpers of the GPU parity tests: seeded states, error metrics, and a
+free-running driver that steps the HIP path over a whole grouped layer list
+while the float64 oracle follows a sample of its layers."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import oracle as O
+import workloads as W
+from paper_2306_01685_amd import Params, harness as H
+
+TOL_STEP = 1e-4   # relative Frobenius error after one step from the same state
+TOL_FREE = 1e-3   # after up to 50 independently accumulated steps
+NEAR_TIE = 1e-4   # |nu - eps| / eps band in which either stabiliser decision is accepted
+
+
+def rel(a, b) -> float:
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    nb = float(np.linalg.norm(b))
+    if nb == 0.0:
+        return float(np.linalg.norm(a))
+    return float(np.linalg.norm(a - b)) / nb
+
+
+def spd(seed, d, spread=0.25):
+    """Seeded symmetric positive-definite fp32 matrix, bitwise symmetric."""
+    rng = np.random.default_rng(seed)
+    Q = rng.standard_normal((d, max(1, d // 2)))
+    P = np.eye(d) + spread * (Q @ Q.T) / d
+    P = 0.5 * (P + P.T)
+    return P.astype(np.float32)
+
+
+def oparams(p: Params) -> O.Params:
+    return O.Params(gamma=p.gamma, zeta=p.zeta, eps=p.eps, norm_kind=p.norm_kind,
+                    variant=p.variant, rescale=p.rescale, guard_nonfinite=p.guard_nonfinite)
+
+
+def near_tie(nu, eps) -> bool:
+    return math.isfinite(eps) and eps > 0 and abs(nu - eps) / eps < NEAR_TIE
+
+
+def oracle_factor_step(P, x, p: O.Params, gpu_flag):
+    """One oracle factor update, adopting the GPU's stabiliser decision only in
+    the near-tie band."""
+    nu = O.factor_norm(P, p.norm_kind)
+    ov = bool(gpu_flag) if near_tie(nu, p.eps) else None
+    return O.update_factor(P, x, p, ov)
+
+
+class FreeRun:
+    """Steps all layers of a workload on the GPU; the oracle follows `sample`.
+
+    Inputs of sampled layers come from the workload generator; the other
+    layers get seeded values drawn on the GPU (their values never reach a
+    checked output, layers being independent).
+    """
+
+    def __init__(self, w: W.Workload, params: Params, sample, explicit=False, bulk_seed=1234):
+        self.w, self.p, self.op = w, params, oparams(params)
+        self.sample = list(sample)
+        self.explicit = explicit
+        self.layers = H.allocate_layers(w.shapes, w.grad_dtype)
+        self.gen = torch.Generator(device="cuda")
+        self.gen.manual_seed(bulk_seed)
+        self.state = {}
+        for i in range(w.n_layers):
+            if w.init != "identity" or i in self.sample:
+                L0, R0 = W.initial_factors(w, i)
+                if w.init != "identity":
+                    H.set_factors(self.layers[i], L0, R0)
+                if i in self.sample:
+                    self.state[i] = [L0.astype(np.float64), R0.astype(np.float64)]
+        self.plan = H.make_plan(self.layers)
+        self.t = 0
+        self.flags = {i: [] for i in self.sample}
+
+    def _inputs(self, t):
+        host = {}
+        for i, L in enumerate(self.layers):
+            if i in self.sample:
+                a, g = W.rank1_vectors(self.w, i, t, explicit=self.explicit)
+                G = W.gradient(self.w, i, t)
+                H.set_inputs(L, a, g, G)
+                host[i] = (a, g, G)
+            else:
+                d_in, d_out = L["d_in"], L["d_out"]
+                s_a = math.sqrt((2.0 if self.w.act_dist == "student_t4" else 1.0) / self.w.rows)
+                L["a"].normal_(0.0, s_a, generator=self.gen)
+                L["g"].normal_(0.0, self.w.grad_row_std / math.sqrt(self.w.rows), generator=self.gen)
+                if L["G"].dtype == torch.bfloat16:
+                    tmp = torch.empty((d_in, d_out), dtype=torch.float32, device="cuda")
+                    tmp.normal_(0.0, self.w.G_std, generator=self.gen)
+                    L["G"].copy_(tmp)
+                    del tmp
+                else:
+                    L["G"].normal_(0.0, self.w.G_std, generator=self.gen)
+        return host
+
+    def step(self, precond_oracle=False):
+        """One step on both sides; returns the oracle's dW per sampled layer
+        when precond_oracle is set (else None)."""
+        host = self._inputs(self.t)
+        self.plan.step(self.p)
+        torch.cuda.synchronize()
+        out = {}
+        for i in self.sample:
+            st = H.get_stats(self.layers[i])
+            a, g, G = host[i]
+            Lp, Rp = self.state[i]
+            Ln, sL = oracle_factor_step(Lp, a, self.op, st["stab_L"])
+            Rn, sR = oracle_factor_step(Rp, g, self.op, st["stab_R"])
+            self.state[i] = [Ln, Rn]
+            self.flags[i].append(((sL.stab, st["stab_L"], sL.nu), (sR.stab, st["stab_R"], sR.nu)))
+            if precond_oracle:
+                _, _, dW, ost = O.layer_step(Ln, Rn, a, g, G, self.op, update=False)
+                out[i] = (dW, ost)
+        self.t += 1
+        return out if precond_oracle else None
+
+    def check_factors(self, tol):
+        worst = 0.0
+        for i in self.sample:
+            Lg, Rg = H.get_factors(self.layers[i])
+            eL, eR = rel(Lg, self.state[i][0]), rel(Rg, self.state[i][1])
+            worst = max(worst, eL, eR)
+            assert eL <= tol and eR <= tol, (self.w.name, i, self.t, eL, eR)
+        return worst
+
+    def check_dW(self, oracle_out, tol):
+        worst = 0.0
+        for i, (dW, ost) in oracle_out.items():
+            e = rel(H.get_dW(self.layers[i]), dW)
+            worst = max(worst, e)
+            assert e <= tol, (self.w.name, i, self.t, e)
+        return worst
+
+    def check_flags(self):
+        """Stabiliser decisions agree everywhere outside the near-tie band."""
+        fired = 0
+        for i, seq in self.flags.items():
+            for t, pair in enumerate(seq):
+                for (o, gflag, nu) in pair:
+                    fired += int(o)
+                    if not near_tie(nu, self.op.eps):
+                        assert bool(o) == bool(gflag), (self.w.name, i, t, o, gflag, nu)
+        return fired

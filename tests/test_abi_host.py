@@ -1,0 +1,203 @@
+"""C ABI host-side behaviour, without a GPU.
+
+Every validation path of include/mkor.h returns its status before the first
+HIP call, so these tests pass fake (never dereferenced) device addresses.
+"""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2306_01685_amd as M
+from paper_2306_01685_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(M.LIB_PATH):
+        pytest.fail("libmkor.so is not built (run python -m paper_2306_01685_amd.build)")
+    return M.load_library()
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "mkor.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mkor_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(M.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.mkor_abi_version() == 1
+
+
+def test_status_strings(lib):
+    for code, name in [(0, "MKOR_OK"), (-1, "MKOR_INVALID_ARG"), (-2, "MKOR_WORKSPACE_TOO_SMALL"),
+                       (-3, "MKOR_UNSUPPORTED"), (-4, "MKOR_HIP_ERROR")]:
+        assert M.status_string(code) == name
+    assert M.status_string(7) == "MKOR_UNKNOWN_STATUS"
+
+
+def test_struct_sizes():
+    assert ctypes.sizeof(B.mkor_params) == 28
+    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8
+    assert M.STATS_BYTES == 48
+
+
+@pytest.mark.parametrize("field,value", [
+    ("gamma", 0.0), ("gamma", 1.0), ("gamma", math.nan), ("gamma", -0.5),
+    ("zeta", 0.0), ("zeta", 1.5), ("zeta", math.nan),
+    ("eps", math.nan), ("eps", -1.0),
+    ("norm_kind", 2), ("variant", 7), ("rescale", 2), ("guard_nonfinite", 3),
+])
+def test_params_rejected(lib, field, value):
+    p = M.Params()
+    setattr(p, field, value)
+    c = p.to_c()
+    if field in ("rescale", "guard_nonfinite"):
+        setattr(c, field, value)
+    assert M.params_check(c) == M.MKOR_INVALID_ARG
+    assert M.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(eps=math.inf), dict(eps=0.0), dict(zeta=1.0),
+                                dict(variant=1, norm_kind=1, rescale=False, guard_nonfinite=False)])
+def test_params_accepted(lib, kw):
+    assert M.params_check(M.Params(**kw)) == M.MKOR_OK
+
+
+def test_params_null(lib):
+    assert lib.mkor_params_check(None) == M.MKOR_INVALID_ARG
+
+
+# ------------------------------------------------------------------ fake address space
+
+class Fake:
+    """Hands out disjoint, 256-byte aligned fake device addresses."""
+
+    def __init__(self):
+        self.next = 0x7F0000000000
+
+    def alloc(self, nbytes):
+        p = self.next
+        self.next += (nbytes + 4095) // 4096 * 4096 + 4096
+        return p
+
+
+def layer(fk, d_in, d_out, so=1, dt=0, stats=False):
+    esz = 2 if dt == 1 else 4
+    return dict(d_in=d_in, d_out=d_out, second_order=so, grad_dtype=dt,
+                Linv=fk.alloc(d_in * d_in * 4), Rinv=fk.alloc(d_out * d_out * 4),
+                a=fk.alloc(d_in * 4), g=fk.alloc(d_out * 4), G=fk.alloc(d_in * d_out * esz),
+                dW=fk.alloc(d_in * d_out * 4), stats=fk.alloc(48) if stats else None)
+
+
+def ws_status(descs):
+    arr = B.make_layer_array(descs)
+    out = ctypes.c_size_t(0)
+    st = M.load_library().mkor_workspace_size(arr, len(descs), ctypes.byref(out))
+    return st, out.value
+
+
+def test_workspace_size_covers_intermediate(lib):
+    fk = Fake()
+    descs = [layer(fk, 1024, 4096, dt=1), layer(fk, 4096, 1024), layer(fk, 37, 100, so=0)]
+    st, size = ws_status(descs)
+    assert st == M.MKOR_OK
+    # X = Linv G is kept per second-order layer (fp32), plus tables and vectors
+    assert size >= 4 * (1024 * 4096 * 2)
+    assert size < 4 * (1024 * 4096 * 2) + (8 << 20)
+    assert size % 256 == 0
+
+
+def test_empty_list(lib):
+    st, size = ws_status([])
+    assert st == M.MKOR_OK and size == 0
+    plan = ctypes.c_void_p(None)
+    assert lib.mkor_plan_create(None, 0, None, 0, ctypes.byref(plan)) == M.MKOR_OK
+    p = M.Params().to_c()
+    for fn in (lib.mkor_update_factors, lib.mkor_precondition, lib.mkor_step):
+        assert fn(plan, ctypes.byref(p), None) == M.MKOR_OK
+    lib.mkor_plan_destroy(plan)
+    lib.mkor_plan_destroy(None)
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda L: L.update(d_in=0), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(d_out=M.MAX_DIM + 1), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(second_order=2), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(grad_dtype=5), M.MKOR_UNSUPPORTED),
+    (lambda L: L.update(G=None), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(dW=None), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(Linv=None), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(g=None), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(a=L["a"] + 4), M.MKOR_INVALID_ARG),        # misaligned
+    (lambda L: L.update(dW=L["G"]), M.MKOR_INVALID_ARG),           # output aliases input
+    (lambda L: L.update(Rinv=L["Linv"] + 256), M.MKOR_INVALID_ARG),  # factors overlap
+    (lambda L: L.update(stats=L["dW"] + 64), M.MKOR_INVALID_ARG),  # stats inside dW
+])
+def test_layer_rejected(lib, mutate, status):
+    fk = Fake()
+    descs = [layer(fk, 64, 96), layer(fk, 40, 40)]
+    mutate(descs[0])
+    st, _ = ws_status(descs)
+    assert st == status, M.last_error()
+    assert M.last_error()
+
+
+def test_cross_layer_aliasing(lib):
+    fk = Fake()
+    a, b = layer(fk, 64, 64), layer(fk, 64, 64)
+    b["dW"] = a["dW"]                      # two outputs on one buffer
+    assert ws_status([a, b])[0] == M.MKOR_INVALID_ARG
+    a, b = layer(fk, 64, 64), layer(fk, 64, 64)
+    b["Linv"] = a["G"]                     # factor written over another layer's input
+    assert ws_status([a, b])[0] == M.MKOR_INVALID_ARG
+    a, b = layer(fk, 64, 64), layer(fk, 64, 64)
+    b["a"] = a["a"]                        # read-only inputs may be shared
+    b["G"] = a["G"]
+    assert ws_status([a, b])[0] == M.MKOR_OK
+
+
+def test_first_order_layer_needs_no_factors(lib):
+    fk = Fake()
+    L = layer(fk, 50, 70, so=0)
+    L.update(Linv=None, Rinv=None, a=None, g=None)
+    assert ws_status([L])[0] == M.MKOR_OK
+
+
+def test_plan_create_workspace_errors(lib):
+    fk = Fake()
+    descs = [layer(fk, 64, 96)]
+    st, size = ws_status(descs)
+    arr = B.make_layer_array(descs)
+    plan = ctypes.c_void_p(None)
+    ws = fk.alloc(size + 4096)
+    assert lib.mkor_plan_create(arr, 1, ws, size - 256, ctypes.byref(plan)) == M.MKOR_WORKSPACE_TOO_SMALL
+    assert lib.mkor_plan_create(arr, 1, None, size, ctypes.byref(plan)) == M.MKOR_INVALID_ARG
+    assert lib.mkor_plan_create(arr, 1, ws + 16, size, ctypes.byref(plan)) == M.MKOR_INVALID_ARG
+    assert lib.mkor_plan_create(arr, 1, ws, size, None) == M.MKOR_INVALID_ARG
+    # workspace overlapping a layer buffer
+    assert lib.mkor_plan_create(arr, 1, descs[0]["dW"] // 256 * 256, size,
+                                ctypes.byref(plan)) == M.MKOR_INVALID_ARG
+    assert lib.mkor_plan_create(arr, -1, ws, size, ctypes.byref(plan)) == M.MKOR_INVALID_ARG
+    assert not plan.value
+
+
+def test_entry_points_reject_before_device(lib):
+    p = M.Params().to_c()
+    for fn in (lib.mkor_update_factors, lib.mkor_precondition, lib.mkor_step):
+        assert fn(None, ctypes.byref(p), None) == M.MKOR_INVALID_ARG
+    plan = ctypes.c_void_p(None)
+    assert lib.mkor_plan_create(None, 0, None, 0, ctypes.byref(plan)) == M.MKOR_OK
+    bad = M.Params(gamma=2.0).to_c()
+    for fn in (lib.mkor_update_factors, lib.mkor_precondition, lib.mkor_step):
+        assert fn(plan, ctypes.byref(bad), None) == M.MKOR_INVALID_ARG
+        assert fn(plan, None, None) == M.MKOR_INVALID_ARG
+    lib.mkor_plan_destroy(plan)
