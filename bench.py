@@ -41,7 +41,34 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stage-timing", action="store_true")
+    ap.add_argument("--mode", choices=["step", "copy"], default="step",
+                    help="copy: time a plain device-to-device copy of --copy-mib MiB (the reference "
+                         "kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures)")
+    ap.add_argument("--copy-mib", type=int, default=1024)
     return ap.parse_args()
+
+
+def copy_reference(args):
+    """A plain copy kernel of known size: reads and writes copy_mib MiB once."""
+    import torch
+    n = args.copy_mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nbytes = 2 * n * 4
+    print(json.dumps({"mode": "copy", "bytes_read": n * 4, "bytes_written": n * 4, "ms": ms,
+                      "gbs": nbytes / (ms / 1e3) / 1e9, "frac_hbm": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}),
+          flush=True)
 
 
 def workload_desc(w):
@@ -113,6 +140,10 @@ def main():
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               "(the hot path runs on a single MI355X)", file=sys.stderr)
         sys.exit(2)
+
+    if args.mode == "copy":
+        copy_reference(args)
+        return
 
     import torch
 
