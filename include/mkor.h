@@ -38,6 +38,21 @@
  *                      (Eq. 6/7 exactly as printed, which is not the inverse
  *                      of Eq. 4/5; kept as an option)
  *
+ * Factor state.  The library carries each inverse factor as its caller
+ * buffer S plus one pending rank-1 term kept in the workspace:
+ *     current factor  P = c1 S + c2 I + sgn w w^T.
+ * A step streams every factor once: it first writes the previous step's
+ * pending term into S, computes the norm and the matrix-vector product of the
+ * stabiliser and SM update on those values, and leaves this step's update as
+ * the new pending term; the preconditioning applies that term while it loads
+ * the factor, so it multiplies with the updated factor.  Results are the same
+ * values a write-back after every update would give (element for element the
+ * same roundings).  Consequently, after mkor_step or mkor_update_factors the
+ * buffers Linv and Rinv hold the factors as of the previous update;
+ * mkor_sync_factors writes the current factors into them.  Call it before
+ * reading, saving or modifying Linv / Rinv, and before mkor_plan_destroy if
+ * the factors are to be kept.  A new plan starts with no pending term.
+ *
  * Memory and ownership.
  *   - Every buffer named in mkor_layer, and the workspace, is device memory
  *     owned by the caller.  The library never allocates or frees device
@@ -47,7 +62,8 @@
  *     256-byte aligned.
  *   - Pointers are captured by mkor_plan_create.  Before each step the
  *     caller refills a, g and G in place; Linv and Rinv are updated in place
- *     and must hold symmetric matrices (initially I in the paper).
+ *     (see "Factor state") and must hold symmetric matrices (initially I in
+ *     the paper).
  *   - Writable buffers (Linv, Rinv, dW, stats) must not overlap any other
  *     buffer of any layer or the workspace.  Read-only inputs may be shared.
  *
@@ -70,7 +86,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 1
+#define MKOR_ABI_VERSION 2
 
 /* status codes */
 #define MKOR_OK                   0
@@ -90,8 +106,8 @@ extern "C" {
 #define MKOR_DTYPE_BF16    1
 
 /* kernels of one step, in launch order (mkor_run_stage) */
-#define MKOR_STAGE_SM_MATVEC  0   /* u_raw = P x, norm and s partials, all factors */
-#define MKOR_STAGE_SM_UPDATE  1   /* stabiliser decision + in-place rank-1 update */
+#define MKOR_STAGE_SM_PASS    0   /* write pending term into S; u_raw = P x, norm and s partials */
+#define MKOR_STAGE_SM_FINALIZE 1  /* stabiliser decision, new pending rank-1 term */
 #define MKOR_STAGE_GEMM_XT    2   /* X^T = (Linv G)^T, ||G||^2 partials */
 #define MKOR_STAGE_GEMM_DW    3   /* dW_hat = X Rinv, ||dW_hat||^2 partials */
 #define MKOR_STAGE_RESCALE    4   /* rescale / first-order pass-through */
@@ -165,11 +181,14 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace,
                      size_t ws_bytes, mkor_plan** out);
 
 /* Stabiliser + SM update of Linv and Rinv of every second-order layer
- * (Algorithm 1, stabilisation and SM lines), in one grouped pass. */
+ * (Algorithm 1, stabilisation and SM lines), in one grouped streaming pass
+ * plus one small per-factor launch.  The update is left as the pending term
+ * (see "Factor state"). */
 int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream);
 
-/* Preconditioning with the current factors, rescale, and the first-order
- * pass-through (Algorithm 1, precondition, rescale and else lines). */
+/* Preconditioning with the current factors (buffer + pending term), rescale,
+ * and the first-order pass-through (Algorithm 1, precondition, rescale and
+ * else lines). */
 int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream);
 
 /* mkor_update_factors followed by mkor_precondition: one full step. */
@@ -180,6 +199,13 @@ int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream);
  * exactly mkor_step; a stage launched out of that order reads whatever the
  * workspace holds from earlier launches. */
 int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, void* stream);
+
+/* Writes the current value of every inverse factor (buffer + pending term)
+ * into its buffer Linv / Rinv and clears the pending terms: one grouped
+ * read + write of the factors that have a pending term.  Afterwards the
+ * buffers hold exactly the factors the next step starts from.  Asynchronous
+ * on `stream`; INVALID_ARG if plan is NULL. */
+int mkor_sync_factors(mkor_plan* plan, void* stream);
 
 /* Frees the host-side plan (NULL is allowed).  The workspace stays the
  * caller's. */

@@ -33,7 +33,7 @@ NORM_MAXABS = 1
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MAX_DIM = 32768
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 
 class mkor_params(ctypes.Structure):
@@ -64,11 +64,12 @@ STATS_FIELDS = [f for f, _ in mkor_layer_stats._fields_]
 
 EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_params_check",
             "mkor_workspace_size", "mkor_plan_create", "mkor_update_factors",
-            "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_plan_destroy"]
+            "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_sync_factors",
+            "mkor_plan_destroy"]
 
-STAGE_SM_MATVEC, STAGE_SM_UPDATE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(5)
+STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(5)
 NUM_STAGES = 5
-STAGE_NAMES = ["sm_matvec", "sm_update", "gemm_xt", "gemm_dw", "rescale"]
+STAGE_NAMES = ["sm_pass", "sm_finalize", "gemm_xt", "gemm_dw", "rescale"]
 
 
 class MkorError(RuntimeError):
@@ -108,6 +109,8 @@ def load_library(path: str = LIB_PATH):
         fn.argtypes = [P, ctypes.POINTER(mkor_params), P]
     lib.mkor_run_stage.restype = ctypes.c_int
     lib.mkor_run_stage.argtypes = [P, ctypes.POINTER(mkor_params), I32, P]
+    lib.mkor_sync_factors.restype = ctypes.c_int
+    lib.mkor_sync_factors.argtypes = [P, P]
     lib.mkor_plan_destroy.restype = None
     lib.mkor_plan_destroy.argtypes = [P]
     if lib.mkor_abi_version() != ABI_VERSION:
@@ -186,6 +189,10 @@ class MkorPlan:
     d_in x d_out), optional second_order (default True) and optional stats
     (a uint8 device tensor of STATS_BYTES bytes).  The plan owns its workspace
     (a torch uint8 tensor) and keeps references to every tensor it was given.
+
+    After step() / update_factors() the Linv / Rinv tensors lag the current
+    factors by one pending rank-1 term held in the workspace; sync_factors()
+    writes the current factors into them (include/mkor.h, "Factor state").
     """
 
     def __init__(self, layers, device=None):
@@ -244,6 +251,9 @@ class MkorPlan:
         p = params.to_c() if isinstance(params, Params) else params
         _check(self._lib.mkor_run_stage(self._plan, ctypes.byref(p), int(stage), _stream_handle(stream)),
                "mkor_run_stage")
+
+    def sync_factors(self, stream=None):
+        _check(self._lib.mkor_sync_factors(self._plan, _stream_handle(stream)), "mkor_sync_factors")
 
     def close(self):
         if getattr(self, "_plan", None) is not None and self._plan.value:

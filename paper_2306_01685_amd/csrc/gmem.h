@@ -1,0 +1,51 @@
+// Device-side global-memory accessors.
+//
+// Buffer pointers reach the kernels inside descriptor tables, so the compiler
+// cannot tell that they point to global memory and would emit flat
+// instructions.  Flat loads count against the LDS wait counter as well as the
+// vector-memory one, so a wait for an LDS read would also wait for every
+// outstanding prefetch.  These helpers cast to the global address space (and
+// use native vector types, which the cast needs to stay a single 16-byte
+// access), so every access below is a global_load / global_store.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace mkor {
+
+#define MKOR_GLOBAL __attribute__((address_space(1)))
+
+typedef float        mk_f4 __attribute__((ext_vector_type(4)));
+typedef unsigned int mk_u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int mk_u2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float gld(const float* p) { return *(const MKOR_GLOBAL float*)p; }
+
+__device__ __forceinline__ unsigned short gld_u16(const unsigned short* p) {
+    return *(const MKOR_GLOBAL unsigned short*)p;
+}
+
+__device__ __forceinline__ float4 gld4(const float* p) {
+    const mk_f4 v = *(const MKOR_GLOBAL mk_f4*)p;
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint4 gld_u4(const void* p) {
+    const mk_u4 v = *(const MKOR_GLOBAL mk_u4*)p;
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint2 gld_u2(const void* p) {
+    const mk_u2 v = *(const MKOR_GLOBAL mk_u2*)p;
+    return make_uint2(v.x, v.y);
+}
+
+__device__ __forceinline__ void gst(float* p, float v) { *(MKOR_GLOBAL float*)p = v; }
+
+__device__ __forceinline__ void gst4(float* p, const float4& v) {
+    mk_f4 w;
+    w.x = v.x; w.y = v.y; w.z = v.z; w.w = v.w;
+    *(MKOR_GLOBAL mk_f4*)p = w;
+}
+
+}  // namespace mkor

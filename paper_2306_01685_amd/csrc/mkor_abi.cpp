@@ -103,17 +103,58 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
 
 // ------------------------------------------------------------------ layout
 struct Layout {
-    size_t off_factors = 0, off_rowblocks = 0, off_u = 0, off_smpart = 0;
+    size_t off_factors = 0, off_rowblocks = 0, off_pend = 0, off_smpart = 0;
     size_t off_g1l = 0, off_g1t = 0, off_g2l = 0, off_g2t = 0, off_gpart = 0, off_dpart = 0;
     size_t off_rsl = 0, off_rsb = 0, off_x = 0;
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
     int32_t nsecond = 0;
-    std::vector<size_t> u_off, x_off;   // per factor / per layer offsets (bytes)
+    std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
 };
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
+
+// Tile table of one GEMM stage (1: X^T = (Linv G)^T, K = d_in; 2: dW_hat =
+// X Rinv, K = d_out).  Each layer's tile grid is cut into super-tiles of up to
+// GEMM_SUPER_M x GEMM_SUPER_N tiles; super-tiles are taken longest K first and
+// each goes whole to the XCD with the least work so far, so the tiles an XCD
+// runs together share A and B panels in its L2 and the long tiles do not form
+// the tail.  Workgroup b runs on XCD b % GEMM_XCDS, so position
+// q * GEMM_XCDS + x of the table holds the q-th tile of XCD x; shorter queues
+// are padded with tiles of layer -1.
+std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage) {
+    struct Super { int32_t layer, tm0, tn0, nm, nn, K; };
+    std::vector<Super> sup;
+    for (int32_t i = 0; i < n; ++i) {
+        const mkor_layer& L = layers[i];
+        if (!L.second_order) continue;
+        const int32_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
+        const int32_t K = stage == 1 ? L.d_in : L.d_out;
+        for (int32_t a = 0; a < tm; a += GEMM_SUPER_M)
+            for (int32_t b = 0; b < tn; b += GEMM_SUPER_N)
+                sup.push_back(Super{i, a, b, std::min(GEMM_SUPER_M, tm - a), std::min(GEMM_SUPER_N, tn - b), K});
+    }
+    std::stable_sort(sup.begin(), sup.end(), [](const Super& x, const Super& y) {
+        if (x.K != y.K) return x.K > y.K;
+        return x.nm * x.nn > y.nm * y.nn;
+    });
+    std::vector<std::vector<GemmTile>> queue(GEMM_XCDS);
+    std::vector<int64_t> work(GEMM_XCDS, 0);
+    for (const Super& S : sup) {
+        const int x = (int)(std::min_element(work.begin(), work.end()) - work.begin());
+        for (int32_t a = 0; a < S.nm; ++a)
+            for (int32_t b = 0; b < S.nn; ++b)
+                queue[x].push_back(GemmTile{S.layer, S.tm0 + a, S.tn0 + b, 0});
+        work[x] += (int64_t)S.nm * S.nn * S.K;
+    }
+    size_t len = 0;
+    for (const auto& q : queue) len = std::max(len, q.size());
+    std::vector<GemmTile> table(len * GEMM_XCDS, GemmTile{-1, 0, 0, 0});
+    for (int x = 0; x < GEMM_XCDS; ++x)
+        for (size_t q = 0; q < queue[x].size(); ++q) table[q * GEMM_XCDS + x] = queue[x][q];
+    return table;
+}
 
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0;
@@ -132,7 +173,11 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
     Lo.nfactors = 2 * Lo.nsecond;
     Lo.nrowblocks = (int32_t)rowblocks;
-    Lo.ng1 = Lo.ng2 = (int32_t)g1;
+    const size_t t1 = schedule_tiles(layers, n, 1).size(), t2 = schedule_tiles(layers, n, 2).size();
+    if (t1 > INT32_MAX || t2 > INT32_MAX)
+        return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
+    Lo.ng1 = (int32_t)t1;
+    Lo.ng2 = (int32_t)t2;
     Lo.ngpart = (int32_t)gpart;
     Lo.ndpart = (int32_t)g1;
     Lo.nrsblocks = (int32_t)rsb;
@@ -147,16 +192,21 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_g2t = take(sizeof(GemmTile) * Lo.ng2);
     Lo.off_rsl = take(sizeof(RescaleLayer) * n);
     Lo.off_rsb = take(sizeof(RescaleBlock) * Lo.nrsblocks);
+    // pending terms start out empty (has = 0): the upload initialises them
+    Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
     Lo.table_bytes = align_up(o, 256);
     Lo.off_smpart = take(sizeof(float4) * Lo.nrowblocks);
     Lo.off_gpart = take(sizeof(float) * Lo.ngpart);
     Lo.off_dpart = take(sizeof(float) * Lo.ndpart);
     Lo.u_off.clear();
+    Lo.w_off.clear();
     Lo.x_off.assign(n, 0);
     for (int32_t i = 0; i < n; ++i) {
         if (!layers[i].second_order) continue;
-        Lo.u_off.push_back(take(sizeof(float) * layers[i].d_in));
-        Lo.u_off.push_back(take(sizeof(float) * layers[i].d_out));
+        for (const int32_t d : {layers[i].d_in, layers[i].d_out}) {
+            Lo.u_off.push_back(take(sizeof(float) * d));
+            Lo.w_off.push_back(take(sizeof(float) * d));
+        }
     }
     for (int32_t i = 0; i < n; ++i) {
         if (!layers[i].second_order) continue;
@@ -259,11 +309,10 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     GemmTile* g2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_g2t);
     RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
     RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
+    Pending* pend_h = reinterpret_cast<Pending*>(host.data() + lo.off_pend);
+    Pending* pend_d = reinterpret_cast<Pending*>(base + lo.off_pend);
 
     int32_t fi = 0, bi = 0, gp = 0, dp = 0, rbi = 0;
-    std::vector<GemmTile> t1, t2;
-    t1.reserve(lo.ng1);
-    t2.reserve(lo.ng2);
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         mkor_layer_stats* stats = static_cast<mkor_layer_stats*>(L.stats);
@@ -282,6 +331,9 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             f.P = side == 0 ? L.Linv : L.Rinv;
             f.x = side == 0 ? L.a : L.g;
             f.u = reinterpret_cast<float*>(base + lo.u_off[fi]);
+            f.w = reinterpret_cast<float*>(base + lo.w_off[fi]);
+            f.pend = pend_d + fi;
+            pend_h[fi] = Pending{1.f, 0.f, 0.f, 0};
             f.stats = stats;
             f.d = side == 0 ? L.d_in : L.d_out;
             f.blk0 = bi;
@@ -293,14 +345,18 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         float* X = reinterpret_cast<float*>(base + lo.x_off[i]);
         const int32_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
         const bool bf16 = L.grad_dtype == MKOR_DTYPE_BF16;
+        const FactorDesc& fL = fd[fi - 2];
+        const FactorDesc& fR = fd[fi - 1];
         GemmLayer& A = g1l[i];
         A.At = L.Linv; A.B = L.G; A.C = X;
+        A.pend = fL.pend; A.w = fL.w;
         A.M = L.d_in; A.N = L.d_out; A.K = L.d_in;
         A.b_bf16 = bf16;
-        A.vec = (L.d_in % 4 == 0) && (L.d_out % (bf16 ? 8 : 4) == 0);
+        A.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
         A.part0 = gp; A.ntn = tn;
         GemmLayer& B = g2l[i];
         B.At = X; B.B = L.Rinv; B.C = L.dW;
+        B.pend = fR.pend; B.w = fR.w;
         B.M = L.d_in; B.N = L.d_out; B.K = L.d_out;
         B.b_bf16 = 0;
         B.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
@@ -309,19 +365,8 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         R.dpart0 = dp; R.ndpart = tm * tn;
         gp += tn;
         dp += tm * tn;
-        for (int32_t a = 0; a < tm; ++a)
-            for (int32_t b = 0; b < tn; ++b) {
-                t1.push_back(GemmTile{i, a, b, 0});
-                t2.push_back(GemmTile{i, a, b, 0});
-            }
     }
-    // longest K first, so the long tiles do not form the tail of the launch
-    std::stable_sort(t1.begin(), t1.end(), [&](const GemmTile& x, const GemmTile& y) {
-        return layers[x.layer].d_in > layers[y.layer].d_in;
-    });
-    std::stable_sort(t2.begin(), t2.end(), [&](const GemmTile& x, const GemmTile& y) {
-        return layers[x.layer].d_out > layers[y.layer].d_out;
-    });
+    const std::vector<GemmTile> t1 = schedule_tiles(layers, n, 1), t2 = schedule_tiles(layers, n, 2);
     std::copy(t1.begin(), t1.end(), g1t);
     std::copy(t2.begin(), t2.end(), g2t);
 
@@ -351,15 +396,15 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
     float* dpart = reinterpret_cast<float*>(ws + lo.off_dpart);
     hipError_t e = hipSuccess;
     switch (stage) {
-        case MKOR_STAGE_SM_MATVEC:
+        case MKOR_STAGE_SM_PASS:
             if (lo.nrowblocks == 0) return MKOR_OK;
-            e = launch_sm_matvec(fd, rb, lo.nrowblocks, smpart, prm->norm_kind, s);
-            if (e != hipSuccess) return hip_fail(e, "sm_matvec launch");
+            e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, prm->norm_kind, 1, s);
+            if (e != hipSuccess) return hip_fail(e, "sm_pass launch");
             return MKOR_OK;
-        case MKOR_STAGE_SM_UPDATE:
-            if (lo.nrowblocks == 0) return MKOR_OK;
-            e = launch_sm_update(fd, rb, lo.nrowblocks, smpart, *prm, s);
-            if (e != hipSuccess) return hip_fail(e, "sm_update launch");
+        case MKOR_STAGE_SM_FINALIZE:
+            if (lo.nfactors == 0) return MKOR_OK;
+            e = launch_sm_finalize(fd, lo.nfactors, smpart, *prm, s);
+            if (e != hipSuccess) return hip_fail(e, "sm_finalize launch");
             return MKOR_OK;
         case MKOR_STAGE_GEMM_XT:
             e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
@@ -396,7 +441,7 @@ int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_params(params);
     if (st != MKOR_OK) return st;
-    return run_range(plan, params, MKOR_STAGE_SM_MATVEC, MKOR_STAGE_SM_UPDATE,
+    return run_range(plan, params, MKOR_STAGE_SM_PASS, MKOR_STAGE_SM_FINALIZE,
                      static_cast<hipStream_t>(stream));
 }
 
@@ -414,7 +459,7 @@ int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_params(params);
     if (st != MKOR_OK) return st;
-    return run_range(plan, params, MKOR_STAGE_SM_MATVEC, MKOR_STAGE_RESCALE,
+    return run_range(plan, params, MKOR_STAGE_SM_PASS, MKOR_STAGE_RESCALE,
                      static_cast<hipStream_t>(stream));
 }
 
@@ -426,6 +471,22 @@ int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, vo
     if (stage < 0 || stage >= MKOR_NUM_STAGES) return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
     if (plan->n == 0) return MKOR_OK;
     return run_stage(plan, params, stage, static_cast<hipStream_t>(stream));
+}
+
+int mkor_sync_factors(mkor_plan* plan, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    const Layout& lo = plan->lo;
+    if (plan->n == 0 || lo.nfactors == 0) return MKOR_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(plan->ws + lo.off_factors);
+    const RowBlock* rb = reinterpret_cast<const RowBlock*>(plan->ws + lo.off_rowblocks);
+    float4* smpart = reinterpret_cast<float4*>(plan->ws + lo.off_smpart);
+    hipError_t e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, MKOR_NORM_INF, 0, s);
+    if (e != hipSuccess) return hip_fail(e, "sm_pass launch");
+    e = launch_sm_reset(fd, lo.nfactors, s);
+    if (e != hipSuccess) return hip_fail(e, "sm_reset launch");
+    return MKOR_OK;
 }
 
 void mkor_plan_destroy(mkor_plan* plan) { delete plan; }

@@ -13,11 +13,28 @@
 namespace mkor {
 
 // ---------------------------------------------------------------- SM update
+// The current value of an inverse factor is its caller buffer S with one
+// pending rank-1 term applied:
+//
+//   P = c1 * S + c2 * I + sgn * w w^T      (has = 1)
+//   P = S                                   (has = 0)
+//
+// Element (i, j) is evaluated as fadd(fma(c1, S_ij, sgn * fmul(w_i, w_j)), c2 * [i == j])
+// with every rounding pinned, by every kernel that reads a factor, so the
+// streaming pass that later writes P into S and the GEMM loads that apply it
+// on the fly see bit-identical values.
+struct Pending {
+    float   c1, c2, sgn;
+    int32_t has;
+};
+
 // One inverse factor P (d x d) and its driving vector x.
 struct FactorDesc {
-    float*            P;
+    float*            P;       // caller buffer S
     const float*      x;
-    float*            u;       // workspace, d floats: u_raw = P x (before blending)
+    float*            u;       // workspace, d floats: u_raw = P x (current P, before blending)
+    float*            w;       // workspace, d floats: w of the pending term
+    Pending*          pend;    // workspace
     mkor_layer_stats* stats;   // may be null
     int32_t           d;
     int32_t           blk0;    // first row block of this factor in the row-block table
@@ -25,7 +42,7 @@ struct FactorDesc {
     int32_t           side;    // 0 = Linv (driven by a), 1 = Rinv (driven by g)
 };
 
-// Rows handled by one workgroup of the SM kernels (4 waves x 4 rows).
+// Rows handled by one workgroup of the SM pass (4 waves x 4 rows).
 constexpr int SM_THREADS = 256;
 constexpr int SM_ROWS_PER_WAVE = 4;
 constexpr int SM_ROWS = (SM_THREADS / 64) * SM_ROWS_PER_WAVE;
@@ -35,40 +52,68 @@ struct RowBlock {
     int32_t row0;
 };
 
-// Scalars of one factor's update, decided on the device from the K1 partials.
-struct SmScalars {
-    float c1, c2, sgn, sqc;   // P <- c1 P + c2 I + sgn * w w^T,  w = sqc * u
-    float zp, zq;             // u = zp * u_raw + zq * x
-    int   stab, skip;
-    float nu, s;
-};
-
 // ---------------------------------------------------------------- GEMMs
 // C = At^T * B for one layer: At is K x M (row-major, M contiguous), B is
 // K x N (row-major, N contiguous), C is M x N, stored row-major (ldc = N) or
 // transposed (N x M, ldc = M).
 struct GemmLayer {
-    const float* At;
-    const void*  B;
-    float*       C;
-    int32_t      M, N, K;
-    int32_t      b_bf16;      // element type of B
-    int32_t      vec;         // rows of At, B and C allow 16-byte vector access
-    int32_t      part0;       // first partial-sum slot of this layer
-    int32_t      ntn;         // number of N tiles
-    int32_t      _pad;
+    const float*   At;
+    const void*    B;
+    float*         C;
+    const Pending* pend;      // pending term of the factor operand (At in stage 1, B in stage 2)
+    const float*   w;         // its w vector
+    int32_t        M, N, K;
+    int32_t        b_bf16;    // element type of B
+    int32_t        vec;       // rows of At, B and C allow 16-byte vector access
+    int32_t        part0;     // first partial-sum slot of this layer
+    int32_t        ntn;       // number of N tiles
+    int32_t        _pad;
 };
 
 struct GemmTile {
-    int32_t layer;
+    int32_t layer;            // -1: padding, the workgroup exits
     int32_t tm, tn;
     int32_t _pad;
 };
 
-constexpr int GEMM_BM = 128;
-constexpr int GEMM_BN = 128;
-constexpr int GEMM_BK = 16;
-constexpr int GEMM_THREADS = 256;
+// Tile shape of the preconditioning GEMMs: a workgroup of GEMM_WM x GEMM_WN
+// waves computes a GEMM_BM x GEMM_BN tile, K in GEMM_BK-deep slabs.
+#ifndef MKOR_GEMM_BM
+#define MKOR_GEMM_BM 128
+#endif
+#ifndef MKOR_GEMM_BN
+#define MKOR_GEMM_BN 128
+#endif
+#ifndef MKOR_GEMM_BK
+#define MKOR_GEMM_BK 16
+#endif
+#ifndef MKOR_GEMM_WM
+#define MKOR_GEMM_WM 2
+#endif
+#ifndef MKOR_GEMM_WN
+#define MKOR_GEMM_WN 2
+#endif
+#ifndef MKOR_GEMM_MIN_BLOCKS
+#define MKOR_GEMM_MIN_BLOCKS 2
+#endif
+constexpr int GEMM_BM = MKOR_GEMM_BM;
+constexpr int GEMM_BN = MKOR_GEMM_BN;
+constexpr int GEMM_BK = MKOR_GEMM_BK;
+constexpr int GEMM_WM = MKOR_GEMM_WM;
+constexpr int GEMM_WN = MKOR_GEMM_WN;
+constexpr int GEMM_MIN_BLOCKS = MKOR_GEMM_MIN_BLOCKS;
+constexpr int GEMM_THREADS = GEMM_WM * GEMM_WN * 64;
+
+// Tile scheduling: workgroup b of a launch runs on XCD b % GEMM_XCDS (the
+// hardware's round-robin dispatch), and each XCD takes super-tiles of up to
+// GEMM_SUPER_M x GEMM_SUPER_N tiles of one layer, so the tiles that run
+// together on an XCD share their operand panels in that XCD's L2.
+constexpr int GEMM_XCDS = 8;
+#ifndef MKOR_GEMM_SUPER
+#define MKOR_GEMM_SUPER 8
+#endif
+constexpr int GEMM_SUPER_M = MKOR_GEMM_SUPER;
+constexpr int GEMM_SUPER_N = MKOR_GEMM_SUPER;
 
 // ---------------------------------------------------------------- rescale
 struct RescaleLayer {
@@ -95,11 +140,19 @@ struct RescaleBlock {
 
 // ---------------------------------------------------------------- launchers
 // Each returns the hipError_t of its launch.
-hipError_t launch_sm_matvec(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
-                            float4* partials, int32_t norm_kind, hipStream_t stream);
+// Streaming pass over every factor: applies the pending term in place (when
+// there is one) and, with matvec = 1, forms u_raw = P x, the row norms and the
+// per-row-block partials of the current P.
+hipError_t launch_sm_pass(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
+                          float4* partials, int32_t norm_kind, int32_t matvec, hipStream_t stream);
 
-hipError_t launch_sm_update(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
-                            const float4* partials, const mkor_params& p, hipStream_t stream);
+// One workgroup per factor: stabiliser decision and update coefficients from
+// the pass partials, new pending term (coefficients and w), stats.
+hipError_t launch_sm_finalize(const FactorDesc* factors, int32_t nfactors, const float4* partials,
+                              const mkor_params& p, hipStream_t stream);
+
+// Marks every pending term applied (after a materialising pass).
+hipError_t launch_sm_reset(const FactorDesc* factors, int32_t nfactors, hipStream_t stream);
 
 // GEMM 1: X^T = (Linv G)^T, plus ||G||^2 partials from the tiles of the first M row.
 hipError_t launch_gemm_xt(const GemmLayer* layers, const GemmTile* tiles, int32_t ntiles,

@@ -14,11 +14,20 @@
 //             (d_in x d_out, row-major) written straight into dW, plus one
 //             sum of dW_hat^2 per tile for the rescale.
 //
-// Each workgroup (4 waves, 2 x 2) computes a 128 x 128 tile; each wave owns
-// 64 x 64 = 2 x 2 blocks of v_mfma_f32_32x32x2_f32.  K advances in 16-deep
-// slabs, double-buffered in LDS; the next slab's global loads are issued
-// before the current slab's MFMAs.  The grid is one grouped launch over a
-// tile table that the host orders longest-K first.
+// The factor operand (Linv in stage 1, Rinv in stage 2) is the caller buffer S
+// plus the pending rank-1 term of the SM update (struct Pending).  The stores
+// into LDS apply that term element by element with the same pinned roundings
+// as the SM pass, so the GEMMs multiply with the current factor without it
+// being written first; doing it on the store side keeps the arithmetic off
+// the path between a global load and the MFMAs that overlap it.
+//
+// A workgroup of GEMM_WM x GEMM_WN waves computes a GEMM_BM x GEMM_BN tile;
+// each wave owns a (BM / WM) x (BN / WN) sub-tile of 32 x 32 blocks of
+// v_mfma_f32_32x32x2_f32.  K advances in GEMM_BK-deep slabs, double-buffered
+// in LDS; the next slab's global loads are issued before the current slab's
+// MFMAs and stored after them.  The grid is one grouped launch over a tile
+// table that the host orders for the XCDs (see the plan code).
+#include "gmem.h"
 #include "mkor_internal.h"
 
 namespace mkor {
@@ -27,7 +36,23 @@ namespace {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = GEMM_BM, BN = GEMM_BN, BK = GEMM_BK;
+constexpr int WM = GEMM_WM, WN = GEMM_WN;
 constexpr int NT = GEMM_THREADS;
+constexpr int TM = BM / WM, TN = BN / WN;   // wave sub-tile
+constexpr int FM = TM / 32, FN = TN / 32;   // 32 x 32 MFMA blocks per wave
+constexpr int AC4 = BM / 4, BC4 = BN / 4, BC8 = BN / 8;   // vectors per slab row
+constexpr int A4 = BK * BM / 4 / NT;        // float4 of At per thread and slab
+constexpr int B4 = BK * BN / 4 / NT;        // float4 of fp32 B per thread and slab
+constexpr int B8 = BK * BN / 8 / NT;        // 2 x 4 bf16 of B per thread and slab
+// ds_read2_b32 instructions per k-step: the FM (FN) operands of a wave are
+// 32 floats apart, two per instruction
+constexpr int DS_PER_K = (FM + 1) / 2 + (FN + 1) / 2;
+static_assert(NT == WM * WN * 64, "one wave per sub-tile");
+static_assert(TM % 32 == 0 && TN % 32 == 0 && BK % 2 == 0, "tile shape");
+static_assert(A4 * NT * 4 == BK * BM && B4 * NT * 4 == BK * BN && B8 * NT * 8 == BK * BN,
+              "slab divides evenly among the threads");
+static_assert(NT % AC4 == 0 && NT % BC4 == 0 && NT % BC8 == 0,
+              "a thread stages the same columns in every slab");
 
 __device__ __forceinline__ float bf16_to_f32(unsigned short h) {
     return __uint_as_float(((unsigned)h) << 16);
@@ -51,68 +76,164 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
     return s;
 }
 
-// Register staging of one K slab of At and B for the vector paths.
-struct SlabRegs {
-    float4 a[2];
-    float4 b[2];   // fp32 B: two float4; bf16 B: 8 values packed in b[0] and b[1]
+// Pending rank-1 term of the factor operand, and the w values of the columns
+// this thread stages (fixed for a tile in the vector paths).
+struct Xform {
+    float c1, c2, sgn;
+    const float* w;
+    float4 wc;
 };
 
-template <bool BF16, bool VEC>
+// Element (k, c) of the current factor from stored value v: see Pending.
+__device__ __forceinline__ float xf1(const Xform& x, float v, float wk, float wc, int k, int c) {
+    v = __fmaf_rn(x.c1, v, x.sgn * __fmul_rn(wk, wc));
+    return k == c ? __fadd_rn(v, x.c2) : v;
+}
+
+__device__ __forceinline__ float4 xf4(const Xform& x, float4 v, float wk, int k, int c) {
+    v.x = xf1(x, v.x, wk, x.wc.x, k, c + 0);
+    v.y = xf1(x, v.y, wk, x.wc.y, k, c + 1);
+    v.z = xf1(x, v.z, wk, x.wc.z, k, c + 2);
+    v.w = xf1(x, v.w, wk, x.wc.w, k, c + 3);
+    return v;
+}
+
+__device__ __forceinline__ void sq4(float& acc, const float4& v) {
+    acc = fmaf(v.x, v.x, acc);
+    acc = fmaf(v.y, v.y, acc);
+    acc = fmaf(v.z, v.z, acc);
+    acc = fmaf(v.w, v.w, acc);
+}
+
+// Register staging of one K slab (vector paths).  wk holds w of the slab rows
+// this thread stages when the pending term is applied.
+template <bool BF16>
+struct SlabRegs {
+    float4 a[A4];
+    float4 b[B4];
+    float  wk[A4 > B4 ? A4 : B4];
+};
+template <>
+struct SlabRegs<true> {
+    float4 a[A4];
+    uint2  h[2 * B8];   // 4 bf16 of the left half of the tile, 4 of the right half
+    float  wk[A4];
+};
+
+// XF: 0 = plain operands, 1 = apply the pending term to At, 2 = to B (fp32).
+// FULL: the tile lies inside the matrices and K is a multiple of BK, so the
+// vector paths need no range checks.  Partial tiles load from a clamped (valid)
+// address and zero the out-of-range values at store time, which keeps the
+// loads unconditional and lets them all be in flight during the MFMAs.
+template <bool BF16, bool VEC, bool FULL, int XF>
 struct Loader {
-    // Global -> registers (VEC) or global -> LDS directly (scalar path).
-    __device__ static void load(SlabRegs& r, const GemmLayer& L, int m0, int n0, int k0,
-                                float* As, float* Bs, float& gsq, bool want_gsq) {
-        const int t = threadIdx.x;
+    // Vector paths: global -> registers, issued before the slab's MFMAs.
+    __device__ static void load(SlabRegs<BF16>& r, const GemmLayer& L, int m0, int n0, int k0) {
         if constexpr (VEC) {
+            const int t = threadIdx.x;
+            const int m = m0 + 4 * (t % AC4);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int idx = t + i * NT;
-                const int row = idx >> 5, c4 = idx & 31;
-                const int k = k0 + row, m = m0 + 4 * c4;
-                r.a[i] = (k < L.K && m < L.M)
-                    ? *reinterpret_cast<const float4*>(L.At + (size_t)k * L.M + m)
-                    : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int i = 0; i < A4; ++i) {
+                const int k = k0 + (t + i * NT) / AC4;
+                const bool ok = FULL || (k < L.K && m < L.M);
+                r.a[i] = gld4(L.At + (ok ? (size_t)k * L.M + m : 0));
+                if constexpr (XF == 1) r.wk[i] = gld(L.w + (ok ? k : 0));
             }
             if constexpr (!BF16) {
+                const int n = n0 + 4 * (t % BC4);
+                const float* B = static_cast<const float*>(L.B);
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int idx = t + i * NT;
-                    const int row = idx >> 5, c4 = idx & 31;
-                    const int k = k0 + row, n = n0 + 4 * c4;
-                    r.b[i] = (k < L.K && n < L.N)
-                        ? *reinterpret_cast<const float4*>(
-                              static_cast<const float*>(L.B) + (size_t)k * L.N + n)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int i = 0; i < B4; ++i) {
+                    const int k = k0 + (t + i * NT) / BC4;
+                    const bool ok = FULL || (k < L.K && n < L.N);
+                    r.b[i] = gld4(B + (ok ? (size_t)k * L.N + n : 0));
+                    if constexpr (XF == 2) r.wk[i] = gld(L.w + (ok ? k : 0));
                 }
             } else {
-                const int row = t >> 4, c8 = t & 15;
-                const int k = k0 + row, n = n0 + 8 * c8;
-                uint4 h = make_uint4(0u, 0u, 0u, 0u);
-                if (k < L.K && n < L.N)
-                    h = *reinterpret_cast<const uint4*>(
-                        static_cast<const unsigned short*>(L.B) + (size_t)k * L.N + n);
-                r.b[0] = make_float4(__uint_as_float(h.x << 16), __uint_as_float(h.x & 0xffff0000u),
-                                     __uint_as_float(h.y << 16), __uint_as_float(h.y & 0xffff0000u));
-                r.b[1] = make_float4(__uint_as_float(h.z << 16), __uint_as_float(h.z & 0xffff0000u),
-                                     __uint_as_float(h.w << 16), __uint_as_float(h.w & 0xffff0000u));
-            }
-            if (want_gsq) {
+                // columns n and n + BN / 2, so that the LDS stores of a wave
+                // are contiguous (no bank conflicts)
+                const int n = n0 + 4 * (t % BC8);
+                const unsigned short* B = static_cast<const unsigned short*>(L.B);
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    gsq = fmaf(r.b[i].x, r.b[i].x, gsq);
-                    gsq = fmaf(r.b[i].y, r.b[i].y, gsq);
-                    gsq = fmaf(r.b[i].z, r.b[i].z, gsq);
-                    gsq = fmaf(r.b[i].w, r.b[i].w, gsq);
+                for (int i = 0; i < B8; ++i) {
+                    const int k = k0 + (t + i * NT) / BC8;
+                    const bool ok0 = FULL || (k < L.K && n < L.N);
+                    const bool ok1 = FULL || (k < L.K && n + BN / 2 < L.N);
+                    r.h[2 * i] = gld_u2(B + (ok0 ? (size_t)k * L.N + n : 0));
+                    r.h[2 * i + 1] = gld_u2(B + (ok1 ? (size_t)k * L.N + n + BN / 2 : 0));
+                }
+            }
+        }
+    }
+
+    // Registers -> LDS after the MFMAs (vector paths; range masking, the
+    // pending term and the bf16 upcast are applied here), or global -> LDS
+    // directly (scalar path for ragged sizes).
+    __device__ static void store(const SlabRegs<BF16>& r, const GemmLayer& L, const Xform& xf,
+                                 int m0, int n0, int k0, float* As, float* Bs, float& gsq,
+                                 bool want_gsq) {
+        const int t = threadIdx.x;
+        const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+        if constexpr (VEC) {
+            const int ca = 4 * (t % AC4);
+#pragma unroll
+            for (int i = 0; i < A4; ++i) {
+                const int row = (t + i * NT) / AC4;
+                const int k = k0 + row, m = m0 + ca;
+                const bool ok = FULL || (k < L.K && m < L.M);
+                float4 v = ok ? r.a[i] : zero;
+                if constexpr (XF == 1) {
+                    if (ok) v = xf4(xf, v, r.wk[i], k, m);
+                }
+                *reinterpret_cast<float4*>(As + row * BM + ca) = v;
+            }
+            if constexpr (!BF16) {
+                const int cb = 4 * (t % BC4);
+#pragma unroll
+                for (int i = 0; i < B4; ++i) {
+                    const int row = (t + i * NT) / BC4;
+                    const int k = k0 + row, n = n0 + cb;
+                    const bool ok = FULL || (k < L.K && n < L.N);
+                    float4 v = ok ? r.b[i] : zero;
+                    if constexpr (XF == 2) {
+                        if (ok) v = xf4(xf, v, r.wk[i], k, n);
+                    }
+                    if (want_gsq) sq4(gsq, v);
+                    *reinterpret_cast<float4*>(Bs + row * BN + cb) = v;
+                }
+            } else {
+                const int cb = 4 * (t % BC8);
+#pragma unroll
+                for (int i = 0; i < B8; ++i) {
+                    const int row = (t + i * NT) / BC8;
+                    const int k = k0 + row, n = n0 + cb;
+                    const bool ok0 = FULL || (k < L.K && n < L.N);
+                    const bool ok1 = FULL || (k < L.K && n + BN / 2 < L.N);
+                    const uint2 h0 = ok0 ? r.h[2 * i] : make_uint2(0u, 0u);
+                    const uint2 h1 = ok1 ? r.h[2 * i + 1] : make_uint2(0u, 0u);
+                    const float4 v0 = make_float4(
+                        __uint_as_float(h0.x << 16), __uint_as_float(h0.x & 0xffff0000u),
+                        __uint_as_float(h0.y << 16), __uint_as_float(h0.y & 0xffff0000u));
+                    const float4 v1 = make_float4(
+                        __uint_as_float(h1.x << 16), __uint_as_float(h1.x & 0xffff0000u),
+                        __uint_as_float(h1.y << 16), __uint_as_float(h1.y & 0xffff0000u));
+                    if (want_gsq) { sq4(gsq, v0); sq4(gsq, v1); }
+                    *reinterpret_cast<float4*>(Bs + row * BN + cb) = v0;
+                    *reinterpret_cast<float4*>(Bs + row * BN + cb + BN / 2) = v1;
                 }
             }
         } else {
-            // scalar path: ragged sizes, straight into LDS
 #pragma unroll
             for (int i = 0; i < (BK * BM) / NT; ++i) {
                 const int idx = t + i * NT;
                 const int row = idx / BM, col = idx % BM;
                 const int k = k0 + row, m = m0 + col;
-                As[row * BM + col] = (k < L.K && m < L.M) ? L.At[(size_t)k * L.M + m] : 0.f;
+                float v = 0.f;
+                if (k < L.K && m < L.M) {
+                    v = gld(L.At + (size_t)k * L.M + m);
+                    if constexpr (XF == 1) v = xf1(xf, v, gld(xf.w + k), gld(xf.w + m), k, m);
+                }
+                As[row * BM + col] = v;
             }
 #pragma unroll
             for (int i = 0; i < (BK * BN) / NT; ++i) {
@@ -122,43 +243,21 @@ struct Loader {
                 float v = 0.f;
                 if (k < L.K && n < L.N) {
                     const size_t off = (size_t)k * L.N + n;
-                    v = BF16 ? bf16_to_f32(static_cast<const unsigned short*>(L.B)[off])
-                             : static_cast<const float*>(L.B)[off];
+                    v = BF16 ? bf16_to_f32(gld_u16(static_cast<const unsigned short*>(L.B) + off))
+                             : gld(static_cast<const float*>(L.B) + off);
+                    if constexpr (XF == 2) v = xf1(xf, v, gld(xf.w + k), gld(xf.w + n), k, n);
                 }
                 if (want_gsq) gsq = fmaf(v, v, gsq);
                 Bs[row * BN + col] = v;
             }
         }
     }
-
-    __device__ static void store(const SlabRegs& r, float* As, float* Bs) {
-        if constexpr (VEC) {
-            const int t = threadIdx.x;
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int idx = t + i * NT;
-                const int row = idx >> 5, c4 = idx & 31;
-                *reinterpret_cast<float4*>(As + row * BM + 4 * c4) = r.a[i];
-            }
-            if constexpr (!BF16) {
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int idx = t + i * NT;
-                    const int row = idx >> 5, c4 = idx & 31;
-                    *reinterpret_cast<float4*>(Bs + row * BN + 4 * c4) = r.b[i];
-                }
-            } else {
-                const int row = t >> 4, c8 = t & 15;
-                *reinterpret_cast<float4*>(Bs + row * BN + 8 * c8) = r.b[0];
-                *reinterpret_cast<float4*>(Bs + row * BN + 8 * c8 + 4) = r.b[1];
-            }
-        }
-    }
 };
 
-template <bool BF16, bool VEC, int STAGE>
-__device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, float* partials,
-                          float* smem) {
+template <bool BF16, bool VEC, bool FULL, int STAGE, int XF>
+__device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pending& q,
+                          float* partials, float* smem) {
+    using Ld = Loader<BF16, VEC, FULL, XF>;
     float* As0 = smem;
     float* Bs0 = smem + BK * BM;
     float* As1 = smem + BK * (BM + BN);
@@ -167,56 +266,79 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, float* parti
 
     const int m0 = tile.tm * BM, n0 = tile.tn * BN;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % WM, wn = wave / WM;
     const int li = lane & 31, lk = lane >> 5;
     const bool want_gsq = (STAGE == 1) && tile.tm == 0;
 
-    floatx16 acc[2][2];
+    floatx16 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    Xform xf{q.c1, q.c2, q.sgn, L.w, make_float4(0.f, 0.f, 0.f, 0.f)};
+    if constexpr (XF != 0 && VEC) {
+        // the columns this thread stages are fixed for the tile
+        const int c = XF == 1 ? m0 + 4 * (threadIdx.x % AC4) : n0 + 4 * (threadIdx.x % BC4);
+        if (c < (XF == 1 ? L.M : L.N)) xf.wc = gld4(L.w + c);
+    }
+
     float gsq = 0.f;
-    SlabRegs regs;
+    SlabRegs<BF16> regs;
     const int nslab = (L.K + BK - 1) / BK;
 
-    Loader<BF16, VEC>::load(regs, L, m0, n0, 0, As0, Bs0, gsq, want_gsq);
-    Loader<BF16, VEC>::store(regs, As0, Bs0);
+    Ld::load(regs, L, m0, n0, 0);
+    Ld::store(regs, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
     __syncthreads();
 
     for (int s = 0; s < nslab; ++s) {
-        float* As = (s & 1) ? As1 : As0;
-        float* Bs = (s & 1) ? Bs1 : Bs0;
+        const float* As = (s & 1) ? As1 : As0;
+        const float* Bs = (s & 1) ? Bs1 : Bs0;
         float* An = (s & 1) ? As0 : As1;
         float* Bn = (s & 1) ? Bs0 : Bs1;
         const bool more = s + 1 < nslab;
-        if (more && VEC) Loader<BF16, VEC>::load(regs, L, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
+        if (more) Ld::load(regs, L, m0, n0, (s + 1) * BK);
 
+        // operands of k-step kk + 1 are read from LDS before the MFMAs of
+        // k-step kk are issued, so the LDS latency overlaps those MFMAs
+        const float* Aw = As + wm * TM + li + lk * BM;
+        const float* Bw = Bs + wn * TN + li + lk * BN;
+        float a[2][FM], b[2][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[0][i] = Aw[i * 32];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[0][j] = Bw[j * 32];
 #pragma unroll
         for (int kk = 0; kk < BK / 2; ++kk) {
-            const int k = 2 * kk + lk;
-            const float a0 = As[k * BM + wm * 64 + li];
-            const float a1 = As[k * BM + wm * 64 + 32 + li];
-            const float b0 = Bs[k * BN + wn * 64 + li];
-            const float b1 = Bs[k * BN + wn * 64 + 32 + li];
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
-        }
-
-        if (more) {
-            if constexpr (VEC) {
-                Loader<BF16, VEC>::store(regs, An, Bn);
-            } else {
-                // scalar path loads straight into the other buffer, which no
-                // wave reads during this slab
-                Loader<BF16, VEC>::load(regs, L, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk + 1 < BK / 2) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) a[nxt][i] = Aw[(2 * kk + 2) * BM + i * 32];
+#pragma unroll
+                for (int j = 0; j < FN; ++j) b[nxt][j] = Bw[(2 * kk + 2) * BN + j * 32];
             }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i], b[cur][j], acc[i][j],
+                                                                    0, 0, 0);
         }
+        // pin that order in the schedule: reads of k-steps 0 and 1, MFMAs of
+        // 0, reads of 2, MFMAs of 1, ..., MFMAs of the last k-step
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS_PER_K, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+#pragma unroll
+        for (int kk = 1; kk + 1 < BK / 2; ++kk) {
+            __builtin_amdgcn_sched_group_barrier(0x100, DS_PER_K, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+
+        // the other buffer was last read in slab s - 1, before the barrier
+        if (more) Ld::store(regs, L, xf, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
         __syncthreads();
     }
 
@@ -224,13 +346,13 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, float* parti
     //   i = 8 * (r / 4) + 4 * (lane / 32) + r % 4,  j = lane % 32.
     float csq = 0.f;
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
+    for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-            const int n = n0 + wn * 64 + ni * 32 + li;
+        for (int ni = 0; ni < FN; ++ni) {
+            const int n = n0 + wn * TN + ni * 32 + li;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int mb = m0 + wm * 64 + mi * 32 + 8 * g + 4 * lk;
+                const int mb = m0 + wm * TM + mi * 32 + 8 * g + 4 * lk;
                 const float v0 = acc[mi][ni][4 * g + 0], v1 = acc[mi][ni][4 * g + 1];
                 const float v2 = acc[mi][ni][4 * g + 2], v3 = acc[mi][ni][4 * g + 3];
                 if constexpr (STAGE == 1) {
@@ -238,21 +360,21 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, float* parti
                     if (n < L.N) {
                         float* dst = L.C + (size_t)n * L.M + mb;
                         if (VEC && mb + 3 < L.M) {
-                            *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
+                            gst4(dst, make_float4(v0, v1, v2, v3));
                         } else {
-                            if (mb + 0 < L.M) dst[0] = v0;
-                            if (mb + 1 < L.M) dst[1] = v1;
-                            if (mb + 2 < L.M) dst[2] = v2;
-                            if (mb + 3 < L.M) dst[3] = v3;
+                            if (mb + 0 < L.M) gst(dst + 0, v0);
+                            if (mb + 1 < L.M) gst(dst + 1, v1);
+                            if (mb + 2 < L.M) gst(dst + 2, v2);
+                            if (mb + 3 < L.M) gst(dst + 3, v3);
                         }
                     }
                 } else {
                     if (n < L.N) {
                         float* dst = L.C + (size_t)mb * L.N + n;
-                        if (mb + 0 < L.M) { dst[0] = v0; csq = fmaf(v0, v0, csq); }
-                        if (mb + 1 < L.M) { dst[(size_t)L.N] = v1; csq = fmaf(v1, v1, csq); }
-                        if (mb + 2 < L.M) { dst[2 * (size_t)L.N] = v2; csq = fmaf(v2, v2, csq); }
-                        if (mb + 3 < L.M) { dst[3 * (size_t)L.N] = v3; csq = fmaf(v3, v3, csq); }
+                        if (mb + 0 < L.M) { gst(dst, v0); csq = fmaf(v0, v0, csq); }
+                        if (mb + 1 < L.M) { gst(dst + (size_t)L.N, v1); csq = fmaf(v1, v1, csq); }
+                        if (mb + 2 < L.M) { gst(dst + 2 * (size_t)L.N, v2); csq = fmaf(v2, v2, csq); }
+                        if (mb + 3 < L.M) { gst(dst + 3 * (size_t)L.N, v3); csq = fmaf(v3, v3, csq); }
                     }
                 }
             }
@@ -262,30 +384,53 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, float* parti
     if constexpr (STAGE == 1) {
         if (want_gsq) {
             const float s = block_sum(gsq, red);
-            if (threadIdx.x == 0) partials[L.part0 + tile.tn] = s;
+            if (threadIdx.x == 0) gst(partials + L.part0 + tile.tn, s);
         }
     } else {
         const float s = block_sum(csq, red);
-        if (threadIdx.x == 0) partials[L.part0 + tile.tm * L.ntn + tile.tn] = s;
+        if (threadIdx.x == 0) gst(partials + L.part0 + tile.tm * L.ntn + tile.tn, s);
     }
 }
 
 constexpr int SMEM_FLOATS = 2 * BK * (BM + BN) + NT / 64;
 
+template <bool BF16, int STAGE, int XF>
+__device__ __forceinline__ void run_tile_dt(const GemmLayer& L, const GemmTile& tile,
+                                            const Pending& q, float* partials, float* smem) {
+    if (L.vec) {
+        const bool full = (tile.tm + 1) * BM <= L.M && (tile.tn + 1) * BN <= L.N && L.K % BK == 0;
+        if (full) gemm_tile<BF16, true, true, STAGE, XF>(L, tile, q, partials, smem);
+        else      gemm_tile<BF16, true, false, STAGE, XF>(L, tile, q, partials, smem);
+    } else {
+        gemm_tile<BF16, false, false, STAGE, XF>(L, tile, q, partials, smem);
+    }
+}
+
+// Stage 2's B operand is always fp32 (Rinv), so only stage 1 has bf16 variants.
+template <int STAGE, int XF>
+__device__ __forceinline__ void run_tile(const GemmLayer& L, const GemmTile& tile, const Pending& q,
+                                         float* partials, float* smem) {
+    if constexpr (STAGE == 1) {
+        if (L.b_bf16) {
+            run_tile_dt<true, STAGE, XF>(L, tile, q, partials, smem);
+            return;
+        }
+    }
+    run_tile_dt<false, STAGE, XF>(L, tile, q, partials, smem);
+}
+
 template <int STAGE>
-__global__ __launch_bounds__(NT, 2) void gemm_kernel(const GemmLayer* __restrict__ layers,
-                                                     const GemmTile* __restrict__ tiles,
-                                                     float* __restrict__ partials) {
+__global__ __launch_bounds__(NT, GEMM_MIN_BLOCKS) void gemm_kernel(
+    const GemmLayer* __restrict__ layers, const GemmTile* __restrict__ tiles,
+    float* __restrict__ partials) {
     __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
     const GemmTile tile = tiles[blockIdx.x];
+    if (tile.layer < 0) return;   // padding of the XCD interleave
     const GemmLayer L = layers[tile.layer];
-    if (L.b_bf16) {
-        if (L.vec) gemm_tile<true, true, STAGE>(L, tile, partials, smem);
-        else       gemm_tile<true, false, STAGE>(L, tile, partials, smem);
-    } else {
-        if (L.vec) gemm_tile<false, true, STAGE>(L, tile, partials, smem);
-        else       gemm_tile<false, false, STAGE>(L, tile, partials, smem);
-    }
+    const Pending q = *L.pend;
+    // the factor operand is At in stage 1 and B in stage 2
+    if (q.has) run_tile<STAGE, STAGE>(L, tile, q, partials, smem);
+    else       run_tile<STAGE, 0>(L, tile, q, partials, smem);
 }
 
 }  // namespace

@@ -6,6 +6,7 @@
 // ||dW_hat||^2 partials in a fixed order (so all of them agree), forms
 // scale = ||G||_F / ||dW_hat||_F (0 when dW_hat is zero) and scales its
 // chunk of dW in place.  First-order layers copy G into dW (bf16 upcast).
+#include "gmem.h"
 #include "mkor_internal.h"
 
 #include <math.h>
@@ -25,15 +26,14 @@ __global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
         if (L.g_bf16) {
             const unsigned short* G = static_cast<const unsigned short*>(L.G);
             for (int64_t i = b.start + t; i < end; i += RS_THREADS)
-                L.dW[i] = __uint_as_float(((unsigned)G[i]) << 16);
+                gst(L.dW + i, __uint_as_float(((unsigned)gld_u16(G + i)) << 16));
         } else {
             const float* G = static_cast<const float*>(L.G);
             if ((L.numel & 3) == 0) {
-                const float4* G4 = reinterpret_cast<const float4*>(G);
-                float4* D4 = reinterpret_cast<float4*>(L.dW);
-                for (int64_t i = (b.start >> 2) + t; i < (end >> 2); i += RS_THREADS) D4[i] = G4[i];
+                for (int64_t i = (b.start >> 2) + t; i < (end >> 2); i += RS_THREADS)
+                    gst4(L.dW + 4 * i, gld4(G + 4 * i));
             } else {
-                for (int64_t i = b.start + t; i < end; i += RS_THREADS) L.dW[i] = G[i];
+                for (int64_t i = b.start + t; i < end; i += RS_THREADS) gst(L.dW + i, gld(G + i));
             }
         }
         return;
@@ -42,8 +42,8 @@ __global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
     __shared__ double s_g[RS_THREADS], s_d[RS_THREADS];
     __shared__ float s_scale;
     double g2 = 0.0, d2 = 0.0;
-    for (int i = t; i < L.ngpart; i += RS_THREADS) g2 += (double)gpart[L.gpart0 + i];
-    for (int i = t; i < L.ndpart; i += RS_THREADS) d2 += (double)dpart[L.dpart0 + i];
+    for (int i = t; i < L.ngpart; i += RS_THREADS) g2 += (double)gld(gpart + L.gpart0 + i);
+    for (int i = t; i < L.ndpart; i += RS_THREADS) d2 += (double)gld(dpart + L.dpart0 + i);
     s_g[t] = g2; s_d[t] = d2;
     __syncthreads();
     for (int o = RS_THREADS / 2; o > 0; o >>= 1) {
@@ -65,14 +65,13 @@ __global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
     if (!rescale) return;
     const float sc = s_scale;
     if ((L.numel & 3) == 0) {
-        float4* D4 = reinterpret_cast<float4*>(L.dW);
         for (int64_t i = (b.start >> 2) + t; i < (end >> 2); i += RS_THREADS) {
-            float4 v = D4[i];
+            float4 v = gld4(L.dW + 4 * i);
             v.x *= sc; v.y *= sc; v.z *= sc; v.w *= sc;
-            D4[i] = v;
+            gst4(L.dW + 4 * i, v);
         }
     } else {
-        for (int64_t i = b.start + t; i < end; i += RS_THREADS) L.dW[i] *= sc;
+        for (int64_t i = b.start + t; i < end; i += RS_THREADS) gst(L.dW + i, gld(L.dW + i) * sc);
     }
 }
 

@@ -1,29 +1,41 @@
 // Grouped momentum Sherman-Morrison update of all inverse factors
 // (Algorithm 1: norm-based stabilisation, then SM-based factor inversion;
-// Eq. 4-7, Eq. 9-11).
+// Eq. 4-7, Eq. 9-11), as one streaming pass per step.
 //
-// Two grouped launches over row blocks of every factor of every layer:
+// The update P_t = c1 P_hat + ... needs u = P_hat x over the whole of P before
+// any element of P_t can be written, so an update that writes P_t in the same
+// step reads P twice.  Here each factor is carried as its buffer S plus one
+// pending rank-1 term (struct Pending), and a step is:
 //
-//   sm_matvec_kernel  reads each row of P once: u_raw_i = (P x)_i (row dot
-//                     product, wave-shuffle reduction), the row's absolute sum
-//                     (or max |entry|), and per-block partials
-//                     {norm max, sum x_i u_raw_i, sum x_i^2}.
-//   sm_update_kernel  every workgroup of a factor reduces that factor's
-//                     partials in the same fixed order, so all of them take the
-//                     same stabiliser decision without a host round trip, then
-//                     streams its rows once:  P <- c1 P + c2 I + sgn w w^T.
+//   sm_pass_kernel      one read + one write of S: applies the previous
+//                       step's pending term (S <- P_{t-1}), and over those
+//                       values forms u_raw = P_{t-1} x_t (row dot products,
+//                       wave-shuffle reductions), the row absolute sums (or
+//                       max |entry|) and per-row-block partials
+//                       {norm max, sum x_i u_raw_i, sum x_i^2}.
+//   sm_finalize_kernel  one workgroup per factor reduces the partials in a
+//                       fixed order, takes the stabiliser decision, and stores
+//                       the new pending term  P_t = c1 S + c2 I + sgn w w^T.
+//
+// The preconditioning GEMMs apply the pending term in their operand loads, so
+// they multiply with P_t itself; the next step's pass writes the same values
+// into S.  8 bytes of HBM traffic per factor element and step, the minimum
+// for reading and rewriting a dense fp32 factor.
 //
 // The stabiliser blend P_hat = zeta P + (1 - zeta) I is never materialised: it
 // is folded into u = zeta u_raw + (1 - zeta) x, s = zeta x^T u_raw +
 // (1 - zeta) x^T x and the coefficients c1, c2.  The rank-1 term is written as
-// sgn * w_i * w_j with w = sqrt(|c3|) u so that (i,j) and (j,i) round
-// identically and a symmetric factor stays bitwise symmetric.
+// sgn * w_i * w_j with w = sqrt(|c3|) u, so (i,j) and (j,i) round identically
+// and a symmetric factor stays bitwise symmetric.
+#include "gmem.h"
 #include "mkor_internal.h"
 
 #include <math.h>
 
 namespace mkor {
 namespace {
+
+constexpr int R = SM_ROWS_PER_WAVE;
 
 __device__ __forceinline__ float nanmax(float a, float b) {
     return (a != a || b != b) ? __builtin_nanf("") : fmaxf(a, b);
@@ -45,87 +57,130 @@ __device__ __forceinline__ float absacc(float acc, float v, int maxabs) {
     return maxabs ? nanmax(acc, fabsf(v)) : acc + fabsf(v);
 }
 
-// w = sqc * (zp * u_raw + zq * x) with every rounding pinned, so the row-side
-// and column-side evaluations of w_i agree bit for bit.
-__device__ __forceinline__ float wval(const SmScalars& c, float ur, float xv) {
-    return __fmul_rn(c.sqc, __fmaf_rn(c.zp, ur, __fmul_rn(c.zq, xv)));
+// Off-diagonal part of one element of the current factor (see Pending).
+__device__ __forceinline__ float apply(const Pending& q, float s, float wi, float wj) {
+    return __fmaf_rn(q.c1, s, q.sgn * __fmul_rn(wi, wj));
 }
 
-__device__ __forceinline__ float upd(const SmScalars& c, float p, float wi, float wj) {
-    return __fmaf_rn(c.c1, p, c.sgn * __fmul_rn(wi, wj));
-}
-
-// ------------------------------------------------------------------ K1
-__global__ __launch_bounds__(SM_THREADS) void sm_matvec_kernel(
-    const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
-    float4* __restrict__ partials, int maxabs) {
-    const RowBlock rb = blocks[blockIdx.x];
-    const FactorDesc f = factors[rb.factor];
-    const int d = f.d;
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int rbase = rb.row0 + wave * SM_ROWS_PER_WAVE;
-
-    float dot[SM_ROWS_PER_WAVE], nrm[SM_ROWS_PER_WAVE];
+// ------------------------------------------------------------------ pass
+// Rows rbase .. rbase + nr - 1 of one factor, d a multiple of 4.  FULL: nr = R.
+template <bool HAS, bool MV, bool FULL>
+__device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q, int rbase, int nr,
+                                           int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
+    const int d = f.d, d4 = d >> 2;
+    float* __restrict__ P = f.P + (size_t)rbase * d;
+    float wi[R];
 #pragma unroll
-    for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) { dot[r] = 0.f; nrm[r] = 0.f; }
-    const int nr = max(0, min(SM_ROWS_PER_WAVE, d - rbase));
+    for (int r = 0; r < R; ++r) wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
 
-    if ((d & 3) == 0) {
-        const int d4 = d >> 2;
-        const float4* __restrict__ x4 = reinterpret_cast<const float4*>(f.x);
-        const float4* __restrict__ P4 = reinterpret_cast<const float4*>(f.P) + (size_t)rbase * d4;
-        if (nr == SM_ROWS_PER_WAVE) {
-#pragma unroll 4
-            for (int j = lane; j < d4; j += 64) {
-                const float4 xv = x4[j];
+    for (int j = lane; j < d4; j += 64) {
+        float4 p[R];
 #pragma unroll
-                for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
-                    const float4 p = P4[(size_t)r * d4 + j];
-                    dot[r] = fmaf(p.x, xv.x, dot[r]);
-                    dot[r] = fmaf(p.y, xv.y, dot[r]);
-                    dot[r] = fmaf(p.z, xv.z, dot[r]);
-                    dot[r] = fmaf(p.w, xv.w, dot[r]);
-                    nrm[r] = absacc(nrm[r], p.x, maxabs);
-                    nrm[r] = absacc(nrm[r], p.y, maxabs);
-                    nrm[r] = absacc(nrm[r], p.z, maxabs);
-                    nrm[r] = absacc(nrm[r], p.w, maxabs);
+        for (int r = 0; r < R; ++r)
+            if (FULL || r < nr) p[r] = gld4(P + (size_t)r * d + 4 * j);
+        float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), wv = xv;
+        if constexpr (MV) xv = gld4(f.x + 4 * j);
+        if constexpr (HAS) wv = gld4(f.w + 4 * j);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            if (!FULL && r >= nr) break;
+            if constexpr (HAS) {
+                p[r].x = apply(q, p[r].x, wi[r], wv.x);
+                p[r].y = apply(q, p[r].y, wi[r], wv.y);
+                p[r].z = apply(q, p[r].z, wi[r], wv.z);
+                p[r].w = apply(q, p[r].w, wi[r], wv.w);
+                const int row = rbase + r;
+                if ((row >> 2) == j) {
+                    const int c = row & 3;
+                    if (c == 0) p[r].x = __fadd_rn(p[r].x, q.c2);
+                    else if (c == 1) p[r].y = __fadd_rn(p[r].y, q.c2);
+                    else if (c == 2) p[r].z = __fadd_rn(p[r].z, q.c2);
+                    else p[r].w = __fadd_rn(p[r].w, q.c2);
                 }
+                gst4(P + (size_t)r * d + 4 * j, p[r]);
             }
-        } else {
-            for (int j = lane; j < d4; j += 64) {
-                const float4 xv = x4[j];
-#pragma unroll
-                for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
-                    if (r >= nr) break;
-                    const float4 p = P4[(size_t)r * d4 + j];
-                    dot[r] = fmaf(p.x, xv.x, dot[r]);
-                    dot[r] = fmaf(p.y, xv.y, dot[r]);
-                    dot[r] = fmaf(p.z, xv.z, dot[r]);
-                    dot[r] = fmaf(p.w, xv.w, dot[r]);
-                    nrm[r] = absacc(nrm[r], p.x, maxabs);
-                    nrm[r] = absacc(nrm[r], p.y, maxabs);
-                    nrm[r] = absacc(nrm[r], p.z, maxabs);
-                    nrm[r] = absacc(nrm[r], p.w, maxabs);
-                }
+            if constexpr (MV) {
+                dot[r] = fmaf(p[r].x, xv.x, dot[r]);
+                dot[r] = fmaf(p[r].y, xv.y, dot[r]);
+                dot[r] = fmaf(p[r].z, xv.z, dot[r]);
+                dot[r] = fmaf(p[r].w, xv.w, dot[r]);
+                nrm[r] = absacc(nrm[r], p[r].x, maxabs);
+                nrm[r] = absacc(nrm[r], p[r].y, maxabs);
+                nrm[r] = absacc(nrm[r], p[r].z, maxabs);
+                nrm[r] = absacc(nrm[r], p[r].w, maxabs);
             }
         }
-    } else {
-        const float* __restrict__ P = f.P + (size_t)rbase * d;
-        for (int j = lane; j < d; j += 64) {
-            const float xv = f.x[j];
+    }
+}
+
+// Any d (scalar accesses).
+template <bool HAS, bool MV>
+__device__ __forceinline__ void pass_rows1(const FactorDesc& f, const Pending& q, int rbase, int nr,
+                                           int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
+    const int d = f.d;
+    float* __restrict__ P = f.P + (size_t)rbase * d;
+    float wi[R];
 #pragma unroll
-            for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
-                if (r >= nr) break;
-                const float p = P[(size_t)r * d + j];
+    for (int r = 0; r < R; ++r) wi[r] = (HAS && r < nr) ? gld(f.w + rbase + r) : 0.f;
+    for (int j = lane; j < d; j += 64) {
+        const float xv = MV ? gld(f.x + j) : 0.f;
+        const float wj = HAS ? gld(f.w + j) : 0.f;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            if (r >= nr) break;
+            float p = gld(P + (size_t)r * d + j);
+            if constexpr (HAS) {
+                p = apply(q, p, wi[r], wj);
+                if (rbase + r == j) p = __fadd_rn(p, q.c2);
+                gst(P + (size_t)r * d + j, p);
+            }
+            if constexpr (MV) {
                 dot[r] = fmaf(p, xv, dot[r]);
                 nrm[r] = absacc(nrm[r], p, maxabs);
             }
         }
     }
+}
+
+template <bool HAS, bool MV>
+__device__ __forceinline__ void pass_rows(const FactorDesc& f, const Pending& q, int rbase, int nr,
+                                          int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
+    if ((f.d & 3) == 0) {
+        if (nr == R) pass_rows4<HAS, MV, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        else         pass_rows4<HAS, MV, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+    } else {
+        pass_rows1<HAS, MV>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+    }
+}
+
+__global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
+    const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
+    float4* __restrict__ partials, int maxabs, int matvec) {
+    const RowBlock rb = blocks[blockIdx.x];
+    const FactorDesc f = factors[rb.factor];
+    const Pending q = *f.pend;
+    const bool has = q.has != 0;
+    if (!has && !matvec) return;   // nothing pending to write, no matvec wanted
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int rbase = rb.row0 + wave * R;
+    const int nr = max(0, min(R, f.d - rbase));
+
+    float dot[R], nrm[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) { dot[r] = 0.f; nrm[r] = 0.f; }
+    if (nr > 0) {
+        if (matvec) {
+            if (has) pass_rows<true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else     pass_rows<false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        } else {
+            pass_rows<true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        }
+    }
+    if (!matvec) return;
 
 #pragma unroll
-    for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
+    for (int r = 0; r < R; ++r) {
         dot[r] = wave_sum(dot[r]);
         nrm[r] = maxabs ? wave_nanmax(nrm[r]) : wave_sum(nrm[r]);
     }
@@ -134,11 +189,11 @@ __global__ __launch_bounds__(SM_THREADS) void sm_matvec_kernel(
     if (lane == 0) {
         float mx = 0.f, sxu = 0.f, sxx = 0.f;
 #pragma unroll
-        for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
+        for (int r = 0; r < R; ++r) {
             if (r >= nr) break;
             const int row = rbase + r;
-            f.u[row] = dot[r];
-            const float xr = f.x[row];
+            gst(f.u + row, dot[r]);
+            const float xr = gld(f.x + row);
             mx = nanmax(mx, nrm[r]);
             sxu = fmaf(xr, dot[r], sxu);
             sxx = fmaf(xr, xr, sxx);
@@ -153,26 +208,34 @@ __global__ __launch_bounds__(SM_THREADS) void sm_matvec_kernel(
             acc.y += sred[w].y;
             acc.z += sred[w].z;
         }
-        partials[blockIdx.x] = acc;
+        gst4(reinterpret_cast<float*>(partials + blockIdx.x), acc);
     }
 }
 
-// ------------------------------------------------------------------ K2
+// ------------------------------------------------------------------ finalize
 struct UpdateArgs {
     float gamma, zeta, eps;
     int   variant, guard;
 };
 
-__device__ SmScalars decide(const FactorDesc& f, const float4* __restrict__ partials,
-                            const UpdateArgs& a) {
+struct SmScalars {
+    float c1, c2, sgn, sqc;   // P_t = c1 P + c2 I + sgn w w^T,  w = sqc * u
+    float zp, zq;             // u = zp * u_raw + zq * x
+    int   stab, skip;
+    float nu, s;
+};
+
+__global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
+    const FactorDesc* __restrict__ factors, const float4* __restrict__ partials, UpdateArgs a) {
+    const FactorDesc f = factors[blockIdx.x];
     __shared__ float s_mx[SM_THREADS];
     __shared__ double s_xu[SM_THREADS], s_xx[SM_THREADS];
-    __shared__ SmScalars s_out;
+    __shared__ SmScalars s_c;
     const int t = threadIdx.x;
     float mx = 0.f;
     double xu = 0.0, xx = 0.0;
     for (int b = t; b < f.nblk; b += SM_THREADS) {
-        const float4 p = partials[f.blk0 + b];
+        const float4 p = gld4(reinterpret_cast<const float*>(partials + f.blk0 + b));
         mx = nanmax(mx, p.x);
         xu += (double)p.y;
         xx += (double)p.z;
@@ -197,9 +260,11 @@ __device__ SmScalars decide(const FactorDesc& f, const float4* __restrict__ part
         const double s = zp * s_xu[0] + zq * s_xx[0];
         double c1, c2, c3;
         if (a.variant == MKOR_SM_EXACT) {
+            // Sherman-Morrison inverse of gamma * M_hat + (1 - gamma) x x^T
             const double k = (1.0 - g) / (g + (1.0 - g) * s);
             c1 = zp / g; c2 = zq / g; c3 = -k / g;
         } else {
+            // Eq. 6/7 as printed
             const double k = (1.0 - g) / (g * g * (1.0 + g * (1.0 - g) * s));
             c1 = g * zp; c2 = g * zq; c3 = k;
         }
@@ -209,97 +274,56 @@ __device__ SmScalars decide(const FactorDesc& f, const float4* __restrict__ part
         c.sqc = (float)sqrt(fabs(c3));
         c.zp = (float)zp; c.zq = (float)zq;
         c.nu = (float)nu; c.s = (float)s;
-        s_out = c;
+        s_c = c;
+        if (f.stats != nullptr) {
+            mkor_layer_stats* st = f.stats;
+            if (f.side == 0) { st->nu_L = c.nu; st->s_L = c.s; st->stab_L = c.stab; st->skip_L = c.skip; }
+            else             { st->nu_R = c.nu; st->s_R = c.s; st->stab_R = c.stab; st->skip_R = c.skip; }
+        }
+        Pending q;
+        if (c.skip && a.guard) {   // leave the factor unchanged
+            q.c1 = 1.f; q.c2 = 0.f; q.sgn = 0.f; q.has = 0;
+        } else {
+            q.c1 = c.c1; q.c2 = c.c2; q.sgn = c.sgn; q.has = 1;
+        }
+        *f.pend = q;
     }
     __syncthreads();
-    return s_out;
+    const SmScalars c = s_c;
+    if (c.skip && a.guard) return;
+    // w = sqc * (zp * u_raw + zq * x), each rounding pinned
+    for (int i = t; i < f.d; i += SM_THREADS)
+        gst(f.w + i, __fmul_rn(c.sqc, __fmaf_rn(c.zp, gld(f.u + i), __fmul_rn(c.zq, gld(f.x + i)))));
 }
 
-__global__ __launch_bounds__(SM_THREADS) void sm_update_kernel(
-    const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
-    const float4* __restrict__ partials, UpdateArgs args) {
-    const RowBlock rb = blocks[blockIdx.x];
-    const FactorDesc f = factors[rb.factor];
-    const SmScalars c = decide(f, partials, args);
-
-    if (rb.row0 == 0 && threadIdx.x == 0 && f.stats != nullptr) {
-        mkor_layer_stats* st = f.stats;
-        if (f.side == 0) { st->nu_L = c.nu; st->s_L = c.s; st->stab_L = c.stab; st->skip_L = c.skip; }
-        else             { st->nu_R = c.nu; st->s_R = c.s; st->stab_R = c.stab; st->skip_R = c.skip; }
-    }
-    if (c.skip && args.guard) return;   // leave the factor unchanged
-
-    const int d = f.d;
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int rbase = rb.row0 + wave * SM_ROWS_PER_WAVE;
-    const int nr = max(0, min(SM_ROWS_PER_WAVE, d - rbase));
-    if (nr == 0) return;
-
-    float wi[SM_ROWS_PER_WAVE];
-#pragma unroll
-    for (int r = 0; r < SM_ROWS_PER_WAVE; ++r)
-        wi[r] = (r < nr) ? wval(c, f.u[rbase + r], f.x[rbase + r]) : 0.f;
-
-    if ((d & 3) == 0) {
-        const int d4 = d >> 2;
-        const float4* __restrict__ x4 = reinterpret_cast<const float4*>(f.x);
-        const float4* __restrict__ u4 = reinterpret_cast<const float4*>(f.u);
-        float4* __restrict__ P4 = reinterpret_cast<float4*>(f.P) + (size_t)rbase * d4;
-        for (int j = lane; j < d4; j += 64) {
-            const float4 ur = u4[j], xv = x4[j];
-            const float w0 = wval(c, ur.x, xv.x), w1 = wval(c, ur.y, xv.y);
-            const float w2 = wval(c, ur.z, xv.z), w3 = wval(c, ur.w, xv.w);
-#pragma unroll
-            for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
-                if (r >= nr) break;
-                float4 p = P4[(size_t)r * d4 + j];
-                p.x = upd(c, p.x, wi[r], w0);
-                p.y = upd(c, p.y, wi[r], w1);
-                p.z = upd(c, p.z, wi[r], w2);
-                p.w = upd(c, p.w, wi[r], w3);
-                const int row = rbase + r;
-                if ((row >> 2) == j) {
-                    const int q = row & 3;
-                    if (q == 0) p.x = __fadd_rn(p.x, c.c2);
-                    else if (q == 1) p.y = __fadd_rn(p.y, c.c2);
-                    else if (q == 2) p.z = __fadd_rn(p.z, c.c2);
-                    else p.w = __fadd_rn(p.w, c.c2);
-                }
-                P4[(size_t)r * d4 + j] = p;
-            }
-        }
-    } else {
-        float* __restrict__ P = f.P + (size_t)rbase * d;
-        for (int j = lane; j < d; j += 64) {
-            const float wj = wval(c, f.u[j], f.x[j]);
-#pragma unroll
-            for (int r = 0; r < SM_ROWS_PER_WAVE; ++r) {
-                if (r >= nr) break;
-                float p = upd(c, P[(size_t)r * d + j], wi[r], wj);
-                if (rbase + r == j) p = __fadd_rn(p, c.c2);
-                P[(size_t)r * d + j] = p;
-            }
-        }
-    }
+__global__ void sm_reset_kernel(const FactorDesc* __restrict__ factors, int32_t nfactors) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < nfactors) *factors[i].pend = Pending{1.f, 0.f, 0.f, 0};
 }
 
 }  // namespace
 
-hipError_t launch_sm_matvec(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
-                            float4* partials, int32_t norm_kind, hipStream_t stream) {
+hipError_t launch_sm_pass(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
+                          float4* partials, int32_t norm_kind, int32_t matvec, hipStream_t stream) {
     if (nblocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(sm_matvec_kernel, dim3(nblocks), dim3(SM_THREADS), 0, stream,
-                       factors, blocks, partials, norm_kind == MKOR_NORM_MAXABS ? 1 : 0);
+    hipLaunchKernelGGL(sm_pass_kernel, dim3(nblocks), dim3(SM_THREADS), 0, stream, factors, blocks,
+                       partials, norm_kind == MKOR_NORM_MAXABS ? 1 : 0, matvec ? 1 : 0);
     return hipGetLastError();
 }
 
-hipError_t launch_sm_update(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
-                            const float4* partials, const mkor_params& p, hipStream_t stream) {
-    if (nblocks <= 0) return hipSuccess;
+hipError_t launch_sm_finalize(const FactorDesc* factors, int32_t nfactors, const float4* partials,
+                              const mkor_params& p, hipStream_t stream) {
+    if (nfactors <= 0) return hipSuccess;
     UpdateArgs a{p.gamma, p.zeta, p.stab_eps, p.sm_variant, p.guard_nonfinite};
-    hipLaunchKernelGGL(sm_update_kernel, dim3(nblocks), dim3(SM_THREADS), 0, stream,
-                       factors, blocks, partials, a);
+    hipLaunchKernelGGL(sm_finalize_kernel, dim3(nfactors), dim3(SM_THREADS), 0, stream, factors,
+                       partials, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_sm_reset(const FactorDesc* factors, int32_t nfactors, hipStream_t stream) {
+    if (nfactors <= 0) return hipSuccess;
+    hipLaunchKernelGGL(sm_reset_kernel, dim3((nfactors + 255) / 256), dim3(256), 0, stream, factors,
+                       nfactors);
     return hipGetLastError();
 }
 

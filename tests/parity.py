@@ -123,6 +123,10 @@ class FreeRun:
         return out if precond_oracle else None
 
     def check_factors(self, tol):
+        """Writes the current factors into their buffers (the plan keeps the
+        last update pending) and compares them with the oracle's."""
+        self.plan.sync_factors()
+        torch.cuda.synchronize()
         worst = 0.0
         for i in self.sample:
             Lg, Rg = H.get_factors(self.layers[i])

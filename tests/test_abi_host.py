@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 1
+    assert lib.mkor_abi_version() == 2
 
 
 def test_status_strings(lib):
@@ -124,6 +124,7 @@ def test_empty_list(lib):
     p = M.Params().to_c()
     for fn in (lib.mkor_update_factors, lib.mkor_precondition, lib.mkor_step):
         assert fn(plan, ctypes.byref(p), None) == M.MKOR_OK
+    assert lib.mkor_sync_factors(plan, None) == M.MKOR_OK
     lib.mkor_plan_destroy(plan)
     lib.mkor_plan_destroy(None)
 
@@ -194,10 +195,14 @@ def test_entry_points_reject_before_device(lib):
     p = M.Params().to_c()
     for fn in (lib.mkor_update_factors, lib.mkor_precondition, lib.mkor_step):
         assert fn(None, ctypes.byref(p), None) == M.MKOR_INVALID_ARG
+    assert lib.mkor_sync_factors(None, None) == M.MKOR_INVALID_ARG
+    assert lib.mkor_run_stage(None, ctypes.byref(p), 0, None) == M.MKOR_INVALID_ARG
     plan = ctypes.c_void_p(None)
     assert lib.mkor_plan_create(None, 0, None, 0, ctypes.byref(plan)) == M.MKOR_OK
     bad = M.Params(gamma=2.0).to_c()
     for fn in (lib.mkor_update_factors, lib.mkor_precondition, lib.mkor_step):
         assert fn(plan, ctypes.byref(bad), None) == M.MKOR_INVALID_ARG
         assert fn(plan, None, None) == M.MKOR_INVALID_ARG
+    for stage in (-1, M.NUM_STAGES):
+        assert lib.mkor_run_stage(plan, ctypes.byref(p), stage, None) == M.MKOR_INVALID_ARG
     lib.mkor_plan_destroy(plan)

@@ -84,6 +84,7 @@ def test_update_factors_single_step(variant, norm_kind, eps):
     p = Params(eps=eps, variant=variant, norm_kind=norm_kind, zeta=0.3)
     op = oparams(p)
     plan.update_factors(p)
+    plan.sync_factors()
     torch.cuda.synchronize()
     for i, (L, (Li, Ri, a, g, G)) in enumerate(zip(layers, host)):
         Lo, sL = O.update_factor(Li, a, op)
@@ -138,6 +139,7 @@ def test_guard_nonfinite():
     L0_before = H.get_factors(layers[0])[0]
     plan = H.make_plan(layers)
     plan.step(Params(eps=math.inf, guard_nonfinite=True))
+    plan.sync_factors()
     torch.cuda.synchronize()
     s = H.get_stats(layers[0])
     assert s["skip_L"] == 1 and s["skip_R"] == 0
@@ -148,12 +150,13 @@ def test_guard_nonfinite():
     assert rel(H.get_factors(layers[1])[0], Lo) <= TOL_STEP
     # without the guard the NaN propagates into the factor
     plan.step(Params(eps=math.inf, guard_nonfinite=False))
+    plan.sync_factors()
     torch.cuda.synchronize()
     assert np.isnan(H.get_factors(layers[0])[0]).any()
     assert H.get_stats(layers[0])["skip_L"] == 1
 
 
-def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0):
+def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0, sync_every=False):
     if layers is None:
         layers = H.allocate_layers(shapes, dt)
     plan = H.make_plan(layers)
@@ -163,6 +166,9 @@ def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0):
             a, g, G = _random_inputs(seed + 1000 * t + i, L["d_in"], L["d_out"], dt)
             H.set_inputs(L, a, g, G)
         plan.step(p)
+        if sync_every:
+            plan.sync_factors()
+    plan.sync_factors()
     torch.cuda.synchronize()
     return layers
 
@@ -184,6 +190,43 @@ def test_determinism_and_checkpoint_resume():
     for x, y in zip(A, D):
         for k in ("Linv", "Rinv", "dW"):
             assert torch.equal(x[k], y[k]), k
+
+
+def test_pending_term_matches_write_back_every_step():
+    """Keeping each update pending (applied in the GEMM loads and written by
+    the next pass) gives the same bits as writing it back after every step."""
+    shapes = [(128, 256), (37, 100), (256, 128), (64, 64)]
+    A = _run_steps(shapes, 8, seed=11, dt="fp32")
+    B = _run_steps(shapes, 8, seed=11, dt="fp32", sync_every=True)
+    for x, y in zip(A, B):
+        for k in ("Linv", "Rinv", "dW"):
+            assert torch.equal(x[k], y[k]), k
+
+
+def test_buffers_lag_until_sync():
+    """After a step the buffers hold the factors before that step's update;
+    sync_factors writes the updated ones, and a second sync changes nothing."""
+    layers, host = _setup([(64, 96), (37, 100)], "fp32", seed=700)
+    before = [H.get_factors(L) for L in layers]
+    plan = H.make_plan(layers)
+    p = Params(eps=math.inf)
+    plan.step(p)
+    torch.cuda.synchronize()
+    for L, (Lb, Rb) in zip(layers, before):
+        Lg, Rg = H.get_factors(L)
+        np.testing.assert_array_equal(Lg, Lb)
+        np.testing.assert_array_equal(Rg, Rb)
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    synced = [H.get_factors(L) for L in layers]
+    for L, (Li, Ri, a, g, G), (Lg, Rg) in zip(layers, host, synced):
+        Lo, Ro, _, _ = O.layer_step(Li, Ri, a, g, G, oparams(p))
+        assert rel(Lg, Lo) <= TOL_STEP and rel(Rg, Ro) <= TOL_STEP
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    for L, (Lg, Rg) in zip(layers, synced):
+        np.testing.assert_array_equal(H.get_factors(L)[0], Lg)
+        np.testing.assert_array_equal(H.get_factors(L)[1], Rg)
 
 
 def test_plan_reuse_two_plans_same_buffers():
