@@ -40,6 +40,18 @@ __device__ __forceinline__ uint2 gld_u2(const void* p) {
     return make_uint2(v.x, v.y);
 }
 
+// Streaming variants (non-temporal hint: the data is not re-read soon).
+__device__ __forceinline__ float4 gld4_nt(const float* p) {
+    const mk_f4 v = __builtin_nontemporal_load((const MKOR_GLOBAL mk_f4*)p);
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void gst4_nt(float* p, const float4& v) {
+    mk_f4 w;
+    w.x = v.x; w.y = v.y; w.z = v.z; w.w = v.w;
+    __builtin_nontemporal_store(w, (MKOR_GLOBAL mk_f4*)p);
+}
+
 __device__ __forceinline__ void gst(float* p, float v) { *(MKOR_GLOBAL float*)p = v; }
 
 __device__ __forceinline__ void gst4(float* p, const float4& v) {

@@ -42,9 +42,19 @@ struct FactorDesc {
     int32_t           side;    // 0 = Linv (driven by a), 1 = Rinv (driven by g)
 };
 
-// Rows handled by one workgroup of the SM pass (4 waves x 4 rows).
+// Rows handled by one workgroup of the SM pass (4 waves x SM_ROWS_PER_WAVE).
+#ifndef MKOR_SM_RPW
+#define MKOR_SM_RPW 4
+#endif
+#ifndef MKOR_SM_NT
+#define MKOR_SM_NT 1
+#endif
+#ifndef MKOR_SM_GRID
+#define MKOR_SM_GRID 512
+#endif
+constexpr int SM_GRID = MKOR_SM_GRID;   // workgroups of the SM pass (0: one per row block)
 constexpr int SM_THREADS = 256;
-constexpr int SM_ROWS_PER_WAVE = 4;
+constexpr int SM_ROWS_PER_WAVE = MKOR_SM_RPW;
 constexpr int SM_ROWS = (SM_THREADS / 64) * SM_ROWS_PER_WAVE;
 
 struct RowBlock {
@@ -96,6 +106,12 @@ struct GemmTile {
 #ifndef MKOR_GEMM_MIN_BLOCKS
 #define MKOR_GEMM_MIN_BLOCKS 2
 #endif
+#ifndef MKOR_GEMM_PIPE1
+#define MKOR_GEMM_PIPE1 0
+#endif
+#ifndef MKOR_GEMM_PIPE2
+#define MKOR_GEMM_PIPE2 1
+#endif
 constexpr int GEMM_BM = MKOR_GEMM_BM;
 constexpr int GEMM_BN = MKOR_GEMM_BN;
 constexpr int GEMM_BK = MKOR_GEMM_BK;
@@ -129,8 +145,15 @@ struct RescaleLayer {
     int32_t           _pad;
 };
 
+#ifndef MKOR_RS_GRID
+#define MKOR_RS_GRID 1024
+#endif
 constexpr int RS_THREADS = 256;
-constexpr int RS_ELEMS = 8192;   // elements per rescale workgroup
+constexpr int RS_GRID = MKOR_RS_GRID;   // workgroups of the rescale (0: one per block)
+#ifndef MKOR_RS_ELEMS
+#define MKOR_RS_ELEMS 8192
+#endif
+constexpr int RS_ELEMS = MKOR_RS_ELEMS;   // elements per rescale block
 
 struct RescaleBlock {
     int32_t layer;

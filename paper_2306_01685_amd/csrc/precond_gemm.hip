@@ -254,6 +254,63 @@ struct Loader {
     }
 };
 
+// MFMAs of one K slab held in LDS (As: BK x BM, Bs: BK x BN).  Operands of
+// k-step kk + 1 are read before the MFMAs of k-step kk are issued, so the LDS
+// latency overlaps those MFMAs; the caller pins that order with
+// sched_barriers_slab in the same basic block.
+__device__ __forceinline__ void mma_slab(floatx16 (&acc)[FM][FN], const float* As, const float* Bs,
+                                         int wm, int wn, int li, int lk) {
+    const float* Aw = As + wm * TM + li + lk * BM;
+    const float* Bw = Bs + wn * TN + li + lk * BN;
+    float a[2][FM], b[2][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) a[0][i] = Aw[i * 32];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) b[0][j] = Bw[j * 32];
+#pragma unroll
+    for (int kk = 0; kk < BK / 2; ++kk) {
+        const int cur = kk & 1, nxt = cur ^ 1;
+        if (kk + 1 < BK / 2) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i) a[nxt][i] = Aw[(2 * kk + 2) * BM + i * 32];
+#pragma unroll
+            for (int j = 0; j < FN; ++j) b[nxt][j] = Bw[(2 * kk + 2) * BN + j * 32];
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
+    }
+}
+
+// Schedule of one slab: the global loads of a later slab first (VMEM), then
+// reads of k-steps 0 and 1, MFMAs of 0, reads of 2, MFMAs of 1, ...; when the
+// slab also stores the next slab into LDS, the VALU work and LDS writes of
+// that store are spread over the second half of the MFMAs.
+// Interior tiles of stage 1 / stage 2 use the deeper pipeline of gemm_tile
+// (measured: it pays for stage 2, whose factor operand B is fp32, but not
+// for stage 1 with its bf16 B).
+constexpr bool GEMM_PIPELINE[2] = {MKOR_GEMM_PIPE1 != 0, MKOR_GEMM_PIPE2 != 0};
+
+template <bool LOAD, bool STORE>
+__device__ __forceinline__ void sched_barriers_slab() {
+    constexpr int KS = BK / 2;
+    if constexpr (LOAD) __builtin_amdgcn_sched_group_barrier(0x020, 4 * (A4 + B4 + B8) + 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS_PER_K, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+#pragma unroll
+    for (int kk = 1; kk + 1 < KS; ++kk) {
+        __builtin_amdgcn_sched_group_barrier(0x100, DS_PER_K, 0);
+        if (STORE && kk >= KS / 2) {
+            __builtin_amdgcn_sched_group_barrier(0x002, 24, 0);
+            __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+}
+
 template <bool BF16, bool VEC, bool FULL, int STAGE, int XF>
 __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pending& q,
                           float* partials, float* smem) {
@@ -286,60 +343,74 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pendin
     }
 
     float gsq = 0.f;
-    SlabRegs<BF16> regs;
     const int nslab = (L.K + BK - 1) / BK;
 
-    Ld::load(regs, L, m0, n0, 0);
-    Ld::store(regs, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
-    __syncthreads();
-
-    for (int s = 0; s < nslab; ++s) {
-        const float* As = (s & 1) ? As1 : As0;
-        const float* Bs = (s & 1) ? Bs1 : Bs0;
-        float* An = (s & 1) ? As0 : As1;
-        float* Bn = (s & 1) ? Bs0 : Bs1;
-        const bool more = s + 1 < nslab;
-        if (more) Ld::load(regs, L, m0, n0, (s + 1) * BK);
-
-        // operands of k-step kk + 1 are read from LDS before the MFMAs of
-        // k-step kk are issued, so the LDS latency overlaps those MFMAs
-        const float* Aw = As + wm * TM + li + lk * BM;
-        const float* Bw = Bs + wn * TN + li + lk * BN;
-        float a[2][FM], b[2][FN];
-#pragma unroll
-        for (int i = 0; i < FM; ++i) a[0][i] = Aw[i * 32];
-#pragma unroll
-        for (int j = 0; j < FN; ++j) b[0][j] = Bw[j * 32];
-#pragma unroll
-        for (int kk = 0; kk < BK / 2; ++kk) {
-            const int cur = kk & 1, nxt = cur ^ 1;
-            if (kk + 1 < BK / 2) {
-#pragma unroll
-                for (int i = 0; i < FM; ++i) a[nxt][i] = Aw[(2 * kk + 2) * BM + i * 32];
-#pragma unroll
-                for (int j = 0; j < FN; ++j) b[nxt][j] = Bw[(2 * kk + 2) * BN + j * 32];
-            }
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i], b[cur][j], acc[i][j],
-                                                                    0, 0, 0);
-        }
-        // pin that order in the schedule: reads of k-steps 0 and 1, MFMAs of
-        // 0, reads of 2, MFMAs of 1, ..., MFMAs of the last k-step
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS_PER_K, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
-#pragma unroll
-        for (int kk = 1; kk + 1 < BK / 2; ++kk) {
-            __builtin_amdgcn_sched_group_barrier(0x100, DS_PER_K, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
-
-        // the other buffer was last read in slab s - 1, before the barrier
-        if (more) Ld::store(regs, L, xf, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
+    if constexpr (VEC && FULL && GEMM_PIPELINE[STAGE - 1]) {
+        // Interior tile: slab s + 2 is fetched into registers while slab s is
+        // multiplied, and slab s + 1 (fetched one slab earlier) is written
+        // into the other LDS buffer in the second half of slab s's MFMAs.
+        // LDS buffer (s & 1) holds slab s; registers r0 / r1 alternate.
+        SlabRegs<BF16> r0, r1;
+        Ld::load(r0, L, m0, n0, 0);
+        if (nslab > 1) Ld::load(r1, L, m0, n0, BK);
+        Ld::store(r0, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
         __syncthreads();
+        int s = 0;
+        for (; s + 3 < nslab; s += 2) {
+            Ld::load(r0, L, m0, n0, (s + 2) * BK);
+            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
+            Ld::store(r1, L, xf, m0, n0, (s + 1) * BK, As1, Bs1, gsq, want_gsq);
+            sched_barriers_slab<true, true>();
+            __syncthreads();
+            Ld::load(r1, L, m0, n0, (s + 3) * BK);
+            mma_slab(acc, As1, Bs1, wm, wn, li, lk);
+            Ld::store(r0, L, xf, m0, n0, (s + 2) * BK, As0, Bs0, gsq, want_gsq);
+            sched_barriers_slab<true, true>();
+            __syncthreads();
+        }
+        // 1, 2 or 3 slabs remain; s is even
+        const int rem = nslab - s;
+        if (rem == 3) {
+            Ld::load(r0, L, m0, n0, (s + 2) * BK);
+            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
+            Ld::store(r1, L, xf, m0, n0, (s + 1) * BK, As1, Bs1, gsq, want_gsq);
+            sched_barriers_slab<true, true>();
+            __syncthreads();
+            mma_slab(acc, As1, Bs1, wm, wn, li, lk);
+            Ld::store(r0, L, xf, m0, n0, (s + 2) * BK, As0, Bs0, gsq, want_gsq);
+            sched_barriers_slab<false, true>();
+            __syncthreads();
+            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
+            sched_barriers_slab<false, false>();
+        } else if (rem == 2) {
+            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
+            Ld::store(r1, L, xf, m0, n0, (s + 1) * BK, As1, Bs1, gsq, want_gsq);
+            sched_barriers_slab<false, true>();
+            __syncthreads();
+            mma_slab(acc, As1, Bs1, wm, wn, li, lk);
+            sched_barriers_slab<false, false>();
+        } else {
+            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
+            sched_barriers_slab<false, false>();
+        }
+    } else {
+        SlabRegs<BF16> regs;
+        Ld::load(regs, L, m0, n0, 0);
+        Ld::store(regs, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
+        __syncthreads();
+        for (int s = 0; s < nslab; ++s) {
+            const float* As = (s & 1) ? As1 : As0;
+            const float* Bs = (s & 1) ? Bs1 : Bs0;
+            float* An = (s & 1) ? As0 : As1;
+            float* Bn = (s & 1) ? Bs0 : Bs1;
+            const bool more = s + 1 < nslab;
+            if (more) Ld::load(regs, L, m0, n0, (s + 1) * BK);
+            mma_slab(acc, As, Bs, wm, wn, li, lk);
+            sched_barriers_slab<false, false>();
+            // the other buffer was last read in slab s - 1, before the barrier
+            if (more) Ld::store(regs, L, xf, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
+            __syncthreads();
+        }
     }
 
     // Epilogue.  Output element (i, j) of block (mi, ni) of this wave:

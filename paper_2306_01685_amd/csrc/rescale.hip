@@ -14,10 +14,12 @@
 namespace mkor {
 namespace {
 
-__global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
-    const RescaleLayer* __restrict__ layers, const RescaleBlock* __restrict__ blocks,
-    const float* __restrict__ gpart, const float* __restrict__ dpart, int rescale) {
-    const RescaleBlock b = blocks[blockIdx.x];
+__device__ __forceinline__ void rescale_block(const RescaleLayer* __restrict__ layers,
+                                              const RescaleBlock* __restrict__ blocks,
+                                              const float* __restrict__ gpart,
+                                              const float* __restrict__ dpart, int rescale, int bi,
+                                              double* s_g, double* s_d, float* s_scale) {
+    const RescaleBlock b = blocks[bi];
     const RescaleLayer L = layers[b.layer];
     const int t = threadIdx.x;
     const int64_t end = min(b.start + (int64_t)RS_ELEMS, L.numel);
@@ -39,8 +41,6 @@ __global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
         return;
     }
 
-    __shared__ double s_g[RS_THREADS], s_d[RS_THREADS];
-    __shared__ float s_scale;
     double g2 = 0.0, d2 = 0.0;
     for (int i = t; i < L.ngpart; i += RS_THREADS) g2 += (double)gld(gpart + L.gpart0 + i);
     for (int i = t; i < L.ndpart; i += RS_THREADS) d2 += (double)gld(dpart + L.dpart0 + i);
@@ -53,8 +53,8 @@ __global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
     if (t == 0) {
         const double nG = sqrt(s_g[0]), nD = sqrt(s_d[0]);
         const double sc = rescale ? (nD > 0.0 ? nG / nD : 0.0) : 1.0;
-        s_scale = (float)sc;
-        if (blockIdx.x == L.first_blk && L.stats != nullptr) {
+        *s_scale = (float)sc;
+        if (bi == L.first_blk && L.stats != nullptr) {
             L.stats->norm_G = (float)nG;
             L.stats->norm_dW_hat = (float)nD;
             L.stats->scale = (float)sc;
@@ -62,17 +62,28 @@ __global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
         }
     }
     __syncthreads();
+    const float sc = *s_scale;
+    __syncthreads();   // s_g, s_d and s_scale are reused by the next block
     if (!rescale) return;
-    const float sc = s_scale;
     if ((L.numel & 3) == 0) {
         for (int64_t i = (b.start >> 2) + t; i < (end >> 2); i += RS_THREADS) {
-            float4 v = gld4(L.dW + 4 * i);
+            float4 v = gld4_nt(L.dW + 4 * i);
             v.x *= sc; v.y *= sc; v.z *= sc; v.w *= sc;
-            gst4(L.dW + 4 * i, v);
+            gst4_nt(L.dW + 4 * i, v);
         }
     } else {
         for (int64_t i = b.start + t; i < end; i += RS_THREADS) gst(L.dW + i, gld(L.dW + i) * sc);
     }
+}
+
+// Grid-stride over the rescale blocks (long streams per workgroup).
+__global__ __launch_bounds__(RS_THREADS) void rescale_kernel(
+    const RescaleLayer* __restrict__ layers, const RescaleBlock* __restrict__ blocks, int nblocks,
+    const float* __restrict__ gpart, const float* __restrict__ dpart, int rescale) {
+    __shared__ double s_g[RS_THREADS], s_d[RS_THREADS];
+    __shared__ float s_scale;
+    for (int bi = blockIdx.x; bi < nblocks; bi += gridDim.x)
+        rescale_block(layers, blocks, gpart, dpart, rescale, bi, s_g, s_d, &s_scale);
 }
 
 }  // namespace
@@ -81,7 +92,8 @@ hipError_t launch_rescale(const RescaleLayer* layers, const RescaleBlock* blocks
                           const float* gpart, const float* dpart, int32_t rescale,
                           hipStream_t stream) {
     if (nblocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(rescale_kernel, dim3(nblocks), dim3(RS_THREADS), 0, stream, layers, blocks,
+    const int32_t grid = (RS_GRID > 0 && nblocks > RS_GRID) ? RS_GRID : nblocks;
+    hipLaunchKernelGGL(rescale_kernel, dim3(grid), dim3(RS_THREADS), 0, stream, layers, blocks, nblocks,
                        gpart, dpart, rescale);
     return hipGetLastError();
 }

@@ -77,7 +77,8 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
         float4 p[R];
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            if (FULL || r < nr) p[r] = gld4(P + (size_t)r * d + 4 * j);
+            if (FULL || r < nr) p[r] = MKOR_SM_NT ? gld4_nt(P + (size_t)r * d + 4 * j)
+                                                  : gld4(P + (size_t)r * d + 4 * j);
         float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), wv = xv;
         if constexpr (MV) xv = gld4(f.x + 4 * j);
         if constexpr (HAS) wv = gld4(f.w + 4 * j);
@@ -97,7 +98,8 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
                     else if (c == 2) p[r].z = __fadd_rn(p[r].z, q.c2);
                     else p[r].w = __fadd_rn(p[r].w, q.c2);
                 }
-                gst4(P + (size_t)r * d + 4 * j, p[r]);
+                if (MKOR_SM_NT) gst4_nt(P + (size_t)r * d + 4 * j, p[r]);
+                else            gst4(P + (size_t)r * d + 4 * j, p[r]);
             }
             if constexpr (MV) {
                 dot[r] = fmaf(p[r].x, xv.x, dot[r]);
@@ -153,10 +155,12 @@ __device__ __forceinline__ void pass_rows(const FactorDesc& f, const Pending& q,
     }
 }
 
-__global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
-    const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
-    float4* __restrict__ partials, int maxabs, int matvec) {
-    const RowBlock rb = blocks[blockIdx.x];
+// One row block of the pass.
+__device__ __forceinline__ void pass_block(const FactorDesc* __restrict__ factors,
+                                           const RowBlock* __restrict__ blocks,
+                                           float4* __restrict__ partials, int b, int maxabs,
+                                           int matvec, float4* sred) {
+    const RowBlock rb = blocks[b];
     const FactorDesc f = factors[rb.factor];
     const Pending q = *f.pend;
     const bool has = q.has != 0;
@@ -185,7 +189,6 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
         nrm[r] = maxabs ? wave_nanmax(nrm[r]) : wave_sum(nrm[r]);
     }
 
-    __shared__ float4 sred[SM_THREADS / 64];
     if (lane == 0) {
         float mx = 0.f, sxu = 0.f, sxx = 0.f;
 #pragma unroll
@@ -208,8 +211,20 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
             acc.y += sred[w].y;
             acc.z += sred[w].z;
         }
-        gst4(reinterpret_cast<float*>(partials + blockIdx.x), acc);
+        gst4(reinterpret_cast<float*>(partials + b), acc);
     }
+    __syncthreads();   // sred is reused by the next row block
+}
+
+// Grid-stride over the row blocks: a grid of about SM_GRID workgroups keeps
+// long streams per workgroup, which measured best for this read + write
+// traffic.
+__global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
+    const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
+    float4* __restrict__ partials, int nblocks, int maxabs, int matvec) {
+    __shared__ float4 sred[SM_THREADS / 64];
+    for (int b = blockIdx.x; b < nblocks; b += gridDim.x)
+        pass_block(factors, blocks, partials, b, maxabs, matvec, sred);
 }
 
 // ------------------------------------------------------------------ finalize
@@ -306,8 +321,9 @@ __global__ void sm_reset_kernel(const FactorDesc* __restrict__ factors, int32_t 
 hipError_t launch_sm_pass(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
                           float4* partials, int32_t norm_kind, int32_t matvec, hipStream_t stream) {
     if (nblocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(sm_pass_kernel, dim3(nblocks), dim3(SM_THREADS), 0, stream, factors, blocks,
-                       partials, norm_kind == MKOR_NORM_MAXABS ? 1 : 0, matvec ? 1 : 0);
+    const int32_t grid = (SM_GRID > 0 && nblocks > SM_GRID) ? SM_GRID : nblocks;
+    hipLaunchKernelGGL(sm_pass_kernel, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
+                       partials, nblocks, norm_kind == MKOR_NORM_MAXABS ? 1 : 0, matvec ? 1 : 0);
     return hipGetLastError();
 }
 
