@@ -52,6 +52,22 @@ __device__ __forceinline__ void gst4_nt(float* p, const float4& v) {
     __builtin_nontemporal_store(w, (MKOR_GLOBAL mk_f4*)p);
 }
 
+// base (wave-uniform) + 32-bit byte offset: the form of the scalar-base
+// addressing mode, so per-thread addresses need one 32-bit register.
+__device__ __forceinline__ float4 gld4_off(const void* base, unsigned byte_off) {
+    const mk_f4 v = *(const MKOR_GLOBAL mk_f4*)((const MKOR_GLOBAL char*)base + byte_off);
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint2 gld_u2_off(const void* base, unsigned byte_off) {
+    const mk_u2 v = *(const MKOR_GLOBAL mk_u2*)((const MKOR_GLOBAL char*)base + byte_off);
+    return make_uint2(v.x, v.y);
+}
+
+__device__ __forceinline__ float gld_off(const void* base, unsigned byte_off) {
+    return *(const MKOR_GLOBAL float*)((const MKOR_GLOBAL char*)base + byte_off);
+}
+
 __device__ __forceinline__ void gst(float* p, float v) { *(MKOR_GLOBAL float*)p = v; }
 
 __device__ __forceinline__ void gst4(float* p, const float4& v) {

@@ -125,15 +125,17 @@ int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 // are padded with tiles of layer -1.
 std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage) {
     struct Super { int32_t layer, tm0, tn0, nm, nn, K; };
+    const GemmShape& sh = GEMM_SHAPE[stage - 1];
+    const int32_t sm = std::max(1, GEMM_SUPER / sh.bm), sn = std::max(1, GEMM_SUPER / sh.bn);
     std::vector<Super> sup;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         if (!L.second_order) continue;
-        const int32_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
+        const int32_t tm = ceil_div(L.d_in, sh.bm), tn = ceil_div(L.d_out, sh.bn);
         const int32_t K = stage == 1 ? L.d_in : L.d_out;
-        for (int32_t a = 0; a < tm; a += GEMM_SUPER_M)
-            for (int32_t b = 0; b < tn; b += GEMM_SUPER_N)
-                sup.push_back(Super{i, a, b, std::min(GEMM_SUPER_M, tm - a), std::min(GEMM_SUPER_N, tn - b), K});
+        for (int32_t a = 0; a < tm; a += sm)
+            for (int32_t b = 0; b < tn; b += sn)
+                sup.push_back(Super{i, a, b, std::min(sm, tm - a), std::min(sn, tn - b), K});
     }
     std::stable_sort(sup.begin(), sup.end(), [](const Super& x, const Super& y) {
         if (x.K != y.K) return x.K > y.K;
@@ -164,9 +166,11 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         if (!L.second_order) continue;
         Lo.nsecond++;
         rowblocks += ceil_div(L.d_in, SM_ROWS) + ceil_div(L.d_out, SM_ROWS);
-        const int64_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
-        g1 += tm * tn;
-        gpart += tn;
+        // ||G||^2 partials: one per stage-1 tile column; ||dW_hat||^2: one per stage-2 tile
+        const int64_t tn1 = ceil_div(L.d_out, GEMM_SHAPE[0].bn);
+        const int64_t tm2 = ceil_div(L.d_in, GEMM_SHAPE[1].bm), tn2 = ceil_div(L.d_out, GEMM_SHAPE[1].bn);
+        g1 += tm2 * tn2;
+        gpart += tn1;
         usum += L.d_in + L.d_out;
     }
     if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX)
@@ -343,7 +347,8 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             ++fi;
         }
         float* X = reinterpret_cast<float*>(base + lo.x_off[i]);
-        const int32_t tm = ceil_div(L.d_in, GEMM_BM), tn = ceil_div(L.d_out, GEMM_BN);
+        const int32_t tn1 = ceil_div(L.d_out, GEMM_SHAPE[0].bn);
+        const int32_t tm2 = ceil_div(L.d_in, GEMM_SHAPE[1].bm), tn2 = ceil_div(L.d_out, GEMM_SHAPE[1].bn);
         const bool bf16 = L.grad_dtype == MKOR_DTYPE_BF16;
         const FactorDesc& fL = fd[fi - 2];
         const FactorDesc& fR = fd[fi - 1];
@@ -353,18 +358,18 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         A.M = L.d_in; A.N = L.d_out; A.K = L.d_in;
         A.b_bf16 = bf16;
         A.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
-        A.part0 = gp; A.ntn = tn;
+        A.part0 = gp; A.ntn = tn1;
         GemmLayer& B = g2l[i];
         B.At = X; B.B = L.Rinv; B.C = L.dW;
         B.pend = fR.pend; B.w = fR.w;
         B.M = L.d_in; B.N = L.d_out; B.K = L.d_out;
         B.b_bf16 = 0;
         B.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
-        B.part0 = dp; B.ntn = tn;
-        R.gpart0 = gp; R.ngpart = tn;
-        R.dpart0 = dp; R.ndpart = tm * tn;
-        gp += tn;
-        dp += tm * tn;
+        B.part0 = dp; B.ntn = tn2;
+        R.gpart0 = gp; R.ngpart = tn1;
+        R.dpart0 = dp; R.ndpart = tm2 * tn2;
+        gp += tn1;
+        dp += tm2 * tn2;
     }
     const std::vector<GemmTile> t1 = schedule_tiles(layers, n, 1), t2 = schedule_tiles(layers, n, 2);
     std::copy(t1.begin(), t1.end(), g1t);

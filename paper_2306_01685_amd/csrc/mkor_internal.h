@@ -86,50 +86,30 @@ struct GemmTile {
     int32_t _pad;
 };
 
-// Tile shape of the preconditioning GEMMs: a workgroup of GEMM_WM x GEMM_WN
-// waves computes a GEMM_BM x GEMM_BN tile, K in GEMM_BK-deep slabs.
-#ifndef MKOR_GEMM_BM
-#define MKOR_GEMM_BM 128
+// Tile shapes of the preconditioning GEMMs, per stage (stage 1: X^T =
+// (Linv G)^T, stage 2: dW_hat = X Rinv): a workgroup of wm x wn waves computes
+// a bm x bn tile, K in bk-deep slabs, at least minb workgroups per CU.
+#ifndef MKOR_GEMM1_SHAPE
+#define MKOR_GEMM1_SHAPE 128, 256, 16, 2, 2, 2
 #endif
-#ifndef MKOR_GEMM_BN
-#define MKOR_GEMM_BN 128
+#ifndef MKOR_GEMM2_SHAPE
+#define MKOR_GEMM2_SHAPE 256, 128, 16, 2, 2, 2
 #endif
-#ifndef MKOR_GEMM_BK
-#define MKOR_GEMM_BK 16
-#endif
-#ifndef MKOR_GEMM_WM
-#define MKOR_GEMM_WM 2
-#endif
-#ifndef MKOR_GEMM_WN
-#define MKOR_GEMM_WN 2
-#endif
-#ifndef MKOR_GEMM_MIN_BLOCKS
-#define MKOR_GEMM_MIN_BLOCKS 2
-#endif
-#ifndef MKOR_GEMM_PIPE1
-#define MKOR_GEMM_PIPE1 0
-#endif
-#ifndef MKOR_GEMM_PIPE2
-#define MKOR_GEMM_PIPE2 1
-#endif
-constexpr int GEMM_BM = MKOR_GEMM_BM;
-constexpr int GEMM_BN = MKOR_GEMM_BN;
-constexpr int GEMM_BK = MKOR_GEMM_BK;
-constexpr int GEMM_WM = MKOR_GEMM_WM;
-constexpr int GEMM_WN = MKOR_GEMM_WN;
-constexpr int GEMM_MIN_BLOCKS = MKOR_GEMM_MIN_BLOCKS;
-constexpr int GEMM_THREADS = GEMM_WM * GEMM_WN * 64;
+struct GemmShape {
+    int bm, bn, bk, wm, wn, minb;
+    constexpr int threads() const { return wm * wn * 64; }
+};
+constexpr GemmShape GEMM_SHAPE[2] = {GemmShape{MKOR_GEMM1_SHAPE}, GemmShape{MKOR_GEMM2_SHAPE}};
 
 // Tile scheduling: workgroup b of a launch runs on XCD b % GEMM_XCDS (the
-// hardware's round-robin dispatch), and each XCD takes super-tiles of up to
-// GEMM_SUPER_M x GEMM_SUPER_N tiles of one layer, so the tiles that run
+// hardware's round-robin dispatch), and each XCD takes super-tiles of one
+// layer covering up to GEMM_SUPER x GEMM_SUPER outputs, so the tiles that run
 // together on an XCD share their operand panels in that XCD's L2.
 constexpr int GEMM_XCDS = 8;
 #ifndef MKOR_GEMM_SUPER
-#define MKOR_GEMM_SUPER 8
+#define MKOR_GEMM_SUPER 1024
 #endif
-constexpr int GEMM_SUPER_M = MKOR_GEMM_SUPER;
-constexpr int GEMM_SUPER_N = MKOR_GEMM_SUPER;
+constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 
 // ---------------------------------------------------------------- rescale
 struct RescaleLayer {

@@ -21,12 +21,19 @@
 // being written first; doing it on the store side keeps the arithmetic off
 // the path between a global load and the MFMAs that overlap it.
 //
-// A workgroup of GEMM_WM x GEMM_WN waves computes a GEMM_BM x GEMM_BN tile;
-// each wave owns a (BM / WM) x (BN / WN) sub-tile of 32 x 32 blocks of
-// v_mfma_f32_32x32x2_f32.  K advances in GEMM_BK-deep slabs, double-buffered
-// in LDS; the next slab's global loads are issued before the current slab's
+// A workgroup of WM x WN waves computes a BM x BN tile (GEMM_SHAPE of the
+// stage); each wave owns a (BM / WM) x (BN / WN) sub-tile of 32 x 32 blocks of
+// v_mfma_f32_32x32x2_f32.  K advances in BK-deep slabs, double-buffered in
+// LDS; the next slab's global loads are issued before the current slab's
 // MFMAs and stored after them.  The grid is one grouped launch over a tile
 // table that the host orders for the XCDs (see the plan code).
+//
+// This file is the implementation of one stage: it is included by
+// precond_gemm_xt.hip (MKOR_GEMM_STAGE 1) and precond_gemm_dw.hip
+// (MKOR_GEMM_STAGE 2), so each stage is compiled with its own tile shape.
+#ifndef MKOR_GEMM_STAGE
+#error "define MKOR_GEMM_STAGE (1 or 2) before including this file"
+#endif
 #include "gmem.h"
 #include "mkor_internal.h"
 
@@ -35,9 +42,11 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = GEMM_BM, BN = GEMM_BN, BK = GEMM_BK;
-constexpr int WM = GEMM_WM, WN = GEMM_WN;
-constexpr int NT = GEMM_THREADS;
+constexpr int STAGE_OF_TU = MKOR_GEMM_STAGE;
+constexpr GemmShape SHP = GEMM_SHAPE[STAGE_OF_TU - 1];
+constexpr int BM = SHP.bm, BN = SHP.bn, BK = SHP.bk;
+constexpr int WM = SHP.wm, WN = SHP.wn;
+constexpr int NT = SHP.threads();
 constexpr int TM = BM / WM, TN = BN / WN;   // wave sub-tile
 constexpr int FM = TM / 32, FN = TN / 32;   // 32 x 32 MFMA blocks per wave
 constexpr int AC4 = BM / 4, BC4 = BN / 4, BC8 = BN / 8;   // vectors per slab row
@@ -76,25 +85,30 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
     return s;
 }
 
-// Pending rank-1 term of the factor operand, and the w values of the columns
-// this thread stages (fixed for a tile in the vector paths).
+// Pending rank-1 term of the factor operand.  swc = sgn * w of the columns this
+// thread stages (fixed for a tile in the vector paths); multiplying by sgn = +-1
+// is exact, so sgn * (w_k * w_c) = w_k * (sgn * w_c) bit for bit.
 struct Xform {
     float c1, c2, sgn;
     const float* w;
-    float4 wc;
+    float4 swc;
 };
 
 // Element (k, c) of the current factor from stored value v: see Pending.
-__device__ __forceinline__ float xf1(const Xform& x, float v, float wk, float wc, int k, int c) {
-    v = __fmaf_rn(x.c1, v, x.sgn * __fmul_rn(wk, wc));
-    return k == c ? __fadd_rn(v, x.c2) : v;
+// DIAG: the element may lie on the diagonal (k == c is checked).
+template <bool DIAG>
+__device__ __forceinline__ float xf1(const Xform& x, float v, float wk, float swc, int k, int c) {
+    v = __fmaf_rn(x.c1, v, __fmul_rn(wk, swc));
+    if (DIAG && k == c) v = __fadd_rn(v, x.c2);
+    return v;
 }
 
+template <bool DIAG>
 __device__ __forceinline__ float4 xf4(const Xform& x, float4 v, float wk, int k, int c) {
-    v.x = xf1(x, v.x, wk, x.wc.x, k, c + 0);
-    v.y = xf1(x, v.y, wk, x.wc.y, k, c + 1);
-    v.z = xf1(x, v.z, wk, x.wc.z, k, c + 2);
-    v.w = xf1(x, v.w, wk, x.wc.w, k, c + 3);
+    v.x = xf1<DIAG>(x, v.x, wk, x.swc.x, k, c + 0);
+    v.y = xf1<DIAG>(x, v.y, wk, x.swc.y, k, c + 1);
+    v.z = xf1<DIAG>(x, v.z, wk, x.swc.z, k, c + 2);
+    v.w = xf1<DIAG>(x, v.w, wk, x.swc.w, k, c + 3);
     return v;
 }
 
@@ -127,40 +141,67 @@ struct SlabRegs<true> {
 // loads unconditional and lets them all be in flight during the MFMAs.
 template <bool BF16, bool VEC, bool FULL, int XF>
 struct Loader {
-    // Vector paths: global -> registers, issued before the slab's MFMAs.
+    // Vector paths: global -> registers, issued before the slab's MFMAs.  In
+    // interior tiles every address is a uniform slab base plus a per-thread
+    // 32-bit offset that does not change from slab to slab.
     __device__ static void load(SlabRegs<BF16>& r, const GemmLayer& L, int m0, int n0, int k0) {
         if constexpr (VEC) {
             const int t = threadIdx.x;
             const int m = m0 + 4 * (t % AC4);
+            if constexpr (FULL) {
+                const float* Ab = L.At + (size_t)k0 * L.M + m0;
 #pragma unroll
-            for (int i = 0; i < A4; ++i) {
-                const int k = k0 + (t + i * NT) / AC4;
-                const bool ok = FULL || (k < L.K && m < L.M);
-                r.a[i] = gld4(L.At + (ok ? (size_t)k * L.M + m : 0));
-                if constexpr (XF == 1) r.wk[i] = gld(L.w + (ok ? k : 0));
+                for (int i = 0; i < A4; ++i) {
+                    const unsigned row = (unsigned)((t + i * NT) / AC4);
+                    r.a[i] = gld4_off(Ab, 4u * (row * (unsigned)L.M + 4u * (t % AC4)));
+                    if constexpr (XF == 1) r.wk[i] = gld_off(L.w + k0, 4u * row);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < A4; ++i) {
+                    const int k = k0 + (t + i * NT) / AC4;
+                    const bool ok = k < L.K && m < L.M;
+                    r.a[i] = gld4(L.At + (ok ? (size_t)k * L.M + m : 0));
+                    if constexpr (XF == 1) r.wk[i] = gld(L.w + (ok ? k : 0));
+                }
             }
             if constexpr (!BF16) {
                 const int n = n0 + 4 * (t % BC4);
                 const float* B = static_cast<const float*>(L.B);
+                const float* Bb = B + (size_t)k0 * L.N + n0;
 #pragma unroll
                 for (int i = 0; i < B4; ++i) {
-                    const int k = k0 + (t + i * NT) / BC4;
-                    const bool ok = FULL || (k < L.K && n < L.N);
-                    r.b[i] = gld4(B + (ok ? (size_t)k * L.N + n : 0));
-                    if constexpr (XF == 2) r.wk[i] = gld(L.w + (ok ? k : 0));
+                    const int row = (t + i * NT) / BC4;
+                    if constexpr (FULL) {
+                        r.b[i] = gld4_off(Bb, 4u * ((unsigned)row * (unsigned)L.N + 4u * (t % BC4)));
+                        if constexpr (XF == 2) r.wk[i] = gld_off(L.w + k0, 4u * (unsigned)row);
+                    } else {
+                        const int k = k0 + row;
+                        const bool ok = k < L.K && n < L.N;
+                        r.b[i] = gld4(B + (ok ? (size_t)k * L.N + n : 0));
+                        if constexpr (XF == 2) r.wk[i] = gld(L.w + (ok ? k : 0));
+                    }
                 }
             } else {
                 // columns n and n + BN / 2, so that the LDS stores of a wave
                 // are contiguous (no bank conflicts)
                 const int n = n0 + 4 * (t % BC8);
                 const unsigned short* B = static_cast<const unsigned short*>(L.B);
+                const unsigned short* Bb = B + (size_t)k0 * L.N + n0;
 #pragma unroll
                 for (int i = 0; i < B8; ++i) {
-                    const int k = k0 + (t + i * NT) / BC8;
-                    const bool ok0 = FULL || (k < L.K && n < L.N);
-                    const bool ok1 = FULL || (k < L.K && n + BN / 2 < L.N);
-                    r.h[2 * i] = gld_u2(B + (ok0 ? (size_t)k * L.N + n : 0));
-                    r.h[2 * i + 1] = gld_u2(B + (ok1 ? (size_t)k * L.N + n + BN / 2 : 0));
+                    const int row = (t + i * NT) / BC8;
+                    if constexpr (FULL) {
+                        const unsigned off = 2u * ((unsigned)row * (unsigned)L.N + 4u * (t % BC8));
+                        r.h[2 * i] = gld_u2_off(Bb, off);
+                        r.h[2 * i + 1] = gld_u2_off(Bb, off + BN);
+                    } else {
+                        const int k = k0 + row;
+                        const bool ok0 = k < L.K && n < L.N;
+                        const bool ok1 = k < L.K && n + BN / 2 < L.N;
+                        r.h[2 * i] = gld_u2(B + (ok0 ? (size_t)k * L.N + n : 0));
+                        r.h[2 * i + 1] = gld_u2(B + (ok1 ? (size_t)k * L.N + n + BN / 2 : 0));
+                    }
                 }
             }
         }
@@ -168,7 +209,9 @@ struct Loader {
 
     // Registers -> LDS after the MFMAs (vector paths; range masking, the
     // pending term and the bf16 upcast are applied here), or global -> LDS
-    // directly (scalar path for ragged sizes).
+    // directly (scalar path for ragged sizes).  DIAG: the slab may hold
+    // diagonal elements of the factor operand.
+    template <bool DIAG>
     __device__ static void store(const SlabRegs<BF16>& r, const GemmLayer& L, const Xform& xf,
                                  int m0, int n0, int k0, float* As, float* Bs, float& gsq,
                                  bool want_gsq) {
@@ -183,7 +226,7 @@ struct Loader {
                 const bool ok = FULL || (k < L.K && m < L.M);
                 float4 v = ok ? r.a[i] : zero;
                 if constexpr (XF == 1) {
-                    if (ok) v = xf4(xf, v, r.wk[i], k, m);
+                    if (ok) v = xf4<DIAG>(xf, v, r.wk[i], k, m);
                 }
                 *reinterpret_cast<float4*>(As + row * BM + ca) = v;
             }
@@ -196,7 +239,7 @@ struct Loader {
                     const bool ok = FULL || (k < L.K && n < L.N);
                     float4 v = ok ? r.b[i] : zero;
                     if constexpr (XF == 2) {
-                        if (ok) v = xf4(xf, v, r.wk[i], k, n);
+                        if (ok) v = xf4<DIAG>(xf, v, r.wk[i], k, n);
                     }
                     if (want_gsq) sq4(gsq, v);
                     *reinterpret_cast<float4*>(Bs + row * BN + cb) = v;
@@ -231,7 +274,7 @@ struct Loader {
                 float v = 0.f;
                 if (k < L.K && m < L.M) {
                     v = gld(L.At + (size_t)k * L.M + m);
-                    if constexpr (XF == 1) v = xf1(xf, v, gld(xf.w + k), gld(xf.w + m), k, m);
+                    if constexpr (XF == 1) v = xf1<true>(xf, v, gld(xf.w + k), xf.sgn * gld(xf.w + m), k, m);
                 }
                 As[row * BM + col] = v;
             }
@@ -245,7 +288,7 @@ struct Loader {
                     const size_t off = (size_t)k * L.N + n;
                     v = BF16 ? bf16_to_f32(gld_u16(static_cast<const unsigned short*>(L.B) + off))
                              : gld(static_cast<const float*>(L.B) + off);
-                    if constexpr (XF == 2) v = xf1(xf, v, gld(xf.w + k), gld(xf.w + n), k, n);
+                    if constexpr (XF == 2) v = xf1<true>(xf, v, gld(xf.w + k), xf.sgn * gld(xf.w + n), k, n);
                 }
                 if (want_gsq) gsq = fmaf(v, v, gsq);
                 Bs[row * BN + col] = v;
@@ -254,167 +297,92 @@ struct Loader {
     }
 };
 
-// MFMAs of one K slab held in LDS (As: BK x BM, Bs: BK x BN).  Operands of
-// k-step kk + 1 are read before the MFMAs of k-step kk are issued, so the LDS
-// latency overlaps those MFMAs; the caller pins that order with
-// sched_barriers_slab in the same basic block.
+// MFMAs of one K slab held in LDS (As: BK x BM, Bs: BK x BN).  With OP_DB the
+// operands of k-step kk + 1 are read before the MFMAs of k-step kk are issued,
+// so the LDS latency overlaps those MFMAs (the caller pins that order with
+// sched_barriers_slab in the same basic block); without it, each k-step reads
+// its own operands (fewer live registers; enough when a k-step has many MFMAs).
+#ifndef MKOR_GEMM_OPDB
+#define MKOR_GEMM_OPDB (FM * FN < 8)
+#endif
+constexpr bool OP_DB = MKOR_GEMM_OPDB;
+
 __device__ __forceinline__ void mma_slab(floatx16 (&acc)[FM][FN], const float* As, const float* Bs,
                                          int wm, int wn, int li, int lk) {
     const float* Aw = As + wm * TM + li + lk * BM;
     const float* Bw = Bs + wn * TN + li + lk * BN;
-    float a[2][FM], b[2][FN];
+    if constexpr (OP_DB) {
+        float a[2][FM], b[2][FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) a[0][i] = Aw[i * 32];
+        for (int i = 0; i < FM; ++i) a[0][i] = Aw[i * 32];
 #pragma unroll
-    for (int j = 0; j < FN; ++j) b[0][j] = Bw[j * 32];
+        for (int j = 0; j < FN; ++j) b[0][j] = Bw[j * 32];
 #pragma unroll
-    for (int kk = 0; kk < BK / 2; ++kk) {
-        const int cur = kk & 1, nxt = cur ^ 1;
-        if (kk + 1 < BK / 2) {
+        for (int kk = 0; kk < BK / 2; ++kk) {
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk + 1 < BK / 2) {
 #pragma unroll
-            for (int i = 0; i < FM; ++i) a[nxt][i] = Aw[(2 * kk + 2) * BM + i * 32];
+                for (int i = 0; i < FM; ++i) a[nxt][i] = Aw[(2 * kk + 2) * BM + i * 32];
 #pragma unroll
-            for (int j = 0; j < FN; ++j) b[nxt][j] = Bw[(2 * kk + 2) * BN + j * 32];
+                for (int j = 0; j < FN; ++j) b[nxt][j] = Bw[(2 * kk + 2) * BN + j * 32];
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
         }
+    } else {
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int kk = 0; kk < BK / 2; ++kk) {
+            float a[FM], b[FN];
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
+            for (int i = 0; i < FM; ++i) a[i] = Aw[2 * kk * BM + i * 32];
+#pragma unroll
+            for (int j = 0; j < FN; ++j) b[j] = Bw[2 * kk * BN + j * 32];
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
     }
 }
 
-// Schedule of one slab: the global loads of a later slab first (VMEM), then
-// reads of k-steps 0 and 1, MFMAs of 0, reads of 2, MFMAs of 1, ...; when the
-// slab also stores the next slab into LDS, the VALU work and LDS writes of
-// that store are spread over the second half of the MFMAs.
-// Interior tiles of stage 1 / stage 2 use the deeper pipeline of gemm_tile
-// (measured: it pays for stage 2, whose factor operand B is fp32, but not
-// for stage 1 with its bf16 B).
-constexpr bool GEMM_PIPELINE[2] = {MKOR_GEMM_PIPE1 != 0, MKOR_GEMM_PIPE2 != 0};
-
-template <bool LOAD, bool STORE>
+// Schedule of one slab's MFMA block.  OP_DB: reads of k-steps 0 and 1, MFMAs
+// of 0, reads of 2, MFMAs of 1, ..., MFMAs of the last k-step; otherwise the
+// reads of each k-step right before its MFMAs.
 __device__ __forceinline__ void sched_barriers_slab() {
     constexpr int KS = BK / 2;
-    if constexpr (LOAD) __builtin_amdgcn_sched_group_barrier(0x020, 4 * (A4 + B4 + B8) + 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS_PER_K, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+    if constexpr (OP_DB) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS_PER_K, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
 #pragma unroll
-    for (int kk = 1; kk + 1 < KS; ++kk) {
-        __builtin_amdgcn_sched_group_barrier(0x100, DS_PER_K, 0);
-        if (STORE && kk >= KS / 2) {
-            __builtin_amdgcn_sched_group_barrier(0x002, 24, 0);
-            __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+        for (int kk = 1; kk + 1 < KS; ++kk) {
+            __builtin_amdgcn_sched_group_barrier(0x100, DS_PER_K, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
         }
         __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+    } else {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+            __builtin_amdgcn_sched_group_barrier(0x100, DS_PER_K, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+        }
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
 }
 
-template <bool BF16, bool VEC, bool FULL, int STAGE, int XF>
-__device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pending& q,
-                          float* partials, float* smem) {
-    using Ld = Loader<BF16, VEC, FULL, XF>;
-    float* As0 = smem;
-    float* Bs0 = smem + BK * BM;
-    float* As1 = smem + BK * (BM + BN);
-    float* Bs1 = As1 + BK * BM;
-    float* red = smem + 2 * BK * (BM + BN);
-
+// Stores the accumulators of one tile and its norm partials.  Output element
+// (i, j) of block (mi, ni) of a wave: i = 8 * (r / 4) + 4 * (lane / 32) + r % 4,
+// j = lane % 32.
+template <bool VEC, int STAGE>
+__device__ __forceinline__ void tile_epilogue(const GemmLayer& L, const GemmTile& tile,
+                                              const floatx16 (&acc)[FM][FN], float gsq,
+                                              bool want_gsq, float* partials, float* red) {
     const int m0 = tile.tm * BM, n0 = tile.tn * BN;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int wm = wave % WM, wn = wave / WM;
     const int li = lane & 31, lk = lane >> 5;
-    const bool want_gsq = (STAGE == 1) && tile.tm == 0;
-
-    floatx16 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    Xform xf{q.c1, q.c2, q.sgn, L.w, make_float4(0.f, 0.f, 0.f, 0.f)};
-    if constexpr (XF != 0 && VEC) {
-        // the columns this thread stages are fixed for the tile
-        const int c = XF == 1 ? m0 + 4 * (threadIdx.x % AC4) : n0 + 4 * (threadIdx.x % BC4);
-        if (c < (XF == 1 ? L.M : L.N)) xf.wc = gld4(L.w + c);
-    }
-
-    float gsq = 0.f;
-    const int nslab = (L.K + BK - 1) / BK;
-
-    if constexpr (VEC && FULL && GEMM_PIPELINE[STAGE - 1]) {
-        // Interior tile: slab s + 2 is fetched into registers while slab s is
-        // multiplied, and slab s + 1 (fetched one slab earlier) is written
-        // into the other LDS buffer in the second half of slab s's MFMAs.
-        // LDS buffer (s & 1) holds slab s; registers r0 / r1 alternate.
-        SlabRegs<BF16> r0, r1;
-        Ld::load(r0, L, m0, n0, 0);
-        if (nslab > 1) Ld::load(r1, L, m0, n0, BK);
-        Ld::store(r0, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
-        __syncthreads();
-        int s = 0;
-        for (; s + 3 < nslab; s += 2) {
-            Ld::load(r0, L, m0, n0, (s + 2) * BK);
-            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
-            Ld::store(r1, L, xf, m0, n0, (s + 1) * BK, As1, Bs1, gsq, want_gsq);
-            sched_barriers_slab<true, true>();
-            __syncthreads();
-            Ld::load(r1, L, m0, n0, (s + 3) * BK);
-            mma_slab(acc, As1, Bs1, wm, wn, li, lk);
-            Ld::store(r0, L, xf, m0, n0, (s + 2) * BK, As0, Bs0, gsq, want_gsq);
-            sched_barriers_slab<true, true>();
-            __syncthreads();
-        }
-        // 1, 2 or 3 slabs remain; s is even
-        const int rem = nslab - s;
-        if (rem == 3) {
-            Ld::load(r0, L, m0, n0, (s + 2) * BK);
-            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
-            Ld::store(r1, L, xf, m0, n0, (s + 1) * BK, As1, Bs1, gsq, want_gsq);
-            sched_barriers_slab<true, true>();
-            __syncthreads();
-            mma_slab(acc, As1, Bs1, wm, wn, li, lk);
-            Ld::store(r0, L, xf, m0, n0, (s + 2) * BK, As0, Bs0, gsq, want_gsq);
-            sched_barriers_slab<false, true>();
-            __syncthreads();
-            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
-            sched_barriers_slab<false, false>();
-        } else if (rem == 2) {
-            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
-            Ld::store(r1, L, xf, m0, n0, (s + 1) * BK, As1, Bs1, gsq, want_gsq);
-            sched_barriers_slab<false, true>();
-            __syncthreads();
-            mma_slab(acc, As1, Bs1, wm, wn, li, lk);
-            sched_barriers_slab<false, false>();
-        } else {
-            mma_slab(acc, As0, Bs0, wm, wn, li, lk);
-            sched_barriers_slab<false, false>();
-        }
-    } else {
-        SlabRegs<BF16> regs;
-        Ld::load(regs, L, m0, n0, 0);
-        Ld::store(regs, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
-        __syncthreads();
-        for (int s = 0; s < nslab; ++s) {
-            const float* As = (s & 1) ? As1 : As0;
-            const float* Bs = (s & 1) ? Bs1 : Bs0;
-            float* An = (s & 1) ? As0 : As1;
-            float* Bn = (s & 1) ? Bs0 : Bs1;
-            const bool more = s + 1 < nslab;
-            if (more) Ld::load(regs, L, m0, n0, (s + 1) * BK);
-            mma_slab(acc, As, Bs, wm, wn, li, lk);
-            sched_barriers_slab<false, false>();
-            // the other buffer was last read in slab s - 1, before the barrier
-            if (more) Ld::store(regs, L, xf, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
-            __syncthreads();
-        }
-    }
-
-    // Epilogue.  Output element (i, j) of block (mi, ni) of this wave:
-    //   i = 8 * (r / 4) + 4 * (lane / 32) + r % 4,  j = lane % 32.
     float csq = 0.f;
 #pragma unroll
     for (int mi = 0; mi < FM; ++mi) {
@@ -463,7 +431,81 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pendin
     }
 }
 
-constexpr int SMEM_FLOATS = 2 * BK * (BM + BN) + NT / 64;
+
+template <bool BF16, bool VEC, bool FULL, int STAGE, int XF>
+__device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pending& q,
+                          float* partials, float* smem) {
+    using Ld = Loader<BF16, VEC, FULL, XF>;
+    using Regs = SlabRegs<BF16>;
+    float* As0 = smem;
+    float* Bs0 = smem + BK * BM;
+    float* As1 = smem + BK * (BM + BN);
+    float* Bs1 = As1 + BK * BM;
+    float* red = smem + 2 * BK * (BM + BN);
+
+    const int m0 = tile.tm * BM, n0 = tile.tn * BN;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wm = wave % WM, wn = wave / WM;
+    const int li = lane & 31, lk = lane >> 5;
+    const bool want_gsq = (STAGE == 1) && tile.tm == 0;
+
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    Xform xf{q.c1, q.c2, q.sgn, L.w, make_float4(0.f, 0.f, 0.f, 0.f)};
+    if constexpr (XF != 0 && VEC) {
+        // the columns this thread stages are fixed for the tile
+        const int c = XF == 1 ? m0 + 4 * (threadIdx.x % AC4) : n0 + 4 * (threadIdx.x % BC4);
+        if (c < (XF == 1 ? L.M : L.N)) {
+            const float4 w = gld4(L.w + c);
+            xf.swc = make_float4(q.sgn * w.x, q.sgn * w.y, q.sgn * w.z, q.sgn * w.w);
+        }
+    }
+    // does slab [k0, k0 + BK) of the factor operand cross its diagonal?
+    auto diag_of = [&](int k0) -> bool {
+        if constexpr (XF == 0) return false;
+        if constexpr (!FULL) return true;
+        const int c0 = XF == 1 ? m0 : n0;
+        const int cw = XF == 1 ? BM : BN;
+        return k0 < c0 + cw && c0 < k0 + BK;
+    };
+
+    float gsq = 0.f;
+    const int nslab = (L.K + BK - 1) / BK;
+
+    Regs regs;
+    Ld::load(regs, L, m0, n0, 0);
+    if (diag_of(0)) Ld::template store<true>(regs, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
+    else            Ld::template store<false>(regs, L, xf, m0, n0, 0, As0, Bs0, gsq, want_gsq);
+    __syncthreads();
+    for (int s = 0; s < nslab; ++s) {
+        const float* As = (s & 1) ? As1 : As0;
+        const float* Bs = (s & 1) ? Bs1 : Bs0;
+        float* An = (s & 1) ? As0 : As1;
+        float* Bn = (s & 1) ? Bs0 : Bs1;
+        const bool more = s + 1 < nslab;
+        if (more) Ld::load(regs, L, m0, n0, (s + 1) * BK);
+        mma_slab(acc, As, Bs, wm, wn, li, lk);
+        sched_barriers_slab();
+        // the other buffer was last read in slab s - 1, before the barrier
+        if (more) {
+            if (diag_of((s + 1) * BK))
+                Ld::template store<true>(regs, L, xf, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
+            else
+                Ld::template store<false>(regs, L, xf, m0, n0, (s + 1) * BK, An, Bn, gsq, want_gsq);
+        }
+        __syncthreads();
+    }
+
+    tile_epilogue<VEC, STAGE>(L, tile, acc, gsq, want_gsq, partials, red);
+}
+
+constexpr int SMEM_BYTES = 4 * (2 * BK * (BM + BN) + NT / 64);
 
 template <bool BF16, int STAGE, int XF>
 __device__ __forceinline__ void run_tile_dt(const GemmLayer& L, const GemmTile& tile,
@@ -491,10 +533,10 @@ __device__ __forceinline__ void run_tile(const GemmLayer& L, const GemmTile& til
 }
 
 template <int STAGE>
-__global__ __launch_bounds__(NT, GEMM_MIN_BLOCKS) void gemm_kernel(
+__global__ __launch_bounds__(NT, SHP.minb) void gemm_kernel(
     const GemmLayer* __restrict__ layers, const GemmTile* __restrict__ tiles,
     float* __restrict__ partials) {
-    __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
+    __shared__ __attribute__((aligned(16))) float smem[SMEM_BYTES / 4];
     const GemmTile tile = tiles[blockIdx.x];
     if (tile.layer < 0) return;   // padding of the XCD interleave
     const GemmLayer L = layers[tile.layer];
@@ -504,20 +546,14 @@ __global__ __launch_bounds__(NT, GEMM_MIN_BLOCKS) void gemm_kernel(
     else       run_tile<STAGE, 0>(L, tile, q, partials, smem);
 }
 
+template <int STAGE>
+hipError_t launch_stage(const GemmLayer* layers, const GemmTile* tiles, int32_t ntiles,
+                        float* partials, hipStream_t stream) {
+    static_assert(STAGE == STAGE_OF_TU, "each translation unit launches its own stage");
+    if (ntiles <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gemm_kernel<STAGE>, dim3(ntiles), dim3(NT), 0, stream, layers, tiles, partials);
+    return hipGetLastError();
+}
+
 }  // namespace
-
-hipError_t launch_gemm_xt(const GemmLayer* layers, const GemmTile* tiles, int32_t ntiles,
-                          float* partials, hipStream_t stream) {
-    if (ntiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(gemm_kernel<1>, dim3(ntiles), dim3(NT), 0, stream, layers, tiles, partials);
-    return hipGetLastError();
-}
-
-hipError_t launch_gemm_dw(const GemmLayer* layers, const GemmTile* tiles, int32_t ntiles,
-                          float* partials, hipStream_t stream) {
-    if (ntiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(gemm_kernel<2>, dim3(ntiles), dim3(NT), 0, stream, layers, tiles, partials);
-    return hipGetLastError();
-}
-
 }  // namespace mkor
