@@ -76,6 +76,12 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stage-timing", action="store_true")
+    ap.add_argument("--rows", type=int, default=0,
+                    help="form a and g inside each step from this many bf16 token rows per layer "
+                         "(Algorithm 1's rank-1 means); 0 (default): a and g are given, as in the "
+                         "headline metric")
+    ap.add_argument("--no-schedule", action="store_true",
+                    help="skip the update-every-10-steps measurement")
     ap.add_argument("--mode", choices=["step", "copy"], default="step",
                     help="copy: time a plain device-to-device copy of --copy-mib MiB (the reference "
                          "kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures)")
@@ -112,6 +118,23 @@ def workload_desc(w):
         counts[s] = counts.get(s, 0) + 1
     inner = ", ".join(f"{c}x {i}x{o}" if c > 1 else f"{i}x{o}" for (i, o), c in counts.items())
     return f"{w.name}: {w.blocks} x {{{inner}}}, fp32 factors, {w.grad_dtype} G"
+
+
+def fill_rows(layers, seed=2307):
+    """Seeded bf16 token rows on the GPU: activations N(0, 1), output gradients
+    N(0, 1e-6), the distributions of the workload's rows."""
+    import torch
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    for L in layers:
+        for k, std in (("A", 1.0), ("Gout", 1e-3)):
+            if k in L:
+                for r0 in range(0, L[k].shape[0], 4096):   # bounded temporaries
+                    blk = L[k][r0:r0 + 4096]
+                    tmp = torch.empty(blk.shape, dtype=torch.float32, device="cuda")
+                    tmp.normal_(0.0, std, generator=gen)
+                    blk.copy_(tmp)
+                    del tmp
 
 
 def fill_inputs(layers, w, seed=2306):
@@ -189,11 +212,13 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     w = W.CONFIGS[args.config]
-    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False)
+    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=args.rows, act_dtype="bf16")
     if w.init != "identity":
         for i, L in enumerate(layers):
             H.set_factors(L, *W.initial_factors(w, i))
     fill_inputs(layers, w)
+    if args.rows:
+        fill_rows(layers)
     plan = H.make_plan(layers)
     params = Params(gamma=w.gamma, zeta=0.5, eps=args.eps)
     stream = torch.cuda.current_stream()
@@ -234,6 +259,7 @@ def main():
         gb = 1e-9
         gbytes_G = nel * (2 if w.grad_dtype == "bf16" else 4)
         sd = sum(i + o for i, o in w.shapes)
+        means_ms, ms = ms[0], ms[1:]   # stage 0: rank-1 means (no work when a and g are given)
         kernels = {
             # steady state: every factor has a pending term, so the pass reads
             # and writes each element once
@@ -244,6 +270,11 @@ def main():
             "gemm_dw": dict(ms=ms[3], flops=f2, tflops=f2 / (ms[3] / 1e3) / 1e12),
             "rescale": dict(ms=ms[4], alg_bytes=8 * nel, gbs=8 * nel * gb / (ms[4] / 1e3)),
         }
+        if args.rows:
+            mb = args.rows * sd * 2   # every bf16 token row read once
+            kernels["means"] = dict(ms=means_ms, alg_bytes=mb, gbs=mb * gb / (means_ms / 1e3),
+                                    frac_hbm=mb * gb / (means_ms / 1e3) / HBM_PEAK_GBS,
+                                    rows=args.rows)
         sm_ms = ms[0] + ms[1]
         kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=8 * sq, gbs=8 * sq * gb / (sm_ms / 1e3),
                                    frac_hbm=8 * sq * gb / (sm_ms / 1e3) / HBM_PEAK_GBS)
@@ -255,8 +286,8 @@ def main():
             kernels[k]["frac_hbm"] = kernels[k]["gbs"] / HBM_PEAK_GBS
         for k in ("gemm_xt", "gemm_dw"):
             kernels[k]["frac_mfma"] = kernels[k]["tflops"] / FP32_MFMA_PEAK_TF
-        dom = max(range(NUM_STAGES), key=lambda s: ms[s])
-        name = STAGE_NAMES[dom]
+        dom = max(range(NUM_STAGES - 1), key=lambda s: ms[s])
+        name = STAGE_NAMES[dom + 1]
         k = kernels[name]
         traffic = profiled_traffic(name, args.config)
         if "flops" in k:
@@ -280,6 +311,24 @@ def main():
     else:
         roof = None
 
+    # The paper's schedule: factors updated every 10 iterations (stale factors
+    # precondition the other nine); per-step rate averaged over whole cycles.
+    schedule = None
+    if not args.no_schedule:
+        cycles = max(1, args.steps // 10)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(cycles):
+            plan.step(params)
+            for _ in range(9):
+                plan.precondition(params)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        f_ms = e0.elapsed_time(e1) / (10 * cycles)
+        schedule = dict(update_every=10, steps=10 * cycles, ms_per_step=f_ms,
+                        value=w.n_layers / (f_ms / 1e3), unit="layer-updates/s")
+
     out = {
         "metric": METRIC, "value": value, "unit": "layer-updates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
@@ -287,8 +336,10 @@ def main():
         "data": "synthetic (seeded; layer shapes only)",
         "config": {"workload": workload_desc(w), "n_layers": w.n_layers,
                    "factor_elems": w.factor_elems, "precond_flops": w.precond_flops,
-                   "gamma": w.gamma, "zeta": 0.5, "eps": args.eps, "grad_dtype": w.grad_dtype},
+                   "gamma": w.gamma, "zeta": 0.5, "eps": args.eps, "grad_dtype": w.grad_dtype,
+                   "token_rows": args.rows},
         "roofline": roof,
+        "schedule_f10": schedule,
         "kernels": kernels,
         "device": torch.cuda.get_device_name(0),
     }

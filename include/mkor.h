@@ -86,7 +86,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 2
+#define MKOR_ABI_VERSION 3
 
 /* status codes */
 #define MKOR_OK                   0
@@ -106,15 +106,17 @@ extern "C" {
 #define MKOR_DTYPE_BF16    1
 
 /* kernels of one step, in launch order (mkor_run_stage) */
-#define MKOR_STAGE_SM_PASS    0   /* write pending term into S; u_raw = P x, norm and s partials */
-#define MKOR_STAGE_SM_FINALIZE 1  /* stabiliser decision, new pending rank-1 term */
-#define MKOR_STAGE_GEMM_XT    2   /* X^T = (Linv G)^T, ||G||^2 partials */
-#define MKOR_STAGE_GEMM_DW    3   /* dW_hat = X Rinv, ||dW_hat||^2 partials */
-#define MKOR_STAGE_RESCALE    4   /* rescale / first-order pass-through */
-#define MKOR_NUM_STAGES       5
+#define MKOR_STAGE_MEANS      0   /* a, g = row means of A, Gout (layers with rows > 0) */
+#define MKOR_STAGE_SM_PASS    1   /* write pending term into S; u_raw = P x, norm and s partials */
+#define MKOR_STAGE_SM_FINALIZE 2  /* stabiliser decision, new pending rank-1 term */
+#define MKOR_STAGE_GEMM_XT    3   /* X^T = (Linv G)^T, ||G||^2 partials */
+#define MKOR_STAGE_GEMM_DW    4   /* dW_hat = X Rinv, ||dW_hat||^2 partials */
+#define MKOR_STAGE_RESCALE    5   /* rescale / first-order pass-through */
+#define MKOR_NUM_STAGES       6
 
-/* largest supported d_in / d_out */
+/* largest supported d_in / d_out, and token rows of A / Gout */
 #define MKOR_MAX_DIM       32768
+#define MKOR_MAX_ROWS      (1 << 26)
 
 typedef struct mkor_params {
     float   gamma;            /* momentum of Eq. 4/5, 0 < gamma < 1 */
@@ -134,11 +136,20 @@ typedef struct mkor_layer {
     int32_t      grad_dtype;    /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (element type of G) */
     float*       Linv;          /* d_in x d_in, in/out (unused if second_order = 0) */
     float*       Rinv;          /* d_out x d_out, in/out (unused if second_order = 0) */
-    const float* a;             /* d_in, mean activation (unused if second_order = 0) */
-    const float* g;             /* d_out, mean output gradient (unused if second_order = 0) */
+    float*       a;             /* d_in, mean activation: input, or output when rows > 0 */
+    float*       g;             /* d_out, mean output gradient: input, or output when rows > 0
+                                   (a and g unused if second_order = 0) */
     const void*  G;             /* d_in x d_out gradient, grad_dtype elements */
     float*       dW;            /* d_in x d_out fp32 output */
     void*        stats;         /* optional device mkor_layer_stats*, may be NULL */
+    /* Rank-1 approximation from token rows (Algorithm 1, its first two lines).
+     * rows = 0: the caller supplies a and g.  rows > 0 (second-order layers
+     * only): each step first sets a = mean of the rows of A and g = mean of
+     * the rows of Gout (float64 sums, one fp32 rounding). */
+    int32_t      rows;          /* 0 .. MKOR_MAX_ROWS */
+    int32_t      act_dtype;     /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (elements of A and Gout) */
+    const void*  A;             /* rows x d_in activations, row-major (rows > 0) */
+    const void*  Gout;          /* rows x d_out output gradients, row-major (rows > 0) */
 } mkor_layer;
 
 /* Per-layer observability record, written on the device when
@@ -180,10 +191,13 @@ int mkor_workspace_size(const mkor_layer* layers, int32_t n, size_t* bytes);
 int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace,
                      size_t ws_bytes, mkor_plan** out);
 
-/* Stabiliser + SM update of Linv and Rinv of every second-order layer
- * (Algorithm 1, stabilisation and SM lines), in one grouped streaming pass
- * plus one small per-factor launch.  The update is left as the pending term
- * (see "Factor state"). */
+/* Rank-1 means (layers with rows > 0), then stabiliser + SM update of Linv
+ * and Rinv of every second-order layer (Algorithm 1, rank-1 approximation,
+ * stabilisation and SM lines), in one grouped streaming pass plus one small
+ * per-factor launch.  The update is left as the pending term (see "Factor
+ * state").  Update frequency f (the paper updates every 10 iterations): call
+ * mkor_step on update steps and mkor_precondition on the others, which
+ * preconditions with the factors of the last update. */
 int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream);
 
 /* Preconditioning with the current factors (buffer + pending term), rescale,

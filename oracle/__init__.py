@@ -8,5 +8,5 @@ from .mkor_oracle import (  # noqa: F401
     NONFINITE_L, NONFINITE_R, NONFINITE_SCALE,
     Params, FactorStats, LayerStats,
     factor_norm, stabilize, sm_update, update_factor,
-    precondition, rescale, layer_step, oracle_step,
+    precondition, rescale, layer_step, oracle_step, rank1_means, layer_step_rows,
 )

@@ -93,6 +93,23 @@ class LayerStats:
     nonfinite: int = 0
 
 
+def rank1_means(rows: np.ndarray) -> np.ndarray:
+    """Rank-1 approximation vector of Algorithm 1 (its first two lines and the
+    "Rank-1 Approximation" paragraph): the average of the samples.
+
+    ``rows`` holds one sample per row (b x d, the transpose of the paper's
+    d x b matrix whose columns are the samples); returns the length-d float64
+    mean (1/b) * sum_i rows[i, :].  Summed in float64 in row order.
+    """
+    R = np.asarray(rows, dtype=np.float64)
+    if R.ndim != 2 or R.shape[0] == 0:
+        raise ValueError("rows must be a non-empty b x d array")
+    acc = np.zeros(R.shape[1], dtype=np.float64)
+    for i in range(R.shape[0]):
+        acc += R[i]
+    return acc / R.shape[0]
+
+
 def factor_norm(P: np.ndarray, norm_kind: int = NORM_INF) -> float:
     """Norm watched by the stabiliser: the infinity norm of the factor.
 
@@ -214,6 +231,17 @@ def layer_step(Linv, Rinv, a, g, G, p: Params, second_order: bool = True,
         if not (math.isfinite(st.norm_G) and math.isfinite(st.norm_dW_hat)):
             st.nonfinite |= NONFINITE_SCALE
     return Linv, Rinv, dW, st
+
+
+def layer_step_rows(Linv, Rinv, A_rows, Gout_rows, G, p: Params, stab_override=(None, None)):
+    """One MKOR step for one second-order layer from its token rows: a and g
+    are the rank-1 means of the activation rows A_rows (b x d_in) and of the
+    output-gradient rows Gout_rows (b x d_out), then ``layer_step``.  Returns
+    (Linv', Rinv', dW, LayerStats, a, g)."""
+    a = rank1_means(A_rows)
+    g = rank1_means(Gout_rows)
+    Li, Ri, dW, st = layer_step(Linv, Rinv, a, g, G, p, True, stab_override)
+    return Li, Ri, dW, st, a, g
 
 
 def oracle_step(layers, p: Params, update: bool = True, precond: bool = True,

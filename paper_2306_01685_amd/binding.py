@@ -33,7 +33,8 @@ NORM_MAXABS = 1
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MAX_DIM = 32768
-ABI_VERSION = 2
+MAX_ROWS = 1 << 26
+ABI_VERSION = 3
 
 
 class mkor_params(ctypes.Structure):
@@ -47,7 +48,9 @@ class mkor_layer(ctypes.Structure):
                 ("second_order", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
                 ("Linv", ctypes.c_void_p), ("Rinv", ctypes.c_void_p),
                 ("a", ctypes.c_void_p), ("g", ctypes.c_void_p),
-                ("G", ctypes.c_void_p), ("dW", ctypes.c_void_p), ("stats", ctypes.c_void_p)]
+                ("G", ctypes.c_void_p), ("dW", ctypes.c_void_p), ("stats", ctypes.c_void_p),
+                ("rows", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
+                ("A", ctypes.c_void_p), ("Gout", ctypes.c_void_p)]
 
 
 class mkor_layer_stats(ctypes.Structure):
@@ -67,9 +70,9 @@ EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_p
             "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_sync_factors",
             "mkor_plan_destroy"]
 
-STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(5)
-NUM_STAGES = 5
-STAGE_NAMES = ["sm_pass", "sm_finalize", "gemm_xt", "gemm_dw", "rescale"]
+STAGE_MEANS, STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(6)
+NUM_STAGES = 6
+STAGE_NAMES = ["means", "sm_pass", "sm_finalize", "gemm_xt", "gemm_dw", "rescale"]
 
 
 class MkorError(RuntimeError):
@@ -160,7 +163,8 @@ def make_layer_array(descs):
         arr[i] = mkor_layer(d["d_in"], d["d_out"], d.get("second_order", 1), d.get("grad_dtype", 0),
                             d.get("Linv") or None, d.get("Rinv") or None, d.get("a") or None,
                             d.get("g") or None, d.get("G") or None, d.get("dW") or None,
-                            d.get("stats") or None)
+                            d.get("stats") or None, d.get("rows", 0), d.get("act_dtype", 0),
+                            d.get("A") or None, d.get("Gout") or None)
     return arr
 
 
@@ -186,8 +190,10 @@ class MkorPlan:
 
     Each layer is a dict with d_in, d_out and tensors Linv, Rinv (fp32,
     symmetric), a, g (fp32 vectors), G (fp32 or bf16, d_in x d_out), dW (fp32,
-    d_in x d_out), optional second_order (default True) and optional stats
-    (a uint8 device tensor of STATS_BYTES bytes).  The plan owns its workspace
+    d_in x d_out), optional second_order (default True), optional stats
+    (a uint8 device tensor of STATS_BYTES bytes), and optionally token rows A
+    (rows x d_in) and Gout (rows x d_out), fp32 or bf16, from which each step
+    forms a and g (their means).  The plan owns its workspace
     (a torch uint8 tensor) and keeps references to every tensor it was given.
 
     After step() / update_factors() the Linv / Rinv tensors lag the current
@@ -208,14 +214,22 @@ class MkorPlan:
                 gdt = DTYPE_F32
             else:
                 raise TypeError(f"unsupported gradient dtype {G.dtype}")
-            for k in ("Linv", "Rinv", "a", "g", "G", "dW"):
+            for k in ("Linv", "Rinv", "a", "g", "G", "dW", "A", "Gout"):
                 t = L.get(k)
                 if t is not None and not t.is_contiguous():
                     raise ValueError(f"{k} must be contiguous")
+            A = L.get("A")
+            rows, adt = 0, DTYPE_F32
+            if A is not None:
+                rows = int(A.shape[0])
+                adt = DTYPE_BF16 if A.dtype == torch.bfloat16 else DTYPE_F32
+                if A.dtype not in (torch.bfloat16, torch.float32) or L["Gout"].dtype != A.dtype:
+                    raise TypeError("A and Gout must both be fp32 or both bf16")
             descs.append(dict(d_in=int(L["d_in"]), d_out=int(L["d_out"]), second_order=so,
                               grad_dtype=gdt, Linv=_ptr(L.get("Linv")), Rinv=_ptr(L.get("Rinv")),
                               a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
-                              stats=_ptr(L.get("stats"))))
+                              stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
+                              Gout=_ptr(L.get("Gout"))))
         self._arr = make_layer_array(descs)
         n = len(descs)
         size = ctypes.c_size_t(0)

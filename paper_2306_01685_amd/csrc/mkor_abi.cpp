@@ -46,7 +46,7 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
     if (n < 0) return fail(MKOR_INVALID_ARG, "n = %d is negative", n);
     if (n > 0 && layers == nullptr) return fail(MKOR_INVALID_ARG, "layers is NULL with n = %d", n);
     std::vector<Interval> iv;
-    iv.reserve((size_t)n * 7 + 1);
+    iv.reserve((size_t)n * 9 + 1);
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         if (L.d_in < 1 || L.d_in > MKOR_MAX_DIM || L.d_out < 1 || L.d_out > MKOR_MAX_DIM)
@@ -56,16 +56,26 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
             return fail(MKOR_INVALID_ARG, "layer %d: second_order = %d is not 0 or 1", i, L.second_order);
         if (L.grad_dtype != MKOR_DTYPE_F32 && L.grad_dtype != MKOR_DTYPE_BF16)
             return fail(MKOR_UNSUPPORTED, "layer %d: grad_dtype = %d is not supported", i, L.grad_dtype);
+        if (L.rows < 0 || L.rows > MKOR_MAX_ROWS)
+            return fail(MKOR_INVALID_ARG, "layer %d: rows = %d outside 0..%d", i, L.rows, MKOR_MAX_ROWS);
+        const bool means = L.rows > 0;
+        if (means && L.second_order != 1)
+            return fail(MKOR_INVALID_ARG, "layer %d: rows > 0 needs a second-order layer", i);
+        if (means && L.act_dtype != MKOR_DTYPE_F32 && L.act_dtype != MKOR_DTYPE_BF16)
+            return fail(MKOR_UNSUPPORTED, "layer %d: act_dtype = %d is not supported", i, L.act_dtype);
         const size_t din = (size_t)L.d_in, dout = (size_t)L.d_out;
         const size_t gsz = din * dout * (L.grad_dtype == MKOR_DTYPE_BF16 ? 2 : 4);
+        const size_t asz = means ? (size_t)L.rows * (L.act_dtype == MKOR_DTYPE_BF16 ? 2 : 4) : 0;
         struct { const void* p; size_t bytes; bool w; const char* what; bool used; } bufs[] = {
             {L.G, gsz, false, "G", true},
             {L.dW, din * dout * 4, true, "dW", true},
             {L.Linv, din * din * 4, true, "Linv", L.second_order == 1},
             {L.Rinv, dout * dout * 4, true, "Rinv", L.second_order == 1},
-            {L.a, din * 4, false, "a", L.second_order == 1},
-            {L.g, dout * 4, false, "g", L.second_order == 1},
+            {L.a, din * 4, means, "a", L.second_order == 1},
+            {L.g, dout * 4, means, "g", L.second_order == 1},
             {L.stats, sizeof(mkor_layer_stats), true, "stats", L.stats != nullptr},
+            {L.A, asz * din, false, "A", means},
+            {L.Gout, asz * dout, false, "Gout", means},
         };
         for (auto& b : bufs) {
             if (!b.used) continue;
@@ -106,10 +116,13 @@ struct Layout {
     size_t off_factors = 0, off_rowblocks = 0, off_pend = 0, off_smpart = 0;
     size_t off_g1l = 0, off_g1t = 0, off_g2l = 0, off_g2t = 0, off_gpart = 0, off_dpart = 0;
     size_t off_rsl = 0, off_rsb = 0, off_x = 0;
+    size_t off_mmat = 0, off_mitem = 0, off_mchunk = 0, off_mpart = 0;
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
     int32_t nsecond = 0;
+    int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
+    int64_t nmeanpart = 0;   // doubles
     std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
 };
 
@@ -173,8 +186,25 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         gpart += tn1;
         usum += L.d_in + L.d_out;
     }
-    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX)
+    int64_t mitems = 0, mchunks = 0, mpart = 0, mmats = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const mkor_layer& L = layers[i];
+        if (L.rows <= 0) continue;
+        const int64_t nrb = ceil_div(L.rows, MEAN_ROWS);
+        for (const int32_t d : {L.d_in, L.d_out}) {
+            const int64_t nch = ceil_div(d, MEAN_COLS);
+            mmats += 1;
+            mchunks += nch;
+            mitems += nch * nrb;
+            mpart += nch * nrb * MEAN_COLS;
+        }
+    }
+    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX || mitems > INT32_MAX)
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
+    Lo.nmeanmat = (int32_t)mmats;
+    Lo.nmeanitem = (int32_t)mitems;
+    Lo.nmeanchunk = (int32_t)mchunks;
+    Lo.nmeanpart = mpart;
     Lo.nfactors = 2 * Lo.nsecond;
     Lo.nrowblocks = (int32_t)rowblocks;
     const size_t t1 = schedule_tiles(layers, n, 1).size(), t2 = schedule_tiles(layers, n, 2).size();
@@ -196,12 +226,16 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_g2t = take(sizeof(GemmTile) * Lo.ng2);
     Lo.off_rsl = take(sizeof(RescaleLayer) * n);
     Lo.off_rsb = take(sizeof(RescaleBlock) * Lo.nrsblocks);
+    Lo.off_mmat = take(sizeof(MeanMat) * Lo.nmeanmat);
+    Lo.off_mitem = take(sizeof(MeanItem) * Lo.nmeanitem);
+    Lo.off_mchunk = take(sizeof(MeanItem) * Lo.nmeanchunk);
     // pending terms start out empty (has = 0): the upload initialises them
     Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
     Lo.table_bytes = align_up(o, 256);
     Lo.off_smpart = take(sizeof(float4) * Lo.nrowblocks);
     Lo.off_gpart = take(sizeof(float) * Lo.ngpart);
     Lo.off_dpart = take(sizeof(float) * Lo.ndpart);
+    Lo.off_mpart = take(sizeof(double) * (size_t)Lo.nmeanpart);
     Lo.u_off.clear();
     Lo.w_off.clear();
     Lo.x_off.assign(n, 0);
@@ -314,6 +348,34 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
     RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
     Pending* pend_h = reinterpret_cast<Pending*>(host.data() + lo.off_pend);
+    MeanMat* mm = reinterpret_cast<MeanMat*>(host.data() + lo.off_mmat);
+    MeanItem* mi = reinterpret_cast<MeanItem*>(host.data() + lo.off_mitem);
+    MeanItem* mc = reinterpret_cast<MeanItem*>(host.data() + lo.off_mchunk);
+    {
+        int32_t k = 0, ki = 0, kc = 0;
+        int64_t p0 = 0;
+        for (int32_t i = 0; i < n; ++i) {
+            const mkor_layer& L = layers[i];
+            if (L.rows <= 0) continue;
+            for (int side = 0; side < 2; ++side) {
+                MeanMat& M = mm[k];
+                M.X = side == 0 ? L.A : L.Gout;
+                M.out = side == 0 ? L.a : L.g;
+                M.rows = L.rows;
+                M.cols = side == 0 ? L.d_in : L.d_out;
+                M.bf16 = L.act_dtype == MKOR_DTYPE_BF16;
+                M.vec = (M.cols % 8) == 0;
+                M.nchunk = ceil_div(M.cols, MEAN_COLS);
+                M.nrb = ceil_div(M.rows, MEAN_ROWS);
+                M.part0 = p0;
+                p0 += (int64_t)M.nchunk * M.nrb * MEAN_COLS;
+                for (int32_t rb = 0; rb < M.nrb; ++rb)
+                    for (int32_t c = 0; c < M.nchunk; ++c) mi[ki++] = MeanItem{k, c, rb, 0};
+                for (int32_t c = 0; c < M.nchunk; ++c) mc[kc++] = MeanItem{k, c, 0, 0};
+                ++k;
+            }
+        }
+    }
     Pending* pend_d = reinterpret_cast<Pending*>(base + lo.off_pend);
 
     int32_t fi = 0, bi = 0, gp = 0, dp = 0, rbi = 0;
@@ -401,6 +463,14 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
     float* dpart = reinterpret_cast<float*>(ws + lo.off_dpart);
     hipError_t e = hipSuccess;
     switch (stage) {
+        case MKOR_STAGE_MEANS:
+            if (lo.nmeanitem == 0) return MKOR_OK;
+            e = launch_colmean(reinterpret_cast<const MeanMat*>(ws + lo.off_mmat),
+                               reinterpret_cast<const MeanItem*>(ws + lo.off_mitem), lo.nmeanitem,
+                               reinterpret_cast<const MeanItem*>(ws + lo.off_mchunk), lo.nmeanchunk,
+                               reinterpret_cast<double*>(ws + lo.off_mpart), s);
+            if (e != hipSuccess) return hip_fail(e, "colmean launch");
+            return MKOR_OK;
         case MKOR_STAGE_SM_PASS:
             if (lo.nrowblocks == 0) return MKOR_OK;
             e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, prm->norm_kind, 1, s);
@@ -446,7 +516,7 @@ int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_params(params);
     if (st != MKOR_OK) return st;
-    return run_range(plan, params, MKOR_STAGE_SM_PASS, MKOR_STAGE_SM_FINALIZE,
+    return run_range(plan, params, MKOR_STAGE_MEANS, MKOR_STAGE_SM_FINALIZE,
                      static_cast<hipStream_t>(stream));
 }
 
@@ -464,7 +534,7 @@ int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_params(params);
     if (st != MKOR_OK) return st;
-    return run_range(plan, params, MKOR_STAGE_SM_PASS, MKOR_STAGE_RESCALE,
+    return run_range(plan, params, MKOR_STAGE_MEANS, MKOR_STAGE_RESCALE,
                      static_cast<hipStream_t>(stream));
 }
 

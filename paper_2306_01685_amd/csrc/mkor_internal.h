@@ -12,6 +12,27 @@
 
 namespace mkor {
 
+// ---------------------------------------------------------------- rank-1 means
+// Column means of the rows x cols activation / output-gradient matrices.
+constexpr int MEAN_COLS = 512;      // columns per chunk: 8 per lane of one wave
+constexpr int MEAN_ROWS = 1024;     // rows per block of the partial sums
+constexpr int MEAN_THREADS = 256;   // 4 waves, each taking every 4th row of a block
+
+struct MeanMat {
+    const void* X;        // rows x cols, row-major
+    float*      out;      // cols
+    int32_t     rows, cols;
+    int32_t     bf16;     // element type of X
+    int32_t     vec;      // cols % 8 == 0: vector loads of 8 columns
+    int32_t     nchunk;   // column chunks of MEAN_COLS
+    int32_t     nrb;      // row blocks of MEAN_ROWS
+    int64_t     part0;    // first partial (double) of this matrix
+};
+
+struct MeanItem {
+    int32_t mat, chunk, rb, _pad;
+};
+
 // ---------------------------------------------------------------- SM update
 // The current value of an inverse factor is its caller buffer S with one
 // pending rank-1 term applied:
@@ -143,6 +164,12 @@ struct RescaleBlock {
 
 // ---------------------------------------------------------------- launchers
 // Each returns the hipError_t of its launch.
+// a = mean of the rows of A, g = mean of the rows of Gout (Algorithm 1, the
+// rank-1 approximation lines): partial sums per (matrix, column chunk, row
+// block), then one fixed-order combine per column.
+hipError_t launch_colmean(const MeanMat* mats, const MeanItem* items, int32_t nitems,
+                          const MeanItem* chunks, int32_t nchunks, double* part, hipStream_t stream);
+
 // Streaming pass over every factor: applies the pending term in place (when
 // there is one) and, with matvec = 1, forms u_raw = P x, the row norms and the
 // per-row-block partials of the current P.

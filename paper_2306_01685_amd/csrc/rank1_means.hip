@@ -1,0 +1,124 @@
+// Rank-1 approximation vectors of Algorithm 1 (its first two lines, and the
+// "Rank-1 Approximation" paragraph): a = mean of the layer's activation rows,
+// g = mean of its output-gradient rows, i.e. the column means of the row-major
+// rows x d matrices A and Gout.
+//
+// Two grouped launches over every such matrix of the plan:
+//
+//   colmean_partial_kernel  one workgroup per (matrix, 512-column chunk,
+//                           MEAN_ROWS-row block): each thread sums its 8
+//                           columns over the block's rows (one row per wave
+//                           and step, so a wave reads 1 KB (bf16) or 2 KB
+//                           (fp32) of a row at a time) in float64, the four
+//                           waves are combined in a fixed order, and the
+//                           block's partial sums are stored.
+//   colmean_final_kernel    one thread per column: sums the row-block partials
+//                           in a fixed order and stores sum / rows as fp32.
+//
+// The stream is read-only and HBM-bound, so the float64 accumulation costs no
+// time; it makes the result the float64 mean rounded once to fp32, and the
+// fixed orders make it deterministic.
+#include "gmem.h"
+#include "mkor_internal.h"
+
+namespace mkor {
+namespace {
+
+constexpr int MT = MEAN_THREADS;   // 4 waves
+constexpr int MW = MT / 64;
+
+__device__ __forceinline__ void acc_bf16x2(double& lo, double& hi, unsigned h) {
+    lo += (double)__uint_as_float(h << 16);
+    hi += (double)__uint_as_float(h & 0xffff0000u);
+}
+
+__global__ __launch_bounds__(MT) void colmean_partial_kernel(const MeanMat* __restrict__ mats,
+                                                             const MeanItem* __restrict__ items,
+                                                             double* __restrict__ part) {
+    const MeanItem it = items[blockIdx.x];
+    const MeanMat m = mats[it.mat];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    constexpr int CPT = MEAN_COLS / 64;                // columns per thread (8)
+    const int c0 = it.chunk * MEAN_COLS + CPT * lane;  // this thread's columns
+    const int r0 = it.rb * MEAN_ROWS;
+    const int r1 = min(r0 + MEAN_ROWS, m.rows);
+    double s[CPT];
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) s[e] = 0.0;
+    if (m.vec && c0 + CPT - 1 < m.cols) {
+        if (m.bf16) {
+            // 8 bf16 = 16 bytes per lane: a wave reads 1 KB of a row at a time
+            const unsigned short* X = static_cast<const unsigned short*>(m.X) + c0;
+#pragma unroll 4
+            for (int r = r0 + wave; r < r1; r += MW) {
+                const uint4 h = gld_u4(X + (size_t)r * m.cols);
+                acc_bf16x2(s[0], s[1], h.x);
+                acc_bf16x2(s[2], s[3], h.y);
+                acc_bf16x2(s[4], s[5], h.z);
+                acc_bf16x2(s[6], s[7], h.w);
+            }
+        } else {
+            const float* X = static_cast<const float*>(m.X) + c0;
+#pragma unroll 4
+            for (int r = r0 + wave; r < r1; r += MW) {
+                const float4 v0 = gld4(X + (size_t)r * m.cols);
+                const float4 v1 = gld4(X + (size_t)r * m.cols + 4);
+                s[0] += (double)v0.x; s[1] += (double)v0.y; s[2] += (double)v0.z; s[3] += (double)v0.w;
+                s[4] += (double)v1.x; s[5] += (double)v1.y; s[6] += (double)v1.z; s[7] += (double)v1.w;
+            }
+        }
+    } else {
+        // ragged: any column count, element by element
+        for (int r = r0 + wave; r < r1; r += MW) {
+#pragma unroll
+            for (int e = 0; e < CPT; ++e) {
+                const int c = c0 + e;
+                if (c < m.cols) {
+                    const size_t off = (size_t)r * m.cols + c;
+                    s[e] += m.bf16 ? (double)__uint_as_float(
+                                         ((unsigned)gld_u16(static_cast<const unsigned short*>(m.X) + off)) << 16)
+                                   : (double)gld(static_cast<const float*>(m.X) + off);
+                }
+            }
+        }
+    }
+    __shared__ double red[MW][MEAN_COLS];
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) red[wave][CPT * lane + e] = s[e];
+    __syncthreads();
+    // partial slot of this block: part0 + (rb * nchunk + chunk) * MEAN_COLS
+    double* dst = part + m.part0 + ((size_t)it.rb * m.nchunk + it.chunk) * MEAN_COLS;
+    for (int c = t; c < MEAN_COLS; c += MT) {
+        double acc = red[0][c];
+#pragma unroll
+        for (int w = 1; w < MW; ++w) acc += red[w][c];
+        dst[c] = acc;
+    }
+}
+
+__global__ __launch_bounds__(MEAN_COLS) void colmean_final_kernel(const MeanMat* __restrict__ mats,
+                                                                  const MeanItem* __restrict__ chunks,
+                                                                  const double* __restrict__ part) {
+    const MeanItem ch = chunks[blockIdx.x];
+    const MeanMat m = mats[ch.mat];
+    const int c = ch.chunk * MEAN_COLS + threadIdx.x;
+    if (c >= m.cols) return;
+    const double* p = part + m.part0 + (size_t)ch.chunk * MEAN_COLS + threadIdx.x;
+    double acc = 0.0;
+    for (int rb = 0; rb < m.nrb; ++rb) acc += p[(size_t)rb * m.nchunk * MEAN_COLS];
+    gst(m.out + c, (float)(acc / (double)m.rows));
+}
+
+}  // namespace
+
+hipError_t launch_colmean(const MeanMat* mats, const MeanItem* items, int32_t nitems,
+                          const MeanItem* chunks, int32_t nchunks, double* part, hipStream_t stream) {
+    if (nitems <= 0) return hipSuccess;
+    hipLaunchKernelGGL(colmean_partial_kernel, dim3(nitems), dim3(MT), 0, stream, mats, items, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(colmean_final_kernel, dim3(nchunks), dim3(MEAN_COLS), 0, stream, mats, chunks, part);
+    return hipGetLastError();
+}
+
+}  // namespace mkor

@@ -11,8 +11,11 @@ import torch
 from .binding import STATS_BYTES, MkorPlan, read_stats
 
 
-def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True):
-    """One dict of device tensors per (d_in, d_out); factors start as I."""
+def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True,
+                    rows=0, act_dtype="fp32"):
+    """One dict of device tensors per (d_in, d_out); factors start as I.  With
+    rows > 0 each second-order layer also gets token-row buffers A (rows x d_in)
+    and Gout (rows x d_out), from which the library forms a and g."""
     gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
     layers = []
     for i, (d_in, d_out) in enumerate(shapes):
@@ -27,6 +30,10 @@ def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None,
             L["g"] = torch.zeros(d_out, dtype=torch.float32, device=device)
         if stats:
             L["stats"] = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=device)
+        if so and rows:
+            adt = torch.bfloat16 if act_dtype == "bf16" else torch.float32
+            L["A"] = torch.zeros((rows, d_in), dtype=adt, device=device)
+            L["Gout"] = torch.zeros((rows, d_out), dtype=adt, device=device)
         layers.append(L)
     return layers
 
@@ -45,6 +52,17 @@ def set_inputs(L, a=None, g=None, G=None):
         _put(L["g"], g)
     if G is not None:
         _put(L["G"], G)
+
+
+def set_rows(L, A, Gout):
+    """Copies host token rows into the layer's A and Gout (given as float32; for
+    bf16 buffers the values must already be bf16-representable)."""
+    _put(L["A"], A)
+    _put(L["Gout"], Gout)
+
+
+def get_means(L):
+    return L["a"].cpu().numpy(), L["g"].cpu().numpy()
 
 
 def set_factors(L, Linv, Rinv):

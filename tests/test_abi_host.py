@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 2
+    assert lib.mkor_abi_version() == 3
 
 
 def test_status_strings(lib):
@@ -46,7 +46,7 @@ def test_status_strings(lib):
 
 def test_struct_sizes():
     assert ctypes.sizeof(B.mkor_params) == 28
-    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8
+    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8
     assert M.STATS_BYTES == 48
 
 
@@ -90,12 +90,16 @@ class Fake:
         return p
 
 
-def layer(fk, d_in, d_out, so=1, dt=0, stats=False):
+def layer(fk, d_in, d_out, so=1, dt=0, stats=False, rows=0, adt=0):
     esz = 2 if dt == 1 else 4
+    aesz = 2 if adt == 1 else 4
     return dict(d_in=d_in, d_out=d_out, second_order=so, grad_dtype=dt,
                 Linv=fk.alloc(d_in * d_in * 4), Rinv=fk.alloc(d_out * d_out * 4),
                 a=fk.alloc(d_in * 4), g=fk.alloc(d_out * 4), G=fk.alloc(d_in * d_out * esz),
-                dW=fk.alloc(d_in * d_out * 4), stats=fk.alloc(48) if stats else None)
+                dW=fk.alloc(d_in * d_out * 4), stats=fk.alloc(48) if stats else None,
+                rows=rows, act_dtype=adt,
+                A=fk.alloc(rows * d_in * aesz) if rows else None,
+                Gout=fk.alloc(rows * d_out * aesz) if rows else None)
 
 
 def ws_status(descs):
@@ -142,6 +146,9 @@ def test_empty_list(lib):
     (lambda L: L.update(dW=L["G"]), M.MKOR_INVALID_ARG),           # output aliases input
     (lambda L: L.update(Rinv=L["Linv"] + 256), M.MKOR_INVALID_ARG),  # factors overlap
     (lambda L: L.update(stats=L["dW"] + 64), M.MKOR_INVALID_ARG),  # stats inside dW
+    (lambda L: L.update(rows=-1), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(rows=M.MAX_ROWS + 1), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(rows=8), M.MKOR_INVALID_ARG),              # rows > 0 without A / Gout
 ])
 def test_layer_rejected(lib, mutate, status):
     fk = Fake()
@@ -164,6 +171,38 @@ def test_cross_layer_aliasing(lib):
     b["a"] = a["a"]                        # read-only inputs may be shared
     b["G"] = a["G"]
     assert ws_status([a, b])[0] == M.MKOR_OK
+
+
+def test_rank1_rows_validation(lib):
+    fk = Fake()
+    L = layer(fk, 64, 96, rows=128, adt=1)
+    assert ws_status([L])[0] == M.MKOR_OK
+    L = layer(fk, 64, 96, rows=128, adt=1)
+    L["act_dtype"] = 7
+    assert ws_status([L])[0] == M.MKOR_UNSUPPORTED
+    L = layer(fk, 64, 96, rows=128)
+    L["A"] += 8                                  # misaligned
+    assert ws_status([L])[0] == M.MKOR_INVALID_ARG
+    L = layer(fk, 64, 96, rows=128)
+    L["Gout"] = L["A"]                           # inputs may be shared (read-only)
+    assert ws_status([L])[0] == M.MKOR_OK
+    L = layer(fk, 64, 96, rows=128)
+    L["a"] = L["A"]                              # written mean over an input
+    assert ws_status([L])[0] == M.MKOR_INVALID_ARG
+    a, b = layer(fk, 64, 64), layer(fk, 64, 64, rows=16)
+    b["a"] = a["a"]                              # a is written for b: no sharing
+    assert ws_status([a, b])[0] == M.MKOR_INVALID_ARG
+    L = layer(fk, 64, 96, so=0, rows=16)
+    assert ws_status([L])[0] == M.MKOR_INVALID_ARG   # rows only for second-order layers
+
+
+def test_workspace_grows_with_rows(lib):
+    fk = Fake()
+    base = ws_status([layer(fk, 1024, 4096)])[1]
+    with_rows = ws_status([layer(fk, 1024, 4096, rows=16384, adt=1)])[1]
+    # float64 partial sums: (1024 + 4096) / 512 chunks x 16 row blocks x 512
+    assert with_rows - base >= 8 * (1024 + 4096) * 16
+    assert with_rows - base < 8 * (1024 + 4096) * 16 + (1 << 20)
 
 
 def test_first_order_layer_needs_no_factors(lib):

@@ -308,3 +308,59 @@ def test_guard_nonfinite():
     p.guard_nonfinite = False
     Li, Ri, dW, st = O.layer_step(np.eye(3), np.eye(3), a, np.ones(3), G, p)
     assert np.isnan(Li).any()
+
+
+# ------------------------------------------------------------------ rank-1 means
+def test_rank1_means_exact_rationals():
+    """Integer rows: the mean is computed exactly (Fraction arithmetic by hand)."""
+    rows = np.array([[3, -1, 7], [5, 2, -7], [-2, 2, 0], [6, 1, 4]], dtype=np.float64)
+    want = [Fraction(3 + 5 - 2 + 6, 4), Fraction(-1 + 2 + 2 + 1, 4), Fraction(7 - 7 + 0 + 4, 4)]
+    got = O.rank1_means(rows)
+    assert [Fraction(x) for x in got] == want
+
+
+def test_rank1_means_identical_rows_make_the_approximation_exact():
+    """Algorithm 1 approximates the covariance (1/b) A^T A by a a^T; for b identical
+    samples the two are equal, and the mean is the sample itself."""
+    rng = np.random.default_rng(3)
+    x = rng.integers(-1000, 1000, size=9) / 64.0   # few mantissa bits: every partial sum is exact
+    rows = np.tile(x, (16, 1))
+    a = O.rank1_means(rows)
+    np.testing.assert_array_equal(a, x)
+    cov = rows.T @ rows / rows.shape[0]
+    np.testing.assert_allclose(np.outer(a, a), cov, rtol=1e-14, atol=1e-14)
+
+
+def test_rank1_means_invariances():
+    rng = np.random.default_rng(4)
+    R = rng.standard_normal((37, 11))
+    a = O.rank1_means(R)
+    # duplicating every sample leaves the mean unchanged; row order does not matter
+    np.testing.assert_allclose(O.rank1_means(np.vstack([R, R])), a, rtol=1e-15, atol=1e-15)
+    np.testing.assert_allclose(O.rank1_means(R[::-1]), a, rtol=1e-14, atol=1e-15)
+    # one sample: the mean is that sample; a shifted copy shifts the mean
+    np.testing.assert_array_equal(O.rank1_means(R[:1]), R[0])
+    np.testing.assert_allclose(O.rank1_means(R + 2.5), a + 2.5, rtol=1e-14, atol=1e-14)
+    # samples that cancel in adjacent pairs have mean zero (each pair sums exactly)
+    pairs = np.empty((2 * R.shape[0], R.shape[1]))
+    pairs[0::2], pairs[1::2] = R, -R
+    np.testing.assert_array_equal(O.rank1_means(pairs), np.zeros(11))
+
+
+def test_layer_step_rows_uses_row_means():
+    rng = np.random.default_rng(5)
+    d_in, d_out, b = 6, 4, 10
+    A = rng.standard_normal((b, d_in))
+    Go = rng.standard_normal((b, d_out)) * 1e-3
+    G = rng.standard_normal((d_in, d_out)) * 1e-3
+    p = O.Params(gamma=0.9, eps=math.inf)
+    Li, Ri, dW, st, a, g = O.layer_step_rows(np.eye(d_in), np.eye(d_out), A, Go, G, p)
+    a2 = A.sum(axis=0) / b
+    g2 = Go.sum(axis=0) / b
+    np.testing.assert_allclose(a, a2, rtol=1e-14)
+    np.testing.assert_allclose(g, g2, rtol=1e-14)
+    Lj, Rj, dWj, _ = O.layer_step(np.eye(d_in), np.eye(d_out), a2, g2, G, p)
+    np.testing.assert_allclose(Li, Lj, rtol=1e-12)
+    np.testing.assert_allclose(dW, dWj, rtol=1e-12)
+    with pytest.raises(ValueError):
+        O.rank1_means(np.zeros((0, 3)))

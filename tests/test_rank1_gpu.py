@@ -1,0 +1,149 @@
+"""GPU parity of the rank-1 means (Algorithm 1, its first two lines) and of a
+step driven by token rows, through the C ABI, against the float64 oracle.
+
+The library sums in float64 and rounds once, so a and g must equal the float64
+mean rounded to fp32 up to float64 summation-order effects (checked elementwise
+at 2 fp32 ulps); steps driven by rows meet the usual 1e-4 / 1e-3 bars.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from paper_2306_01685_amd import Params, harness as H
+from tests.parity import TOL_FREE, TOL_STEP, oparams, rel
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(1, 1), (3, 5), (64, 100), (100, 37), (256, 257), (1000, 64)]
+ROWS = [1, 3, 1000, 1025, 2048]
+
+
+def _mean_check(got, rows):
+    want = O.rank1_means(rows).astype(np.float32)
+    np.testing.assert_array_max_ulp(got, want, maxulp=2)
+
+
+@pytest.mark.parametrize("dt", ["fp32", "bf16"])
+@pytest.mark.parametrize("rows", ROWS)
+def test_means_ragged(dt, rows):
+    w = W.custom(SHAPES, rows=rows, cid=300 + rows)
+    layers = H.allocate_layers(SHAPES, "fp32", rows=rows, act_dtype=dt)
+    host = []
+    for i, L in enumerate(layers):
+        A, Go = W.token_rows(w, i, 0, dtype=dt)
+        H.set_rows(L, A, Go)
+        H.set_inputs(L, G=W.gradient(w, i, 0))
+        host.append((A, Go))
+    plan = H.make_plan(layers)
+    plan.run_stage(Params(), 0)   # the means stage alone
+    torch.cuda.synchronize()
+    for L, (A, Go) in zip(layers, host):
+        a, g = H.get_means(L)
+        _mean_check(a, A)
+        _mean_check(g, Go)
+
+
+def test_step_from_rows_free_running():
+    """cfg1 shape (64 x 64, 32 token rows) plus ragged layers, 20 steps, both
+    sides forming the means from the same rows."""
+    shapes = [(64, 64), (37, 100), (128, 256)]
+    w = W.custom(shapes, grad_dtype="bf16", rows=32, cid=333, gamma=0.9)
+    p = Params(gamma=0.9, eps=4.0)
+    op = oparams(p)
+    layers = H.allocate_layers(shapes, "bf16", rows=32, act_dtype="bf16")
+    plan = H.make_plan(layers)
+    state = [(np.eye(i), np.eye(o)) for i, o in shapes]
+    fired = 0
+    for t in range(20):
+        step_in = []
+        for i, L in enumerate(layers):
+            A, Go = W.token_rows(w, i, t, dtype="bf16")
+            G = W.gradient(w, i, t)
+            H.set_rows(L, A, Go)
+            H.set_inputs(L, G=G)
+            step_in.append((A, Go, G))
+        plan.step(p)
+        torch.cuda.synchronize()
+        for i, L in enumerate(layers):
+            A, Go, G = step_in[i]
+            st = H.get_stats(L)
+            Lp, Rp = state[i]
+            Li, Ri, dW, ost, a, g = O.layer_step_rows(Lp, Rp, A, Go, G, op)
+            fired += int(ost.L.stab) + int(ost.R.stab)
+            assert bool(ost.L.stab) == bool(st["stab_L"]) and bool(ost.R.stab) == bool(st["stab_R"])
+            state[i] = (Li, Ri)
+            tol = TOL_STEP if t == 0 else TOL_FREE
+            assert rel(H.get_dW(L), dW) <= tol, (i, t)
+            ga, gg = H.get_means(L)
+            np.testing.assert_array_max_ulp(ga, a.astype(np.float32), maxulp=2)
+            np.testing.assert_array_max_ulp(gg, g.astype(np.float32), maxulp=2)
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    for i, L in enumerate(layers):
+        Lg, Rg = H.get_factors(L)
+        assert rel(Lg, state[i][0]) <= TOL_FREE and rel(Rg, state[i][1]) <= TOL_FREE
+    assert fired > 0
+
+
+def test_update_every_f_steps():
+    """Update frequency f = 3 (the paper updates every 10 iterations): mkor_step
+    on update steps, mkor_precondition (stale factors) on the others."""
+    shapes = [(64, 96), (100, 37)]
+    w = W.custom(shapes, rows=16, cid=350)
+    p = Params(gamma=0.9, eps=math.inf)
+    op = oparams(p)
+    layers = H.allocate_layers(shapes, "fp32")
+    plan = H.make_plan(layers)
+    state = [(np.eye(i), np.eye(o)) for i, o in shapes]
+    for t in range(9):
+        update = t % 3 == 0
+        ins = []
+        for i, L in enumerate(layers):
+            a, g = W.rank1_vectors(w, i, t)
+            G = W.gradient(w, i, t)
+            H.set_inputs(L, a, g, G)
+            ins.append((a, g, G))
+        if update:
+            plan.step(p)
+        else:
+            plan.precondition(p)
+        torch.cuda.synchronize()
+        for i, L in enumerate(layers):
+            a, g, G = ins[i]
+            Li, Ri, dW, _ = O.layer_step(*state[i], a, g, G, op, update=update)
+            state[i] = (Li, Ri)
+            assert rel(H.get_dW(L), dW) <= (TOL_STEP if t == 0 else TOL_FREE), (i, t)
+
+
+@pytest.mark.slow
+def test_bert_large_means_from_16384_bf16_rows():
+    """Full BERT-Large layer set with 16384 bf16 token rows per layer (14.5 GB of
+    rows): means of sampled layers against the oracle, one full step."""
+    w = W.CONFIGS[3]
+    sample = [0, 4, 5]
+    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=w.rows, act_dtype="bf16")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(77)
+    host = {}
+    for i, L in enumerate(layers):
+        if i in sample:
+            A, Go = W.token_rows(w, i, 0, dtype="bf16")
+            H.set_rows(L, A, Go)
+            host[i] = (A, Go)
+        else:
+            for k in ("A", "Gout"):
+                tmp = torch.empty(L[k].shape, dtype=torch.float32, device="cuda")
+                tmp.normal_(0.0, 1.0, generator=gen)
+                L[k].copy_(tmp)
+                del tmp
+    plan = H.make_plan(layers)
+    plan.step(Params(gamma=w.gamma))
+    torch.cuda.synchronize()
+    for i, (A, Go) in host.items():
+        a, g = H.get_means(layers[i])
+        _mean_check(a, A)
+        _mean_check(g, Go)

@@ -66,3 +66,17 @@ def test_perturbed_init_spd_symmetric():
     np.testing.assert_array_equal(L, L.T)
     np.linalg.cholesky(L.astype(np.float64))
     assert abs(np.trace(L) / 96 - 1.0 - 0.01 * 64 / 96) < 0.01
+
+
+def test_token_rows_seeded_and_shaped():
+    w = W.CONFIGS[1]
+    A, Go = W.token_rows(w, 0, 3)
+    assert A.shape == (32, 64) and Go.shape == (32, 64) and A.dtype == np.float32
+    A2, Go2 = W.token_rows(w, 0, 3)
+    np.testing.assert_array_equal(A, A2)
+    np.testing.assert_array_equal(Go, Go2)
+    assert not np.array_equal(A, W.token_rows(w, 0, 4)[0])
+    Ab, Gb = W.token_rows(w, 0, 3, rows=7, dtype="bf16")
+    assert Ab.shape == (7, 64)
+    np.testing.assert_array_equal(Ab, W.round_to_bf16(Ab))
+    assert 0.5 < float(A.std()) < 1.5 and float(Go.std()) < 1e-2

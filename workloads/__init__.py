@@ -7,8 +7,9 @@ that both sides see exactly the same bits.
 
 Seeds: every tensor has its own ``numpy.random.SeedSequence`` with entropy
 230601685 and spawn key (config, layer, step, kind), kind 0 = a, 1 = g,
-2 = G, 3 = Q of the left initial factor, 4 = Q of the right initial factor, so
-any subset can be regenerated on its own.
+2 = G, 3 = Q of the left initial factor, 4 = Q of the right initial factor,
+5 = activation token rows, 6 = output-gradient token rows, so any subset can be
+regenerated on its own.
 
 The layer sets stand in for the paper's BERT-Large pre-training and fine-tuning
 runs (Wikipedia/BookCorpus, SQuAD, GLUE), which are not available here: only
@@ -24,6 +25,7 @@ import numpy as np
 ENTROPY = 2306_01685
 
 KIND_A, KIND_G, KIND_GRAD, KIND_QL, KIND_QR = 0, 1, 2, 3, 4
+KIND_AROWS, KIND_GROWS = 5, 6
 
 
 @dataclass(frozen=True)
@@ -160,6 +162,25 @@ def initial_factors(w: Workload, layer: int):
         P = 0.5 * (P + P.T)
         out.append(P.astype(np.float32))
     return out[0], out[1]
+
+
+def token_rows(w: Workload, layer: int, step: int, rows: int = None, dtype: str = "fp32"):
+    """The token rows a layer's rank-1 means are formed from: activations
+    (rows x d_in, N(0, act_std^2) or Student-t(4) scaled by act_std) and output
+    gradients (rows x d_out, N(0, grad_row_std^2)), float32; for dtype "bf16"
+    the values are rounded to bf16 (the storage format of such rows)."""
+    d_in, d_out = w.shapes[layer]
+    n = w.rows if rows is None else rows
+    ga, gg = rng(w.cid, layer, step, KIND_AROWS), rng(w.cid, layer, step, KIND_GROWS)
+    if w.act_dist == "student_t4":
+        A = ga.standard_t(4.0, size=(n, d_in)).astype(np.float32)
+    else:
+        A = ga.standard_normal((n, d_in), dtype=np.float32)
+    A *= np.float32(w.act_std)
+    Go = gg.standard_normal((n, d_out), dtype=np.float32) * np.float32(w.grad_row_std)
+    if dtype == "bf16":
+        A, Go = round_to_bf16(A), round_to_bf16(Go)
+    return A, Go
 
 
 def custom(shapes, grad_dtype="fp32", gamma=0.9, rows=32, cid=100, steps=1, **kw) -> Workload:
