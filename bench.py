@@ -12,7 +12,10 @@ HBM before the timed region starts.
 
 Prints one JSON line: layer-updates/s, per-kernel times measured with HIP
 events on the launch stream, the roofline of the dominant kernel, and the
-float64 CPU oracle timed on a bounded sample of the same workload.
+float64 CPU oracle timed on a bounded sample of the same workload.  The same
+workload with half-precision (bf16) factors is measured beside it
+("half_factors"; skip with --no-half, or time it as the main line with
+--factor-dtype bf16).
 """
 from __future__ import annotations
 
@@ -30,6 +33,7 @@ sys.path.insert(0, ROOT)
 METRIC = "layer-updates/sec (SM update + precondition), BERT-Large set; % HBM / % MFMA peak"
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 FP32_MFMA_PEAK_TF = 157.3   # MI355X dense fp32 matrix
+BF16_MFMA_PEAK_TF = 2500.0  # MI355X dense bf16 matrix
 
 
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic_bert_large_144.md")
@@ -86,6 +90,11 @@ def parse():
                     help="copy: time a plain device-to-device copy of --copy-mib MiB (the reference "
                          "kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures)")
     ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--factor-dtype", choices=["fp32", "bf16"], default="fp32",
+                    help="storage type of the inverse factors of the timed run (bf16: the "
+                         "half-precision factors, bf16 MFMA preconditioning)")
+    ap.add_argument("--no-half", action="store_true",
+                    help="skip the extra measurement with bf16 factors")
     return ap.parse_args()
 
 
@@ -112,12 +121,12 @@ def copy_reference(args):
           flush=True)
 
 
-def workload_desc(w):
+def workload_desc(w, factor_dtype="fp32"):
     counts = {}
     for s in w.block_shapes:
         counts[s] = counts.get(s, 0) + 1
     inner = ", ".join(f"{c}x {i}x{o}" if c > 1 else f"{i}x{o}" for (i, o), c in counts.items())
-    return f"{w.name}: {w.blocks} x {{{inner}}}, fp32 factors, {w.grad_dtype} G"
+    return f"{w.name}: {w.blocks} x {{{inner}}}, {factor_dtype} factors, {w.grad_dtype} G"
 
 
 def fill_rows(layers, seed=2307):
@@ -192,30 +201,19 @@ def cpu_baseline(w, budget_s):
                        f"float64 steps in {el:.1f} s; host has {len(os.sched_getaffinity(0))} cpus")
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
-              "(the hot path runs on a single MI355X)", file=sys.stderr)
-        sys.exit(2)
-
-    if args.mode == "copy":
-        copy_reference(args)
-        return
-
+def measure(w, args, factor_dtype):
+    """Times mkor_step over the workload with the given factor storage type.
+    Returns (ms_per_step, kernels, roofline, schedule)."""
     import torch
 
-    import workloads as W
     from paper_2306_01685_amd import NUM_STAGES, STAGE_NAMES, Params, harness as H
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    w = W.CONFIGS[args.config]
-    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=args.rows, act_dtype="bf16")
+    half = factor_dtype == "bf16"
+    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=args.rows, act_dtype="bf16",
+                               factor_dtype=factor_dtype)
     if w.init != "identity":
         for i, L in enumerate(layers):
-            H.set_factors(L, *W.initial_factors(w, i))
+            H.set_factors(L, *initial_factors_stored(w, i, half))
     fill_inputs(layers, w)
     if args.rows:
         fill_rows(layers)
@@ -235,11 +233,12 @@ def main():
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / args.steps
-    value = w.n_layers / (ms_step / 1e3)
 
     # per-kernel times: the same steps launched stage by stage with HIP events
     # between consecutive kernels on the launch stream
-    kernels = {}
+    kernels, roof = {}, None
+    esz = 2 if half else 4                                  # factor element bytes
+    mfma_peak = BF16_MFMA_PEAK_TF if half else FP32_MFMA_PEAK_TF
     if not args.no_stage_timing:
         acc = [0.0] * NUM_STAGES
         for _ in range(args.steps):
@@ -253,21 +252,22 @@ def main():
                 acc[s] += ev[s].elapsed_time(ev[s + 1])
         ms = [a / args.steps for a in acc]
         sq = w.factor_elems
-        f1 = sum(2 * i * o * i for i, o in w.shapes)
-        f2 = sum(2 * i * o * o for i, o in w.shapes)
+        # stage 1 contracts over d_in (fp32: Linv G) or d_out (bf16: G Rinv)
+        f1 = sum(2 * i * o * (o if half else i) for i, o in w.shapes)
+        f2 = sum(2 * i * o * (i if half else o) for i, o in w.shapes)
         nel = sum(i * o for i, o in w.shapes)
         gb = 1e-9
-        gbytes_G = nel * (2 if w.grad_dtype == "bf16" else 4)
         sd = sum(i + o for i, o in w.shapes)
         means_ms, ms = ms[0], ms[1:]   # stage 0: rank-1 means (no work when a and g are given)
+        g1, g2 = ("gemm_gr", "gemm_ly") if half else ("gemm_xt", "gemm_dw")
         kernels = {
             # steady state: every factor has a pending term, so the pass reads
             # and writes each element once
-            "sm_pass": dict(ms=ms[0], alg_bytes=8 * sq, gbs=8 * sq * gb / (ms[0] / 1e3)),
+            "sm_pass": dict(ms=ms[0], alg_bytes=2 * esz * sq, gbs=2 * esz * sq * gb / (ms[0] / 1e3)),
             # partials, u_raw and x read, w written: O(sum d)
             "sm_finalize": dict(ms=ms[1], alg_bytes=12 * sd, gbs=12 * sd * gb / (ms[1] / 1e3)),
-            "gemm_xt": dict(ms=ms[2], flops=f1, tflops=f1 / (ms[2] / 1e3) / 1e12),
-            "gemm_dw": dict(ms=ms[3], flops=f2, tflops=f2 / (ms[3] / 1e3) / 1e12),
+            g1: dict(ms=ms[2], flops=f1, tflops=f1 / (ms[2] / 1e3) / 1e12),
+            g2: dict(ms=ms[3], flops=f2, tflops=f2 / (ms[3] / 1e3) / 1e12),
             "rescale": dict(ms=ms[4], alg_bytes=8 * nel, gbs=8 * nel * gb / (ms[4] / 1e3)),
         }
         if args.rows:
@@ -276,23 +276,24 @@ def main():
                                     frac_hbm=mb * gb / (means_ms / 1e3) / HBM_PEAK_GBS,
                                     rows=args.rows)
         sm_ms = ms[0] + ms[1]
-        kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=8 * sq, gbs=8 * sq * gb / (sm_ms / 1e3),
-                                   frac_hbm=8 * sq * gb / (sm_ms / 1e3) / HBM_PEAK_GBS)
+        kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=2 * esz * sq, gbs=2 * esz * sq * gb / (sm_ms / 1e3),
+                                   frac_hbm=2 * esz * sq * gb / (sm_ms / 1e3) / HBM_PEAK_GBS)
         pre_ms = ms[2] + ms[3]
         kernels["gemm_total"] = dict(ms=pre_ms, flops=f1 + f2,
                                      tflops=(f1 + f2) / (pre_ms / 1e3) / 1e12,
-                                     frac_mfma=(f1 + f2) / (pre_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TF)
+                                     frac_mfma=(f1 + f2) / (pre_ms / 1e3) / 1e12 / mfma_peak)
         for k in ("sm_pass", "sm_finalize", "rescale"):
             kernels[k]["frac_hbm"] = kernels[k]["gbs"] / HBM_PEAK_GBS
-        for k in ("gemm_xt", "gemm_dw"):
-            kernels[k]["frac_mfma"] = kernels[k]["tflops"] / FP32_MFMA_PEAK_TF
+        for k in (g1, g2):
+            kernels[k]["frac_mfma"] = kernels[k]["tflops"] / mfma_peak
+        names = ["sm_pass", "sm_finalize", g1, g2, "rescale"]
         dom = max(range(NUM_STAGES - 1), key=lambda s: ms[s])
-        name = STAGE_NAMES[dom + 1]
+        name = names[dom]
         k = kernels[name]
-        traffic = profiled_traffic(name, args.config)
+        traffic = None if half else profiled_traffic(name, args.config)
         if "flops" in k:
-            roof = dict(kernel=name, bound="mfma", achieved=k["tflops"], peak=FP32_MFMA_PEAK_TF,
-                        unit="TFLOP/s", frac=k["tflops"] / FP32_MFMA_PEAK_TF,
+            roof = dict(kernel=name, bound="mfma", achieved=k["tflops"], peak=mfma_peak,
+                        unit="TFLOP/s", frac=k["tflops"] / mfma_peak,
                         traffic=None if traffic is None else traffic["total_bytes"],
                         per_launch=f"{k['flops']:.4e} flop (sum of 2*M*N*K over the layers)")
         else:
@@ -303,13 +304,11 @@ def main():
         roof["traffic_detail"] = traffic
         # the SM update is the benchmark spec's other roofline: report it beside
         k = kernels["sm_pass"]
-        t = profiled_traffic("sm_pass", args.config)
+        t = None if half else profiled_traffic("sm_pass", args.config)
         roof["sm_update"] = dict(kernel="sm_pass", bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS,
                                  unit="GB/s", frac=k["gbs"] / HBM_PEAK_GBS,
                                  traffic=None if t is None else t["total_bytes"],
                                  per_launch=f"{k['alg_bytes']:.4e} B")
-    else:
-        roof = None
 
     # The paper's schedule: factors updated every 10 iterations (stale factors
     # precondition the other nine); per-step rate averaged over whole cycles.
@@ -328,23 +327,65 @@ def main():
         f_ms = e0.elapsed_time(e1) / (10 * cycles)
         schedule = dict(update_every=10, steps=10 * cycles, ms_per_step=f_ms,
                         value=w.n_layers / (f_ms / 1e3), unit="layer-updates/s")
+    del plan, layers
+    torch.cuda.empty_cache()
+    return ms_step, kernels, roof, schedule
+
+
+def initial_factors_stored(w, i, half):
+    """The workload's initial factors, rounded to bf16 for bf16 storage."""
+    import workloads as W
+    L0, R0 = W.initial_factors(w, i)
+    if half:
+        L0, R0 = W.round_to_bf16(L0), W.round_to_bf16(R0)
+    return L0, R0
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the hot path runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    if args.mode == "copy":
+        copy_reference(args)
+        return
+
+    import torch
+
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = W.CONFIGS[args.config]
+    ms_step, kernels, roof, schedule = measure(w, args, args.factor_dtype)
+    value = w.n_layers / (ms_step / 1e3)
+    half = None
+    if args.factor_dtype == "fp32" and not args.no_half:
+        # the same workload with half-precision (bf16) factors, reported beside
+        h_ms, h_k, h_roof, h_sched = measure(w, args, "bf16")
+        half = dict(value=w.n_layers / (h_ms / 1e3), unit="layer-updates/s", ms_per_step=h_ms,
+                    dtype="bf16 factors, bf16 MFMA (fp32 accumulation)", roofline=h_roof,
+                    schedule_f10=h_sched, kernels=h_k)
 
     out = {
         "metric": METRIC, "value": value, "unit": "layer-updates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if args.factor_dtype == "fp32" else "bf16",
         "data": "synthetic (seeded; layer shapes only)",
-        "config": {"workload": workload_desc(w), "n_layers": w.n_layers,
+        "config": {"workload": workload_desc(w, args.factor_dtype), "n_layers": w.n_layers,
                    "factor_elems": w.factor_elems, "precond_flops": w.precond_flops,
                    "gamma": w.gamma, "zeta": 0.5, "eps": args.eps, "grad_dtype": w.grad_dtype,
-                   "token_rows": args.rows},
+                   "factor_dtype": args.factor_dtype, "token_rows": args.rows},
         "roofline": roof,
         "schedule_f10": schedule,
         "kernels": kernels,
+        "half_factors": half,
         "device": torch.cuda.get_device_name(0),
     }
-    del plan, layers
-    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)

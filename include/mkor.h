@@ -52,6 +52,13 @@
  * mkor_sync_factors writes the current factors into them.  Call it before
  * reading, saving or modifying Linv / Rinv, and before mkor_plan_destroy if
  * the factors are to be kept.  A new plan starts with no pending term.
+ * With bf16 factors (factor_dtype) S is the bf16-rounded factor: writing a
+ * pending term into S rounds it to bf16, and the next update's norm and
+ * matrix-vector product use the rounded values, while the preconditioning
+ * multiplies with the updated factor before that rounding (c1 S + c2 I +
+ * sgn w w^T, evaluated in fp32).  So with bf16 factors a mkor_sync_factors
+ * between an update and a preconditioning changes the preconditioning: it
+ * then uses the rounded factor.
  *
  * Memory and ownership.
  *   - Every buffer named in mkor_layer, and the workspace, is device memory
@@ -86,7 +93,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 3
+#define MKOR_ABI_VERSION 4
 
 /* status codes */
 #define MKOR_OK                   0
@@ -134,8 +141,8 @@ typedef struct mkor_layer {
     int32_t      d_in, d_out;   /* 1 .. MKOR_MAX_DIM */
     int32_t      second_order;  /* 1: MKOR branch; 0: dW = G (first-order layer) */
     int32_t      grad_dtype;    /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (element type of G) */
-    float*       Linv;          /* d_in x d_in, in/out (unused if second_order = 0) */
-    float*       Rinv;          /* d_out x d_out, in/out (unused if second_order = 0) */
+    void*        Linv;          /* d_in x d_in, in/out, factor_dtype elements (unused if second_order = 0) */
+    void*        Rinv;          /* d_out x d_out, in/out, factor_dtype elements (unused if second_order = 0) */
     float*       a;             /* d_in, mean activation: input, or output when rows > 0 */
     float*       g;             /* d_out, mean output gradient: input, or output when rows > 0
                                    (a and g unused if second_order = 0) */
@@ -150,6 +157,15 @@ typedef struct mkor_layer {
     int32_t      act_dtype;     /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (elements of A and Gout) */
     const void*  A;             /* rows x d_in activations, row-major (rows > 0) */
     const void*  Gout;          /* rows x d_out output gradients, row-major (rows > 0) */
+    /* Element type of Linv and Rinv.  MKOR_DTYPE_F32: fp32 factors, fp32 MFMA
+     * preconditioning (the default).  MKOR_DTYPE_BF16: half-precision factors
+     * (the paper's half-precision MKOR): the factors are stored in bf16, each
+     * update is computed in fp32 from the stored values and rounded to bf16 (to
+     * nearest, ties to even), and the preconditioning runs on bf16 MFMA with fp32
+     * accumulation as dW_hat = Linv (G Rinv), G and the intermediate G Rinv
+     * entering it in bf16.  Needs d_in and d_out to be multiples of 64. */
+    int32_t      factor_dtype;
+    int32_t      reserved;      /* must be 0 */
 } mkor_layer;
 
 /* Per-layer observability record, written on the device when

@@ -34,7 +34,7 @@ DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class mkor_params(ctypes.Structure):
@@ -50,7 +50,8 @@ class mkor_layer(ctypes.Structure):
                 ("a", ctypes.c_void_p), ("g", ctypes.c_void_p),
                 ("G", ctypes.c_void_p), ("dW", ctypes.c_void_p), ("stats", ctypes.c_void_p),
                 ("rows", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
-                ("A", ctypes.c_void_p), ("Gout", ctypes.c_void_p)]
+                ("A", ctypes.c_void_p), ("Gout", ctypes.c_void_p),
+                ("factor_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class mkor_layer_stats(ctypes.Structure):
@@ -164,7 +165,8 @@ def make_layer_array(descs):
                             d.get("Linv") or None, d.get("Rinv") or None, d.get("a") or None,
                             d.get("g") or None, d.get("G") or None, d.get("dW") or None,
                             d.get("stats") or None, d.get("rows", 0), d.get("act_dtype", 0),
-                            d.get("A") or None, d.get("Gout") or None)
+                            d.get("A") or None, d.get("Gout") or None, d.get("factor_dtype", 0),
+                            d.get("reserved", 0))
     return arr
 
 
@@ -188,8 +190,8 @@ def _stream_handle(stream):
 class MkorPlan:
     """A plan over a grouped list of layers, holding torch device tensors.
 
-    Each layer is a dict with d_in, d_out and tensors Linv, Rinv (fp32,
-    symmetric), a, g (fp32 vectors), G (fp32 or bf16, d_in x d_out), dW (fp32,
+    Each layer is a dict with d_in, d_out and tensors Linv, Rinv (symmetric;
+    both fp32, or both bf16 for half-precision factors), a, g (fp32 vectors), G (fp32 or bf16, d_in x d_out), dW (fp32,
     d_in x d_out), optional second_order (default True), optional stats
     (a uint8 device tensor of STATS_BYTES bytes), and optionally token rows A
     (rows x d_in) and Gout (rows x d_out), fp32 or bf16, from which each step
@@ -218,6 +220,13 @@ class MkorPlan:
                 t = L.get(k)
                 if t is not None and not t.is_contiguous():
                     raise ValueError(f"{k} must be contiguous")
+            fdt = DTYPE_F32
+            if so:
+                dts = {L["Linv"].dtype, L["Rinv"].dtype}
+                if dts == {torch.bfloat16}:
+                    fdt = DTYPE_BF16
+                elif dts != {torch.float32}:
+                    raise TypeError("Linv and Rinv must both be fp32 or both bf16")
             A = L.get("A")
             rows, adt = 0, DTYPE_F32
             if A is not None:
@@ -229,7 +238,7 @@ class MkorPlan:
                               grad_dtype=gdt, Linv=_ptr(L.get("Linv")), Rinv=_ptr(L.get("Rinv")),
                               a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
                               stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
-                              Gout=_ptr(L.get("Gout"))))
+                              Gout=_ptr(L.get("Gout")), factor_dtype=fdt))
         self._arr = make_layer_array(descs)
         n = len(descs)
         size = ctypes.c_size_t(0)

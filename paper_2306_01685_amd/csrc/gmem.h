@@ -70,6 +70,22 @@ __device__ __forceinline__ float gld_off(const void* base, unsigned byte_off) {
 
 __device__ __forceinline__ void gst(float* p, float v) { *(MKOR_GLOBAL float*)p = v; }
 
+__device__ __forceinline__ void gst_u2(void* p, uint2 v) {
+    mk_u2 w;
+    w.x = v.x; w.y = v.y;
+    *(MKOR_GLOBAL mk_u2*)p = w;
+}
+
+// bf16 <-> fp32.  f2bf rounds to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ float bf2f(unsigned short h) { return __uint_as_float(((unsigned)h) << 16); }
+
+__device__ __forceinline__ unsigned short f2bf(float f) {
+    unsigned u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (unsigned short)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (unsigned short)(u >> 16);
+}
+
 __device__ __forceinline__ void gst4(float* p, const float4& v) {
     mk_f4 w;
     w.x = v.x; w.y = v.y; w.z = v.z; w.w = v.w;

@@ -56,6 +56,13 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
             return fail(MKOR_INVALID_ARG, "layer %d: second_order = %d is not 0 or 1", i, L.second_order);
         if (L.grad_dtype != MKOR_DTYPE_F32 && L.grad_dtype != MKOR_DTYPE_BF16)
             return fail(MKOR_UNSUPPORTED, "layer %d: grad_dtype = %d is not supported", i, L.grad_dtype);
+        if (L.factor_dtype != MKOR_DTYPE_F32 && L.factor_dtype != MKOR_DTYPE_BF16)
+            return fail(MKOR_UNSUPPORTED, "layer %d: factor_dtype = %d is not supported", i, L.factor_dtype);
+        if (L.reserved != 0) return fail(MKOR_INVALID_ARG, "layer %d: reserved = %d must be 0", i, L.reserved);
+        const bool half = L.second_order == 1 && L.factor_dtype == MKOR_DTYPE_BF16;
+        if (half && (L.d_in % 64 != 0 || L.d_out % 64 != 0))
+            return fail(MKOR_UNSUPPORTED, "layer %d: bf16 factors need d_in and d_out multiples of 64 (%d, %d)",
+                        i, L.d_in, L.d_out);
         if (L.rows < 0 || L.rows > MKOR_MAX_ROWS)
             return fail(MKOR_INVALID_ARG, "layer %d: rows = %d outside 0..%d", i, L.rows, MKOR_MAX_ROWS);
         const bool means = L.rows > 0;
@@ -69,8 +76,8 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
         struct { const void* p; size_t bytes; bool w; const char* what; bool used; } bufs[] = {
             {L.G, gsz, false, "G", true},
             {L.dW, din * dout * 4, true, "dW", true},
-            {L.Linv, din * din * 4, true, "Linv", L.second_order == 1},
-            {L.Rinv, dout * dout * 4, true, "Rinv", L.second_order == 1},
+            {L.Linv, din * din * (half ? 2 : 4), true, "Linv", L.second_order == 1},
+            {L.Rinv, dout * dout * (half ? 2 : 4), true, "Rinv", L.second_order == 1},
             {L.a, din * 4, means, "a", L.second_order == 1},
             {L.g, dout * 4, means, "g", L.second_order == 1},
             {L.stats, sizeof(mkor_layer_stats), true, "stats", L.stats != nullptr},
@@ -117,9 +124,11 @@ struct Layout {
     size_t off_g1l = 0, off_g1t = 0, off_g2l = 0, off_g2t = 0, off_gpart = 0, off_dpart = 0;
     size_t off_rsl = 0, off_rsb = 0, off_x = 0;
     size_t off_mmat = 0, off_mitem = 0, off_mchunk = 0, off_mpart = 0;
+    size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
+    int32_t nh1 = 0, nh2 = 0;
     int32_t nsecond = 0;
     int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
     int64_t nmeanpart = 0;   // doubles
@@ -128,28 +137,45 @@ struct Layout {
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
-// Tile table of one GEMM stage (1: X^T = (Linv G)^T, K = d_in; 2: dW_hat =
-// X Rinv, K = d_out).  Each layer's tile grid is cut into super-tiles of up to
-// GEMM_SUPER_M x GEMM_SUPER_N tiles; super-tiles are taken longest K first and
-// each goes whole to the XCD with the least work so far, so the tiles an XCD
-// runs together share A and B panels in its L2 and the long tiles do not form
-// the tail.  Workgroup b runs on XCD b % GEMM_XCDS, so position
-// q * GEMM_XCDS + x of the table holds the q-th tile of XCD x; shorter queues
-// are padded with tiles of layer -1.
-std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage) {
+bool is_half(const mkor_layer& L) { return L.second_order == 1 && L.factor_dtype == MKOR_DTYPE_BF16; }
+
+// Tile shape and contraction length of a GEMM stage.  fp32 factors: stage 1
+// X^T = (Linv G)^T (K = d_in), stage 2 dW_hat = X Rinv (K = d_out).  bf16
+// factors: stage 1 Y^T = (G Rinv)^T (K = d_out), stage 2 dW_hat = Linv Y
+// (K = d_in).  All tile the d_in x d_out output.
+struct StageGeom { int32_t bm, bn; };
+StageGeom stage_geom(int stage, bool half) {
+    if (half) return StageGeom{HG_BM, HG_BN};
+    return StageGeom{GEMM_SHAPE[stage - 1].bm, GEMM_SHAPE[stage - 1].bn};
+}
+int32_t stage_k(const mkor_layer& L, int stage, bool half) {
+    return (stage == 1) != half ? L.d_in : L.d_out;
+}
+
+// Tile table of one GEMM stage over the second-order layers with fp32
+// factors (half = false) or bf16 factors (half = true).  Each layer's tile
+// grid is cut into super-tiles covering up to GEMM_SUPER x GEMM_SUPER
+// outputs; super-tiles are taken longest K first and each goes whole to the
+// XCD with the least work so far, so the tiles an XCD runs together share A
+// and B panels in its L2 and the long tiles do not form the tail.  Workgroup
+// b runs on XCD b % GEMM_XCDS, so position q * GEMM_XCDS + x of the table
+// holds the q-th tile of XCD x; shorter queues are padded with tiles of layer
+// -1.
+std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage, bool half) {
     struct Super { int32_t layer, tm0, tn0, nm, nn, K; };
-    const GemmShape& sh = GEMM_SHAPE[stage - 1];
+    const StageGeom sh = stage_geom(stage, half);
     const int32_t sm = std::max(1, GEMM_SUPER / sh.bm), sn = std::max(1, GEMM_SUPER / sh.bn);
     std::vector<Super> sup;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
-        if (!L.second_order) continue;
+        if (!L.second_order || is_half(L) != half) continue;
         const int32_t tm = ceil_div(L.d_in, sh.bm), tn = ceil_div(L.d_out, sh.bn);
-        const int32_t K = stage == 1 ? L.d_in : L.d_out;
+        const int32_t K = stage_k(L, stage, half);
         for (int32_t a = 0; a < tm; a += sm)
             for (int32_t b = 0; b < tn; b += sn)
                 sup.push_back(Super{i, a, b, std::min(sm, tm - a), std::min(sn, tn - b), K});
     }
+    if (sup.empty()) return {};
     std::stable_sort(sup.begin(), sup.end(), [](const Super& x, const Super& y) {
         if (x.K != y.K) return x.K > y.K;
         return x.nm * x.nn > y.nm * y.nn;
@@ -171,6 +197,18 @@ std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int st
     return table;
 }
 
+// ||G||^2 partials of a layer (one per stage-1 tile column for fp32 factors,
+// one per stage-1 tile row for bf16 factors) and ||dW_hat||^2 partials (one
+// per tile of the stage that writes dW_hat).
+int64_t gpart_count(const mkor_layer& L) {
+    if (is_half(L)) return ceil_div(L.d_in, HG_BM);
+    return ceil_div(L.d_out, GEMM_SHAPE[0].bn);
+}
+int64_t dpart_count(const mkor_layer& L) {
+    const StageGeom g = stage_geom(2, is_half(L));
+    return (int64_t)ceil_div(L.d_in, g.bm) * ceil_div(L.d_out, g.bn);
+}
+
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0;
     for (int32_t i = 0; i < n; ++i) {
@@ -179,11 +217,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         if (!L.second_order) continue;
         Lo.nsecond++;
         rowblocks += ceil_div(L.d_in, SM_ROWS) + ceil_div(L.d_out, SM_ROWS);
-        // ||G||^2 partials: one per stage-1 tile column; ||dW_hat||^2: one per stage-2 tile
-        const int64_t tn1 = ceil_div(L.d_out, GEMM_SHAPE[0].bn);
-        const int64_t tm2 = ceil_div(L.d_in, GEMM_SHAPE[1].bm), tn2 = ceil_div(L.d_out, GEMM_SHAPE[1].bn);
-        g1 += tm2 * tn2;
-        gpart += tn1;
+        g1 += dpart_count(L);
+        gpart += gpart_count(L);
         usum += L.d_in + L.d_out;
     }
     int64_t mitems = 0, mchunks = 0, mpart = 0, mmats = 0;
@@ -207,11 +242,14 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.nmeanpart = mpart;
     Lo.nfactors = 2 * Lo.nsecond;
     Lo.nrowblocks = (int32_t)rowblocks;
-    const size_t t1 = schedule_tiles(layers, n, 1).size(), t2 = schedule_tiles(layers, n, 2).size();
-    if (t1 > INT32_MAX || t2 > INT32_MAX)
+    const size_t t1 = schedule_tiles(layers, n, 1, false).size(), t2 = schedule_tiles(layers, n, 2, false).size();
+    const size_t h1 = schedule_tiles(layers, n, 1, true).size(), h2 = schedule_tiles(layers, n, 2, true).size();
+    if (t1 > INT32_MAX || t2 > INT32_MAX || h1 > INT32_MAX || h2 > INT32_MAX)
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
     Lo.ng1 = (int32_t)t1;
     Lo.ng2 = (int32_t)t2;
+    Lo.nh1 = (int32_t)h1;
+    Lo.nh2 = (int32_t)h2;
     Lo.ngpart = (int32_t)gpart;
     Lo.ndpart = (int32_t)g1;
     Lo.nrsblocks = (int32_t)rsb;
@@ -224,6 +262,10 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_g1t = take(sizeof(GemmTile) * Lo.ng1);
     Lo.off_g2l = take(sizeof(GemmLayer) * n);
     Lo.off_g2t = take(sizeof(GemmTile) * Lo.ng2);
+    Lo.off_h1l = take(sizeof(HgLayer) * n);
+    Lo.off_h1t = take(sizeof(GemmTile) * Lo.nh1);
+    Lo.off_h2l = take(sizeof(HgLayer) * n);
+    Lo.off_h2t = take(sizeof(GemmTile) * Lo.nh2);
     Lo.off_rsl = take(sizeof(RescaleLayer) * n);
     Lo.off_rsb = take(sizeof(RescaleBlock) * Lo.nrsblocks);
     Lo.off_mmat = take(sizeof(MeanMat) * Lo.nmeanmat);
@@ -248,7 +290,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     }
     for (int32_t i = 0; i < n; ++i) {
         if (!layers[i].second_order) continue;
-        Lo.x_off[i] = take(sizeof(float) * (size_t)layers[i].d_in * layers[i].d_out);
+        // X^T (fp32) of fp32-factor layers, Y^T (bf16) of bf16-factor layers
+        Lo.x_off[i] = take((is_half(layers[i]) ? 2 : 4) * (size_t)layers[i].d_in * layers[i].d_out);
     }
     Lo.total = align_up(o, 256);
     (void)usum;
@@ -345,6 +388,10 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     GemmLayer* g2l = reinterpret_cast<GemmLayer*>(host.data() + lo.off_g2l);
     GemmTile* g1t = reinterpret_cast<GemmTile*>(host.data() + lo.off_g1t);
     GemmTile* g2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_g2t);
+    HgLayer* h1l = reinterpret_cast<HgLayer*>(host.data() + lo.off_h1l);
+    HgLayer* h2l = reinterpret_cast<HgLayer*>(host.data() + lo.off_h2l);
+    GemmTile* h1t = reinterpret_cast<GemmTile*>(host.data() + lo.off_h1t);
+    GemmTile* h2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_h2t);
     RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
     RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
     Pending* pend_h = reinterpret_cast<Pending*>(host.data() + lo.off_pend);
@@ -392,6 +439,7 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         R.first_blk = rbi;
         for (int64_t s = 0; s < R.numel; s += RS_ELEMS) rsb[rbi++] = RescaleBlock{i, 0, s};
         if (!L.second_order) continue;
+        const bool half = is_half(L);
         for (int side = 0; side < 2; ++side) {
             FactorDesc& f = fd[fi];
             f.P = side == 0 ? L.Linv : L.Rinv;
@@ -405,17 +453,40 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             f.blk0 = bi;
             f.nblk = ceil_div(f.d, SM_ROWS);
             f.side = side;
+            f.half = half ? 1 : 0;
             for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * SM_ROWS};
             ++fi;
         }
-        float* X = reinterpret_cast<float*>(base + lo.x_off[i]);
-        const int32_t tn1 = ceil_div(L.d_out, GEMM_SHAPE[0].bn);
-        const int32_t tm2 = ceil_div(L.d_in, GEMM_SHAPE[1].bm), tn2 = ceil_div(L.d_out, GEMM_SHAPE[1].bn);
         const bool bf16 = L.grad_dtype == MKOR_DTYPE_BF16;
         const FactorDesc& fL = fd[fi - 2];
         const FactorDesc& fR = fd[fi - 1];
+        const int32_t ngp = (int32_t)gpart_count(L), ndp = (int32_t)dpart_count(L);
+        R.gpart0 = gp; R.ngpart = ngp;
+        R.dpart0 = dp; R.ndpart = ndp;
+        if (half) {
+            // Y = G R (Y^T stored bf16 in the workspace), then dW_hat = L Y
+            void* Yt = base + lo.x_off[i];
+            HgLayer& A = h1l[i];
+            A.A = L.G; A.B = L.Rinv; A.C = Yt;
+            A.pend = fR.pend; A.w = fR.w;
+            A.M = L.d_in; A.N = L.d_out; A.K = L.d_out;
+            A.a_f32 = bf16 ? 0 : 1;
+            A.part0 = gp; A.ntn = ceil_div(L.d_out, HG_BN);
+            HgLayer& B = h2l[i];
+            B.A = L.Linv; B.B = Yt; B.C = L.dW;
+            B.pend = fL.pend; B.w = fL.w;
+            B.M = L.d_in; B.N = L.d_out; B.K = L.d_in;
+            B.a_f32 = 0;
+            B.part0 = dp; B.ntn = ceil_div(L.d_out, HG_BN);
+            gp += ngp;
+            dp += ndp;
+            continue;
+        }
+        float* X = reinterpret_cast<float*>(base + lo.x_off[i]);
+        const int32_t tn1 = ceil_div(L.d_out, GEMM_SHAPE[0].bn);
+        const int32_t tn2 = ceil_div(L.d_out, GEMM_SHAPE[1].bn);
         GemmLayer& A = g1l[i];
-        A.At = L.Linv; A.B = L.G; A.C = X;
+        A.At = static_cast<const float*>(L.Linv); A.B = L.G; A.C = X;
         A.pend = fL.pend; A.w = fL.w;
         A.M = L.d_in; A.N = L.d_out; A.K = L.d_in;
         A.b_bf16 = bf16;
@@ -428,14 +499,15 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         B.b_bf16 = 0;
         B.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
         B.part0 = dp; B.ntn = tn2;
-        R.gpart0 = gp; R.ngpart = tn1;
-        R.dpart0 = dp; R.ndpart = tm2 * tn2;
-        gp += tn1;
-        dp += tm2 * tn2;
+        gp += ngp;
+        dp += ndp;
     }
-    const std::vector<GemmTile> t1 = schedule_tiles(layers, n, 1), t2 = schedule_tiles(layers, n, 2);
+    const std::vector<GemmTile> t1 = schedule_tiles(layers, n, 1, false), t2 = schedule_tiles(layers, n, 2, false);
     std::copy(t1.begin(), t1.end(), g1t);
     std::copy(t2.begin(), t2.end(), g2t);
+    const std::vector<GemmTile> u1 = schedule_tiles(layers, n, 1, true), u2 = schedule_tiles(layers, n, 2, true);
+    std::copy(u1.begin(), u1.end(), h1t);
+    std::copy(u2.begin(), u2.end(), h2t);
 
     mkor_plan* plan = new (std::nothrow) mkor_plan;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "out of host memory");
@@ -485,11 +557,17 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
                                reinterpret_cast<const GemmTile*>(ws + lo.off_g1t), lo.ng1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "gemm_xt launch");
+            e = launch_hgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_h1l),
+                             reinterpret_cast<const GemmTile*>(ws + lo.off_h1t), lo.nh1, gpart, s);
+            if (e != hipSuccess) return hip_fail(e, "bf16 gemm (G R) launch");
             return MKOR_OK;
         case MKOR_STAGE_GEMM_DW:
             e = launch_gemm_dw(reinterpret_cast<const GemmLayer*>(ws + lo.off_g2l),
                                reinterpret_cast<const GemmTile*>(ws + lo.off_g2t), lo.ng2, dpart, s);
             if (e != hipSuccess) return hip_fail(e, "gemm_dw launch");
+            e = launch_hgemm(2, reinterpret_cast<const HgLayer*>(ws + lo.off_h2l),
+                             reinterpret_cast<const GemmTile*>(ws + lo.off_h2t), lo.nh2, dpart, s);
+            if (e != hipSuccess) return hip_fail(e, "bf16 gemm (L Y) launch");
             return MKOR_OK;
         case MKOR_STAGE_RESCALE:
             e = launch_rescale(reinterpret_cast<const RescaleLayer*>(ws + lo.off_rsl),

@@ -51,7 +51,7 @@ struct Pending {
 
 // One inverse factor P (d x d) and its driving vector x.
 struct FactorDesc {
-    float*            P;       // caller buffer S
+    void*             P;       // caller buffer S (fp32, or bf16 when half = 1)
     const float*      x;
     float*            u;       // workspace, d floats: u_raw = P x (current P, before blending)
     float*            w;       // workspace, d floats: w of the pending term
@@ -61,6 +61,8 @@ struct FactorDesc {
     int32_t           blk0;    // first row block of this factor in the row-block table
     int32_t           nblk;    // number of row blocks of this factor
     int32_t           side;    // 0 = Linv (driven by a), 1 = Rinv (driven by g)
+    int32_t           half;    // 1: S is stored in bf16 (d a multiple of 64)
+    int32_t           _pad;
 };
 
 // Rows handled by one workgroup of the SM pass (4 waves x SM_ROWS_PER_WAVE).
@@ -131,6 +133,27 @@ constexpr int GEMM_XCDS = 8;
 #define MKOR_GEMM_SUPER 1024
 #endif
 constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
+
+// ---------------------------------------------------------------- half factors
+// bf16 MFMA GEMMs of layers with bf16 factors (C[m][n] = sum_k A[m][k] B[n][k],
+// both operands row-major along k): stage 1 Y^T = (G R)^T in bf16, stage 2
+// dW_hat = L Y (see precond_hgemm.hip).
+constexpr int HG_BM = 256, HG_BN = 128, HG_BK = 64, HG_THREADS = 256;
+
+struct HgLayer {
+    const void*    A;      // stage 1: G (bf16, or fp32 when a_f32); stage 2: S_L (bf16)
+    const void*    B;      // stage 1: S_R (bf16); stage 2: Y^T (bf16)
+    void*          C;      // stage 1: Y^T (bf16, d_out x d_in); stage 2: dW_hat (fp32)
+    const Pending* pend;   // pending term of the factor operand (B in stage 1, A in stage 2)
+    const float*   w;      // its w vector
+    int32_t        M, N, K;
+    int32_t        a_f32;
+    int32_t        part0;  // first partial slot of this layer
+    int32_t        ntn;    // number of N tiles
+};
+
+hipError_t launch_hgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
+                        float* partials, hipStream_t stream);
 
 // ---------------------------------------------------------------- rescale
 struct RescaleLayer {

@@ -64,11 +64,25 @@ __device__ __forceinline__ float apply(const Pending& q, float s, float wi, floa
 
 // ------------------------------------------------------------------ pass
 // Rows rbase .. rbase + nr - 1 of one factor, d a multiple of 4.  FULL: nr = R.
-template <bool HAS, bool MV, bool FULL>
+// HALF: the factor is stored in bf16; the pending term is applied in fp32 and
+// the result rounded to bf16 (nearest even), and the norm and the matvec use
+// those rounded values, which are the factor from then on.
+__device__ __forceinline__ float4 bf4(uint2 h) {
+    return make_float4(bf2f((unsigned short)(h.x & 0xffffu)), bf2f((unsigned short)(h.x >> 16)),
+                       bf2f((unsigned short)(h.y & 0xffffu)), bf2f((unsigned short)(h.y >> 16)));
+}
+
+__device__ __forceinline__ uint2 pack_bf4(const float4& v) {
+    return make_uint2((unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16),
+                      (unsigned)f2bf(v.z) | ((unsigned)f2bf(v.w) << 16));
+}
+
+template <bool HAS, bool MV, bool FULL, bool HALF>
 __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q, int rbase, int nr,
                                            int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
     const int d = f.d, d4 = d >> 2;
-    float* __restrict__ P = f.P + (size_t)rbase * d;
+    float* __restrict__ P = static_cast<float*>(f.P) + (size_t)rbase * d;
+    unsigned short* __restrict__ P16 = static_cast<unsigned short*>(f.P) + (size_t)rbase * d;
     float wi[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
@@ -76,9 +90,11 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
     for (int j = lane; j < d4; j += 64) {
         float4 p[R];
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-            if (FULL || r < nr) p[r] = MKOR_SM_NT ? gld4_nt(P + (size_t)r * d + 4 * j)
-                                                  : gld4(P + (size_t)r * d + 4 * j);
+        for (int r = 0; r < R; ++r) {
+            if (!FULL && r >= nr) continue;
+            if constexpr (HALF) p[r] = bf4(gld_u2(P16 + (size_t)r * d + 4 * j));
+            else p[r] = MKOR_SM_NT ? gld4_nt(P + (size_t)r * d + 4 * j) : gld4(P + (size_t)r * d + 4 * j);
+        }
         float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), wv = xv;
         if constexpr (MV) xv = gld4(f.x + 4 * j);
         if constexpr (HAS) wv = gld4(f.w + 4 * j);
@@ -98,8 +114,15 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
                     else if (c == 2) p[r].z = __fadd_rn(p[r].z, q.c2);
                     else p[r].w = __fadd_rn(p[r].w, q.c2);
                 }
-                if (MKOR_SM_NT) gst4_nt(P + (size_t)r * d + 4 * j, p[r]);
-                else            gst4(P + (size_t)r * d + 4 * j, p[r]);
+                if constexpr (HALF) {
+                    const uint2 h = pack_bf4(p[r]);
+                    gst_u2(P16 + (size_t)r * d + 4 * j, h);
+                    p[r] = bf4(h);
+                } else if (MKOR_SM_NT) {
+                    gst4_nt(P + (size_t)r * d + 4 * j, p[r]);
+                } else {
+                    gst4(P + (size_t)r * d + 4 * j, p[r]);
+                }
             }
             if constexpr (MV) {
                 dot[r] = fmaf(p[r].x, xv.x, dot[r]);
@@ -120,7 +143,7 @@ template <bool HAS, bool MV>
 __device__ __forceinline__ void pass_rows1(const FactorDesc& f, const Pending& q, int rbase, int nr,
                                            int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
     const int d = f.d;
-    float* __restrict__ P = f.P + (size_t)rbase * d;
+    float* __restrict__ P = static_cast<float*>(f.P) + (size_t)rbase * d;
     float wi[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) wi[r] = (HAS && r < nr) ? gld(f.w + rbase + r) : 0.f;
@@ -147,9 +170,12 @@ __device__ __forceinline__ void pass_rows1(const FactorDesc& f, const Pending& q
 template <bool HAS, bool MV>
 __device__ __forceinline__ void pass_rows(const FactorDesc& f, const Pending& q, int rbase, int nr,
                                           int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
-    if ((f.d & 3) == 0) {
-        if (nr == R) pass_rows4<HAS, MV, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-        else         pass_rows4<HAS, MV, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+    if (f.half) {   // bf16 factors: d is a multiple of 64
+        if (nr == R) pass_rows4<HAS, MV, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        else         pass_rows4<HAS, MV, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+    } else if ((f.d & 3) == 0) {
+        if (nr == R) pass_rows4<HAS, MV, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        else         pass_rows4<HAS, MV, false, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
     } else {
         pass_rows1<HAS, MV>(f, q, rbase, nr, lane, maxabs, dot, nrm);
     }

@@ -12,10 +12,12 @@ from .binding import STATS_BYTES, MkorPlan, read_stats
 
 
 def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True,
-                    rows=0, act_dtype="fp32"):
+                    rows=0, act_dtype="fp32", factor_dtype="fp32"):
     """One dict of device tensors per (d_in, d_out); factors start as I.  With
     rows > 0 each second-order layer also gets token-row buffers A (rows x d_in)
-    and Gout (rows x d_out), from which the library forms a and g."""
+    and Gout (rows x d_out), from which the library forms a and g.
+    factor_dtype "bf16" stores Linv and Rinv in bf16 (half-precision factors)."""
+    fdt = torch.bfloat16 if factor_dtype == "bf16" else torch.float32
     gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
     layers = []
     for i, (d_in, d_out) in enumerate(shapes):
@@ -24,8 +26,8 @@ def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None,
                  G=torch.zeros((d_in, d_out), dtype=gdt, device=device),
                  dW=torch.zeros((d_in, d_out), dtype=torch.float32, device=device))
         if so:
-            L["Linv"] = torch.eye(d_in, dtype=torch.float32, device=device)
-            L["Rinv"] = torch.eye(d_out, dtype=torch.float32, device=device)
+            L["Linv"] = torch.eye(d_in, dtype=fdt, device=device)
+            L["Rinv"] = torch.eye(d_out, dtype=fdt, device=device)
             L["a"] = torch.zeros(d_in, dtype=torch.float32, device=device)
             L["g"] = torch.zeros(d_out, dtype=torch.float32, device=device)
         if stats:
@@ -66,12 +68,15 @@ def get_means(L):
 
 
 def set_factors(L, Linv, Rinv):
+    """Copies host factors in (bf16 factors: the values must already be
+    bf16-representable)."""
     _put(L["Linv"], np.asarray(Linv, dtype=np.float32))
     _put(L["Rinv"], np.asarray(Rinv, dtype=np.float32))
 
 
 def get_factors(L):
-    return L["Linv"].cpu().numpy(), L["Rinv"].cpu().numpy()
+    """The stored factors as float32 host arrays (bf16 values widened)."""
+    return L["Linv"].float().cpu().numpy(), L["Rinv"].float().cpu().numpy()
 
 
 def get_dW(L):

@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 3
+    assert lib.mkor_abi_version() == 4
 
 
 def test_status_strings(lib):
@@ -46,7 +46,7 @@ def test_status_strings(lib):
 
 def test_struct_sizes():
     assert ctypes.sizeof(B.mkor_params) == 28
-    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8
+    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8 + 8
     assert M.STATS_BYTES == 48
 
 
@@ -90,11 +90,12 @@ class Fake:
         return p
 
 
-def layer(fk, d_in, d_out, so=1, dt=0, stats=False, rows=0, adt=0):
+def layer(fk, d_in, d_out, so=1, dt=0, stats=False, rows=0, adt=0, fdt=0):
     esz = 2 if dt == 1 else 4
     aesz = 2 if adt == 1 else 4
-    return dict(d_in=d_in, d_out=d_out, second_order=so, grad_dtype=dt,
-                Linv=fk.alloc(d_in * d_in * 4), Rinv=fk.alloc(d_out * d_out * 4),
+    fsz = 2 if fdt == 1 else 4
+    return dict(d_in=d_in, d_out=d_out, second_order=so, grad_dtype=dt, factor_dtype=fdt,
+                Linv=fk.alloc(d_in * d_in * fsz), Rinv=fk.alloc(d_out * d_out * fsz),
                 a=fk.alloc(d_in * 4), g=fk.alloc(d_out * 4), G=fk.alloc(d_in * d_out * esz),
                 dW=fk.alloc(d_in * d_out * 4), stats=fk.alloc(48) if stats else None,
                 rows=rows, act_dtype=adt,
@@ -149,6 +150,9 @@ def test_empty_list(lib):
     (lambda L: L.update(rows=-1), M.MKOR_INVALID_ARG),
     (lambda L: L.update(rows=M.MAX_ROWS + 1), M.MKOR_INVALID_ARG),
     (lambda L: L.update(rows=8), M.MKOR_INVALID_ARG),              # rows > 0 without A / Gout
+    (lambda L: L.update(factor_dtype=2), M.MKOR_UNSUPPORTED),
+    (lambda L: L.update(reserved=1), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(factor_dtype=1, d_out=100), M.MKOR_UNSUPPORTED),  # bf16: multiples of 64
 ])
 def test_layer_rejected(lib, mutate, status):
     fk = Fake()
@@ -245,3 +249,30 @@ def test_entry_points_reject_before_device(lib):
     for stage in (-1, M.NUM_STAGES):
         assert lib.mkor_run_stage(plan, ctypes.byref(p), stage, None) == M.MKOR_INVALID_ARG
     lib.mkor_plan_destroy(plan)
+
+
+def test_bf16_factor_layers(lib):
+    fk = Fake()
+    # bf16 factors: d_in, d_out multiples of 64, factor buffers 2 bytes/element
+    assert ws_status([layer(fk, 64, 192, fdt=1)])[0] == M.MKOR_OK
+    assert ws_status([layer(fk, 64, 96, fdt=1)])[0] == M.MKOR_UNSUPPORTED
+    # a first-order layer ignores factor_dtype's shape rule
+    assert ws_status([layer(fk, 50, 70, so=0, fdt=1)])[0] == M.MKOR_OK
+    # the bf16 factor of one layer may sit right after the other (2-byte extent)
+    L = layer(fk, 128, 128, fdt=1)
+    L["Rinv"] = L["Linv"] + 128 * 128 * 2
+    assert ws_status([L])[0] == M.MKOR_OK
+    L["Rinv"] = L["Linv"] + 128 * 128 * 2 - 256
+    assert ws_status([L])[0] == M.MKOR_INVALID_ARG
+
+
+def test_workspace_bf16_factors(lib):
+    fk = Fake()
+    f32 = ws_status([layer(fk, 1024, 4096)])[1]
+    h = ws_status([layer(fk, 1024, 4096, fdt=1)])[1]
+    # the intermediate (X^T fp32, or Y^T bf16) is d_in x d_out
+    assert f32 - h >= 2 * 1024 * 4096 - (1 << 20)
+    assert h >= 2 * 1024 * 4096
+    # mixed lists plan both GEMM kinds
+    st, _ = ws_status([layer(fk, 1024, 4096, fdt=1), layer(fk, 4096, 1024), layer(fk, 37, 100)])
+    assert st == M.MKOR_OK
