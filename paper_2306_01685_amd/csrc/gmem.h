@@ -70,20 +70,33 @@ __device__ __forceinline__ float gld_off(const void* base, unsigned byte_off) {
 
 __device__ __forceinline__ void gst(float* p, float v) { *(MKOR_GLOBAL float*)p = v; }
 
+__device__ __forceinline__ void gst_u4(void* p, uint4 v) {
+    mk_u4 w;
+    w.x = v.x; w.y = v.y; w.z = v.z; w.w = v.w;
+    *(MKOR_GLOBAL mk_u4*)p = w;
+}
+
 __device__ __forceinline__ void gst_u2(void* p, uint2 v) {
     mk_u2 w;
     w.x = v.x; w.y = v.y;
     *(MKOR_GLOBAL mk_u2*)p = w;
 }
 
-// bf16 <-> fp32.  f2bf rounds to nearest, ties to even; NaN stays NaN.
+// bf16 <-> fp32.  The conversion to bf16 is the hardware's (v_cvt_pk_bf16_f32):
+// round to nearest, ties to even; NaN stays NaN.
+typedef __bf16 mk_bf2 __attribute__((ext_vector_type(2)));
+typedef float  mk_f2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ float bf2f(unsigned short h) { return __uint_as_float(((unsigned)h) << 16); }
 
+// two floats -> packed bf16 pair (a in the low half)
+__device__ __forceinline__ unsigned f2bf2(float a, float b) {
+    const mk_f2 v = {a, b};
+    return __builtin_bit_cast(unsigned, __builtin_convertvector(v, mk_bf2));
+}
+
 __device__ __forceinline__ unsigned short f2bf(float f) {
-    unsigned u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (unsigned short)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (unsigned short)(u >> 16);
+    return __builtin_bit_cast(unsigned short, (__bf16)f);
 }
 
 __device__ __forceinline__ void gst4(float* p, const float4& v) {

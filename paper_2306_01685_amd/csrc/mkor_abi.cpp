@@ -216,7 +216,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         rsb += ceil_div((int64_t)L.d_in * L.d_out, RS_ELEMS);
         if (!L.second_order) continue;
         Lo.nsecond++;
-        rowblocks += ceil_div(L.d_in, SM_ROWS) + ceil_div(L.d_out, SM_ROWS);
+        const int32_t rows = is_half(L) ? SM_ROWS_HALF : SM_ROWS;
+        rowblocks += ceil_div(L.d_in, rows) + ceil_div(L.d_out, rows);
         g1 += dpart_count(L);
         gpart += gpart_count(L);
         usum += L.d_in + L.d_out;
@@ -451,10 +452,11 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             f.stats = stats;
             f.d = side == 0 ? L.d_in : L.d_out;
             f.blk0 = bi;
-            f.nblk = ceil_div(f.d, SM_ROWS);
+            const int32_t rows = half ? SM_ROWS_HALF : SM_ROWS;
+            f.nblk = ceil_div(f.d, rows);
             f.side = side;
             f.half = half ? 1 : 0;
-            for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * SM_ROWS};
+            for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * rows};
             ++fi;
         }
         const bool bf16 = L.grad_dtype == MKOR_DTYPE_BF16;

@@ -79,6 +79,9 @@ constexpr int SM_GRID = MKOR_SM_GRID;   // workgroups of the SM pass (0: one per
 constexpr int SM_THREADS = 256;
 constexpr int SM_ROWS_PER_WAVE = MKOR_SM_RPW;
 constexpr int SM_ROWS = (SM_THREADS / 64) * SM_ROWS_PER_WAVE;
+// bf16 factors: twice the rows per wave (the same bytes per row block)
+constexpr int SM_ROWS_PER_WAVE_HALF = 2 * SM_ROWS_PER_WAVE;
+constexpr int SM_ROWS_HALF = (SM_THREADS / 64) * SM_ROWS_PER_WAVE_HALF;
 
 struct RowBlock {
     int32_t factor;
@@ -138,7 +141,15 @@ constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 // bf16 MFMA GEMMs of layers with bf16 factors (C[m][n] = sum_k A[m][k] B[n][k],
 // both operands row-major along k): stage 1 Y^T = (G R)^T in bf16, stage 2
 // dW_hat = L Y (see precond_hgemm.hip).
-constexpr int HG_BM = 256, HG_BN = 128, HG_BK = 64, HG_THREADS = 256;
+#ifndef MKOR_HG_BN
+#define MKOR_HG_BN 256
+#endif
+#ifndef MKOR_HG_WN
+#define MKOR_HG_WN 4
+#endif
+constexpr int HG_BM = 256, HG_BN = MKOR_HG_BN, HG_BK = 64;
+constexpr int HG_WM = 2, HG_WN = MKOR_HG_WN;       // wave grid of a tile
+constexpr int HG_THREADS = 64 * HG_WM * HG_WN;
 
 struct HgLayer {
     const void*    A;      // stage 1: G (bf16, or fp32 when a_f32); stage 2: S_L (bf16)

@@ -24,11 +24,13 @@
 // positions is read in the epilogue.  So the MFMA loop stays free of per-element
 // arithmetic.
 //
-// Tiles: 256 x 128 per workgroup of 4 waves (each 128 x 64 = 4 x 2 MFMA blocks),
-// K in 64-deep slabs double-buffered in LDS as [row][k] bf16 with the 16-byte
-// chunk index XOR-swizzled by the row, so the 16-byte operand reads of a wave
-// hit distinct banks.  d_in and d_out must be multiples of 64 (checked by the
-// plan); M and N edges are masked.
+// Tiles: 256 x 256 per workgroup of 8 waves (2 x 4, each 128 x 64 = 4 x 2 MFMA
+// blocks), so two waves share each SIMD and one issues MFMAs while the other
+// waits on LDS or the slab barrier.  K runs in 64-deep slabs double-buffered in
+// LDS (128 KB of the 160 KB) as [row][k] bf16 with the 16-byte chunk index
+// XOR-swizzled by the row, so the 16-byte operand reads of a wave hit distinct
+// banks.  d_in and d_out must be multiples of 64 (checked by the plan); M and
+// N edges are masked.
 #include "gmem.h"
 #include "mkor_internal.h"
 
@@ -36,16 +38,23 @@ namespace mkor {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+// LDS pointers carry their address space, so every operand access is a
+// ds_read / ds_write (a generic pointer would become a flat access, which
+// waits on the global-load counter too).
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) mk_u4 lds_u4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
+typedef __attribute__((address_space(3))) float lds_float;
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = HG_BM, BN = HG_BN, BK = HG_BK, NT = HG_THREADS;
-constexpr int WM = 2, WN = 2;
+constexpr int WM = HG_WM, WN = HG_WN;
 constexpr int TM = BM / WM, TN = BN / WN;   // 128 x 64 per wave
 constexpr int FM = TM / 32, FN = TN / 32;   // 4 x 2 MFMA blocks
 constexpr int KCH = BK / 8;                 // 16-byte chunks per slab row (8)
-constexpr int ACH = BM * KCH / NT;          // A chunks per thread and slab (8)
-constexpr int BCH = BN * KCH / NT;          // B chunks per thread and slab (4)
-static_assert(NT == WM * WN * 64 && KCH == 8, "layout");
+constexpr int ACH = BM * KCH / NT;          // A chunks per thread and slab
+constexpr int BCH = BN * KCH / NT;          // B chunks per thread and slab
+static_assert(NT == WM * WN * 64 && KCH == 8 && TM == 128 && TN == 64, "layout");
 static_assert(ACH * NT == BM * KCH && BCH * NT == BN * KCH, "staging");
 static_assert(NT % KCH == 0, "a thread stages one fixed chunk column");
 
@@ -90,40 +99,35 @@ __device__ __forceinline__ float sq8(const uint4& h, float acc) {
 
 // 8 fp32 -> 8 bf16 (rounded) packed into 16 bytes
 __device__ __forceinline__ uint4 pack8(const float4& a, const float4& b) {
-    uint4 h;
-    h.x = (unsigned)f2bf(a.x) | ((unsigned)f2bf(a.y) << 16);
-    h.y = (unsigned)f2bf(a.z) | ((unsigned)f2bf(a.w) << 16);
-    h.z = (unsigned)f2bf(b.x) | ((unsigned)f2bf(b.y) << 16);
-    h.w = (unsigned)f2bf(b.z) | ((unsigned)f2bf(b.w) << 16);
-    return h;
+    return make_uint4(f2bf2(a.x, a.y), f2bf2(a.z, a.w), f2bf2(b.x, b.y), f2bf2(b.z, b.w));
 }
 
-// Loads 16-byte chunk (row, k0 + 8c) of a row-major bf16 (or fp32, rounded)
-// operand with leading dimension ld; rows >= nrows give zeros.
+// Loads the 8 elements (row, k .. k + 7) of a row-major bf16 (or fp32,
+// rounded) operand with leading dimension ld.  Rows at or past nrows are
+// clamped to the last row (no branch in the K loop); their products land in
+// output rows or columns the epilogue never stores.
 template <bool F32>
 __device__ __forceinline__ uint4 load_chunk(const void* base, int ld, int row, int nrows, int k) {
-    const bool ok = row < nrows;
-    const size_t off = ok ? (size_t)row * ld + k : 0;
-    uint4 h;
+    const size_t off = (size_t)min(row, nrows - 1) * ld + k;
     if constexpr (F32) {
         const float* p = static_cast<const float*>(base) + off;
-        h = pack8(gld4(p), gld4(p + 4));
+        return pack8(gld4(p), gld4(p + 4));
     } else {
-        h = gld_u4(static_cast<const unsigned short*>(base) + off);
+        return gld_u4(static_cast<const unsigned short*>(base) + off);
     }
-    if (!ok) h = make_uint4(0u, 0u, 0u, 0u);
-    return h;
 }
 
 // STAGE 1: A = G (AF32: fp32 G), B = S_R (factor), rank-1 vector from A (G w_R).
 // STAGE 2: A = S_L (factor), B = Y^T, rank-1 vector from B (w_L^T Y).
 template <int STAGE, bool AF32, bool PEND>
 __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
-                           char* smem) {
-    char* As[2] = {smem, smem + BM * BK * 2};
-    char* Bs[2] = {smem + 2 * BM * BK * 2, smem + 2 * BM * BK * 2 + BN * BK * 2};
-    float* rvec = reinterpret_cast<float*>(smem + 2 * (BM + BN) * BK * 2);   // BM (stage 1) or BN floats
-    float* red = rvec + BM;
+                           lds_char* smem) {
+    lds_char* const A0 = smem;
+    lds_char* const A1 = smem + BM * BK * 2;
+    lds_char* const B0 = smem + 2 * BM * BK * 2;
+    lds_char* const B1 = B0 + BN * BK * 2;
+    lds_float* rvec = (lds_float*)(smem + 2 * (BM + BN) * BK * 2);   // BM (stage 1) or BN floats
+    lds_float* red = rvec + (BM > BN ? BM : BN);
 
     const int m0 = tile.tm * BM, n0 = tile.tn * BN;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -164,7 +168,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             rb[i] = load_chunk<false>(L.B, K, n0 + row, N, k0 + 8 * cch);
         }
     };
-    auto store = [&](int k0, char* Ad, char* Bd) {
+    auto store = [&](int k0, lds_char* Ad, lds_char* Bd) {
         float wk[8];
         if (PEND) {
             const float4 w0 = gld4(L.w + k0 + 8 * cch), w1 = gld4(L.w + k0 + 8 * cch + 4);
@@ -174,52 +178,65 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
         for (int i = 0; i < ACH; ++i) {
             const int row = (t + i * NT) / KCH;
-            *reinterpret_cast<uint4*>(Ad + swz(row, cch)) = ra[i];
+            *(lds_u4*)(Ad + swz(row, cch)) = mk_u4{ra[i].x, ra[i].y, ra[i].z, ra[i].w};
             if constexpr (STAGE == 1) {
                 if (PEND) rdot[i] = dot8(ra[i], wk, rdot[i]);
-                if (want_gsq) gsq = sq8(ra[i], gsq);
+                // ||G||^2 over real rows only (clamped rows repeat the last one)
+                if (want_gsq) gsq = (m0 + row < M) ? sq8(ra[i], gsq) : gsq;
             }
         }
 #pragma unroll
         for (int i = 0; i < BCH; ++i) {
             const int row = (t + i * NT) / KCH;
-            *reinterpret_cast<uint4*>(Bd + swz(row, cch)) = rb[i];
+            *(lds_u4*)(Bd + swz(row, cch)) = mk_u4{rb[i].x, rb[i].y, rb[i].z, rb[i].w};
             if constexpr (STAGE == 2) {
                 if (PEND) rdot[i] = dot8(rb[i], wk, rdot[i]);
             }
         }
     };
 
+    // operands of one 16-deep k-step of a slab
+    auto frags = [&](const lds_char* Ac, const lds_char* Bc, int ks, bf16x8 (&a)[FM], bf16x8 (&b)[FN]) {
+        const int c = 2 * ks + lk;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[i] = *(const lds_bf8*)(Ac + swz(wm * TM + i * 32 + li, c));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[j] = *(const lds_bf8*)(Bc + swz(wn * TN + j * 32 + li, c));
+    };
+    auto mma = [&](const bf16x8 (&a)[FM], const bf16x8 (&b)[FN]) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    constexpr int KS = BK / 16;         // k-steps per slab
+    constexpr int DS = FM + FN;         // LDS operand reads per k-step
+
     load(0);
-    store(0, As[0], Bs[0]);
+    store(0, A0, B0);
     __syncthreads();
     for (int s = 0; s < nslab; ++s) {
         const int cur = s & 1;
         const bool more = s + 1 < nslab;
         if (more) load((s + 1) * BK);
-        const char* Ac = As[cur];
-        const char* Bc = Bs[cur];
+        const lds_char* Ac = cur ? A1 : A0;
+        const lds_char* Bc = cur ? B1 : B0;
+        // one operand set per k-step: the other wave on the SIMD issues its
+        // MFMAs while this one waits for its LDS reads
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            const int c = 2 * ks + lk;
+        for (int ks = 0; ks < KS; ++ks) {
             bf16x8 a[FM], b[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int r = wm * TM + i * 32 + li;
-                a[i] = *reinterpret_cast<const bf16x8*>(Ac + swz(r, c));
-            }
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int r = wn * TN + j * 32 + li;
-                b[j] = *reinterpret_cast<const bf16x8*>(Bc + swz(r, c));
-            }
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            frags(Ac, Bc, ks, a, b);
+            mma(a, b);
         }
-        if (more) store((s + 1) * BK, As[cur ^ 1], Bs[cur ^ 1]);
+        __builtin_amdgcn_sched_group_barrier(0x020, 32, 0);   // global loads of the next slab
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+        }
+        if (more) store((s + 1) * BK, cur ? A0 : A1, cur ? B0 : B1);
         __syncthreads();
     }
 
@@ -264,8 +281,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                         }
                     }
                     unsigned short* dst = static_cast<unsigned short*>(L.C) + (size_t)n * M + mb;
-                    const uint2 h = make_uint2((unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16),
-                                               (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16));
+                    const uint2 h = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
                     gst_u2(dst, h);
                 } else {
                     // dW_hat = c1 (S Y) + c2 Y + sgn w (w^T Y); Y[m][n] = Y^T[n][m]
@@ -303,11 +319,12 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     }
 }
 
-constexpr int HG_SMEM = 2 * (BM + BN) * BK * 2 + 4 * (BM + NT / 64);
+constexpr int HG_SMEM = 2 * (BM + BN) * BK * 2 + 4 * ((BM > BN ? BM : BN) + NT / 64);
 
 template <int STAGE>
 __global__ __launch_bounds__(NT, 1) void hgemm_kernel(HgArgs args) {
-    __shared__ __attribute__((aligned(16))) char smem[HG_SMEM];
+    __shared__ __attribute__((aligned(16))) char smem_[HG_SMEM];
+    lds_char* smem = (lds_char*)smem_;
     const GemmTile tile = args.tiles[blockIdx.x];
     if (tile.layer < 0) return;   // padding of the XCD interleave
     const HgLayer L = args.layers[tile.layer];

@@ -35,8 +35,6 @@
 namespace mkor {
 namespace {
 
-constexpr int R = SM_ROWS_PER_WAVE;
-
 __device__ __forceinline__ float nanmax(float a, float b) {
     return (a != a || b != b) ? __builtin_nanf("") : fmaxf(a, b);
 }
@@ -63,43 +61,28 @@ __device__ __forceinline__ float apply(const Pending& q, float s, float wi, floa
 }
 
 // ------------------------------------------------------------------ pass
-// Rows rbase .. rbase + nr - 1 of one factor, d a multiple of 4.  FULL: nr = R.
-// HALF: the factor is stored in bf16; the pending term is applied in fp32 and
-// the result rounded to bf16 (nearest even), and the norm and the matvec use
-// those rounded values, which are the factor from then on.
-__device__ __forceinline__ float4 bf4(uint2 h) {
-    return make_float4(bf2f((unsigned short)(h.x & 0xffffu)), bf2f((unsigned short)(h.x >> 16)),
-                       bf2f((unsigned short)(h.y & 0xffffu)), bf2f((unsigned short)(h.y >> 16)));
-}
-
-__device__ __forceinline__ uint2 pack_bf4(const float4& v) {
-    return make_uint2((unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16),
-                      (unsigned)f2bf(v.z) | ((unsigned)f2bf(v.w) << 16));
-}
-
-template <bool HAS, bool MV, bool FULL, bool HALF>
+// Rows rbase .. rbase + nr - 1 of one fp32 factor, d a multiple of 4.  FULL: nr = R.
+template <int RW, bool HAS, bool MV, bool FULL>
 __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q, int rbase, int nr,
-                                           int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
+                                           int lane, int maxabs, float (&dot)[RW], float (&nrm)[RW]) {
     const int d = f.d, d4 = d >> 2;
     float* __restrict__ P = static_cast<float*>(f.P) + (size_t)rbase * d;
-    unsigned short* __restrict__ P16 = static_cast<unsigned short*>(f.P) + (size_t)rbase * d;
-    float wi[R];
+    float wi[RW];
 #pragma unroll
-    for (int r = 0; r < R; ++r) wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
+    for (int r = 0; r < RW; ++r) wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
 
     for (int j = lane; j < d4; j += 64) {
-        float4 p[R];
+        float4 p[RW];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < RW; ++r) {
             if (!FULL && r >= nr) continue;
-            if constexpr (HALF) p[r] = bf4(gld_u2(P16 + (size_t)r * d + 4 * j));
-            else p[r] = MKOR_SM_NT ? gld4_nt(P + (size_t)r * d + 4 * j) : gld4(P + (size_t)r * d + 4 * j);
+            p[r] = MKOR_SM_NT ? gld4_nt(P + (size_t)r * d + 4 * j) : gld4(P + (size_t)r * d + 4 * j);
         }
         float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), wv = xv;
         if constexpr (MV) xv = gld4(f.x + 4 * j);
         if constexpr (HAS) wv = gld4(f.w + 4 * j);
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < RW; ++r) {
             if (!FULL && r >= nr) break;
             if constexpr (HAS) {
                 p[r].x = apply(q, p[r].x, wi[r], wv.x);
@@ -114,11 +97,7 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
                     else if (c == 2) p[r].z = __fadd_rn(p[r].z, q.c2);
                     else p[r].w = __fadd_rn(p[r].w, q.c2);
                 }
-                if constexpr (HALF) {
-                    const uint2 h = pack_bf4(p[r]);
-                    gst_u2(P16 + (size_t)r * d + 4 * j, h);
-                    p[r] = bf4(h);
-                } else if (MKOR_SM_NT) {
+                if (MKOR_SM_NT) {
                     gst4_nt(P + (size_t)r * d + 4 * j, p[r]);
                 } else {
                     gst4(P + (size_t)r * d + 4 * j, p[r]);
@@ -138,20 +117,93 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
     }
 }
 
+// bf16 factor, d a multiple of 64: 8 elements (16 bytes) per lane and row.
+// The pending term is applied in fp32 and the result rounded to bf16 (nearest
+// even); the norm and the matvec use those rounded values, which are the
+// factor from then on.
+__device__ __forceinline__ void unpack8(const uint4& h, float (&v)[8]) {
+    const unsigned u[4] = {h.x, h.y, h.z, h.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = bf2f((unsigned short)(u[i] & 0xffffu));
+        v[2 * i + 1] = bf2f((unsigned short)(u[i] >> 16));
+    }
+}
+
+__device__ __forceinline__ uint4 pack8(const float (&v)[8]) {
+    return make_uint4(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7]));
+}
+
+template <int RW, bool HAS, bool MV, bool FULL>
+__device__ __forceinline__ void pass_rows8h(const FactorDesc& f, const Pending& q, int rbase, int nr,
+                                            int lane, int maxabs, float (&dot)[RW], float (&nrm)[RW]) {
+    const int d = f.d, d8 = d >> 3;
+    unsigned short* __restrict__ P16 = static_cast<unsigned short*>(f.P) + (size_t)rbase * d;
+    float wi[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
+
+    for (int j = lane; j < d8; j += 64) {
+        uint4 h[RW];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            if (!FULL && r >= nr) continue;
+            h[r] = gld_u4(P16 + (size_t)r * d + 8 * j);
+        }
+        float xv[8], wv[8];
+        if constexpr (MV) {
+            const float4 x0 = gld4(f.x + 8 * j), x1 = gld4(f.x + 8 * j + 4);
+            xv[0] = x0.x; xv[1] = x0.y; xv[2] = x0.z; xv[3] = x0.w;
+            xv[4] = x1.x; xv[5] = x1.y; xv[6] = x1.z; xv[7] = x1.w;
+        }
+        if constexpr (HAS) {
+            const float4 w0 = gld4(f.w + 8 * j), w1 = gld4(f.w + 8 * j + 4);
+            wv[0] = w0.x; wv[1] = w0.y; wv[2] = w0.z; wv[3] = w0.w;
+            wv[4] = w1.x; wv[5] = w1.y; wv[6] = w1.z; wv[7] = w1.w;
+        }
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            if (!FULL && r >= nr) break;
+            float p[8];
+            unpack8(h[r], p);
+            if constexpr (HAS) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) p[e] = apply(q, p[e], wi[r], wv[e]);
+                const int row = rbase + r;
+                if ((row >> 3) == j) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if ((row & 7) == e) p[e] = __fadd_rn(p[e], q.c2);
+                }
+                const uint4 hn = pack8(p);
+                gst_u4(P16 + (size_t)r * d + 8 * j, hn);
+                unpack8(hn, p);   // the stored (rounded) values are the factor from now on
+            }
+            if constexpr (MV) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    dot[r] = fmaf(p[e], xv[e], dot[r]);
+                    nrm[r] = absacc(nrm[r], p[e], maxabs);
+                }
+            }
+        }
+    }
+}
+
 // Any d (scalar accesses).
-template <bool HAS, bool MV>
+template <int RW, bool HAS, bool MV>
 __device__ __forceinline__ void pass_rows1(const FactorDesc& f, const Pending& q, int rbase, int nr,
-                                           int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
+                                           int lane, int maxabs, float (&dot)[RW], float (&nrm)[RW]) {
     const int d = f.d;
     float* __restrict__ P = static_cast<float*>(f.P) + (size_t)rbase * d;
-    float wi[R];
+    float wi[RW];
 #pragma unroll
-    for (int r = 0; r < R; ++r) wi[r] = (HAS && r < nr) ? gld(f.w + rbase + r) : 0.f;
+    for (int r = 0; r < RW; ++r) wi[r] = (HAS && r < nr) ? gld(f.w + rbase + r) : 0.f;
     for (int j = lane; j < d; j += 64) {
         const float xv = MV ? gld(f.x + j) : 0.f;
         const float wj = HAS ? gld(f.w + j) : 0.f;
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < RW; ++r) {
             if (r >= nr) break;
             float p = gld(P + (size_t)r * d + j);
             if constexpr (HAS) {
@@ -167,50 +219,51 @@ __device__ __forceinline__ void pass_rows1(const FactorDesc& f, const Pending& q
     }
 }
 
-template <bool HAS, bool MV>
+// HALF (bf16 factor, d a multiple of 64) or fp32; RW rows per wave.
+template <int RW, bool HALF, bool HAS, bool MV>
 __device__ __forceinline__ void pass_rows(const FactorDesc& f, const Pending& q, int rbase, int nr,
-                                          int lane, int maxabs, float (&dot)[R], float (&nrm)[R]) {
-    if (f.half) {   // bf16 factors: d is a multiple of 64
-        if (nr == R) pass_rows4<HAS, MV, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-        else         pass_rows4<HAS, MV, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+                                          int lane, int maxabs, float (&dot)[RW], float (&nrm)[RW]) {
+    if constexpr (HALF) {
+        if (nr == RW) pass_rows8h<RW, HAS, MV, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        else          pass_rows8h<RW, HAS, MV, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
     } else if ((f.d & 3) == 0) {
-        if (nr == R) pass_rows4<HAS, MV, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-        else         pass_rows4<HAS, MV, false, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        if (nr == RW) pass_rows4<RW, HAS, MV, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        else          pass_rows4<RW, HAS, MV, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
     } else {
-        pass_rows1<HAS, MV>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        pass_rows1<RW, HAS, MV>(f, q, rbase, nr, lane, maxabs, dot, nrm);
     }
 }
 
 // One row block of the pass.
-__device__ __forceinline__ void pass_block(const FactorDesc* __restrict__ factors,
-                                           const RowBlock* __restrict__ blocks,
+// RW rows per wave: SM_ROWS_PER_WAVE for fp32 factors, SM_ROWS_PER_WAVE_HALF
+// for bf16 ones (the same bytes in flight per lane).
+template <int RW, bool HALF>
+__device__ __forceinline__ void pass_block(const FactorDesc& f, const RowBlock& rb,
                                            float4* __restrict__ partials, int b, int maxabs,
                                            int matvec, float4* sred) {
-    const RowBlock rb = blocks[b];
-    const FactorDesc f = factors[rb.factor];
     const Pending q = *f.pend;
     const bool has = q.has != 0;
     if (!has && !matvec) return;   // nothing pending to write, no matvec wanted
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
-    const int rbase = rb.row0 + wave * R;
-    const int nr = max(0, min(R, f.d - rbase));
+    const int rbase = rb.row0 + wave * RW;
+    const int nr = max(0, min(RW, f.d - rbase));
 
-    float dot[R], nrm[R];
+    float dot[RW], nrm[RW];
 #pragma unroll
-    for (int r = 0; r < R; ++r) { dot[r] = 0.f; nrm[r] = 0.f; }
+    for (int r = 0; r < RW; ++r) { dot[r] = 0.f; nrm[r] = 0.f; }
     if (nr > 0) {
         if (matvec) {
-            if (has) pass_rows<true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-            else     pass_rows<false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            if (has) pass_rows<RW, HALF, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else     pass_rows<RW, HALF, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
         } else {
-            pass_rows<true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            pass_rows<RW, HALF, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
         }
     }
     if (!matvec) return;
 
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
+    for (int r = 0; r < RW; ++r) {
         dot[r] = wave_sum(dot[r]);
         nrm[r] = maxabs ? wave_nanmax(nrm[r]) : wave_sum(nrm[r]);
     }
@@ -218,7 +271,7 @@ __device__ __forceinline__ void pass_block(const FactorDesc* __restrict__ factor
     if (lane == 0) {
         float mx = 0.f, sxu = 0.f, sxx = 0.f;
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < RW; ++r) {
             if (r >= nr) break;
             const int row = rbase + r;
             gst(f.u + row, dot[r]);
@@ -249,8 +302,12 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
     const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
     float4* __restrict__ partials, int nblocks, int maxabs, int matvec) {
     __shared__ float4 sred[SM_THREADS / 64];
-    for (int b = blockIdx.x; b < nblocks; b += gridDim.x)
-        pass_block(factors, blocks, partials, b, maxabs, matvec, sred);
+    for (int b = blockIdx.x; b < nblocks; b += gridDim.x) {
+        const RowBlock rb = blocks[b];
+        const FactorDesc f = factors[rb.factor];
+        if (f.half) pass_block<SM_ROWS_PER_WAVE_HALF, true>(f, rb, partials, b, maxabs, matvec, sred);
+        else        pass_block<SM_ROWS_PER_WAVE, false>(f, rb, partials, b, maxabs, matvec, sred);
+    }
 }
 
 // ------------------------------------------------------------------ finalize
