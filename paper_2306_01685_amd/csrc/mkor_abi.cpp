@@ -125,31 +125,39 @@ struct Layout {
     size_t off_rsl = 0, off_rsb = 0, off_x = 0;
     size_t off_mmat = 0, off_mitem = 0, off_mchunk = 0, off_mpart = 0;
     size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
+    size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
     int32_t nh1 = 0, nh2 = 0;
+    int32_t ncvt = 0, ncvtblk = 0;
     int32_t nsecond = 0;
     int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
     int64_t nmeanpart = 0;   // doubles
     std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
+    std::vector<size_t> gh_off;                // per layer: bf16 copy of an fp32 G (bf16 factors)
 };
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
 bool is_half(const mkor_layer& L) { return L.second_order == 1 && L.factor_dtype == MKOR_DTYPE_BF16; }
 
-// Tile shape and contraction length of a GEMM stage.  fp32 factors: stage 1
-// X^T = (Linv G)^T (K = d_in), stage 2 dW_hat = X Rinv (K = d_out).  bf16
-// factors: stage 1 Y^T = (G Rinv)^T (K = d_out), stage 2 dW_hat = Linv Y
-// (K = d_in).  All tile the d_in x d_out output.
-struct StageGeom { int32_t bm, bn; };
-StageGeom stage_geom(int stage, bool half) {
-    if (half) return StageGeom{HG_BM, HG_BN};
-    return StageGeom{GEMM_SHAPE[stage - 1].bm, GEMM_SHAPE[stage - 1].bn};
-}
-int32_t stage_k(const mkor_layer& L, int stage, bool half) {
-    return (stage == 1) != half ? L.d_in : L.d_out;
+// Output tile grid and contraction length of a GEMM stage.  fp32 factors:
+// stage 1 X^T = (Linv G)^T (K = d_in), stage 2 dW_hat = X Rinv (K = d_out),
+// both tiled over d_in x d_out.  bf16 factors: stage 1 Y^T = Rinv G^T
+// (d_out x d_in, K = d_out), stage 2 dW_hat = Linv Y (d_in x d_out, K = d_in).
+struct StageGeom {
+    int32_t bm, bn;      // tile rows, columns
+    int32_t rows, cols;  // output rows, columns
+    int32_t K;
+};
+StageGeom stage_geom(const mkor_layer& L, int stage) {
+    if (is_half(L)) {
+        if (stage == 1) return StageGeom{HG_BI, HG_BJ, L.d_out, L.d_in, L.d_out};
+        return StageGeom{HG_BI, HG_BJ, L.d_in, L.d_out, L.d_in};
+    }
+    const GemmShape& sh = GEMM_SHAPE[stage - 1];
+    return StageGeom{sh.bm, sh.bn, L.d_in, L.d_out, stage == 1 ? L.d_in : L.d_out};
 }
 
 // Tile table of one GEMM stage over the second-order layers with fp32
@@ -163,17 +171,16 @@ int32_t stage_k(const mkor_layer& L, int stage, bool half) {
 // -1.
 std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage, bool half) {
     struct Super { int32_t layer, tm0, tn0, nm, nn, K; };
-    const StageGeom sh = stage_geom(stage, half);
-    const int32_t sm = std::max(1, GEMM_SUPER / sh.bm), sn = std::max(1, GEMM_SUPER / sh.bn);
     std::vector<Super> sup;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         if (!L.second_order || is_half(L) != half) continue;
-        const int32_t tm = ceil_div(L.d_in, sh.bm), tn = ceil_div(L.d_out, sh.bn);
-        const int32_t K = stage_k(L, stage, half);
+        const StageGeom g = stage_geom(L, stage);
+        const int32_t sm = std::max(1, GEMM_SUPER / g.bm), sn = std::max(1, GEMM_SUPER / g.bn);
+        const int32_t tm = ceil_div(g.rows, g.bm), tn = ceil_div(g.cols, g.bn);
         for (int32_t a = 0; a < tm; a += sm)
             for (int32_t b = 0; b < tn; b += sn)
-                sup.push_back(Super{i, a, b, std::min(sm, tm - a), std::min(sn, tn - b), K});
+                sup.push_back(Super{i, a, b, std::min(sm, tm - a), std::min(sn, tn - b), g.K});
     }
     if (sup.empty()) return {};
     std::stable_sort(sup.begin(), sup.end(), [](const Super& x, const Super& y) {
@@ -198,22 +205,29 @@ std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int st
 }
 
 // ||G||^2 partials of a layer (one per stage-1 tile column for fp32 factors,
-// one per stage-1 tile row for bf16 factors) and ||dW_hat||^2 partials (one
-// per tile of the stage that writes dW_hat).
+// one per stage-1 tile column, i.e. per block of G rows, for bf16 factors) and
+// ||dW_hat||^2 partials (one per tile of the stage that writes dW_hat).
 int64_t gpart_count(const mkor_layer& L) {
-    if (is_half(L)) return ceil_div(L.d_in, HG_BM);
-    return ceil_div(L.d_out, GEMM_SHAPE[0].bn);
+    const StageGeom g = stage_geom(L, 1);
+    return ceil_div(g.cols, g.bn);
 }
 int64_t dpart_count(const mkor_layer& L) {
-    const StageGeom g = stage_geom(2, is_half(L));
-    return (int64_t)ceil_div(L.d_in, g.bm) * ceil_div(L.d_out, g.bn);
+    const StageGeom g = stage_geom(L, 2);
+    return (int64_t)ceil_div(g.rows, g.bm) * ceil_div(g.cols, g.bn);
 }
 
+// bf16-factor layer whose gradient is fp32: the GEMMs read a bf16 copy
+bool needs_cvt(const mkor_layer& L) { return is_half(L) && L.grad_dtype == MKOR_DTYPE_F32; }
+
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
-    int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0;
+    int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0, ncvt = 0, ncvtblk = 0;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         rsb += ceil_div((int64_t)L.d_in * L.d_out, RS_ELEMS);
+        if (needs_cvt(L)) {
+            ncvt += 1;
+            ncvtblk += ceil_div((int64_t)L.d_in * L.d_out, CVT_ELEMS);
+        }
         if (!L.second_order) continue;
         Lo.nsecond++;
         const int32_t rows = is_half(L) ? SM_ROWS_HALF : SM_ROWS;
@@ -235,7 +249,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
             mpart += nch * nrb * MEAN_COLS;
         }
     }
-    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX || mitems > INT32_MAX)
+    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX || mitems > INT32_MAX || ncvtblk > INT32_MAX)
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
     Lo.nmeanmat = (int32_t)mmats;
     Lo.nmeanitem = (int32_t)mitems;
@@ -254,6 +268,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.ngpart = (int32_t)gpart;
     Lo.ndpart = (int32_t)g1;
     Lo.nrsblocks = (int32_t)rsb;
+    Lo.ncvt = (int32_t)ncvt;
+    Lo.ncvtblk = (int32_t)ncvtblk;
 
     size_t o = 0;
     auto take = [&](size_t bytes) { o = align_up(o, 256); size_t r = o; o += bytes; return r; };
@@ -272,6 +288,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_mmat = take(sizeof(MeanMat) * Lo.nmeanmat);
     Lo.off_mitem = take(sizeof(MeanItem) * Lo.nmeanitem);
     Lo.off_mchunk = take(sizeof(MeanItem) * Lo.nmeanchunk);
+    Lo.off_cvti = take(sizeof(CvtItem) * Lo.ncvt);
+    Lo.off_cvtb = take(sizeof(CvtBlock) * Lo.ncvtblk);
     // pending terms start out empty (has = 0): the upload initialises them
     Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
     Lo.table_bytes = align_up(o, 256);
@@ -294,6 +312,9 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         // X^T (fp32) of fp32-factor layers, Y^T (bf16) of bf16-factor layers
         Lo.x_off[i] = take((is_half(layers[i]) ? 2 : 4) * (size_t)layers[i].d_in * layers[i].d_out);
     }
+    Lo.gh_off.assign(n, 0);
+    for (int32_t i = 0; i < n; ++i)
+        if (needs_cvt(layers[i])) Lo.gh_off[i] = take(2 * (size_t)layers[i].d_in * layers[i].d_out);
     Lo.total = align_up(o, 256);
     (void)usum;
     return MKOR_OK;
@@ -393,6 +414,9 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     HgLayer* h2l = reinterpret_cast<HgLayer*>(host.data() + lo.off_h2l);
     GemmTile* h1t = reinterpret_cast<GemmTile*>(host.data() + lo.off_h1t);
     GemmTile* h2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_h2t);
+    CvtItem* cvi = reinterpret_cast<CvtItem*>(host.data() + lo.off_cvti);
+    CvtBlock* cvb = reinterpret_cast<CvtBlock*>(host.data() + lo.off_cvtb);
+    int32_t nci = 0, ncb = 0;
     RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
     RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
     Pending* pend_h = reinterpret_cast<Pending*>(host.data() + lo.off_pend);
@@ -466,20 +490,29 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         R.gpart0 = gp; R.ngpart = ngp;
         R.dpart0 = dp; R.ndpart = ndp;
         if (half) {
-            // Y = G R (Y^T stored bf16 in the workspace), then dW_hat = L Y
+            // Y^T = R G^T (stored bf16 in the workspace), then dW_hat = L Y;
+            // an fp32 G is first copied to bf16 in the workspace
             void* Yt = base + lo.x_off[i];
+            const void* Gq = L.G;
+            if (needs_cvt(L)) {
+                unsigned short* gh = reinterpret_cast<unsigned short*>(base + lo.gh_off[i]);
+                const int64_t ne = (int64_t)L.d_in * L.d_out;
+                cvi[nci] = CvtItem{static_cast<const float*>(L.G), gh, ne};
+                for (int64_t o = 0; o < ne; o += CVT_ELEMS) cvb[ncb++] = CvtBlock{nci, 0, o};
+                ++nci;
+                Gq = gh;
+            }
+            const StageGeom s1 = stage_geom(L, 1), s2 = stage_geom(L, 2);
             HgLayer& A = h1l[i];
-            A.A = L.G; A.B = L.Rinv; A.C = Yt;
+            A.P = L.Rinv; A.Q = Gq; A.C = Yt;
             A.pend = fR.pend; A.w = fR.w;
-            A.M = L.d_in; A.N = L.d_out; A.K = L.d_out;
-            A.a_f32 = bf16 ? 0 : 1;
-            A.part0 = gp; A.ntn = ceil_div(L.d_out, HG_BN);
+            A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
+            A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
             HgLayer& B = h2l[i];
-            B.A = L.Linv; B.B = Yt; B.C = L.dW;
+            B.P = L.Linv; B.Q = Yt; B.C = L.dW;
             B.pend = fL.pend; B.w = fL.w;
-            B.M = L.d_in; B.N = L.d_out; B.K = L.d_in;
-            B.a_f32 = 0;
-            B.part0 = dp; B.ntn = ceil_div(L.d_out, HG_BN);
+            B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
+            B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
             gp += ngp;
             dp += ndp;
             continue;
@@ -559,9 +592,12 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
                                reinterpret_cast<const GemmTile*>(ws + lo.off_g1t), lo.ng1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "gemm_xt launch");
+            e = launch_cvt_bf16(reinterpret_cast<const CvtItem*>(ws + lo.off_cvti),
+                                reinterpret_cast<const CvtBlock*>(ws + lo.off_cvtb), lo.ncvtblk, s);
+            if (e != hipSuccess) return hip_fail(e, "bf16 gradient copy launch");
             e = launch_hgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_h1l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_h1t), lo.nh1, gpart, s);
-            if (e != hipSuccess) return hip_fail(e, "bf16 gemm (G R) launch");
+            if (e != hipSuccess) return hip_fail(e, "bf16 gemm (R G^T) launch");
             return MKOR_OK;
         case MKOR_STAGE_GEMM_DW:
             e = launch_gemm_dw(reinterpret_cast<const GemmLayer*>(ws + lo.off_g2l),

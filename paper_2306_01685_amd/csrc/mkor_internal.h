@@ -138,33 +138,52 @@ constexpr int GEMM_XCDS = 8;
 constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 
 // ---------------------------------------------------------------- half factors
-// bf16 MFMA GEMMs of layers with bf16 factors (C[m][n] = sum_k A[m][k] B[n][k],
-// both operands row-major along k): stage 1 Y^T = (G R)^T in bf16, stage 2
-// dW_hat = L Y (see precond_hgemm.hip).
-#ifndef MKOR_HG_BN
-#define MKOR_HG_BN 256
+// bf16 MFMA GEMMs of layers with bf16 factors (see precond_hgemm.hip).  Both
+// stages are  C = P_eff Q^T  with the factor as P (rows i of C) and a data
+// matrix as Q (rows j of C), both contiguous along k:
+//   stage 1:  Y^T = R G^T        P = S_R, Q = G (bf16), C = Y^T (bf16, d_out x d_in)
+//   stage 2:  dW_hat = L Y       P = S_L, Q = Y^T,      C = dW_hat (fp32, d_in x d_out)
+// where P_eff = c1 S + c2 I + sgn w w^T is the factor with its pending term.
+#ifndef MKOR_HG_BI
+#define MKOR_HG_BI 256
 #endif
-#ifndef MKOR_HG_WN
-#define MKOR_HG_WN 4
+#ifndef MKOR_HG_BJ
+#define MKOR_HG_BJ 256
 #endif
-constexpr int HG_BM = 256, HG_BN = MKOR_HG_BN, HG_BK = 64;
-constexpr int HG_WM = 2, HG_WN = MKOR_HG_WN;       // wave grid of a tile
-constexpr int HG_THREADS = 64 * HG_WM * HG_WN;
+#ifndef MKOR_HG_NS
+#define MKOR_HG_NS 4
+#endif
+constexpr int HG_BI = MKOR_HG_BI, HG_BJ = MKOR_HG_BJ;   // tile of C (rows i x columns j)
+constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 x 64
+constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
 
 struct HgLayer {
-    const void*    A;      // stage 1: G (bf16, or fp32 when a_f32); stage 2: S_L (bf16)
-    const void*    B;      // stage 1: S_R (bf16); stage 2: Y^T (bf16)
-    void*          C;      // stage 1: Y^T (bf16, d_out x d_in); stage 2: dW_hat (fp32)
-    const Pending* pend;   // pending term of the factor operand (B in stage 1, A in stage 2)
-    const float*   w;      // its w vector
-    int32_t        M, N, K;
-    int32_t        a_f32;
+    const void*    P;      // factor S (bf16, I x K)
+    const void*    Q;      // bf16 J x K
+    void*          C;      // I x J: bf16 (stage 1) or fp32 (stage 2)
+    const Pending* pend;   // pending term of the factor
+    const float*   w;      // its w vector (K = I entries)
+    int32_t        I, J, K;
     int32_t        part0;  // first partial slot of this layer
-    int32_t        ntn;    // number of N tiles
+    int32_t        ntj;    // number of column tiles
+    int32_t        _pad;
 };
+
+// fp32 -> bf16 copy of fp32 gradients of bf16-factor layers (the stage-1 Q)
+struct CvtItem {
+    const float*    src;
+    unsigned short* dst;
+    int64_t         n;      // elements (a multiple of 8)
+};
+struct CvtBlock {
+    int32_t item, _pad;
+    int64_t off;            // first element of this workgroup's range
+};
+constexpr int CVT_ELEMS = 1 << 16;   // elements per workgroup of the conversion
 
 hipError_t launch_hgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream);
+hipError_t launch_cvt_bf16(const CvtItem* items, const CvtBlock* blocks, int32_t nblocks, hipStream_t stream);
 
 // ---------------------------------------------------------------- rescale
 struct RescaleLayer {

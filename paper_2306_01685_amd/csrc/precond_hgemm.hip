@@ -1,36 +1,47 @@
 // Preconditioning for layers whose inverse factors are stored in bf16
-// (half-precision factors: the paper's "half-precision" MKOR; its Table 1 halves
-// the memory and the communication for it).  bf16 MFMA GEMMs
-// (v_mfma_f32_32x32x16_bf16, fp32 accumulation), in the association
-// dW_hat = L (G R):
+// (half-precision factors: the paper's half-precision MKOR, whose Table 1
+// halves the memory and the communication).  bf16 MFMA GEMMs
+// (v_mfma_f32_32x32x16_bf16, fp32 accumulation) in the association
+// dW_hat = L (G R), each stage written as  C = P_eff Q^T  with the factor as P:
 //
-//   stage H1:  Y = G R          A = G (d_in x d_out, bf16 or fp32 rounded to
-//                               bf16), B = R (d_out x d_out), stored Y^T in bf16
-//                               (d_out x d_in), plus ||G||^2 partials;
-//   stage H2:  dW_hat = L Y     A = L (d_in x d_in), B = Y^T; dW_hat fp32 into
-//                               dW, plus one ||dW_hat||^2 partial per tile.
+//   stage 1:  Y^T = R G^T     P = S_R (d_out x d_out), Q = G in bf16 (d_in x
+//                             d_out), C = Y^T rounded to bf16 (d_out x d_in),
+//                             plus ||G||^2 partials;
+//   stage 2:  dW_hat = L Y    P = S_L (d_in x d_in), Q = Y^T (d_out x d_in),
+//                             C = dW_hat in fp32 (d_in x d_out), plus one
+//                             ||dW_hat||^2 partial per tile.
 //
-// Both are C[m][n] = sum_k A[m][k] B[n][k] with both operands contiguous along
-// k in their natural layout (the factors are symmetric, and Y is stored
-// transposed), which is the layout the MFMA wants: each lane supplies 8
-// consecutive k of one row.
+// Both operands are contiguous along k in their natural layout (the factors
+// are symmetric), which is what the MFMA wants: each lane supplies 8
+// consecutive k of one row of P (output row i) and of Q (output column j).
 //
-// The current factor is its stored (bf16) value S plus the pending rank-1
-// term of the SM update, P = c1 S + c2 I + sgn w w^T (see struct Pending).
-// The GEMMs multiply with S and add the rest in the epilogue:
-//   G P = c1 (G S) + c2 G + sgn (G w) w^T,   P Y = c1 (S Y) + c2 Y + sgn w (w^T Y),
-// where the vector G w (or w^T Y) is summed from the other operand while it is
-// staged into LDS (one fma per staged element), and G (or Y) at the output
-// positions is read in the epilogue.  So the MFMA loop stays free of per-element
-// arithmetic.
+// The factor is its stored bf16 value S plus the pending rank-1 term of the SM
+// update, P_eff = c1 S + c2 I + sgn w w^T (struct Pending).  The MFMAs multiply
+// with S; the epilogue adds the rest,
+//   C[i][j] = c1 (S Q^T)[i][j] + c2 Q[j][i] + sgn w[i] (Q w)[j],
+// where (Q w) is summed from the Q rows while they sit in LDS, and Q[j][i] is
+// read at the output positions (4 consecutive i of one row j: one 8-byte load).
 //
-// Tiles: 256 x 256 per workgroup of 8 waves (2 x 4, each 128 x 64 = 4 x 2 MFMA
-// blocks), so two waves share each SIMD and one issues MFMAs while the other
-// waits on LDS or the slab barrier.  K runs in 64-deep slabs double-buffered in
-// LDS (128 KB of the 160 KB) as [row][k] bf16 with the 16-byte chunk index
-// XOR-swizzled by the row, so the 16-byte operand reads of a wave hit distinct
-// banks.  d_in and d_out must be multiples of 64 (checked by the plan); M and
-// N edges are masked.
+// Tiles of HG_BI x HG_BJ outputs (256 x 256), waves of 128 x 64 (4 x 2 MFMA
+// blocks), two waves per SIMD.  K runs in slabs of 32 through an HG_NS-stage
+// LDS ring (4 stages, 128 KB) filled by direct global-to-LDS loads
+// (global_load_lds_dwordx4: lane l of a wave's instruction writes 16 bytes at
+// M0 + 16 l), so up to three slabs are in flight while one is multiplied and no
+// registers hold staged data.  (256 x 128 tiles with two workgroups per CU,
+// which overlap one workgroup's epilogue with the other's MFMAs, measured a
+// few per cent slower: the vector memory path then carries 1.5x the bytes.)  Each lane loads the
+// global chunk that belongs at its LDS slot, which realises the swizzle
+//   byte(r, c) = 64 r + 16 (c ^ ((r >> 2) & 3))     (64-byte rows, 4 chunks)
+// under which the 16 rows of an MFMA operand read, and the 8 rows x 2 chunks
+// of a rank-1 read, fall on 16 distinct 16-byte bank groups.
+//
+// The K loop holds no compiler-visible global access: completion of the
+// direct loads is tracked by hand with s_waitcnt vmcnt (loads complete in
+// order, so waiting until at most n are outstanding leaves exactly the last n
+// issued), and the slab barrier is a bare s_barrier (the compiler's barrier
+// would also wait for every prefetch).  d_in and d_out are multiples of 64
+// (checked by the plan); tile edges are masked, rows past the edge are loaded
+// clamped to the last row and never stored.
 #include "gmem.h"
 #include "mkor_internal.h"
 
@@ -38,33 +49,74 @@ namespace mkor {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 // LDS pointers carry their address space, so every operand access is a
 // ds_read / ds_write (a generic pointer would become a flat access, which
-// waits on the global-load counter too).
+// also waits on the global-load counter).
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) mk_u4 lds_u4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
 typedef __attribute__((address_space(3))) float lds_float;
-typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) unsigned short lds_u16;
 
-constexpr int BM = HG_BM, BN = HG_BN, BK = HG_BK, NT = HG_THREADS;
-constexpr int WM = HG_WM, WN = HG_WN;
-constexpr int TM = BM / WM, TN = BN / WN;   // 128 x 64 per wave
-constexpr int FM = TM / 32, FN = TN / 32;   // 4 x 2 MFMA blocks
-constexpr int KCH = BK / 8;                 // 16-byte chunks per slab row (8)
-constexpr int ACH = BM * KCH / NT;          // A chunks per thread and slab
-constexpr int BCH = BN * KCH / NT;          // B chunks per thread and slab
-static_assert(NT == WM * WN * 64 && KCH == 8 && TM == 128 && TN == 64, "layout");
-static_assert(ACH * NT == BM * KCH && BCH * NT == BN * KCH, "staging");
-static_assert(NT % KCH == 0, "a thread stages one fixed chunk column");
+constexpr int BI = HG_BI, BJ = HG_BJ, NT = HG_THREADS;
+constexpr int WI = BI / 128, WJ = BJ / 64;   // wave grid
+constexpr int TI = BI / WI, TJ = BJ / WJ;     // 128 x 64 per wave
+constexpr int FI = TI / 32, FJ = TJ / 32;     // 4 x 2 MFMA blocks
+static_assert(NT == WI * WJ * 64 && TI == 128 && TJ == 64, "wave layout");
 
-// byte offset of 16-byte chunk c of row r in a [rows][BK] bf16 slab
-__device__ __forceinline__ int swz(int r, int c) { return r * (BK * 2) + ((c ^ (r & 7)) << 4); }
+constexpr int BK = 32, NS = HG_NS;            // slab depth, ring stages
+constexpr int ROWB = BK * 2;                  // bytes per slab row
+constexpr int PB = BI * ROWB, QB = BJ * ROWB; // P and Q bytes per stage
+constexpr int STB = PB + QB;
+constexpr int WSLOT = 256;                    // w[k0 .. k0 + 64) per stage (32 used)
+constexpr int NW = NT / 64;
+constexpr int PBLK = PB / 1024 / NW, QBLK = QB / 1024 / NW;   // 1-KB load blocks per wave and slab
+static_assert(PB % (1024 * NW) == 0 && QB % (1024 * NW) == 0, "load blocks per wave");
+static_assert(2 * BJ == NT, "rank-1 reads: one half Q row per thread");
+constexpr int RING = NS * STB;
+constexpr int CPITCH = BJ * 2 + 16;           // stage-1 output staging: bf16 row pitch (padded)
+// stage-1 output rows staged per pass (whole waves' rows, as many as the ring holds)
+constexpr int CROWS = (RING / CPITCH) / TI * TI < BI ? (RING / CPITCH) / TI * TI : BI;
+static_assert(CROWS >= TI, "output staging holds a wave's rows");
+constexpr int SMEM = RING + NS * WSLOT + 4 * (BJ + NW);
+
+__device__ __forceinline__ int swz(int r, int c) { return r * ROWB + ((c ^ ((r >> 2) & 3)) << 4); }
+
+__device__ __forceinline__ void dma16(unsigned lds, unsigned voff, const void* base) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
+                 : "memory");
+}
+__device__ __forceinline__ void dma4(unsigned lds, unsigned voff, const void* base) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(voff), "s"(base)
+                 : "memory");
+}
+
+// Wait until this wave's loads of a slab have landed, with `ahead` (at most
+// 2) later slabs of D instructions each still in flight.
+template <int D>
+__device__ __forceinline__ void dma_wait(int ahead) {
+    if (ahead >= 2)      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * D) : "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(D) : "memory");
+    else                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+static_assert(NS >= 2 && NS <= 4, "dma_wait covers up to two slabs in flight behind the awaited one");
+
+__device__ __forceinline__ void slab_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
     return v;
+}
+
+__device__ __forceinline__ void unpack8(const mk_u4& h, float (&v)[8]) {
+    const unsigned u[4] = {h.x, h.y, h.z, h.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = bf2f((unsigned short)(u[i] & 0xffffu));
+        v[2 * i + 1] = bf2f((unsigned short)(u[i] >> 16));
+    }
 }
 
 struct HgArgs {
@@ -73,237 +125,180 @@ struct HgArgs {
     float* partials;
 };
 
-// Dot of 8 staged values with 8 w values (fma chain in a fixed order).
-__device__ __forceinline__ float dot8(const uint4& h, const float* w, float acc) {
-    acc = fmaf(bf2f((unsigned short)(h.x & 0xffffu)), w[0], acc);
-    acc = fmaf(bf2f((unsigned short)(h.x >> 16)), w[1], acc);
-    acc = fmaf(bf2f((unsigned short)(h.y & 0xffffu)), w[2], acc);
-    acc = fmaf(bf2f((unsigned short)(h.y >> 16)), w[3], acc);
-    acc = fmaf(bf2f((unsigned short)(h.z & 0xffffu)), w[4], acc);
-    acc = fmaf(bf2f((unsigned short)(h.z >> 16)), w[5], acc);
-    acc = fmaf(bf2f((unsigned short)(h.w & 0xffffu)), w[6], acc);
-    acc = fmaf(bf2f((unsigned short)(h.w >> 16)), w[7], acc);
-    return acc;
-}
-
-__device__ __forceinline__ float sq8(const uint4& h, float acc) {
-    const unsigned v[4] = {h.x, h.y, h.z, h.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float lo = bf2f((unsigned short)(v[i] & 0xffffu)), hi = bf2f((unsigned short)(v[i] >> 16));
-        acc = fmaf(lo, lo, acc);
-        acc = fmaf(hi, hi, acc);
-    }
-    return acc;
-}
-
-// 8 fp32 -> 8 bf16 (rounded) packed into 16 bytes
-__device__ __forceinline__ uint4 pack8(const float4& a, const float4& b) {
-    return make_uint4(f2bf2(a.x, a.y), f2bf2(a.z, a.w), f2bf2(b.x, b.y), f2bf2(b.z, b.w));
-}
-
-// Loads the 8 elements (row, k .. k + 7) of a row-major bf16 (or fp32,
-// rounded) operand with leading dimension ld.  Rows at or past nrows are
-// clamped to the last row (no branch in the K loop); their products land in
-// output rows or columns the epilogue never stores.
-template <bool F32>
-__device__ __forceinline__ uint4 load_chunk(const void* base, int ld, int row, int nrows, int k) {
-    const size_t off = (size_t)min(row, nrows - 1) * ld + k;
-    if constexpr (F32) {
-        const float* p = static_cast<const float*>(base) + off;
-        return pack8(gld4(p), gld4(p + 4));
-    } else {
-        return gld_u4(static_cast<const unsigned short*>(base) + off);
-    }
-}
-
-// STAGE 1: A = G (AF32: fp32 G), B = S_R (factor), rank-1 vector from A (G w_R).
-// STAGE 2: A = S_L (factor), B = Y^T, rank-1 vector from B (w_L^T Y).
-template <int STAGE, bool AF32, bool PEND>
+template <int STAGE, bool PEND>
 __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
                            lds_char* smem) {
-    lds_char* const A0 = smem;
-    lds_char* const A1 = smem + BM * BK * 2;
-    lds_char* const B0 = smem + 2 * BM * BK * 2;
-    lds_char* const B1 = B0 + BN * BK * 2;
-    lds_float* rvec = (lds_float*)(smem + 2 * (BM + BN) * BK * 2);   // BM (stage 1) or BN floats
-    lds_float* red = rvec + (BM > BN ? BM : BN);
-
-    const int m0 = tile.tm * BM, n0 = tile.tn * BN;
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int wm = wave % WM, wn = wave / WM;
+    const int i0 = tile.tm * BI, j0 = tile.tn * BJ;
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int wi = wave % WI, wj = wave / WI;
     const int li = lane & 31, lk = lane >> 5;
-    const int M = L.M, N = L.N, K = L.K;
-    const int cch = t % KCH;   // the 16-byte chunk column this thread stages
-    // stage 1: ||G||^2 from the A (= G) staging of the first tile column
-    const bool want_gsq = STAGE == 1 && tile.tn == 0;
+    const int I = L.I, J = L.J, K = L.K;
+    const bool want_gsq = STAGE == 1 && tile.tm == 0;   // ||G||^2: each Q row once
+    lds_float* rvec = (lds_float*)(smem + RING + NS * WSLOT);
+    lds_float* red = rvec + BJ;
+    const unsigned lds0 = (unsigned)(size_t)smem;
 
-    floatx16 acc[FM][FN];
+    floatx16 acc[FI][FJ];
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int a = 0; a < FI; ++a)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int b = 0; b < FJ; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-    // rank-1 partial dots of the rows this thread stages (A rows in stage 1,
-    // B rows in stage 2)
-    constexpr int RCH = STAGE == 1 ? ACH : BCH;
-    float rdot[RCH];
+    // this lane's load sources at k0 = 0 (byte offsets from the operand base)
+    const int dc = (lane & 3) ^ ((lane >> 4) & 3);   // chunk that belongs at the lane's LDS slot
+    unsigned vp[PBLK], vq[QBLK];
 #pragma unroll
-    for (int i = 0; i < RCH; ++i) rdot[i] = 0.f;
-    float gsq = 0.f;
-
-    uint4 ra[ACH], rb[BCH];
-    const int nslab = K / BK;
-    auto load = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < ACH; ++i) {
-            const int row = (t + i * NT) / KCH;
-            ra[i] = load_chunk<STAGE == 1 && AF32>(L.A, K, m0 + row, M, k0 + 8 * cch);
-        }
-#pragma unroll
-        for (int i = 0; i < BCH; ++i) {
-            const int row = (t + i * NT) / KCH;
-            rb[i] = load_chunk<false>(L.B, K, n0 + row, N, k0 + 8 * cch);
-        }
-    };
-    auto store = [&](int k0, lds_char* Ad, lds_char* Bd) {
-        float wk[8];
-        if (PEND) {
-            const float4 w0 = gld4(L.w + k0 + 8 * cch), w1 = gld4(L.w + k0 + 8 * cch + 4);
-            wk[0] = w0.x; wk[1] = w0.y; wk[2] = w0.z; wk[3] = w0.w;
-            wk[4] = w1.x; wk[5] = w1.y; wk[6] = w1.z; wk[7] = w1.w;
-        }
-#pragma unroll
-        for (int i = 0; i < ACH; ++i) {
-            const int row = (t + i * NT) / KCH;
-            *(lds_u4*)(Ad + swz(row, cch)) = mk_u4{ra[i].x, ra[i].y, ra[i].z, ra[i].w};
-            if constexpr (STAGE == 1) {
-                if (PEND) rdot[i] = dot8(ra[i], wk, rdot[i]);
-                // ||G||^2 over real rows only (clamped rows repeat the last one)
-                if (want_gsq) gsq = (m0 + row < M) ? sq8(ra[i], gsq) : gsq;
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < BCH; ++i) {
-            const int row = (t + i * NT) / KCH;
-            *(lds_u4*)(Bd + swz(row, cch)) = mk_u4{rb[i].x, rb[i].y, rb[i].z, rb[i].w};
-            if constexpr (STAGE == 2) {
-                if (PEND) rdot[i] = dot8(rb[i], wk, rdot[i]);
-            }
-        }
-    };
-
-    // operands of one 16-deep k-step of a slab
-    auto frags = [&](const lds_char* Ac, const lds_char* Bc, int ks, bf16x8 (&a)[FM], bf16x8 (&b)[FN]) {
-        const int c = 2 * ks + lk;
-#pragma unroll
-        for (int i = 0; i < FM; ++i) a[i] = *(const lds_bf8*)(Ac + swz(wm * TM + i * 32 + li, c));
-#pragma unroll
-        for (int j = 0; j < FN; ++j) b[j] = *(const lds_bf8*)(Bc + swz(wn * TN + j * 32 + li, c));
-    };
-    auto mma = [&](const bf16x8 (&a)[FM], const bf16x8 (&b)[FN]) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    };
-    constexpr int KS = BK / 16;         // k-steps per slab
-    constexpr int DS = FM + FN;         // LDS operand reads per k-step
-
-    load(0);
-    store(0, A0, B0);
-    __syncthreads();
-    for (int s = 0; s < nslab; ++s) {
-        const int cur = s & 1;
-        const bool more = s + 1 < nslab;
-        if (more) load((s + 1) * BK);
-        const lds_char* Ac = cur ? A1 : A0;
-        const lds_char* Bc = cur ? B1 : B0;
-        // one operand set per k-step: the other wave on the SIMD issues its
-        // MFMAs while this one waits for its LDS reads
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            bf16x8 a[FM], b[FN];
-            frags(Ac, Bc, ks, a, b);
-            mma(a, b);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x020, 32, 0);   // global loads of the next slab
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
-        }
-        if (more) store((s + 1) * BK, cur ? A0 : A1, cur ? B0 : B1);
-        __syncthreads();
+    for (int b = 0; b < PBLK; ++b) {
+        const int r = 16 * (PBLK * wave + b) + (lane >> 2);
+        vp[b] = ((unsigned)min(i0 + r, I - 1) * (unsigned)K + 8u * dc) * 2u;
     }
-
-    // complete the rank-1 vector of the tile: the KCH threads of a row (adjacent
-    // lanes) hold partial dots over their chunk columns
-    constexpr int RROWS = STAGE == 1 ? BM : BN;
-    if (PEND) {
 #pragma unroll
-        for (int i = 0; i < RCH; ++i) {
-            float v = rdot[i];
-#pragma unroll
-            for (int o = 1; o < KCH; o <<= 1) v += __shfl_xor(v, o, 64);
-            if (cch == 0) rvec[(t + i * NT) / KCH] = v;
-        }
+    for (int b = 0; b < QBLK; ++b) {
+        const int r = 16 * (QBLK * wave + b) + (lane >> 2);
+        vq[b] = ((unsigned)min(j0 + r, J - 1) * (unsigned)K + 8u * dc) * 2u;
     }
-    (void)RROWS;
-    __syncthreads();
+    const int nst = K / BK;
+    constexpr int D = PBLK + QBLK;               // load instructions per wave and slab
+    const bool wload = PEND && wave == 0;        // wave 0 also brings the slab's slice of w
+    auto issue = [&](int st) {
+        const unsigned buf = lds0 + (unsigned)(st % NS) * STB;
+        const unsigned kb = (unsigned)st * ROWB;
+#pragma unroll
+        for (int b = 0; b < PBLK; ++b) dma16(buf + (PBLK * wave + b) * 1024, vp[b] + kb, L.P);
+#pragma unroll
+        for (int b = 0; b < QBLK; ++b) dma16(buf + PB + (QBLK * wave + b) * 1024, vq[b] + kb, L.Q);
+        if (wload)
+            dma4(lds0 + RING + (unsigned)(st % NS) * WSLOT, (unsigned)min(st * BK + lane, K - 1) * 4u, L.w);
+    };
 
-    const float c1 = PEND ? q.c1 : 1.f, c2 = PEND ? q.c2 : 0.f, sg = PEND ? q.sgn : 0.f;
-    float csq = 0.f;
+    // rank-1 dot (and ||G||^2) of this thread's half Q row: row t / 2, chunks
+    // 2 h and 2 h + 1, summed in a fixed order over the slabs
+    const int rr = t >> 1, rh = t & 1;
+    float rdot = 0.f, gsq = 0.f;
+    const bool gsq_row = want_gsq && j0 + rr < J;
+
+    for (int st = 0; st < NS - 1 && st < nst; ++st) issue(st);
+    for (int s = 0; s < nst; ++s) {
+        const int ahead = min(NS - 2, nst - 1 - s);
+        if (wload) dma_wait<D + 1>(ahead);
+        else       dma_wait<D>(ahead);
+        slab_barrier();   // every wave's slab s has landed; slab s - 1 is no longer read
+        if (s + NS - 1 < nst) issue(s + NS - 1);
+        const lds_char* Pb = smem + (s % NS) * STB;
+        const lds_char* Qb = Pb + PB;
 #pragma unroll
-    for (int mi = 0; mi < FM; ++mi) {
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            const int c = 2 * ks + lk;
+            bf16x8 a[FI], b[FJ];
 #pragma unroll
-        for (int ni = 0; ni < FN; ++ni) {
-            const int nl = wn * TN + ni * 32 + li, n = n0 + nl;
+            for (int x = 0; x < FI; ++x) a[x] = *(const lds_bf8*)(Pb + swz(wi * TI + x * 32 + li, c));
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int ml = wm * TM + mi * 32 + 8 * g + 4 * lk, mb = m0 + ml;
-                if (n >= N || mb >= M) continue;   // M, N are multiples of 64: 4 rows all in or all out
-                float v[4] = {acc[mi][ni][4 * g + 0], acc[mi][ni][4 * g + 1], acc[mi][ni][4 * g + 2],
-                              acc[mi][ni][4 * g + 3]};
-                if constexpr (STAGE == 1) {
-                    // Y = c1 (G S) + c2 G + sgn (G w) w^T, stored transposed in bf16
-                    if (PEND) {
-                        const float wn_ = gld(L.w + n);
+            for (int y = 0; y < FJ; ++y) b[y] = *(const lds_bf8*)(Qb + swz(wj * TJ + y * 32 + li, c));
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const size_t go = (size_t)(mb + e) * K + n;   // G is d_in x d_out, K = d_out
-                            const float gv = AF32 ? bf2f(f2bf(gld(static_cast<const float*>(L.A) + go)))
-                                                  : bf2f(gld_u16(static_cast<const unsigned short*>(L.A) + go));
-                            v[e] = fmaf(c1, v[e], fmaf(c2, gv, sg * rvec[ml + e] * wn_));
-                        }
-                    }
-                    unsigned short* dst = static_cast<unsigned short*>(L.C) + (size_t)n * M + mb;
-                    const uint2 h = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
-                    gst_u2(dst, h);
-                } else {
-                    // dW_hat = c1 (S Y) + c2 Y + sgn w (w^T Y); Y[m][n] = Y^T[n][m]
-                    if (PEND) {
-                        const unsigned short* yt = static_cast<const unsigned short*>(L.B) + (size_t)n * K + mb;
-                        const uint2 yh = gld_u2(yt);
-                        const float y[4] = {bf2f((unsigned short)(yh.x & 0xffffu)), bf2f((unsigned short)(yh.x >> 16)),
-                                            bf2f((unsigned short)(yh.y & 0xffffu)), bf2f((unsigned short)(yh.y >> 16))};
-                        const float rn = rvec[nl];
+            for (int x = 0; x < FI; ++x)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            v[e] = fmaf(c1, v[e], fmaf(c2, y[e], sg * gld(L.w + mb + e) * rn));
-                    }
-                    float* dst = static_cast<float*>(L.C) + (size_t)mb * N + n;
+                for (int y = 0; y < FJ; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
+        }
+        if (PEND || want_gsq) {
+            const lds_float* wsl = (const lds_float*)(smem + RING + (s % NS) * WSLOT);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        gst(dst + (size_t)e * N, v[e]);
-                        csq = fmaf(v[e], v[e], csq);
-                    }
+            for (int e = 0; e < 2; ++e) {
+                const int c = 2 * rh + e;
+                float v[8];
+                const mk_u4 hv = *(const lds_u4*)(Qb + swz(rr, c));
+                unpack8(hv, v);
+                if (PEND) {
+#pragma unroll
+                    for (int x = 0; x < 8; ++x) rdot = fmaf(v[x], wsl[8 * c + x], rdot);
+                }
+                if (STAGE == 1 && gsq_row) {
+#pragma unroll
+                    for (int x = 0; x < 8; ++x) gsq = fmaf(v[x], v[x], gsq);
                 }
             }
         }
+    }
+
+    if (PEND) {
+        const float v = rdot + __shfl_xor(rdot, 1, 64);
+        if (rh == 0) rvec[rr] = v;
+    }
+    __syncthreads();   // rvec complete; the ring is free for the output staging
+
+    const float c1 = PEND ? q.c1 : 1.f, c2 = PEND ? q.c2 : 0.f, sg = PEND ? q.sgn : 0.f;
+    float csq = 0.f;
+    // value of one output group (rows i .. i + 3 of column j) with the rest of
+    // the pending term: C[i][j] += c2 Q[j][i] + sgn w[i] (Q w)[j]
+    auto finish = [&](int x, int y, int g, float (&v)[4]) {
+        const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
+        const int i = i0 + wi * TI + x * 32 + 8 * g + 4 * lk;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[x][y][4 * g + e];
+        if (PEND && i < I && j < J) {
+            const uint2 qh = gld_u2(static_cast<const unsigned short*>(L.Q) + (size_t)j * K + i);
+            const float qv[4] = {bf2f((unsigned short)(qh.x & 0xffffu)), bf2f((unsigned short)(qh.x >> 16)),
+                                 bf2f((unsigned short)(qh.y & 0xffffu)), bf2f((unsigned short)(qh.y >> 16))};
+            const float4 wv = gld4(L.w + i);
+            const float wa[4] = {wv.x, wv.y, wv.z, wv.w};
+            const float rq = rvec[jl];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[e], sg * wa[e] * rq));
+        }
+    };
+    if constexpr (STAGE == 1) {
+        // bf16 through an LDS staging tile, CROWS rows per pass, then stored
+        // 16 bytes per lane along the rows of Y^T
+        constexpr int CH = BJ / 8;   // 16-byte chunks per row
+        for (int p0 = 0; p0 < BI; p0 += CROWS) {
+            if (wi * TI >= p0 && wi * TI < p0 + CROWS) {
+#pragma unroll
+                for (int x = 0; x < FI; ++x)
+#pragma unroll
+                    for (int y = 0; y < FJ; ++y)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            float v[4];
+                            finish(x, y, g, v);
+                            const int jl = wj * TJ + y * 32 + li;
+                            const int il = wi * TI + x * 32 + 8 * g + 4 * lk - p0;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) *(lds_u16*)(smem + (il + e) * CPITCH + 2 * jl) = f2bf(v[e]);
+                        }
+            }
+            __syncthreads();
+            for (int u = t; u < CROWS * CH; u += NT) {
+                const int il = u / CH, cj = u % CH;
+                const int i = i0 + p0 + il, j = j0 + 8 * cj;
+                if (i < I && j < J) {
+                    const mk_u4 h = *(const lds_u4*)(smem + il * CPITCH + 16 * cj);
+                    gst_u4(static_cast<unsigned short*>(L.C) + (size_t)i * J + j, make_uint4(h.x, h.y, h.z, h.w));
+                }
+            }
+            __syncthreads();
+        }
+    } else {
+#pragma unroll
+        for (int x = 0; x < FI; ++x)
+#pragma unroll
+            for (int y = 0; y < FJ; ++y)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int j = j0 + wj * TJ + y * 32 + li;
+                    const int i = i0 + wi * TI + x * 32 + 8 * g + 4 * lk;
+                    if (i >= I || j >= J) continue;   // I, J multiples of 64: 4 rows all in or all out
+                    float v[4];
+                    finish(x, y, g, v);
+                    float* dst = static_cast<float*>(L.C) + (size_t)i * J + j;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        gst(dst + (size_t)e * J, v[e]);
+                        csq = fmaf(v[e], v[e], csq);
+                    }
+                }
     }
 
     // partials: block-wide fixed-order sums
@@ -313,28 +308,34 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     __syncthreads();
     if (t == 0 && (STAGE == 2 || want_gsq)) {
         float s = 0.f;
-        for (int w = 0; w < NT / 64; ++w) s += red[w];
-        if (STAGE == 1) gst(partials + L.part0 + tile.tm, s);
-        else            gst(partials + L.part0 + tile.tm * L.ntn + tile.tn, s);
+        for (int w = 0; w < NW; ++w) s += red[w];
+        if (STAGE == 1) gst(partials + L.part0 + tile.tn, s);
+        else            gst(partials + L.part0 + tile.tm * L.ntj + tile.tn, s);
     }
 }
 
-constexpr int HG_SMEM = 2 * (BM + BN) * BK * 2 + 4 * ((BM > BN ? BM : BN) + NT / 64);
-
+// 8 waves per CU (2 per SIMD): at most 256 VGPRs per lane.
 template <int STAGE>
-__global__ __launch_bounds__(NT, 1) void hgemm_kernel(HgArgs args) {
-    __shared__ __attribute__((aligned(16))) char smem_[HG_SMEM];
+__global__ __launch_bounds__(NT, 512 / NT) void hgemm_kernel(HgArgs args) {
+    __shared__ __attribute__((aligned(16))) char smem_[SMEM];
     lds_char* smem = (lds_char*)smem_;
     const GemmTile tile = args.tiles[blockIdx.x];
     if (tile.layer < 0) return;   // padding of the XCD interleave
     const HgLayer L = args.layers[tile.layer];
     const Pending q = *L.pend;
-    if (STAGE == 1 && L.a_f32) {
-        if (q.has) hgemm_tile<STAGE, true, true>(L, tile, q, args.partials, smem);
-        else       hgemm_tile<STAGE, true, false>(L, tile, q, args.partials, smem);
-    } else {
-        if (q.has) hgemm_tile<STAGE, false, true>(L, tile, q, args.partials, smem);
-        else       hgemm_tile<STAGE, false, false>(L, tile, q, args.partials, smem);
+    if (q.has) hgemm_tile<STAGE, true>(L, tile, q, args.partials, smem);
+    else       hgemm_tile<STAGE, false>(L, tile, q, args.partials, smem);
+}
+
+// fp32 gradients of bf16-factor layers, rounded to bf16 once per step.
+__global__ __launch_bounds__(256) void cvt_bf16_kernel(const CvtItem* __restrict__ items,
+                                                      const CvtBlock* __restrict__ blocks) {
+    const CvtBlock b = blocks[blockIdx.x];
+    const CvtItem it = items[b.item];
+    const int64_t end = min(b.off + (int64_t)CVT_ELEMS, it.n);
+    for (int64_t e = b.off + 8 * (int64_t)threadIdx.x; e < end; e += 8 * 256) {
+        const float4 x0 = gld4_nt(it.src + e), x1 = gld4_nt(it.src + e + 4);
+        gst_u4(it.dst + e, make_uint4(f2bf2(x0.x, x0.y), f2bf2(x0.z, x0.w), f2bf2(x1.x, x1.y), f2bf2(x1.z, x1.w)));
     }
 }
 
@@ -346,6 +347,12 @@ hipError_t launch_hgemm(int stage, const HgLayer* layers, const GemmTile* tiles,
     HgArgs a{layers, tiles, partials};
     if (stage == 1) hipLaunchKernelGGL(hgemm_kernel<1>, dim3(ntiles), dim3(NT), 0, stream, a);
     else            hipLaunchKernelGGL(hgemm_kernel<2>, dim3(ntiles), dim3(NT), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_cvt_bf16(const CvtItem* items, const CvtBlock* blocks, int32_t nblocks, hipStream_t stream) {
+    if (nblocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(cvt_bf16_kernel, dim3(nblocks), dim3(256), 0, stream, items, blocks);
     return hipGetLastError();
 }
 

@@ -268,11 +268,14 @@ def test_bf16_factor_layers(lib):
 
 def test_workspace_bf16_factors(lib):
     fk = Fake()
-    f32 = ws_status([layer(fk, 1024, 4096)])[1]
-    h = ws_status([layer(fk, 1024, 4096, fdt=1)])[1]
+    f32 = ws_status([layer(fk, 1024, 4096, dt=1)])[1]
+    h = ws_status([layer(fk, 1024, 4096, dt=1, fdt=1)])[1]
     # the intermediate (X^T fp32, or Y^T bf16) is d_in x d_out
     assert f32 - h >= 2 * 1024 * 4096 - (1 << 20)
     assert h >= 2 * 1024 * 4096
+    # an fp32 gradient of a bf16-factor layer also gets a bf16 copy
+    h32 = ws_status([layer(fk, 1024, 4096, fdt=1)])[1]
+    assert h32 - h >= 2 * 1024 * 4096
     # mixed lists plan both GEMM kinds
     st, _ = ws_status([layer(fk, 1024, 4096, fdt=1), layer(fk, 4096, 1024), layer(fk, 37, 100)])
     assert st == M.MKOR_OK
