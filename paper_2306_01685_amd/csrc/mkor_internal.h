@@ -151,11 +151,15 @@ constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 #define MKOR_HG_BJ 256
 #endif
 #ifndef MKOR_HG_NS
-#define MKOR_HG_NS 4
+#define MKOR_HG_NS 2
+#endif
+#ifndef MKOR_HG_BK
+#define MKOR_HG_BK 64
 #endif
 constexpr int HG_BI = MKOR_HG_BI, HG_BJ = MKOR_HG_BJ;   // tile of C (rows i x columns j)
 constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 x 64
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
+constexpr int HG_BK = MKOR_HG_BK;                       // k per stage
 
 struct HgLayer {
     const void*    P;      // factor S (bf16, I x K)

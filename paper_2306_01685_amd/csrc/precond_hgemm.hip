@@ -22,18 +22,19 @@
 // where (Q w) is summed from the Q rows while they sit in LDS, and Q[j][i] is
 // read at the output positions (4 consecutive i of one row j: one 8-byte load).
 //
-// Tiles of HG_BI x HG_BJ outputs (256 x 256), waves of 128 x 64 (4 x 2 MFMA
-// blocks), two waves per SIMD.  K runs in slabs of 32 through an HG_NS-stage
-// LDS ring (4 stages, 128 KB) filled by direct global-to-LDS loads
+// Tiles of HG_BI x HG_BJ outputs (256 x 256), eight waves of 128 x 64 (4 x 2
+// MFMA blocks), two per SIMD.  K runs in slabs of HG_BK (64) through an
+// HG_NS-stage LDS ring (2 stages, 128 KB) filled by direct global-to-LDS loads
 // (global_load_lds_dwordx4: lane l of a wave's instruction writes 16 bytes at
-// M0 + 16 l), so up to three slabs are in flight while one is multiplied and no
-// registers hold staged data.  (256 x 128 tiles with two workgroups per CU,
-// which overlap one workgroup's epilogue with the other's MFMAs, measured a
-// few per cent slower: the vector memory path then carries 1.5x the bytes.)  Each lane loads the
-// global chunk that belongs at its LDS slot, which realises the swizzle
-//   byte(r, c) = 64 r + 16 (c ^ ((r >> 2) & 3))     (64-byte rows, 4 chunks)
-// under which the 16 rows of an MFMA operand read, and the 8 rows x 2 chunks
-// of a rank-1 read, fall on 16 distinct 16-byte bank groups.
+// M0 + 16 l), so the next slab streams in while one is multiplied and no
+// registers hold staged data; within a slab the operand reads of k-step
+// ks + 1 go out before the MFMAs of ks.  Each lane loads the global chunk
+// that belongs at its LDS slot, which realises the swizzle of swz() below:
+// the 16 rows of an MFMA operand read, and the rows of a rank-1 read, fall on
+// 16 distinct 16-byte bank groups.  (Measured alternatives: 32-deep slabs in a
+// 4-stage ring, and 256 x 128 tiles with two workgroups per CU, were within a
+// few per cent, the latter moving 1.5x the bytes through the vector memory
+// path.)
 //
 // The K loop holds no compiler-visible global access: completion of the
 // direct loads is tracked by hand with s_waitcnt vmcnt (loads complete in
@@ -65,23 +66,39 @@ constexpr int TI = BI / WI, TJ = BJ / WJ;     // 128 x 64 per wave
 constexpr int FI = TI / 32, FJ = TJ / 32;     // 4 x 2 MFMA blocks
 static_assert(NT == WI * WJ * 64 && TI == 128 && TJ == 64, "wave layout");
 
-constexpr int BK = 32, NS = HG_NS;            // slab depth, ring stages
+constexpr int BK = HG_BK, NS = HG_NS;         // slab depth, ring stages
+static_assert(BK == 32 || BK == 64, "slab rows of 64 or 128 bytes");
+constexpr int KC = BK / 8;                    // 16-byte chunks per slab row
+constexpr int RPB = 64 / KC;                  // rows per 1-KB load block
 constexpr int ROWB = BK * 2;                  // bytes per slab row
 constexpr int PB = BI * ROWB, QB = BJ * ROWB; // P and Q bytes per stage
 constexpr int STB = PB + QB;
-constexpr int WSLOT = 256;                    // w[k0 .. k0 + 64) per stage (32 used)
+constexpr int WSLOT = 256;                    // w[k0 .. k0 + 64) per stage (BK used)
 constexpr int NW = NT / 64;
 constexpr int PBLK = PB / 1024 / NW, QBLK = QB / 1024 / NW;   // 1-KB load blocks per wave and slab
 static_assert(PB % (1024 * NW) == 0 && QB % (1024 * NW) == 0, "load blocks per wave");
 static_assert(2 * BJ == NT, "rank-1 reads: one half Q row per thread");
 constexpr int RING = NS * STB;
-constexpr int CPITCH = BJ * 2 + 16;           // stage-1 output staging: bf16 row pitch (padded)
-// stage-1 output rows staged per pass (whole waves' rows, as many as the ring holds)
-constexpr int CROWS = (RING / CPITCH) / TI * TI < BI ? (RING / CPITCH) / TI * TI : BI;
-static_assert(CROWS >= TI, "output staging holds a wave's rows");
+// Stage-1 output staging: the bf16 tile, rows of BJ * 2 bytes with the
+// 16-byte chunk index XORed with the row, in the ring once the K loop is done.
+constexpr int CPITCH = BJ * 2, CCH = BJ / 8;
+static_assert(BI * CPITCH <= RING && (CCH & (CCH - 1)) == 0, "output staging fits in the ring");
+__device__ __forceinline__ int cst(int r, int cj) { return r * CPITCH + ((cj ^ (r & (CCH - 1))) << 4); }
 constexpr int SMEM = RING + NS * WSLOT + 4 * (BJ + NW);
 
-__device__ __forceinline__ int swz(int r, int c) { return r * ROWB + ((c ^ ((r >> 2) & 3)) << 4); }
+// Row r's chunk c sits in 16-byte slot c ^ f(r): for 64-byte rows f(r) =
+// (r >> 2) & 3, for 128-byte rows f(r) = (r & 7) ^ ((r >> 3) & 1).  Either way
+// the 16 rows an operand read touches at one chunk fill 16 distinct 16-byte
+// bank groups.
+#ifndef MKOR_HG_PRIO
+#define MKOR_HG_PRIO 0
+#endif
+#ifndef MKOR_HG_FDB
+#define MKOR_HG_FDB 1
+#endif
+
+__device__ __forceinline__ int swf(int r) { return KC == 4 ? ((r >> 2) & 3) : ((r & 7) ^ ((r >> 3) & 1)); }
+__device__ __forceinline__ int swz(int r, int c) { return r * ROWB + ((c ^ swf(r)) << 4); }
 
 __device__ __forceinline__ void dma16(unsigned lds, unsigned voff, const void* base) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
@@ -148,17 +165,20 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
     // this lane's load sources at k0 = 0 (byte offsets from the operand base)
-    const int dc = (lane & 3) ^ ((lane >> 4) & 3);   // chunk that belongs at the lane's LDS slot
+    // lane l of a block writes slot l % KC of row l / KC: it loads that row's
+    // chunk (l % KC) ^ f(row)
     unsigned vp[PBLK], vq[QBLK];
 #pragma unroll
     for (int b = 0; b < PBLK; ++b) {
-        const int r = 16 * (PBLK * wave + b) + (lane >> 2);
-        vp[b] = ((unsigned)min(i0 + r, I - 1) * (unsigned)K + 8u * dc) * 2u;
+        const int r = RPB * (PBLK * wave + b) + lane / KC;
+        const int c = (lane % KC) ^ swf(r);
+        vp[b] = ((unsigned)min(i0 + r, I - 1) * (unsigned)K + 8u * c) * 2u;
     }
 #pragma unroll
     for (int b = 0; b < QBLK; ++b) {
-        const int r = 16 * (QBLK * wave + b) + (lane >> 2);
-        vq[b] = ((unsigned)min(j0 + r, J - 1) * (unsigned)K + 8u * dc) * 2u;
+        const int r = RPB * (QBLK * wave + b) + lane / KC;
+        const int c = (lane % KC) ^ swf(r);
+        vq[b] = ((unsigned)min(j0 + r, J - 1) * (unsigned)K + 8u * c) * 2u;
     }
     const int nst = K / BK;
     constexpr int D = PBLK + QBLK;               // load instructions per wave and slab
@@ -175,7 +195,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     };
 
     // rank-1 dot (and ||G||^2) of this thread's half Q row: row t / 2, chunks
-    // 2 h and 2 h + 1, summed in a fixed order over the slabs
+    // h KC / 2 .. (h + 1) KC / 2 - 1, summed in a fixed order over the slabs
     const int rr = t >> 1, rh = t & 1;
     float rdot = 0.f, gsq = 0.f;
     const bool gsq_row = want_gsq && j0 + rr < J;
@@ -189,25 +209,46 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         if (s + NS - 1 < nst) issue(s + NS - 1);
         const lds_char* Pb = smem + (s % NS) * STB;
         const lds_char* Qb = Pb + PB;
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
+        auto frags = [&](int ks, bf16x8 (&a)[FI], bf16x8 (&b)[FJ]) {
             const int c = 2 * ks + lk;
-            bf16x8 a[FI], b[FJ];
 #pragma unroll
             for (int x = 0; x < FI; ++x) a[x] = *(const lds_bf8*)(Pb + swz(wi * TI + x * 32 + li, c));
 #pragma unroll
             for (int y = 0; y < FJ; ++y) b[y] = *(const lds_bf8*)(Qb + swz(wj * TJ + y * 32 + li, c));
+        };
+        auto mma = [&](const bf16x8 (&a)[FI], const bf16x8 (&b)[FJ]) {
+            if (MKOR_HG_PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
             for (int x = 0; x < FI; ++x)
 #pragma unroll
                 for (int y = 0; y < FJ; ++y)
                     acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
+            if (MKOR_HG_PRIO) __builtin_amdgcn_s_setprio(0);
+        };
+        if constexpr (MKOR_HG_FDB) {
+            // two operand sets: the reads of k-step ks + 1 go out before the MFMAs of ks
+            bf16x8 a0[FI], b0[FJ], a1[FI], b1[FJ];
+            frags(0, a0, b0);
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ks += 2) {
+                frags(ks + 1, a1, b1);
+                mma(a0, b0);
+                if (ks + 2 < BK / 16) frags(ks + 2, a0, b0);
+                mma(a1, b1);
+            }
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                bf16x8 a[FI], b[FJ];
+                frags(ks, a, b);
+                mma(a, b);
+            }
         }
         if (PEND || want_gsq) {
             const lds_float* wsl = (const lds_float*)(smem + RING + (s % NS) * WSLOT);
 #pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const int c = 2 * rh + e;
+            for (int e = 0; e < KC / 2; ++e) {
+                const int c = (KC / 2) * rh + e;
                 float v[8];
                 const mk_u4 hv = *(const lds_u4*)(Qb + swz(rr, c));
                 unpack8(hv, v);
@@ -231,67 +272,50 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 
     const float c1 = PEND ? q.c1 : 1.f, c2 = PEND ? q.c2 : 0.f, sg = PEND ? q.sgn : 0.f;
     float csq = 0.f;
-    // value of one output group (rows i .. i + 3 of column j) with the rest of
-    // the pending term: C[i][j] += c2 Q[j][i] + sgn w[i] (Q w)[j]
-    auto finish = [&](int x, int y, int g, float (&v)[4]) {
-        const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
-        const int i = i0 + wi * TI + x * 32 + 8 * g + 4 * lk;
+    // One MFMA row block (x) at a time: first every load its output groups
+    // need (rows past the edge clamped, so the loads go out together without
+    // branches), then C[i][j] = c1 acc + c2 Q[j][i] + sgn w[i] (Q w)[j].
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[x][y][4 * g + e];
-        if (PEND && i < I && j < J) {
-            const uint2 qh = gld_u2(static_cast<const unsigned short*>(L.Q) + (size_t)j * K + i);
-            const float qv[4] = {bf2f((unsigned short)(qh.x & 0xffffu)), bf2f((unsigned short)(qh.x >> 16)),
-                                 bf2f((unsigned short)(qh.y & 0xffffu)), bf2f((unsigned short)(qh.y >> 16))};
-            const float4 wv = gld4(L.w + i);
-            const float wa[4] = {wv.x, wv.y, wv.z, wv.w};
-            const float rq = rvec[jl];
+    for (int x = 0; x < FI; ++x) {
+        uint2 qh[FJ][4];
+        float4 wv[4];
+        if (PEND) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[e], sg * wa[e] * rq));
-        }
-    };
-    if constexpr (STAGE == 1) {
-        // bf16 through an LDS staging tile, CROWS rows per pass, then stored
-        // 16 bytes per lane along the rows of Y^T
-        constexpr int CH = BJ / 8;   // 16-byte chunks per row
-        for (int p0 = 0; p0 < BI; p0 += CROWS) {
-            if (wi * TI >= p0 && wi * TI < p0 + CROWS) {
+            for (int g = 0; g < 4; ++g) {
+                const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
+                wv[g] = gld4(L.w + i);
 #pragma unroll
-                for (int x = 0; x < FI; ++x)
-#pragma unroll
-                    for (int y = 0; y < FJ; ++y)
-#pragma unroll
-                        for (int g = 0; g < 4; ++g) {
-                            float v[4];
-                            finish(x, y, g, v);
-                            const int jl = wj * TJ + y * 32 + li;
-                            const int il = wi * TI + x * 32 + 8 * g + 4 * lk - p0;
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) *(lds_u16*)(smem + (il + e) * CPITCH + 2 * jl) = f2bf(v[e]);
-                        }
-            }
-            __syncthreads();
-            for (int u = t; u < CROWS * CH; u += NT) {
-                const int il = u / CH, cj = u % CH;
-                const int i = i0 + p0 + il, j = j0 + 8 * cj;
-                if (i < I && j < J) {
-                    const mk_u4 h = *(const lds_u4*)(smem + il * CPITCH + 16 * cj);
-                    gst_u4(static_cast<unsigned short*>(L.C) + (size_t)i * J + j, make_uint4(h.x, h.y, h.z, h.w));
+                for (int y = 0; y < FJ; ++y) {
+                    const int j = min(j0 + wj * TJ + y * 32 + li, J - 1);
+                    qh[y][g] = gld_u2(static_cast<const unsigned short*>(L.Q) + (size_t)j * K + i);
                 }
             }
-            __syncthreads();
         }
-    } else {
 #pragma unroll
-        for (int x = 0; x < FI; ++x)
+        for (int y = 0; y < FJ; ++y) {
+            const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
+            const float rq = PEND ? rvec[jl] : 0.f;
 #pragma unroll
-            for (int y = 0; y < FJ; ++y)
+            for (int g = 0; g < 4; ++g) {
+                const int il = wi * TI + x * 32 + 8 * g + 4 * lk, i = i0 + il;
+                float v[4];
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int j = j0 + wj * TJ + y * 32 + li;
-                    const int i = i0 + wi * TI + x * 32 + 8 * g + 4 * lk;
-                    if (i >= I || j >= J) continue;   // I, J multiples of 64: 4 rows all in or all out
-                    float v[4];
-                    finish(x, y, g, v);
+                for (int e = 0; e < 4; ++e) v[e] = acc[x][y][4 * g + e];
+                if (PEND) {
+                    const float qv[4] = {bf2f((unsigned short)(qh[y][g].x & 0xffffu)),
+                                         bf2f((unsigned short)(qh[y][g].x >> 16)),
+                                         bf2f((unsigned short)(qh[y][g].y & 0xffffu)),
+                                         bf2f((unsigned short)(qh[y][g].y >> 16))};
+                    const float wa[4] = {wv[g].x, wv[g].y, wv[g].z, wv[g].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[e], sg * wa[e] * rq));
+                }
+                if constexpr (STAGE == 1) {
+                    // bf16 into the staging tile (stored row by row below)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        *(lds_u16*)(smem + cst(il + e, jl >> 3) + 2 * (jl & 7)) = f2bf(v[e]);
+                } else if (i < I && j < J) {   // I, J multiples of 64: 4 rows all in or all out
                     float* dst = static_cast<float*>(L.C) + (size_t)i * J + j;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -299,6 +323,20 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                         csq = fmaf(v[e], v[e], csq);
                     }
                 }
+            }
+        }
+    }
+    if constexpr (STAGE == 1) {
+        __syncthreads();
+        // Y^T rows of the tile, 16 bytes per lane
+        for (int u = t; u < BI * CCH; u += NT) {
+            const int il = u / CCH, cj = u % CCH;
+            const int i = i0 + il, j = j0 + 8 * cj;
+            if (i < I && j < J) {
+                const mk_u4 h = *(const lds_u4*)(smem + cst(il, cj));
+                gst_u4(static_cast<unsigned short*>(L.C) + (size_t)i * J + j, make_uint4(h.x, h.y, h.z, h.w));
+            }
+        }
     }
 
     // partials: block-wide fixed-order sums
