@@ -36,7 +36,8 @@ FP32_MFMA_PEAK_TF = 157.3   # MI355X dense fp32 matrix
 BF16_MFMA_PEAK_TF = 2500.0  # MI355X dense bf16 matrix
 
 
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic_bert_large_144.md")
+PROFILE_TRAFFIC = {False: os.path.join(ROOT, "profiles", "traffic_bert_large_144.md"),
+                   True: os.path.join(ROOT, "profiles", "traffic_bert_large_144_bf16.md")}
 
 
 def library_source_sha256() -> str:
@@ -53,20 +54,22 @@ def library_source_sha256() -> str:
     return h.hexdigest()
 
 
-def profiled_traffic(kernel: str, config: int):
+def profiled_traffic(kernel: str, config: int, half: bool = False):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary (FETCH_SIZE and WRITE_SIZE, copy-calibrated), or None if there is no
-    record for this workload or the library changed since it was taken."""
-    if config != 3 or not os.path.exists(PROFILE_TRAFFIC):
+    summary (FETCH_SIZE and WRITE_SIZE, copy-calibrated) of the fp32- or
+    bf16-factor run, or None if there is no record for this workload or the
+    library changed since it was taken."""
+    path = PROFILE_TRAFFIC[half]
+    if config != 3 or not os.path.exists(path):
         return None
-    for line in open(PROFILE_TRAFFIC):
+    for line in open(path):
         if line.startswith("traffic-record:"):
             rec = json.loads(line.split(":", 1)[1])
             if rec.get("source_sha256") != library_source_sha256() or kernel not in rec["bytes"]:
                 return None
             rd, wr = rec["bytes"][kernel]
             return dict(read_bytes=rd, write_bytes=wr, total_bytes=rd + wr,
-                        source="profiles/traffic_bert_large_144.md")
+                        source=os.path.relpath(path, ROOT))
     return None
 
 
@@ -290,7 +293,7 @@ def measure(w, args, factor_dtype):
         dom = max(range(NUM_STAGES - 1), key=lambda s: ms[s])
         name = names[dom]
         k = kernels[name]
-        traffic = None if half else profiled_traffic(name, args.config)
+        traffic = profiled_traffic(name, args.config, half)
         if "flops" in k:
             roof = dict(kernel=name, bound="mfma", achieved=k["tflops"], peak=mfma_peak,
                         unit="TFLOP/s", frac=k["tflops"] / mfma_peak,
@@ -304,7 +307,7 @@ def measure(w, args, factor_dtype):
         roof["traffic_detail"] = traffic
         # the SM update is the benchmark spec's other roofline: report it beside
         k = kernels["sm_pass"]
-        t = None if half else profiled_traffic("sm_pass", args.config)
+        t = profiled_traffic("sm_pass", args.config, half)
         roof["sm_update"] = dict(kernel="sm_pass", bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS,
                                  unit="GB/s", frac=k["gbs"] / HBM_PEAK_GBS,
                                  traffic=None if t is None else t["total_bytes"],
