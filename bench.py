@@ -96,6 +96,8 @@ def parse():
     ap.add_argument("--factor-dtype", choices=["fp32", "bf16"], default="fp32",
                     help="storage type of the inverse factors of the timed run (bf16: the "
                          "half-precision factors, bf16 MFMA preconditioning)")
+    ap.add_argument("--rank", type=int, default=1,
+                    help="vectors per factor update (the rank-r extension; fp32 factors)")
     ap.add_argument("--no-half", action="store_true",
                     help="skip the extra measurement with bf16 factors")
     return ap.parse_args()
@@ -212,8 +214,9 @@ def measure(w, args, factor_dtype):
     from paper_2306_01685_amd import NUM_STAGES, STAGE_NAMES, Params, harness as H
 
     half = factor_dtype == "bf16"
+    rank = args.rank if not half else 1
     layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=args.rows, act_dtype="bf16",
-                               factor_dtype=factor_dtype)
+                               factor_dtype=factor_dtype, rank=rank)
     if w.init != "identity":
         for i, L in enumerate(layers):
             H.set_factors(L, *initial_factors_stored(w, i, half))
@@ -263,12 +266,16 @@ def measure(w, args, factor_dtype):
         sd = sum(i + o for i, o in w.shapes)
         means_ms, ms = ms[0], ms[1:]   # stage 0: rank-1 means (no work when a and g are given)
         g1, g2 = ("gemm_gr", "gemm_ly") if half else ("gemm_xt", "gemm_dw")
+        # steady state, rank 1: every factor has a pending term, so the pass reads
+        # and writes each element once, and the finalize moves O(sum d) (partials,
+        # u_raw and x read, w written).  Rank r > 1: the pass only reads (the
+        # previous update is already in the factor) and the finalize stage also
+        # writes the new update into the factor (a read and a write).
+        pass_b = 2 * esz * sq if rank == 1 else esz * sq
+        fin_b = 12 * sd if rank == 1 else 2 * esz * sq + 12 * rank * sd
         kernels = {
-            # steady state: every factor has a pending term, so the pass reads
-            # and writes each element once
-            "sm_pass": dict(ms=ms[0], alg_bytes=2 * esz * sq, gbs=2 * esz * sq * gb / (ms[0] / 1e3)),
-            # partials, u_raw and x read, w written: O(sum d)
-            "sm_finalize": dict(ms=ms[1], alg_bytes=12 * sd, gbs=12 * sd * gb / (ms[1] / 1e3)),
+            "sm_pass": dict(ms=ms[0], alg_bytes=pass_b, gbs=pass_b * gb / (ms[0] / 1e3)),
+            "sm_finalize": dict(ms=ms[1], alg_bytes=fin_b, gbs=fin_b * gb / (ms[1] / 1e3)),
             g1: dict(ms=ms[2], flops=f1, tflops=f1 / (ms[2] / 1e3) / 1e12),
             g2: dict(ms=ms[3], flops=f2, tflops=f2 / (ms[3] / 1e3) / 1e12),
             "rescale": dict(ms=ms[4], alg_bytes=8 * nel, gbs=8 * nel * gb / (ms[4] / 1e3)),
@@ -279,8 +286,9 @@ def measure(w, args, factor_dtype):
                                     frac_hbm=mb * gb / (means_ms / 1e3) / HBM_PEAK_GBS,
                                     rows=args.rows)
         sm_ms = ms[0] + ms[1]
-        kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=2 * esz * sq, gbs=2 * esz * sq * gb / (sm_ms / 1e3),
-                                   frac_hbm=2 * esz * sq * gb / (sm_ms / 1e3) / HBM_PEAK_GBS)
+        sm_b = pass_b + fin_b
+        kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=sm_b, gbs=sm_b * gb / (sm_ms / 1e3),
+                                   frac_hbm=sm_b * gb / (sm_ms / 1e3) / HBM_PEAK_GBS)
         pre_ms = ms[2] + ms[3]
         kernels["gemm_total"] = dict(ms=pre_ms, flops=f1 + f2,
                                      tflops=(f1 + f2) / (pre_ms / 1e3) / 1e12,
@@ -366,7 +374,7 @@ def main():
     ms_step, kernels, roof, schedule = measure(w, args, args.factor_dtype)
     value = w.n_layers / (ms_step / 1e3)
     half = None
-    if args.factor_dtype == "fp32" and not args.no_half:
+    if args.factor_dtype == "fp32" and not args.no_half and args.rank == 1:
         # the same workload with half-precision (bf16) factors, reported beside
         h_ms, h_k, h_roof, h_sched = measure(w, args, "bf16")
         half = dict(value=w.n_layers / (h_ms / 1e3), unit="layer-updates/s", ms_per_step=h_ms,
@@ -382,7 +390,7 @@ def main():
         "config": {"workload": workload_desc(w, args.factor_dtype), "n_layers": w.n_layers,
                    "factor_elems": w.factor_elems, "precond_flops": w.precond_flops,
                    "gamma": w.gamma, "zeta": 0.5, "eps": args.eps, "grad_dtype": w.grad_dtype,
-                   "factor_dtype": args.factor_dtype, "token_rows": args.rows},
+                   "factor_dtype": args.factor_dtype, "token_rows": args.rows, "rank": args.rank},
         "roofline": roof,
         "schedule_f10": schedule,
         "kernels": kernels,

@@ -93,7 +93,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 4
+#define MKOR_ABI_VERSION 5
 
 /* status codes */
 #define MKOR_OK                   0
@@ -124,6 +124,7 @@ extern "C" {
 /* largest supported d_in / d_out, and token rows of A / Gout */
 #define MKOR_MAX_DIM       32768
 #define MKOR_MAX_ROWS      (1 << 26)
+#define MKOR_MAX_RANK      4
 
 typedef struct mkor_params {
     float   gamma;            /* momentum of Eq. 4/5, 0 < gamma < 1 */
@@ -143,8 +144,9 @@ typedef struct mkor_layer {
     int32_t      grad_dtype;    /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (element type of G) */
     void*        Linv;          /* d_in x d_in, in/out, factor_dtype elements (unused if second_order = 0) */
     void*        Rinv;          /* d_out x d_out, in/out, factor_dtype elements (unused if second_order = 0) */
-    float*       a;             /* d_in, mean activation: input, or output when rows > 0 */
-    float*       g;             /* d_out, mean output gradient: input, or output when rows > 0
+    float*       a;             /* d_in x rank, mean activation(s): input, or output when rows > 0;
+                                   vector l at a + l * d_in */
+    float*       g;             /* d_out x rank, mean output gradient(s), vector l at g + l * d_out
                                    (a and g unused if second_order = 0) */
     const void*  G;             /* d_in x d_out gradient, grad_dtype elements */
     float*       dW;            /* d_in x d_out fp32 output */
@@ -165,7 +167,15 @@ typedef struct mkor_layer {
      * accumulation as dW_hat = Linv (G Rinv), G and the intermediate G Rinv
      * entering it in bf16.  Needs d_in and d_out to be multiples of 64. */
     int32_t      factor_dtype;
-    int32_t      reserved;      /* must be 0 */
+    /* Rank of the update (the paper's extension to higher ranks): 0 or 1 for
+     * the rank-1 update; r in 2 .. MKOR_MAX_RANK applies the momentum
+     * accumulation M_t = gamma M_hat + (1 - gamma) sum_l x_l x_l^T by r
+     * sequential Sherman-Morrison updates, x_l the r vectors in a (Linv) and
+     * g (Rinv).  r > 1 needs rows = 0, fp32 factors and, at call time, the
+     * MKOR_SM_EXACT variant (MKOR_UNSUPPORTED otherwise).  A rank-r update is
+     * written into Linv / Rinv within the step that computes it (one more
+     * read and write of the factor), so it leaves no pending term. */
+    int32_t      rank;
 } mkor_layer;
 
 /* Per-layer observability record, written on the device when

@@ -34,7 +34,8 @@ DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
-ABI_VERSION = 4
+MAX_RANK = 4
+ABI_VERSION = 5
 
 
 class mkor_params(ctypes.Structure):
@@ -51,7 +52,7 @@ class mkor_layer(ctypes.Structure):
                 ("G", ctypes.c_void_p), ("dW", ctypes.c_void_p), ("stats", ctypes.c_void_p),
                 ("rows", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
                 ("A", ctypes.c_void_p), ("Gout", ctypes.c_void_p),
-                ("factor_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("factor_dtype", ctypes.c_int32), ("rank", ctypes.c_int32)]
 
 
 class mkor_layer_stats(ctypes.Structure):
@@ -166,7 +167,7 @@ def make_layer_array(descs):
                             d.get("g") or None, d.get("G") or None, d.get("dW") or None,
                             d.get("stats") or None, d.get("rows", 0), d.get("act_dtype", 0),
                             d.get("A") or None, d.get("Gout") or None, d.get("factor_dtype", 0),
-                            d.get("reserved", 0))
+                            d.get("rank", 0))
     return arr
 
 
@@ -191,8 +192,10 @@ class MkorPlan:
     """A plan over a grouped list of layers, holding torch device tensors.
 
     Each layer is a dict with d_in, d_out and tensors Linv, Rinv (symmetric;
-    both fp32, or both bf16 for half-precision factors), a, g (fp32 vectors), G (fp32 or bf16, d_in x d_out), dW (fp32,
-    d_in x d_out), optional second_order (default True), optional stats
+    both fp32, or both bf16 for half-precision factors), a, g (fp32 vectors of
+    length d_in / d_out, or (r, d_in) / (r, d_out) arrays of r vectors for a
+    rank-r update), G (fp32 or bf16, d_in x d_out), dW (fp32, d_in x d_out),
+    optional second_order (default True), optional stats
     (a uint8 device tensor of STATS_BYTES bytes), and optionally token rows A
     (rows x d_in) and Gout (rows x d_out), fp32 or bf16, from which each step
     forms a and g (their means).  The plan owns its workspace
@@ -238,7 +241,8 @@ class MkorPlan:
                               grad_dtype=gdt, Linv=_ptr(L.get("Linv")), Rinv=_ptr(L.get("Rinv")),
                               a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
                               stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
-                              Gout=_ptr(L.get("Gout")), factor_dtype=fdt))
+                              Gout=_ptr(L.get("Gout")), factor_dtype=fdt,
+                              rank=int(L["a"].shape[0]) if so and L["a"].dim() == 2 else 0))
         self._arr = make_layer_array(descs)
         n = len(descs)
         size = ctypes.c_size_t(0)

@@ -42,6 +42,9 @@ struct Interval {
     const char* what;
 };
 
+// vectors per factor update: rank 0 means 1; first-order layers have none
+int32_t layer_rank(const mkor_layer& L) { return L.second_order == 1 ? std::max(1, L.rank) : 1; }
+
 int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_bytes) {
     if (n < 0) return fail(MKOR_INVALID_ARG, "n = %d is negative", n);
     if (n > 0 && layers == nullptr) return fail(MKOR_INVALID_ARG, "layers is NULL with n = %d", n);
@@ -58,8 +61,14 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
             return fail(MKOR_UNSUPPORTED, "layer %d: grad_dtype = %d is not supported", i, L.grad_dtype);
         if (L.factor_dtype != MKOR_DTYPE_F32 && L.factor_dtype != MKOR_DTYPE_BF16)
             return fail(MKOR_UNSUPPORTED, "layer %d: factor_dtype = %d is not supported", i, L.factor_dtype);
-        if (L.reserved != 0) return fail(MKOR_INVALID_ARG, "layer %d: reserved = %d must be 0", i, L.reserved);
+        if (L.rank < 0 || L.rank > MKOR_MAX_RANK)
+            return fail(MKOR_INVALID_ARG, "layer %d: rank = %d outside 0..%d", i, L.rank, MKOR_MAX_RANK);
         const bool half = L.second_order == 1 && L.factor_dtype == MKOR_DTYPE_BF16;
+        const int32_t rk = layer_rank(L);
+        if (rk > 1 && L.rows > 0)
+            return fail(MKOR_UNSUPPORTED, "layer %d: rank %d needs rows = 0 (means are rank-1)", i, rk);
+        if (rk > 1 && half)
+            return fail(MKOR_UNSUPPORTED, "layer %d: rank %d needs fp32 factors", i, rk);
         if (half && (L.d_in % 64 != 0 || L.d_out % 64 != 0))
             return fail(MKOR_UNSUPPORTED, "layer %d: bf16 factors need d_in and d_out multiples of 64 (%d, %d)",
                         i, L.d_in, L.d_out);
@@ -78,8 +87,8 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
             {L.dW, din * dout * 4, true, "dW", true},
             {L.Linv, din * din * (half ? 2 : 4), true, "Linv", L.second_order == 1},
             {L.Rinv, dout * dout * (half ? 2 : 4), true, "Rinv", L.second_order == 1},
-            {L.a, din * 4, means, "a", L.second_order == 1},
-            {L.g, dout * 4, means, "g", L.second_order == 1},
+            {L.a, din * 4 * rk, means, "a", L.second_order == 1},
+            {L.g, dout * 4 * rk, means, "g", L.second_order == 1},
             {L.stats, sizeof(mkor_layer_stats), true, "stats", L.stats != nullptr},
             {L.A, asz * din, false, "A", means},
             {L.Gout, asz * dout, false, "Gout", means},
@@ -126,12 +135,14 @@ struct Layout {
     size_t off_mmat = 0, off_mitem = 0, off_mchunk = 0, off_mpart = 0;
     size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
     size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
+    size_t off_gram = 0;                                         // rank-r Gram partials
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
     int32_t nh1 = 0, nh2 = 0;
     int32_t ncvt = 0, ncvtblk = 0;
     int32_t nsecond = 0;
+    int32_t nranked = 0;      // second-order layers with rank > 1
     int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
     int64_t nmeanpart = 0;   // doubles
     std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
@@ -230,6 +241,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         }
         if (!L.second_order) continue;
         Lo.nsecond++;
+        if (layer_rank(L) > 1) Lo.nranked++;
         const int32_t rows = is_half(L) ? SM_ROWS_HALF : SM_ROWS;
         rowblocks += ceil_div(L.d_in, rows) + ceil_div(L.d_out, rows);
         g1 += dpart_count(L);
@@ -294,6 +306,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
     Lo.table_bytes = align_up(o, 256);
     Lo.off_smpart = take(sizeof(float4) * Lo.nrowblocks);
+    Lo.off_gram = take(Lo.nranked > 0 ? sizeof(float) * GRAM * (size_t)Lo.nrowblocks : 0);
     Lo.off_gpart = take(sizeof(float) * Lo.ngpart);
     Lo.off_dpart = take(sizeof(float) * Lo.ndpart);
     Lo.off_mpart = take(sizeof(double) * (size_t)Lo.nmeanpart);
@@ -303,8 +316,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     for (int32_t i = 0; i < n; ++i) {
         if (!layers[i].second_order) continue;
         for (const int32_t d : {layers[i].d_in, layers[i].d_out}) {
-            Lo.u_off.push_back(take(sizeof(float) * d));
-            Lo.w_off.push_back(take(sizeof(float) * d));
+            Lo.u_off.push_back(take(sizeof(float) * d * layer_rank(layers[i])));
+            Lo.w_off.push_back(take(sizeof(float) * d * layer_rank(layers[i])));
         }
     }
     for (int32_t i = 0; i < n; ++i) {
@@ -480,6 +493,7 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             f.nblk = ceil_div(f.d, rows);
             f.side = side;
             f.half = half ? 1 : 0;
+            f.rank = layer_rank(L);
             for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * rows};
             ++fi;
         }
@@ -566,6 +580,7 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
     const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(ws + lo.off_factors);
     const RowBlock* rb = reinterpret_cast<const RowBlock*>(ws + lo.off_rowblocks);
     float4* smpart = reinterpret_cast<float4*>(ws + lo.off_smpart);
+    float* gram = reinterpret_cast<float*>(ws + lo.off_gram);
     float* gpart = reinterpret_cast<float*>(ws + lo.off_gpart);
     float* dpart = reinterpret_cast<float*>(ws + lo.off_dpart);
     hipError_t e = hipSuccess;
@@ -580,13 +595,16 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             return MKOR_OK;
         case MKOR_STAGE_SM_PASS:
             if (lo.nrowblocks == 0) return MKOR_OK;
-            e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, prm->norm_kind, 1, s);
+            e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, gram, prm->norm_kind, 1, lo.nranked > 0, s);
             if (e != hipSuccess) return hip_fail(e, "sm_pass launch");
             return MKOR_OK;
         case MKOR_STAGE_SM_FINALIZE:
             if (lo.nfactors == 0) return MKOR_OK;
-            e = launch_sm_finalize(fd, lo.nfactors, smpart, *prm, s);
+            e = launch_sm_finalize(fd, lo.nfactors, smpart, gram, *prm, s);
             if (e != hipSuccess) return hip_fail(e, "sm_finalize launch");
+            // rank-r updates are written into their factors at once
+            if (lo.nranked > 0) e = launch_sm_apply_rank(fd, rb, lo.nrowblocks, lo.nfactors, s);
+            if (e != hipSuccess) return hip_fail(e, "rank-r apply launch");
             return MKOR_OK;
         case MKOR_STAGE_GEMM_XT:
             e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
@@ -627,10 +645,20 @@ static int run_range(mkor_plan* p, const mkor_params* prm, int32_t first, int32_
     return MKOR_OK;
 }
 
+// Parameters valid, and valid for this plan: rank-r layers exist for the
+// EXACT variant only.
+static int check_plan_params(const mkor_plan* plan, const mkor_params* params) {
+    const int st = check_params(params);
+    if (st != MKOR_OK) return st;
+    if (plan->lo.nranked > 0 && params->sm_variant != MKOR_SM_EXACT)
+        return fail(MKOR_UNSUPPORTED, "rank-r layers need sm_variant = MKOR_SM_EXACT");
+    return MKOR_OK;
+}
+
 int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
-    int st = check_params(params);
+    int st = check_plan_params(plan, params);
     if (st != MKOR_OK) return st;
     return run_range(plan, params, MKOR_STAGE_MEANS, MKOR_STAGE_SM_FINALIZE,
                      static_cast<hipStream_t>(stream));
@@ -639,7 +667,7 @@ int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream
 int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
-    int st = check_params(params);
+    int st = check_plan_params(plan, params);
     if (st != MKOR_OK) return st;
     return run_range(plan, params, MKOR_STAGE_GEMM_XT, MKOR_STAGE_RESCALE,
                      static_cast<hipStream_t>(stream));
@@ -648,7 +676,7 @@ int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream) 
 int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
-    int st = check_params(params);
+    int st = check_plan_params(plan, params);
     if (st != MKOR_OK) return st;
     return run_range(plan, params, MKOR_STAGE_MEANS, MKOR_STAGE_RESCALE,
                      static_cast<hipStream_t>(stream));
@@ -657,7 +685,7 @@ int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
 int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
-    int st = check_params(params);
+    int st = check_plan_params(plan, params);
     if (st != MKOR_OK) return st;
     if (stage < 0 || stage >= MKOR_NUM_STAGES) return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
     if (plan->n == 0) return MKOR_OK;
@@ -673,7 +701,7 @@ int mkor_sync_factors(mkor_plan* plan, void* stream) {
     const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(plan->ws + lo.off_factors);
     const RowBlock* rb = reinterpret_cast<const RowBlock*>(plan->ws + lo.off_rowblocks);
     float4* smpart = reinterpret_cast<float4*>(plan->ws + lo.off_smpart);
-    hipError_t e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, MKOR_NORM_INF, 0, s);
+    hipError_t e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, nullptr, MKOR_NORM_INF, 0, lo.nranked > 0, s);
     if (e != hipSuccess) return hip_fail(e, "sm_pass launch");
     e = launch_sm_reset(fd, lo.nfactors, s);
     if (e != hipSuccess) return hip_fail(e, "sm_reset launch");

@@ -62,8 +62,13 @@ struct FactorDesc {
     int32_t           nblk;    // number of row blocks of this factor
     int32_t           side;    // 0 = Linv (driven by a), 1 = Rinv (driven by g)
     int32_t           half;    // 1: S is stored in bf16 (d a multiple of 64)
-    int32_t           _pad;
+    int32_t           rank;    // r vectors: x, u and w are d x r (vector l at + l * d)
 };
+
+// Rank-r factors (rank > 1): per row block, the Gram partials
+// sum_rows x_l[i] (P x_m)[i] (MAXR x MAXR) and sum_rows x_l[i] x_m[i] (MAXR x MAXR).
+constexpr int MAXR = MKOR_MAX_RANK;
+constexpr int GRAM = 2 * MAXR * MAXR;
 
 // Rows handled by one workgroup of the SM pass (4 waves x SM_ROWS_PER_WAVE).
 #ifndef MKOR_SM_RPW
@@ -230,13 +235,18 @@ hipError_t launch_colmean(const MeanMat* mats, const MeanItem* items, int32_t ni
 // Streaming pass over every factor: applies the pending term in place (when
 // there is one) and, with matvec = 1, forms u_raw = P x, the row norms and the
 // per-row-block partials of the current P.
+// ranked: the plan has rank-r factors (their blocks run in a kernel of their own)
 hipError_t launch_sm_pass(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
-                          float4* partials, int32_t norm_kind, int32_t matvec, hipStream_t stream);
+                          float4* partials, float* gram, int32_t norm_kind, int32_t matvec, int32_t ranked,
+                          hipStream_t stream);
+// writes the pending rank-r terms into the rank-r factors and clears them
+hipError_t launch_sm_apply_rank(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
+                                int32_t nfactors, hipStream_t stream);
 
 // One workgroup per factor: stabiliser decision and update coefficients from
 // the pass partials, new pending term (coefficients and w), stats.
 hipError_t launch_sm_finalize(const FactorDesc* factors, int32_t nfactors, const float4* partials,
-                              const mkor_params& p, hipStream_t stream);
+                              const float* gram, const mkor_params& p, hipStream_t stream);
 
 // Marks every pending term applied (after a materialising pass).
 hipError_t launch_sm_reset(const FactorDesc* factors, int32_t nfactors, hipStream_t stream);

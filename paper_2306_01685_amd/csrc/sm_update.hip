@@ -305,8 +305,196 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
     for (int b = blockIdx.x; b < nblocks; b += gridDim.x) {
         const RowBlock rb = blocks[b];
         const FactorDesc f = factors[rb.factor];
+        if (f.rank > 1) continue;   // sm_pass_rank_kernel
         if (f.half) pass_block<SM_ROWS_PER_WAVE_HALF, true>(f, rb, partials, b, maxabs, matvec, sred);
         else        pass_block<SM_ROWS_PER_WAVE, false>(f, rb, partials, b, maxabs, matvec, sred);
+    }
+}
+
+// ------------------------------------------------------------------ rank-r pass
+// Factors with r > 1 vectors (fp32): the same stream over P, with the pending
+// term (if any) of rank r,
+//   P_ij = fma(c1, S_ij, t_ij) (+ c2 on the diagonal),
+//   t_ij = fma(sw_r[i], w_r[j], ... fma(sw_2[i], w_2[j], sw_1[i] * w_1[j])),
+// sw_l = sgn * w_l (exact), the same chain for (i, j) and (j, i) so that a
+// symmetric factor stays bitwise symmetric; and r row dot products
+// u_l = P x_l with the Gram partials x_l^T P x_m and x_l^T x_m of the row block.
+constexpr int RR = SM_ROWS_PER_WAVE;
+
+template <bool HAS, bool MV, bool VEC>
+__device__ __forceinline__ void rank_rows(const FactorDesc& f, const Pending& q, int rbase, int nr, int lane,
+                                          int maxabs, float (&dot)[RR][MAXR], float (&nrm)[RR]) {
+    const int d = f.d, rk = f.rank;
+    float* __restrict__ P = static_cast<float*>(f.P) + (size_t)rbase * d;
+    float swi[RR][MAXR];
+#pragma unroll
+    for (int r = 0; r < RR; ++r)
+#pragma unroll
+        for (int l = 0; l < MAXR; ++l)
+            swi[r][l] = (HAS && r < nr && l < rk) ? q.sgn * gld(f.w + (size_t)l * d + rbase + r) : 0.f;
+    auto elem = [&](int r, int j, float v, const float (&wj)[MAXR]) {
+        if constexpr (HAS) {
+            float t = __fmul_rn(swi[r][0], wj[0]);
+#pragma unroll
+            for (int l = 1; l < MAXR; ++l)
+                if (l < rk) t = __fmaf_rn(swi[r][l], wj[l], t);
+            v = __fmaf_rn(q.c1, v, t);
+            if (rbase + r == j) v = __fadd_rn(v, q.c2);
+        }
+        return v;
+    };
+    if constexpr (VEC) {
+        const int d4 = d >> 2;
+        for (int j = lane; j < d4; j += 64) {
+            float4 p[RR];
+#pragma unroll
+            for (int r = 0; r < RR; ++r)
+                if (r < nr) p[r] = gld4(P + (size_t)r * d + 4 * j);
+            float4 xv[MAXR], wv[MAXR];
+#pragma unroll
+            for (int l = 0; l < MAXR; ++l) {
+                xv[l] = make_float4(0.f, 0.f, 0.f, 0.f);
+                wv[l] = xv[l];
+                if (l < rk) {
+                    if (MV) xv[l] = gld4(f.x + (size_t)l * d + 4 * j);
+                    if (HAS) wv[l] = gld4(f.w + (size_t)l * d + 4 * j);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < RR; ++r) {
+                if (r >= nr) break;
+                float wj[4][MAXR];
+#pragma unroll
+                for (int l = 0; l < MAXR; ++l) {
+                    wj[0][l] = wv[l].x; wj[1][l] = wv[l].y; wj[2][l] = wv[l].z; wj[3][l] = wv[l].w;
+                }
+                float v[4] = {p[r].x, p[r].y, p[r].z, p[r].w};
+#pragma unroll
+                for (int c = 0; c < 4; ++c) v[c] = elem(r, 4 * j + c, v[c], wj[c]);
+                if constexpr (HAS) gst4(P + (size_t)r * d + 4 * j, make_float4(v[0], v[1], v[2], v[3]));
+                if constexpr (MV) {
+#pragma unroll
+                    for (int l = 0; l < MAXR; ++l) {
+                        if (l >= rk) break;
+                        const float xs[4] = {xv[l].x, xv[l].y, xv[l].z, xv[l].w};
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) dot[r][l] = fmaf(v[c], xs[c], dot[r][l]);
+                    }
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) nrm[r] = absacc(nrm[r], v[c], maxabs);
+                }
+            }
+        }
+    } else {
+        for (int j = lane; j < d; j += 64) {
+            float wj[MAXR], xj[MAXR];
+#pragma unroll
+            for (int l = 0; l < MAXR; ++l) {
+                wj[l] = (HAS && l < rk) ? gld(f.w + (size_t)l * d + j) : 0.f;
+                xj[l] = (MV && l < rk) ? gld(f.x + (size_t)l * d + j) : 0.f;
+            }
+#pragma unroll
+            for (int r = 0; r < RR; ++r) {
+                if (r >= nr) break;
+                float v = elem(r, j, gld(P + (size_t)r * d + j), wj);
+                if constexpr (HAS) gst(P + (size_t)r * d + j, v);
+                if constexpr (MV) {
+#pragma unroll
+                    for (int l = 0; l < MAXR; ++l)
+                        if (l < rk) dot[r][l] = fmaf(v, xj[l], dot[r][l]);
+                    nrm[r] = absacc(nrm[r], v, maxabs);
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(SM_THREADS) void sm_pass_rank_kernel(
+    const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
+    float4* __restrict__ partials, float* __restrict__ gram, int nblocks, int maxabs, int matvec) {
+    __shared__ float4 sred[SM_THREADS / 64];
+    __shared__ float sgram[SM_THREADS / 64][GRAM];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (int b = blockIdx.x; b < nblocks; b += gridDim.x) {
+        const RowBlock rb = blocks[b];
+        const FactorDesc f = factors[rb.factor];
+        if (f.rank <= 1) continue;
+        const Pending q = *f.pend;
+        const bool has = q.has != 0;
+        if (!has && !matvec) continue;
+        const int rbase = rb.row0 + wave * RR;
+        const int nr = max(0, min(RR, f.d - rbase));
+        const int rk = f.rank;
+        float dot[RR][MAXR], nrm[RR];
+#pragma unroll
+        for (int r = 0; r < RR; ++r) {
+            nrm[r] = 0.f;
+#pragma unroll
+            for (int l = 0; l < MAXR; ++l) dot[r][l] = 0.f;
+        }
+        if (nr > 0) {
+            const bool vec = (f.d & 3) == 0;
+            if (matvec) {
+                if (has) { if (vec) rank_rows<true, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+                           else     rank_rows<true, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm); }
+                else     { if (vec) rank_rows<false, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+                           else     rank_rows<false, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm); }
+            } else {
+                if (vec) rank_rows<true, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+                else     rank_rows<true, false, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            }
+        }
+        if (!matvec) continue;
+#pragma unroll
+        for (int r = 0; r < RR; ++r) {
+#pragma unroll
+            for (int l = 0; l < MAXR; ++l) dot[r][l] = wave_sum(dot[r][l]);
+            nrm[r] = maxabs ? wave_nanmax(nrm[r]) : wave_sum(nrm[r]);
+        }
+        if (lane == 0) {
+            float mx = 0.f, gxu[MAXR][MAXR], gxx[MAXR][MAXR];
+#pragma unroll
+            for (int l = 0; l < MAXR; ++l)
+#pragma unroll
+                for (int m = 0; m < MAXR; ++m) { gxu[l][m] = 0.f; gxx[l][m] = 0.f; }
+            for (int r = 0; r < nr; ++r) {
+                const int row = rbase + r;
+                float xr[MAXR];
+#pragma unroll
+                for (int l = 0; l < MAXR; ++l) {
+                    xr[l] = l < rk ? gld(f.x + (size_t)l * f.d + row) : 0.f;
+                    if (l < rk) gst(f.u + (size_t)l * f.d + row, dot[r][l]);
+                }
+                mx = nanmax(mx, nrm[r]);
+#pragma unroll
+                for (int l = 0; l < MAXR; ++l)
+#pragma unroll
+                    for (int m = 0; m < MAXR; ++m) {
+                        gxu[l][m] = fmaf(xr[l], dot[r][m], gxu[l][m]);
+                        gxx[l][m] = fmaf(xr[l], xr[m], gxx[l][m]);
+                    }
+            }
+            sred[wave] = make_float4(mx, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int l = 0; l < MAXR; ++l)
+#pragma unroll
+                for (int m = 0; m < MAXR; ++m) {
+                    sgram[wave][l * MAXR + m] = gxu[l][m];
+                    sgram[wave][MAXR * MAXR + l * MAXR + m] = gxx[l][m];
+                }
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            float4 acc = sred[0];
+            for (int w = 1; w < SM_THREADS / 64; ++w) acc.x = nanmax(acc.x, sred[w].x);
+            gst4(reinterpret_cast<float*>(partials + b), acc);
+        }
+        if (threadIdx.x < GRAM) {
+            float acc = sgram[0][threadIdx.x];
+            for (int w = 1; w < SM_THREADS / 64; ++w) acc += sgram[w][threadIdx.x];
+            gst(gram + (size_t)b * GRAM + threadIdx.x, acc);
+        }
+        __syncthreads();   // sred / sgram are reused by the next row block
     }
 }
 
@@ -323,9 +511,112 @@ struct SmScalars {
     float nu, s;
 };
 
+// Rank-r factor: the r sequential Sherman-Morrison updates of P^(0) = P_hat /
+// gamma with y_i = sqrt(1 - gamma) x_i (the paper's extension to higher ranks,
+// applied to the momentum accumulation of Eq. 4/5).  Every u_i = P^(i-1) y_i
+// is a combination U0 T_i of the columns of U0 = P_hat X, so all the
+// recursion needs is the r x r matrix A = X^T P_hat X:
+//   T_i   = (q / gamma) e_i - sum_{l<i} beta_l T_l (q T_l^T A e_i),   q = sqrt(1 - gamma)
+//   beta_i = 1 / (1 + q e_i^T A T_i)
+//   P_t   = P_hat / gamma - sum_i beta_i (U0 T_i)(U0 T_i)^T
+// stored as the pending term c1 = zp / gamma, c2 = zq / gamma, sgn = -1,
+// w_i = sqrt(beta_i) U0 T_i (U0 = zp u_raw + zq X).
+__device__ void finalize_rank(const FactorDesc& f, const float4* __restrict__ partials,
+                              const float* __restrict__ gram, const UpdateArgs& a) {
+    const int t = threadIdx.x, rk = f.rank;
+    __shared__ float s_mx[SM_THREADS];
+    __shared__ double s_g[GRAM];
+    __shared__ float s_coef[MAXR][MAXR];   // sqrt(beta_i) T[m][i], as [i][m]
+    __shared__ float s_zp, s_zq;
+    __shared__ int s_go;
+    float mx = 0.f;
+    for (int b = t; b < f.nblk; b += SM_THREADS) mx = nanmax(mx, partials[f.blk0 + b].x);
+    s_mx[t] = mx;
+    if (t < GRAM) {   // fixed-order float64 sum over the row blocks
+        double acc = 0.0;
+        for (int b = 0; b < f.nblk; ++b) acc += (double)gram[(size_t)(f.blk0 + b) * GRAM + t];
+        s_g[t] = acc;
+    }
+    __syncthreads();
+    for (int o = SM_THREADS / 2; o > 0; o >>= 1) {
+        if (t < o) s_mx[t] = nanmax(s_mx[t], s_mx[t + o]);
+        __syncthreads();
+    }
+    if (t == 0) {
+        const double g = (double)a.gamma, q = sqrt(1.0 - g);
+        const double nu = (double)s_mx[0];
+        const int stab = nu > (double)a.eps ? 1 : 0;
+        const double zp = stab ? (double)a.zeta : 1.0, zq = stab ? 1.0 - (double)a.zeta : 0.0;
+        double A[MAXR][MAXR], T[MAXR][MAXR], beta[MAXR];
+        for (int l = 0; l < MAXR; ++l)
+            for (int m = 0; m < MAXR; ++m) {
+                const double v = zp * s_g[l * MAXR + m] + zq * s_g[MAXR * MAXR + l * MAXR + m];
+                const double vt = zp * s_g[m * MAXR + l] + zq * s_g[MAXR * MAXR + m * MAXR + l];
+                A[l][m] = 0.5 * (v + vt);   // x^T P_hat x is symmetric
+                T[l][m] = 0.0;
+            }
+        bool ok = isfinite(nu);
+        for (int i = 0; i < rk; ++i) {
+            T[i][i] = q / g;
+            for (int l = 0; l < i; ++l) {
+                double c = 0.0;   // u_l^T y_i
+                for (int m = 0; m < rk; ++m) c += T[m][l] * A[m][i];
+                c *= q * beta[l];
+                for (int m = 0; m < rk; ++m) T[m][i] -= c * T[m][l];
+            }
+            double s = 0.0;       // y_i^T u_i
+            for (int m = 0; m < rk; ++m) s += A[i][m] * T[m][i];
+            s *= q;
+            beta[i] = 1.0 / (1.0 + s);
+            ok = ok && isfinite(beta[i]) && beta[i] > 0.0;
+        }
+        for (int i = 0; i < MAXR; ++i)
+            for (int m = 0; m < MAXR; ++m)
+                s_coef[i][m] = (ok && i < rk && m < rk) ? (float)(sqrt(beta[i]) * T[m][i]) : 0.f;
+        s_zp = (float)zp;
+        s_zq = (float)zq;
+        const int skip = ok ? 0 : 1;
+        if (f.stats != nullptr) {
+            mkor_layer_stats* st = f.stats;
+            const float nuf = (float)nu, sf = (float)A[0][0];
+            if (f.side == 0) { st->nu_L = nuf; st->s_L = sf; st->stab_L = stab; st->skip_L = skip; }
+            else             { st->nu_R = nuf; st->s_R = sf; st->stab_R = stab; st->skip_R = skip; }
+        }
+        Pending pq;
+        if (skip && a.guard) { pq.c1 = 1.f; pq.c2 = 0.f; pq.sgn = 0.f; pq.has = 0; }
+        else                 { pq.c1 = (float)(zp / g); pq.c2 = (float)(zq / g); pq.sgn = -1.f; pq.has = 1; }
+        *f.pend = pq;
+        s_go = (skip && a.guard) ? 0 : 1;
+    }
+    __syncthreads();
+    if (!s_go) return;
+    const float zp = s_zp, zq = s_zq;
+    for (int k = t; k < f.d; k += SM_THREADS) {
+        float um[MAXR];
+#pragma unroll
+        for (int m = 0; m < MAXR; ++m)
+            um[m] = m < rk ? __fmaf_rn(zp, gld(f.u + (size_t)m * f.d + k), __fmul_rn(zq, gld(f.x + (size_t)m * f.d + k)))
+                           : 0.f;
+#pragma unroll
+        for (int i = 0; i < MAXR; ++i) {
+            if (i >= rk) break;
+            float wv = 0.f;
+#pragma unroll
+            for (int m = 0; m < MAXR; ++m)
+                if (m < rk) wv = __fmaf_rn(s_coef[i][m], um[m], wv);
+            gst(f.w + (size_t)i * f.d + k, wv);
+        }
+    }
+}
+
 __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
-    const FactorDesc* __restrict__ factors, const float4* __restrict__ partials, UpdateArgs a) {
+    const FactorDesc* __restrict__ factors, const float4* __restrict__ partials, const float* __restrict__ gram,
+    UpdateArgs a) {
     const FactorDesc f = factors[blockIdx.x];
+    if (f.rank > 1) {
+        finalize_rank(f, partials, gram, a);
+        return;
+    }
     __shared__ float s_mx[SM_THREADS];
     __shared__ double s_xu[SM_THREADS], s_xx[SM_THREADS];
     __shared__ SmScalars s_c;
@@ -394,35 +685,54 @@ __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
         gst(f.w + i, __fmul_rn(c.sqc, __fmaf_rn(c.zp, gld(f.u + i), __fmul_rn(c.zq, gld(f.x + i)))));
 }
 
-__global__ void sm_reset_kernel(const FactorDesc* __restrict__ factors, int32_t nfactors) {
+__global__ void sm_reset_kernel(const FactorDesc* __restrict__ factors, int32_t nfactors, int ranked_only) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < nfactors) *factors[i].pend = Pending{1.f, 0.f, 0.f, 0};
+    if (i < nfactors && (!ranked_only || factors[i].rank > 1)) *factors[i].pend = Pending{1.f, 0.f, 0.f, 0};
 }
 
 }  // namespace
 
 hipError_t launch_sm_pass(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
-                          float4* partials, int32_t norm_kind, int32_t matvec, hipStream_t stream) {
+                          float4* partials, float* gram, int32_t norm_kind, int32_t matvec, int32_t ranked,
+                          hipStream_t stream) {
     if (nblocks <= 0) return hipSuccess;
     const int32_t grid = (SM_GRID > 0 && nblocks > SM_GRID) ? SM_GRID : nblocks;
+    const int maxabs = norm_kind == MKOR_NORM_MAXABS ? 1 : 0;
     hipLaunchKernelGGL(sm_pass_kernel, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
-                       partials, nblocks, norm_kind == MKOR_NORM_MAXABS ? 1 : 0, matvec ? 1 : 0);
+                       partials, nblocks, maxabs, matvec ? 1 : 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !ranked) return e;
+    hipLaunchKernelGGL(sm_pass_rank_kernel, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
+                       partials, gram, nblocks, maxabs, matvec ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_sm_apply_rank(const FactorDesc* factors, const RowBlock* blocks, int32_t nblocks,
+                                int32_t nfactors, hipStream_t stream) {
+    if (nblocks <= 0 || nfactors <= 0) return hipSuccess;
+    const int32_t grid = (SM_GRID > 0 && nblocks > SM_GRID) ? SM_GRID : nblocks;
+    hipLaunchKernelGGL(sm_pass_rank_kernel, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
+                       (float4*)nullptr, (float*)nullptr, nblocks, 0, 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(sm_reset_kernel, dim3((nfactors + 255) / 256), dim3(256), 0, stream, factors,
+                       nfactors, 1);
     return hipGetLastError();
 }
 
 hipError_t launch_sm_finalize(const FactorDesc* factors, int32_t nfactors, const float4* partials,
-                              const mkor_params& p, hipStream_t stream) {
+                              const float* gram, const mkor_params& p, hipStream_t stream) {
     if (nfactors <= 0) return hipSuccess;
     UpdateArgs a{p.gamma, p.zeta, p.stab_eps, p.sm_variant, p.guard_nonfinite};
     hipLaunchKernelGGL(sm_finalize_kernel, dim3(nfactors), dim3(SM_THREADS), 0, stream, factors,
-                       partials, a);
+                       partials, gram, a);
     return hipGetLastError();
 }
 
 hipError_t launch_sm_reset(const FactorDesc* factors, int32_t nfactors, hipStream_t stream) {
     if (nfactors <= 0) return hipSuccess;
     hipLaunchKernelGGL(sm_reset_kernel, dim3((nfactors + 255) / 256), dim3(256), 0, stream, factors,
-                       nfactors);
+                       nfactors, 0);
     return hipGetLastError();
 }
 

@@ -12,11 +12,13 @@ from .binding import STATS_BYTES, MkorPlan, read_stats
 
 
 def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True,
-                    rows=0, act_dtype="fp32", factor_dtype="fp32"):
+                    rows=0, act_dtype="fp32", factor_dtype="fp32", rank=1):
     """One dict of device tensors per (d_in, d_out); factors start as I.  With
     rows > 0 each second-order layer also gets token-row buffers A (rows x d_in)
     and Gout (rows x d_out), from which the library forms a and g.
-    factor_dtype "bf16" stores Linv and Rinv in bf16 (half-precision factors)."""
+    factor_dtype "bf16" stores Linv and Rinv in bf16 (half-precision factors).
+    rank > 1 gives a and g the shapes (rank, d_in) and (rank, d_out): r vectors
+    per factor (rank-r update)."""
     fdt = torch.bfloat16 if factor_dtype == "bf16" else torch.float32
     gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
     layers = []
@@ -28,8 +30,10 @@ def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None,
         if so:
             L["Linv"] = torch.eye(d_in, dtype=fdt, device=device)
             L["Rinv"] = torch.eye(d_out, dtype=fdt, device=device)
-            L["a"] = torch.zeros(d_in, dtype=torch.float32, device=device)
-            L["g"] = torch.zeros(d_out, dtype=torch.float32, device=device)
+            va = (rank, d_in) if rank > 1 else (d_in,)
+            vg = (rank, d_out) if rank > 1 else (d_out,)
+            L["a"] = torch.zeros(va, dtype=torch.float32, device=device)
+            L["g"] = torch.zeros(vg, dtype=torch.float32, device=device)
         if stats:
             L["stats"] = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=device)
         if so and rows:

@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 4
+    assert lib.mkor_abi_version() == 5
 
 
 def test_status_strings(lib):
@@ -90,13 +90,14 @@ class Fake:
         return p
 
 
-def layer(fk, d_in, d_out, so=1, dt=0, stats=False, rows=0, adt=0, fdt=0):
+def layer(fk, d_in, d_out, so=1, dt=0, stats=False, rows=0, adt=0, fdt=0, rank=0):
     esz = 2 if dt == 1 else 4
     aesz = 2 if adt == 1 else 4
     fsz = 2 if fdt == 1 else 4
     return dict(d_in=d_in, d_out=d_out, second_order=so, grad_dtype=dt, factor_dtype=fdt,
                 Linv=fk.alloc(d_in * d_in * fsz), Rinv=fk.alloc(d_out * d_out * fsz),
-                a=fk.alloc(d_in * 4), g=fk.alloc(d_out * 4), G=fk.alloc(d_in * d_out * esz),
+                a=fk.alloc(d_in * 4 * max(1, rank)), g=fk.alloc(d_out * 4 * max(1, rank)),
+                G=fk.alloc(d_in * d_out * esz), rank=rank,
                 dW=fk.alloc(d_in * d_out * 4), stats=fk.alloc(48) if stats else None,
                 rows=rows, act_dtype=adt,
                 A=fk.alloc(rows * d_in * aesz) if rows else None,
@@ -151,7 +152,8 @@ def test_empty_list(lib):
     (lambda L: L.update(rows=M.MAX_ROWS + 1), M.MKOR_INVALID_ARG),
     (lambda L: L.update(rows=8), M.MKOR_INVALID_ARG),              # rows > 0 without A / Gout
     (lambda L: L.update(factor_dtype=2), M.MKOR_UNSUPPORTED),
-    (lambda L: L.update(reserved=1), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(rank=-1), M.MKOR_INVALID_ARG),
+    (lambda L: L.update(rank=5), M.MKOR_INVALID_ARG),
     (lambda L: L.update(factor_dtype=1, d_out=100), M.MKOR_UNSUPPORTED),  # bf16: multiples of 64
 ])
 def test_layer_rejected(lib, mutate, status):
@@ -279,3 +281,22 @@ def test_workspace_bf16_factors(lib):
     # mixed lists plan both GEMM kinds
     st, _ = ws_status([layer(fk, 1024, 4096, fdt=1), layer(fk, 4096, 1024), layer(fk, 37, 100)])
     assert st == M.MKOR_OK
+
+
+def test_rank_r_layers(lib):
+    fk = Fake()
+    assert ws_status([layer(fk, 37, 100, rank=4)])[0] == M.MKOR_OK
+    assert ws_status([layer(fk, 64, 96, rank=2, rows=16)])[0] == M.MKOR_UNSUPPORTED   # means are rank-1
+    assert ws_status([layer(fk, 64, 128, rank=2, fdt=1)])[0] == M.MKOR_UNSUPPORTED    # fp32 factors only
+    # the r vectors of a factor extend over d * r floats
+    a, b = layer(fk, 64, 64, rank=3), layer(fk, 64, 64, rank=3)
+    b["a"] = a["a"] + 64 * 4 * 2          # read-only vectors may be shared
+    assert ws_status([a, b])[0] == M.MKOR_OK
+    a = layer(fk, 64, 64, rank=3)
+    a["dW"] = a["a"] + 64 * 4 * 2         # a writable buffer over the third vector
+    assert ws_status([a])[0] == M.MKOR_INVALID_ARG
+    # Gram partials and r-wide vectors: the rank-4 plan needs more workspace
+    r1 = ws_status([layer(fk, 1024, 1024)])[1]
+    r4 = ws_status([layer(fk, 1024, 1024, rank=4)])[1]
+    assert r4 > r1
+
