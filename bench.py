@@ -98,6 +98,8 @@ def parse():
                          "half-precision factors, bf16 MFMA preconditioning)")
     ap.add_argument("--rank", type=int, default=1,
                     help="vectors per factor update (the rank-r extension; fp32 factors)")
+    ap.add_argument("--no-opt", action="store_true",
+                    help="skip the measurement of the step with the fused LAMB optimizer")
     ap.add_argument("--no-half", action="store_true",
                     help="skip the extra measurement with bf16 factors")
     return ap.parse_args()
@@ -343,6 +345,51 @@ def measure(w, args, factor_dtype):
     return ms_step, kernels, roof, schedule
 
 
+def measure_opt(w, args):
+    """The same workload stepped with mkor_step_opt (backend LAMB fused into the
+    rescale, weights and moments of every layer in HBM) against mkor_step."""
+    import torch
+
+    from paper_2306_01685_amd import OPT_LAMB, OptParams, Params, harness as H
+
+    layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, optimizer="lamb")
+    fill_inputs(layers, w)
+    for L in layers:
+        L["W"].normal_(0.0, 0.02)
+    plan = H.make_plan(layers)
+    params = Params(gamma=w.gamma, zeta=0.5, eps=args.eps)
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name in ("step", "step_opt"):
+        for t in range(args.warmup):
+            if name == "step":
+                plan.step(params)
+            else:
+                plan.step_opt(params, OptParams(kind=OPT_LAMB, step=t + 1, lr=1e-3))
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for t in range(args.steps):
+            if name == "step":
+                plan.step(params)
+            else:
+                plan.step_opt(params, OptParams(kind=OPT_LAMB, step=args.warmup + t + 1, lr=1e-3))
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / args.steps
+    nel = sum(i * o for i, o in w.shapes)
+    del plan, layers
+    torch.cuda.empty_cache()
+    # LAMB pass A reads dW_hat, W, m, v and writes m, v; pass B reads m, v, W and writes W
+    extra_ms = res["step_opt"] - res["step"]
+    return dict(kind="lamb", ms_per_step=res["step_opt"], ms_per_step_without=res["step"],
+                value=w.n_layers / (res["step_opt"] / 1e3), unit="layer-updates/s",
+                optimizer_bytes=40 * nel, extra_ms=extra_ms,
+                note="step with LAMB fused into the rescale (weights, m, v in HBM) vs the step that only "
+                     "writes dW; the optimizer itself moves 40 B per weight (rescale pass 24 + 12 read/4 "
+                     "write of the second pass) in place of the rescale's 8")
+
+
 def initial_factors_stored(w, i, half):
     """The workload's initial factors, rounded to bf16 for bf16 storage."""
     import workloads as W
@@ -381,6 +428,10 @@ def main():
                     dtype="bf16 factors, bf16 MFMA (fp32 accumulation)", roofline=h_roof,
                     schedule_f10=h_sched, kernels=h_k)
 
+    opt = None
+    if args.factor_dtype == "fp32" and not args.no_opt and args.rank == 1:
+        opt = measure_opt(w, args)
+
     out = {
         "metric": METRIC, "value": value, "unit": "layer-updates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
@@ -395,6 +446,7 @@ def main():
         "schedule_f10": schedule,
         "kernels": kernels,
         "half_factors": half,
+        "fused_optimizer": opt,
         "device": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:

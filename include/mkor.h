@@ -93,7 +93,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 5
+#define MKOR_ABI_VERSION 6
 
 /* status codes */
 #define MKOR_OK                   0
@@ -138,6 +138,24 @@ typedef struct mkor_params {
                                  0: non-finite values propagate */
 } mkor_params;
 
+/* mkor_opt_params.kind */
+#define MKOR_OPT_SGD   1   /* d = dW + wd W, m = mu m + d, W -= lr m */
+#define MKOR_OPT_LAMB  2   /* layer-wise adaptive moments, see mkor_step_opt */
+
+/* Backend optimizer step fused with the rescale (mkor_step_opt). */
+typedef struct mkor_opt_params {
+    int32_t kind;          /* MKOR_OPT_SGD or MKOR_OPT_LAMB */
+    int32_t step;          /* LAMB: t >= 1, the step count of the bias corrections */
+    float   lr;            /* >= 0 */
+    float   momentum;      /* SGD: 0 <= mu < 1 */
+    float   beta1, beta2;  /* LAMB: 0 <= b < 1 */
+    float   eps;           /* LAMB: > 0 */
+    float   weight_decay;  /* >= 0 */
+    int32_t store_dw;      /* 1: also write the rescaled dW into mkor_layer.dW
+                              (layers without W always get dW) */
+    int32_t reserved;      /* must be 0 */
+} mkor_opt_params;
+
 typedef struct mkor_layer {
     int32_t      d_in, d_out;   /* 1 .. MKOR_MAX_DIM */
     int32_t      second_order;  /* 1: MKOR branch; 0: dW = G (first-order layer) */
@@ -176,6 +194,14 @@ typedef struct mkor_layer {
      * written into Linv / Rinv within the step that computes it (one more
      * read and write of the factor), so it leaves no pending term. */
     int32_t      rank;
+    /* Backend optimizer state (Algorithm 1, last line: the weights take an
+     * optimizer step with dW), used by mkor_step_opt / mkor_precondition_opt
+     * only; each d_in x d_out fp32, in/out, NULL when unused.  W: the layer's
+     * weights.  opt_m: the SGD momentum buffer, or LAMB's first moment.
+     * opt_v: LAMB's second moment.  Moments start at 0. */
+    float*       W;
+    float*       opt_m;
+    float*       opt_v;
 } mkor_layer;
 
 /* Per-layer observability record, written on the device when
@@ -246,6 +272,27 @@ int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, vo
  * buffers hold exactly the factors the next step starts from.  Asynchronous
  * on `stream`; INVALID_ARG if plan is NULL. */
 int mkor_sync_factors(mkor_plan* plan, void* stream);
+
+/* Checks an optimizer parameter block without touching the device. */
+int mkor_opt_params_check(const mkor_opt_params* opt);
+
+/* mkor_step with the backend optimizer fused into the rescale (Algorithm 1,
+ * rescale and last lines): for every layer with W the rescaled gradient g
+ * (g = G for first-order layers) updates W in the same pass that scales it,
+ *   MKOR_OPT_SGD:  d = g + wd W,  m = mu m + d,  W = W - lr m;
+ *   MKOR_OPT_LAMB: m = b1 m + (1 - b1) g,  v = b2 v + (1 - b2) g^2,
+ *                  r = (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps) + wd W,
+ *                  W = W - lr (||W||_F / ||r||_F) r   per layer (ratio 1 if a
+ *                  norm is 0), as LAMB's authors define it;
+ * LAMB takes a second pass over m, v and W for the per-layer ratio.  Layers
+ * without W get dW as in mkor_step.  Needs opt_m (SGD) or opt_m and opt_v
+ * (LAMB) on every layer with W (INVALID_ARG otherwise). */
+int mkor_step_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt, void* stream);
+
+/* mkor_precondition with the same fused optimizer step (the steps between
+ * factor updates of an update-every-f schedule). */
+int mkor_precondition_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt,
+                          void* stream);
 
 /* Frees the host-side plan (NULL is allowed).  The workspace stays the
  * caller's. */

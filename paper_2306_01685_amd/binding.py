@@ -35,7 +35,9 @@ DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
 MAX_RANK = 4
-ABI_VERSION = 5
+ABI_VERSION = 6
+OPT_SGD = 1
+OPT_LAMB = 2
 
 
 class mkor_params(ctypes.Structure):
@@ -52,7 +54,15 @@ class mkor_layer(ctypes.Structure):
                 ("G", ctypes.c_void_p), ("dW", ctypes.c_void_p), ("stats", ctypes.c_void_p),
                 ("rows", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
                 ("A", ctypes.c_void_p), ("Gout", ctypes.c_void_p),
-                ("factor_dtype", ctypes.c_int32), ("rank", ctypes.c_int32)]
+                ("factor_dtype", ctypes.c_int32), ("rank", ctypes.c_int32),
+                ("W", ctypes.c_void_p), ("opt_m", ctypes.c_void_p), ("opt_v", ctypes.c_void_p)]
+
+
+class mkor_opt_params(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("step", ctypes.c_int32), ("lr", ctypes.c_float),
+                ("momentum", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("store_dw", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class mkor_layer_stats(ctypes.Structure):
@@ -70,7 +80,7 @@ STATS_FIELDS = [f for f, _ in mkor_layer_stats._fields_]
 EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_params_check",
             "mkor_workspace_size", "mkor_plan_create", "mkor_update_factors",
             "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_sync_factors",
-            "mkor_plan_destroy"]
+            "mkor_opt_params_check", "mkor_step_opt", "mkor_precondition_opt", "mkor_plan_destroy"]
 
 STAGE_MEANS, STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(6)
 NUM_STAGES = 6
@@ -116,6 +126,12 @@ def load_library(path: str = LIB_PATH):
     lib.mkor_run_stage.argtypes = [P, ctypes.POINTER(mkor_params), I32, P]
     lib.mkor_sync_factors.restype = ctypes.c_int
     lib.mkor_sync_factors.argtypes = [P, P]
+    lib.mkor_opt_params_check.restype = ctypes.c_int
+    lib.mkor_opt_params_check.argtypes = [ctypes.POINTER(mkor_opt_params)]
+    for name in ("mkor_step_opt", "mkor_precondition_opt"):
+        fn = getattr(lib, name)
+        fn.restype = ctypes.c_int
+        fn.argtypes = [P, ctypes.POINTER(mkor_params), ctypes.POINTER(mkor_opt_params), P]
     lib.mkor_plan_destroy.restype = None
     lib.mkor_plan_destroy.argtypes = [P]
     if lib.mkor_abi_version() != ABI_VERSION:
@@ -153,6 +169,29 @@ class Params:
                            int(bool(self.guard_nonfinite)))
 
 
+@dataclass
+class OptParams:
+    """Backend optimizer fused with the rescale (mkor_opt_params)."""
+    kind: int = OPT_LAMB
+    step: int = 1
+    lr: float = 1e-3
+    momentum: float = 0.9
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-6
+    weight_decay: float = 0.01
+    store_dw: bool = False
+
+    def to_c(self) -> mkor_opt_params:
+        return mkor_opt_params(int(self.kind), int(self.step), self.lr, self.momentum, self.beta1,
+                               self.beta2, self.eps, self.weight_decay, int(bool(self.store_dw)), 0)
+
+
+def opt_params_check(o) -> int:
+    c = o.to_c() if isinstance(o, OptParams) else o
+    return load_library().mkor_opt_params_check(ctypes.byref(c))
+
+
 def params_check(p) -> int:
     c = p.to_c() if isinstance(p, Params) else p
     return load_library().mkor_params_check(ctypes.byref(c))
@@ -167,7 +206,8 @@ def make_layer_array(descs):
                             d.get("g") or None, d.get("G") or None, d.get("dW") or None,
                             d.get("stats") or None, d.get("rows", 0), d.get("act_dtype", 0),
                             d.get("A") or None, d.get("Gout") or None, d.get("factor_dtype", 0),
-                            d.get("rank", 0))
+                            d.get("rank", 0), d.get("W") or None, d.get("opt_m") or None,
+                            d.get("opt_v") or None)
     return arr
 
 
@@ -219,7 +259,7 @@ class MkorPlan:
                 gdt = DTYPE_F32
             else:
                 raise TypeError(f"unsupported gradient dtype {G.dtype}")
-            for k in ("Linv", "Rinv", "a", "g", "G", "dW", "A", "Gout"):
+            for k in ("Linv", "Rinv", "a", "g", "G", "dW", "A", "Gout", "W", "opt_m", "opt_v"):
                 t = L.get(k)
                 if t is not None and not t.is_contiguous():
                     raise ValueError(f"{k} must be contiguous")
@@ -242,7 +282,8 @@ class MkorPlan:
                               a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
                               stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
                               Gout=_ptr(L.get("Gout")), factor_dtype=fdt,
-                              rank=int(L["a"].shape[0]) if so and L["a"].dim() == 2 else 0))
+                              rank=int(L["a"].shape[0]) if so and L["a"].dim() == 2 else 0,
+                              W=_ptr(L.get("W")), opt_m=_ptr(L.get("opt_m")), opt_v=_ptr(L.get("opt_v"))))
         self._arr = make_layer_array(descs)
         n = len(descs)
         size = ctypes.c_size_t(0)
@@ -278,6 +319,17 @@ class MkorPlan:
         p = params.to_c() if isinstance(params, Params) else params
         _check(self._lib.mkor_run_stage(self._plan, ctypes.byref(p), int(stage), _stream_handle(stream)),
                "mkor_run_stage")
+
+    def step_opt(self, params: Params, opt: "OptParams", stream=None):
+        """mkor_step with the backend optimizer fused into the rescale."""
+        p, o = params.to_c(), opt.to_c()
+        _check(self._lib.mkor_step_opt(self._plan, ctypes.byref(p), ctypes.byref(o), _stream_handle(stream)),
+               "mkor_step_opt")
+
+    def precondition_opt(self, params: Params, opt: "OptParams", stream=None):
+        p, o = params.to_c(), opt.to_c()
+        _check(self._lib.mkor_precondition_opt(self._plan, ctypes.byref(p), ctypes.byref(o),
+                                               _stream_handle(stream)), "mkor_precondition_opt")
 
     def sync_factors(self, stream=None):
         _check(self._lib.mkor_sync_factors(self._plan, _stream_handle(stream)), "mkor_sync_factors")

@@ -49,7 +49,7 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
     if (n < 0) return fail(MKOR_INVALID_ARG, "n = %d is negative", n);
     if (n > 0 && layers == nullptr) return fail(MKOR_INVALID_ARG, "layers is NULL with n = %d", n);
     std::vector<Interval> iv;
-    iv.reserve((size_t)n * 9 + 1);
+    iv.reserve((size_t)n * 12 + 1);
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         if (L.d_in < 1 || L.d_in > MKOR_MAX_DIM || L.d_out < 1 || L.d_out > MKOR_MAX_DIM)
@@ -92,6 +92,9 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
             {L.stats, sizeof(mkor_layer_stats), true, "stats", L.stats != nullptr},
             {L.A, asz * din, false, "A", means},
             {L.Gout, asz * dout, false, "Gout", means},
+            {L.W, din * dout * 4, true, "W", L.W != nullptr},
+            {L.opt_m, din * dout * 4, true, "opt_m", L.opt_m != nullptr},
+            {L.opt_v, din * dout * 4, true, "opt_v", L.opt_v != nullptr},
         };
         for (auto& b : bufs) {
             if (!b.used) continue;
@@ -136,6 +139,7 @@ struct Layout {
     size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
     size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
     size_t off_gram = 0;                                         // rank-r Gram partials
+    size_t off_lpart = 0, off_trust = 0;                         // LAMB block sums, per-layer ratios
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
@@ -307,6 +311,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.table_bytes = align_up(o, 256);
     Lo.off_smpart = take(sizeof(float4) * Lo.nrowblocks);
     Lo.off_gram = take(Lo.nranked > 0 ? sizeof(float) * GRAM * (size_t)Lo.nrowblocks : 0);
+    Lo.off_lpart = take(sizeof(float2) * (size_t)Lo.nrsblocks);
+    Lo.off_trust = take(sizeof(float) * (size_t)n);
     Lo.off_gpart = take(sizeof(float) * Lo.ngpart);
     Lo.off_dpart = take(sizeof(float) * Lo.ndpart);
     Lo.off_mpart = take(sizeof(double) * (size_t)Lo.nmeanpart);
@@ -358,6 +364,7 @@ struct mkor_plan {
     int32_t n = 0;
     char* ws = nullptr;
     Layout lo;
+    std::vector<uint8_t> optbuf;   // per layer: 1 W, 2 opt_m, 4 opt_v
 };
 
 extern "C" {
@@ -476,6 +483,10 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         R.g_bf16 = L.grad_dtype == MKOR_DTYPE_BF16;
         R.first_blk = rbi;
         for (int64_t s = 0; s < R.numel; s += RS_ELEMS) rsb[rbi++] = RescaleBlock{i, 0, s};
+        R.nblk = rbi - R.first_blk;
+        R.W = L.W;
+        R.m = L.opt_m;
+        R.v = L.opt_v;
         if (!L.second_order) continue;
         const bool half = is_half(L);
         for (int side = 0; side < 2; ++side) {
@@ -563,6 +574,9 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     plan->n = n;
     plan->ws = base;
     plan->lo = lo;
+    plan->optbuf.resize(n);
+    for (int32_t i = 0; i < n; ++i)
+        plan->optbuf[i] = (uint8_t)((layers[i].W ? 1 : 0) | (layers[i].opt_m ? 2 : 0) | (layers[i].opt_v ? 4 : 0));
     if (lo.table_bytes > 0) {
         hipError_t e = hipMemcpy(base, host.data(), lo.table_bytes, hipMemcpyHostToDevice);
         if (e != hipSuccess) {
@@ -655,6 +669,58 @@ static int check_plan_params(const mkor_plan* plan, const mkor_params* params) {
     return MKOR_OK;
 }
 
+static int check_opt(const mkor_opt_params* o) {
+    if (o == nullptr) return fail(MKOR_INVALID_ARG, "opt is NULL");
+    if (o->kind != MKOR_OPT_SGD && o->kind != MKOR_OPT_LAMB)
+        return fail(MKOR_INVALID_ARG, "opt kind = %d unknown", o->kind);
+    if (!(o->lr >= 0.f) || !std::isfinite(o->lr)) return fail(MKOR_INVALID_ARG, "lr = %g must be finite and >= 0", (double)o->lr);
+    if (!(o->weight_decay >= 0.f) || !std::isfinite(o->weight_decay))
+        return fail(MKOR_INVALID_ARG, "weight_decay = %g must be finite and >= 0", (double)o->weight_decay);
+    if (o->store_dw != 0 && o->store_dw != 1) return fail(MKOR_INVALID_ARG, "store_dw = %d is not 0 or 1", o->store_dw);
+    if (o->reserved != 0) return fail(MKOR_INVALID_ARG, "reserved = %d must be 0", o->reserved);
+    if (o->kind == MKOR_OPT_SGD && !(o->momentum >= 0.f && o->momentum < 1.f))
+        return fail(MKOR_INVALID_ARG, "momentum = %g outside [0, 1)", (double)o->momentum);
+    if (o->kind == MKOR_OPT_LAMB) {
+        if (!(o->beta1 >= 0.f && o->beta1 < 1.f) || !(o->beta2 >= 0.f && o->beta2 < 1.f))
+            return fail(MKOR_INVALID_ARG, "betas = (%g, %g) outside [0, 1)", (double)o->beta1, (double)o->beta2);
+        if (!(o->eps > 0.f) || !std::isfinite(o->eps)) return fail(MKOR_INVALID_ARG, "eps = %g must be > 0", (double)o->eps);
+        if (o->step < 1) return fail(MKOR_INVALID_ARG, "step = %d must be >= 1", o->step);
+    }
+    return MKOR_OK;
+}
+
+// The fused rescale + optimizer stage (in place of MKOR_STAGE_RESCALE).
+static int run_rescale_opt(mkor_plan* p, const mkor_params* prm, const mkor_opt_params* o, hipStream_t s) {
+    const Layout& lo = p->lo;
+    char* ws = p->ws;
+    OptArgs a{};
+    a.kind = o->kind;
+    a.store_dw = o->store_dw;
+    a.lr = o->lr; a.mom = o->momentum; a.b1 = o->beta1; a.b2 = o->beta2; a.eps = o->eps;
+    a.wd = o->weight_decay;
+    a.bc1 = o->kind == MKOR_OPT_LAMB ? (float)(1.0 / (1.0 - std::pow((double)o->beta1, (double)o->step))) : 1.f;
+    a.bc2 = o->kind == MKOR_OPT_LAMB ? (float)(1.0 / (1.0 - std::pow((double)o->beta2, (double)o->step))) : 1.f;
+    const hipError_t e = launch_rescale_opt(reinterpret_cast<const RescaleLayer*>(ws + lo.off_rsl), p->n,
+                                            reinterpret_cast<const RescaleBlock*>(ws + lo.off_rsb), lo.nrsblocks,
+                                            reinterpret_cast<const float*>(ws + lo.off_gpart),
+                                            reinterpret_cast<const float*>(ws + lo.off_dpart), prm->rescale, a,
+                                            reinterpret_cast<float2*>(ws + lo.off_lpart),
+                                            reinterpret_cast<float*>(ws + lo.off_trust), s);
+    if (e != hipSuccess) return hip_fail(e, "rescale + optimizer launch");
+    return MKOR_OK;
+}
+
+static int check_opt_plan(const mkor_plan* plan, const mkor_opt_params* o) {
+    const int st = check_opt(o);
+    if (st != MKOR_OK) return st;
+    const uint8_t need = o->kind == MKOR_OPT_SGD ? 2 : 6;
+    for (int32_t i = 0; i < plan->n; ++i)
+        if ((plan->optbuf[i] & 1) && (plan->optbuf[i] & need) != need)
+            return fail(MKOR_INVALID_ARG, "layer %d has W but not the %s state", i,
+                        o->kind == MKOR_OPT_SGD ? "opt_m" : "opt_m / opt_v");
+    return MKOR_OK;
+}
+
 int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
@@ -680,6 +746,40 @@ int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
     if (st != MKOR_OK) return st;
     return run_range(plan, params, MKOR_STAGE_MEANS, MKOR_STAGE_RESCALE,
                      static_cast<hipStream_t>(stream));
+}
+
+int mkor_opt_params_check(const mkor_opt_params* opt) {
+    g_err[0] = 0;
+    return check_opt(opt);
+}
+
+int mkor_step_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    int st = check_plan_params(plan, params);
+    if (st != MKOR_OK) return st;
+    st = check_opt_plan(plan, opt);
+    if (st != MKOR_OK) return st;
+    if (plan->n == 0) return MKOR_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = run_range(plan, params, MKOR_STAGE_MEANS, MKOR_STAGE_GEMM_DW, s);
+    if (st != MKOR_OK) return st;
+    return run_rescale_opt(plan, params, opt, s);
+}
+
+int mkor_precondition_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt,
+                          void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    int st = check_plan_params(plan, params);
+    if (st != MKOR_OK) return st;
+    st = check_opt_plan(plan, opt);
+    if (st != MKOR_OK) return st;
+    if (plan->n == 0) return MKOR_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = run_range(plan, params, MKOR_STAGE_GEMM_XT, MKOR_STAGE_GEMM_DW, s);
+    if (st != MKOR_OK) return st;
+    return run_rescale_opt(plan, params, opt, s);
 }
 
 int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, void* stream) {

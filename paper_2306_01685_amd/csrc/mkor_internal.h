@@ -205,7 +205,18 @@ struct RescaleLayer {
     int32_t           gpart0, ngpart;   // ||G||^2 partials (written by GEMM 1)
     int32_t           dpart0, ndpart;   // ||dW_hat||^2 partials (written by GEMM 2)
     int32_t           first_blk;        // first rescale block of this layer
-    int32_t           _pad;
+    int32_t           nblk;             // rescale blocks of this layer
+    float*            W;                // backend optimizer state (null when unused)
+    float*            m;
+    float*            v;
+};
+
+// Backend optimizer fused with the rescale (host-computed scalars).
+struct OptArgs {
+    int32_t kind;            // MKOR_OPT_SGD or MKOR_OPT_LAMB
+    int32_t store_dw;
+    float   lr, mom, b1, b2, eps, wd;
+    float   bc1, bc2;        // 1 / (1 - b1^t), 1 / (1 - b2^t)
 };
 
 #ifndef MKOR_RS_GRID
@@ -258,6 +269,11 @@ hipError_t launch_gemm_xt(const GemmLayer* layers, const GemmTile* tiles, int32_
 hipError_t launch_gemm_dw(const GemmLayer* layers, const GemmTile* tiles, int32_t ntiles,
                           float* partials, hipStream_t stream);
 
+// Rescale fused with the optimizer: pass A (scale, moments, SGD step or LAMB
+// norm partials), then for LAMB the per-layer ratio and pass B (weight step).
+hipError_t launch_rescale_opt(const RescaleLayer* layers, int32_t nlayers, const RescaleBlock* blocks,
+                              int32_t nblocks, const float* gpart, const float* dpart, int32_t rescale,
+                              const OptArgs& opt, float2* lpart, float* trust, hipStream_t stream);
 hipError_t launch_rescale(const RescaleLayer* layers, const RescaleBlock* blocks, int32_t nblocks,
                           const float* gpart, const float* dpart, int32_t rescale,
                           hipStream_t stream);

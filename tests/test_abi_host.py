@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 5
+    assert lib.mkor_abi_version() == 6
 
 
 def test_status_strings(lib):
@@ -46,7 +46,8 @@ def test_status_strings(lib):
 
 def test_struct_sizes():
     assert ctypes.sizeof(B.mkor_params) == 28
-    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8 + 8
+    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8 + 8 + 3 * 8
+    assert ctypes.sizeof(B.mkor_opt_params) == 40
     assert M.STATS_BYTES == 48
 
 
@@ -300,3 +301,30 @@ def test_rank_r_layers(lib):
     r4 = ws_status([layer(fk, 1024, 1024, rank=4)])[1]
     assert r4 > r1
 
+
+
+@pytest.mark.parametrize("kw,ok", [
+    (dict(), True), (dict(kind=M.OPT_SGD), True), (dict(kind=3), False), (dict(lr=-1.0), False),
+    (dict(lr=math.inf), False), (dict(weight_decay=-0.1), False), (dict(kind=M.OPT_SGD, momentum=1.0), False),
+    (dict(beta1=1.0), False), (dict(beta2=-0.1), False), (dict(eps=0.0), False), (dict(step=0), False),
+    (dict(kind=M.OPT_SGD, step=0), True),
+])
+def test_opt_params(lib, kw, ok):
+    st = M.opt_params_check(M.OptParams(**kw))
+    assert (st == M.MKOR_OK) == ok, (kw, st, M.last_error())
+
+
+def test_opt_buffers_validated(lib):
+    fk = Fake()
+    L = layer(fk, 64, 96)
+    L.update(W=fk.alloc(64 * 96 * 4), opt_m=fk.alloc(64 * 96 * 4), opt_v=fk.alloc(64 * 96 * 4))
+    assert ws_status([L])[0] == M.MKOR_OK
+    L2 = dict(L)
+    L2["opt_m"] = L["W"] + 64                 # state over the weights
+    assert ws_status([L2])[0] == M.MKOR_INVALID_ARG
+    L3 = dict(L)
+    L3["W"] = L["G"]                          # weights over the (read-only) gradient
+    assert ws_status([L3])[0] == M.MKOR_INVALID_ARG
+    L4 = dict(L)
+    L4["opt_v"] = L["opt_v"] + 4              # misaligned
+    assert ws_status([L4])[0] == M.MKOR_INVALID_ARG

@@ -1,0 +1,130 @@
+"""GPU parity of the backend optimizer fused with the rescale (mkor_step_opt,
+mkor_precondition_opt) against the float64 oracle: MKOR's step (oracle/
+mkor_oracle.py, oracle/half.py) followed by SGD or LAMB (oracle/optimizer.py).
+
+Bar: relative Frobenius error <= 1e-4 on W, the moments and dW after each of
+several steps (the optimizer adds a few fp32 roundings per element to the
+step's dW error, which the rank-1 bars already bound at 1e-4)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from oracle.half import layer_step_half
+from oracle.optimizer import lamb_step, sgd_step
+from paper_2306_01685_amd import MkorError, OPT_LAMB, OPT_SGD, OptParams, Params, harness as H
+from tests.parity import oparams, rel, spd
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+# (d_in, d_out, kind, with weights): kind "f32" (fp32 factors, bf16 G), "bf16"
+# (bf16 factors), "first" (first-order layer).  Sizes with d_in * d_out odd take
+# the kernels' element-wise path, the others their 16-byte path.
+LAYERS = [(130, 250, "f32", True), (128, 192, "bf16", True), (50, 70, "first", True), (64, 64, "f32", False),
+          (33, 45, "f32", True), (37, 101, "first", True)]
+
+
+def _setup(opt_kind, seed):
+    opt = "lamb" if opt_kind == OPT_LAMB else "sgd"
+    layers, host = [], []
+    for i, (d_in, d_out, kind, weights) in enumerate(LAYERS):
+        L = H.allocate_layers([(d_in, d_out)], "bf16" if kind == "f32" else "fp32",
+                              second_order=[kind != "first"], factor_dtype="bf16" if kind == "bf16" else "fp32",
+                              optimizer=opt if weights else None)[0]
+        rng = np.random.default_rng(seed + i)
+        rec = dict(kind=kind)
+        if kind != "first":
+            Li, Ri = spd(seed * 3 + i, d_in), spd(seed * 5 + i, d_out)
+            if kind == "bf16":
+                Li, Ri = W.round_to_bf16(Li), W.round_to_bf16(Ri)
+            H.set_factors(L, Li, Ri)
+            rec.update(L=Li.astype(np.float64), R=Ri.astype(np.float64))
+        if weights:
+            W0 = (rng.standard_normal((d_in, d_out)) * 0.02).astype(np.float32)
+            L["W"].copy_(torch.from_numpy(W0))
+            rec.update(W=W0.astype(np.float64), m=np.zeros((d_in, d_out)), v=np.zeros((d_in, d_out)))
+        layers.append(L)
+        host.append(rec)
+    return layers, host
+
+
+def _inputs(L, rec, seed, t):
+    d_in, d_out = L["d_in"], L["d_out"]
+    rng = np.random.default_rng(seed * 1000 + t)
+    G = (rng.standard_normal((d_in, d_out)) * 1e-3).astype(np.float32)
+    if L["G"].dtype == torch.bfloat16:
+        G = W.round_to_bf16(G)
+    if rec["kind"] == "first":
+        H.set_inputs(L, G=G)
+        return None, None, G
+    a = (rng.standard_normal(d_in) / math.sqrt(d_in)).astype(np.float32)
+    g = (rng.standard_normal(d_out) / math.sqrt(d_out)).astype(np.float32)
+    H.set_inputs(L, a, g, G)
+    return a, g, G
+
+
+def _oracle_dw(rec, a, g, G, op, update):
+    if rec["kind"] == "first":
+        return np.asarray(G, np.float64)
+    if rec["kind"] == "bf16":
+        PL, PR, dW, _ = layer_step_half(rec["L"], rec["R"], a, g, G, op, update=update)
+    else:
+        PL, PR, dW, _ = O.layer_step(rec["L"], rec["R"], a, g, G, op, update=update)
+    rec["L"], rec["R"] = PL, PR
+    return dW
+
+
+# the C ABI takes the hyper-parameters as fp32: the oracle uses those values
+F = lambda x: float(np.float32(x))  # noqa: E731
+
+
+@pytest.mark.parametrize("kind", [OPT_SGD, OPT_LAMB])
+def test_fused_optimizer_steps(kind):
+    seed = 40 + kind
+    layers, host = _setup(kind, seed)
+    plan = H.make_plan(layers)
+    p = Params(eps=math.inf)
+    op = oparams(p)
+    for t in range(1, 6):
+        opt = OptParams(kind=kind, step=t, lr=0.01, momentum=0.9, beta1=0.9, beta2=0.999, eps=1e-6,
+                        weight_decay=0.01, store_dw=(t % 2 == 1))
+        update = t != 3                      # step 3 preconditions with the previous factors
+        dws = []
+        for L, rec in zip(layers, host):
+            a, g, G = _inputs(L, rec, seed, t)
+            dws.append(_oracle_dw(rec, a, g, G, op, update))
+        if update:
+            plan.step_opt(p, opt)
+        else:
+            plan.precondition_opt(p, opt)
+        torch.cuda.synchronize()
+        for i, (L, rec, dW) in enumerate(zip(layers, host, dws)):
+            weights = "W" in rec
+            if weights:
+                if kind == OPT_SGD:
+                    rec["W"], rec["m"] = sgd_step(rec["W"], rec["m"], dW, F(0.01), F(0.9), F(0.01))
+                else:
+                    rec["W"], rec["m"], rec["v"], _ = lamb_step(rec["W"], rec["m"], rec["v"], dW, t, F(0.01),
+                                                                F(0.9), F(0.999), F(1e-6), F(0.01))
+                eW = rel(L["W"].cpu().numpy(), rec["W"])
+                em = rel(L["opt_m"].cpu().numpy(), rec["m"])
+                ev = rel(L["opt_v"].cpu().numpy(), rec["v"]) if kind == OPT_LAMB else 0.0
+                print(kind, t, i, rec["kind"], "errors W m v", eW, em, ev)
+                assert max(eW, em, ev) <= TOL, (t, i, eW, em, ev)
+            if not weights or opt.store_dw:
+                eD = rel(H.get_dW(L), dW)
+                assert eD <= TOL, (t, i, eD)
+
+
+def test_fused_optimizer_needs_state():
+    L = H.allocate_layers([(64, 64)], "fp32", optimizer="sgd")[0]
+    plan = H.make_plan([L])
+    with pytest.raises(MkorError):
+        plan.step_opt(Params(), OptParams(kind=OPT_LAMB))   # LAMB without opt_v
+    plan.step_opt(Params(), OptParams(kind=OPT_SGD))         # SGD has what it needs
+    torch.cuda.synchronize()
