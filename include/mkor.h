@@ -93,7 +93,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 6
+#define MKOR_ABI_VERSION 7
 
 /* status codes */
 #define MKOR_OK                   0
@@ -116,10 +116,21 @@ extern "C" {
 #define MKOR_STAGE_MEANS      0   /* a, g = row means of A, Gout (layers with rows > 0) */
 #define MKOR_STAGE_SM_PASS    1   /* write pending term into S; u_raw = P x, norm and s partials */
 #define MKOR_STAGE_SM_FINALIZE 2  /* stabiliser decision, new pending rank-1 term */
-#define MKOR_STAGE_GEMM_XT    3   /* X^T = (Linv G)^T, ||G||^2 partials */
-#define MKOR_STAGE_GEMM_DW    4   /* dW_hat = X Rinv, ||dW_hat||^2 partials */
+#define MKOR_STAGE_GEMM_XT    3   /* first GEMM: X^T = (Linv G)^T (fp32 MFMA) or Y^T = Rinv G^T
+                                     (bf16 MFMA paths), ||G||^2 partials */
+#define MKOR_STAGE_GEMM_DW    4   /* second GEMM: dW_hat = X Rinv or Linv Y, ||dW_hat||^2 partials */
 #define MKOR_STAGE_RESCALE    5   /* rescale / first-order pass-through */
 #define MKOR_NUM_STAGES       6
+
+/* mkor_layer.gemm_path: how the preconditioning GEMMs of a layer with fp32
+ * factors multiply.  Both paths give fp32 results to fp32 accuracy. */
+#define MKOR_GEMM_AUTO     0   /* SPLIT where it applies, else FP32 */
+#define MKOR_GEMM_FP32     1   /* fp32 MFMA (v_mfma_f32_32x32x2_f32), any d_in, d_out */
+#define MKOR_GEMM_SPLIT    2   /* bf16 MFMA on an exact three-way bf16 split of each fp32
+                                  operand (x = h + m + l), the three smallest of the nine
+                                  partial products (below 2^-23 |x x'|) left out; needs
+                                  d_in and d_out multiples of 64; exact for operand
+                                  magnitudes in [2^-110, 3.38e38] */
 
 /* largest supported d_in / d_out, and token rows of A / Gout */
 #define MKOR_MAX_DIM       32768
@@ -177,8 +188,8 @@ typedef struct mkor_layer {
     int32_t      act_dtype;     /* MKOR_DTYPE_F32 or MKOR_DTYPE_BF16 (elements of A and Gout) */
     const void*  A;             /* rows x d_in activations, row-major (rows > 0) */
     const void*  Gout;          /* rows x d_out output gradients, row-major (rows > 0) */
-    /* Element type of Linv and Rinv.  MKOR_DTYPE_F32: fp32 factors, fp32 MFMA
-     * preconditioning (the default).  MKOR_DTYPE_BF16: half-precision factors
+    /* Element type of Linv and Rinv.  MKOR_DTYPE_F32: fp32 factors (the
+     * default), preconditioning as gemm_path selects.  MKOR_DTYPE_BF16: half-precision factors
      * (the paper's half-precision MKOR): the factors are stored in bf16, each
      * update is computed in fp32 from the stored values and rounded to bf16 (to
      * nearest, ties to even), and the preconditioning runs on bf16 MFMA with fp32
@@ -202,6 +213,10 @@ typedef struct mkor_layer {
     float*       W;
     float*       opt_m;
     float*       opt_v;
+    /* MKOR_GEMM_AUTO (0), MKOR_GEMM_FP32 or MKOR_GEMM_SPLIT for fp32 factors;
+     * must be MKOR_GEMM_AUTO for bf16 factors and first-order layers. */
+    int32_t      gemm_path;
+    int32_t      reserved0;     /* must be 0 */
 } mkor_layer;
 
 /* Per-layer observability record, written on the device when

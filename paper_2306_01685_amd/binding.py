@@ -35,7 +35,11 @@ DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
 MAX_RANK = 4
-ABI_VERSION = 6
+ABI_VERSION = 7
+GEMM_AUTO = 0
+GEMM_FP32 = 1
+GEMM_SPLIT = 2
+GEMM_PATHS = {"auto": GEMM_AUTO, "fp32": GEMM_FP32, "split": GEMM_SPLIT}
 OPT_SGD = 1
 OPT_LAMB = 2
 
@@ -55,7 +59,8 @@ class mkor_layer(ctypes.Structure):
                 ("rows", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
                 ("A", ctypes.c_void_p), ("Gout", ctypes.c_void_p),
                 ("factor_dtype", ctypes.c_int32), ("rank", ctypes.c_int32),
-                ("W", ctypes.c_void_p), ("opt_m", ctypes.c_void_p), ("opt_v", ctypes.c_void_p)]
+                ("W", ctypes.c_void_p), ("opt_m", ctypes.c_void_p), ("opt_v", ctypes.c_void_p),
+                ("gemm_path", ctypes.c_int32), ("reserved0", ctypes.c_int32)]
 
 
 class mkor_opt_params(ctypes.Structure):
@@ -207,7 +212,7 @@ def make_layer_array(descs):
                             d.get("stats") or None, d.get("rows", 0), d.get("act_dtype", 0),
                             d.get("A") or None, d.get("Gout") or None, d.get("factor_dtype", 0),
                             d.get("rank", 0), d.get("W") or None, d.get("opt_m") or None,
-                            d.get("opt_v") or None)
+                            d.get("opt_v") or None, d.get("gemm_path", 0), d.get("reserved0", 0))
     return arr
 
 
@@ -238,7 +243,9 @@ class MkorPlan:
     optional second_order (default True), optional stats
     (a uint8 device tensor of STATS_BYTES bytes), and optionally token rows A
     (rows x d_in) and Gout (rows x d_out), fp32 or bf16, from which each step
-    forms a and g (their means).  The plan owns its workspace
+    forms a and g (their means), and optionally gemm_path ("auto", "fp32" or
+    "split": how the preconditioning of fp32 factors multiplies; default
+    "auto").  The plan owns its workspace
     (a torch uint8 tensor) and keeps references to every tensor it was given.
 
     After step() / update_factors() the Linv / Rinv tensors lag the current
@@ -283,7 +290,8 @@ class MkorPlan:
                               stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
                               Gout=_ptr(L.get("Gout")), factor_dtype=fdt,
                               rank=int(L["a"].shape[0]) if so and L["a"].dim() == 2 else 0,
-                              W=_ptr(L.get("W")), opt_m=_ptr(L.get("opt_m")), opt_v=_ptr(L.get("opt_v"))))
+                              W=_ptr(L.get("W")), opt_m=_ptr(L.get("opt_m")), opt_v=_ptr(L.get("opt_v")),
+                              gemm_path=GEMM_PATHS[L.get("gemm_path", "auto")]))
         self._arr = make_layer_array(descs)
         n = len(descs)
         size = ctypes.c_size_t(0)

@@ -72,6 +72,15 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
         if (half && (L.d_in % 64 != 0 || L.d_out % 64 != 0))
             return fail(MKOR_UNSUPPORTED, "layer %d: bf16 factors need d_in and d_out multiples of 64 (%d, %d)",
                         i, L.d_in, L.d_out);
+        if (L.gemm_path != MKOR_GEMM_AUTO && L.gemm_path != MKOR_GEMM_FP32 && L.gemm_path != MKOR_GEMM_SPLIT)
+            return fail(MKOR_INVALID_ARG, "layer %d: gemm_path = %d unknown", i, L.gemm_path);
+        if (L.gemm_path != MKOR_GEMM_AUTO && (half || L.second_order != 1))
+            return fail(MKOR_INVALID_ARG, "layer %d: gemm_path applies to second-order layers with fp32 factors",
+                        i);
+        if (L.gemm_path == MKOR_GEMM_SPLIT && (L.d_in % 64 != 0 || L.d_out % 64 != 0))
+            return fail(MKOR_UNSUPPORTED, "layer %d: MKOR_GEMM_SPLIT needs d_in and d_out multiples of 64 (%d, %d)",
+                        i, L.d_in, L.d_out);
+        if (L.reserved0 != 0) return fail(MKOR_INVALID_ARG, "layer %d: reserved0 = %d must be 0", i, L.reserved0);
         if (L.rows < 0 || L.rows > MKOR_MAX_ROWS)
             return fail(MKOR_INVALID_ARG, "layer %d: rows = %d outside 0..%d", i, L.rows, MKOR_MAX_ROWS);
         const bool means = L.rows > 0;
@@ -137,6 +146,7 @@ struct Layout {
     size_t off_rsl = 0, off_rsb = 0, off_x = 0;
     size_t off_mmat = 0, off_mitem = 0, off_mchunk = 0, off_mpart = 0;
     size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
+    size_t off_s1l = 0, off_s1t = 0, off_s2l = 0, off_s2t = 0;   // fp32 factors on the bf16 split
     size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
     size_t off_gram = 0;                                         // rank-r Gram partials
     size_t off_lpart = 0, off_trust = 0;                         // LAMB block sums, per-layer ratios
@@ -144,6 +154,7 @@ struct Layout {
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
     int32_t nh1 = 0, nh2 = 0;
+    int32_t ns1 = 0, ns2 = 0;
     int32_t ncvt = 0, ncvtblk = 0;
     int32_t nsecond = 0;
     int32_t nranked = 0;      // second-order layers with rank > 1
@@ -157,17 +168,30 @@ int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
 bool is_half(const mkor_layer& L) { return L.second_order == 1 && L.factor_dtype == MKOR_DTYPE_BF16; }
 
-// Output tile grid and contraction length of a GEMM stage.  fp32 factors:
+// fp32 factors preconditioned on the three-way bf16 split (MKOR_GEMM_SPLIT, or
+// MKOR_GEMM_AUTO where the shape allows it)
+bool is_split(const mkor_layer& L) {
+    if (L.second_order != 1 || L.factor_dtype != MKOR_DTYPE_F32) return false;
+    if (L.gemm_path == MKOR_GEMM_SPLIT) return true;
+    return L.gemm_path == MKOR_GEMM_AUTO && L.d_in % 64 == 0 && L.d_out % 64 == 0;
+}
+
+// GEMM kernel family of a second-order layer
+enum { FAM_FP32 = 0, FAM_HALF = 1, FAM_SPLIT = 2 };
+int gemm_family(const mkor_layer& L) { return is_half(L) ? FAM_HALF : is_split(L) ? FAM_SPLIT : FAM_FP32; }
+
+// Output tile grid and contraction length of a GEMM stage.  fp32 MFMA:
 // stage 1 X^T = (Linv G)^T (K = d_in), stage 2 dW_hat = X Rinv (K = d_out),
-// both tiled over d_in x d_out.  bf16 factors: stage 1 Y^T = Rinv G^T
-// (d_out x d_in, K = d_out), stage 2 dW_hat = Linv Y (d_in x d_out, K = d_in).
+// both tiled over d_in x d_out.  bf16 MFMA (bf16 factors, or fp32 factors on
+// the split): stage 1 Y^T = Rinv G^T (d_out x d_in, K = d_out), stage 2
+// dW_hat = Linv Y (d_in x d_out, K = d_in).
 struct StageGeom {
     int32_t bm, bn;      // tile rows, columns
     int32_t rows, cols;  // output rows, columns
     int32_t K;
 };
 StageGeom stage_geom(const mkor_layer& L, int stage) {
-    if (is_half(L)) {
+    if (gemm_family(L) != FAM_FP32) {   // hgemm and sgemm tiles are both 256 x 256
         if (stage == 1) return StageGeom{HG_BI, HG_BJ, L.d_out, L.d_in, L.d_out};
         return StageGeom{HG_BI, HG_BJ, L.d_in, L.d_out, L.d_in};
     }
@@ -175,8 +199,8 @@ StageGeom stage_geom(const mkor_layer& L, int stage) {
     return StageGeom{sh.bm, sh.bn, L.d_in, L.d_out, stage == 1 ? L.d_in : L.d_out};
 }
 
-// Tile table of one GEMM stage over the second-order layers with fp32
-// factors (half = false) or bf16 factors (half = true).  Each layer's tile
+// Tile table of one GEMM stage over the second-order layers of one kernel
+// family (FAM_*).  Each layer's tile
 // grid is cut into super-tiles covering up to GEMM_SUPER x GEMM_SUPER
 // outputs; super-tiles are taken longest K first and each goes whole to the
 // XCD with the least work so far, so the tiles an XCD runs together share A
@@ -184,12 +208,12 @@ StageGeom stage_geom(const mkor_layer& L, int stage) {
 // b runs on XCD b % GEMM_XCDS, so position q * GEMM_XCDS + x of the table
 // holds the q-th tile of XCD x; shorter queues are padded with tiles of layer
 // -1.
-std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage, bool half) {
+std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int stage, int family) {
     struct Super { int32_t layer, tm0, tn0, nm, nn, K; };
     std::vector<Super> sup;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
-        if (!L.second_order || is_half(L) != half) continue;
+        if (!L.second_order || gemm_family(L) != family) continue;
         const StageGeom g = stage_geom(L, stage);
         const int32_t sm = std::max(1, GEMM_SUPER / g.bm), sn = std::max(1, GEMM_SUPER / g.bn);
         const int32_t tm = ceil_div(g.rows, g.bm), tn = ceil_div(g.cols, g.bn);
@@ -273,10 +297,13 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.nmeanpart = mpart;
     Lo.nfactors = 2 * Lo.nsecond;
     Lo.nrowblocks = (int32_t)rowblocks;
-    const size_t t1 = schedule_tiles(layers, n, 1, false).size(), t2 = schedule_tiles(layers, n, 2, false).size();
-    const size_t h1 = schedule_tiles(layers, n, 1, true).size(), h2 = schedule_tiles(layers, n, 2, true).size();
-    if (t1 > INT32_MAX || t2 > INT32_MAX || h1 > INT32_MAX || h2 > INT32_MAX)
+    const size_t t1 = schedule_tiles(layers, n, 1, FAM_FP32).size(), t2 = schedule_tiles(layers, n, 2, FAM_FP32).size();
+    const size_t h1 = schedule_tiles(layers, n, 1, FAM_HALF).size(), h2 = schedule_tiles(layers, n, 2, FAM_HALF).size();
+    const size_t s1 = schedule_tiles(layers, n, 1, FAM_SPLIT).size(), s2 = schedule_tiles(layers, n, 2, FAM_SPLIT).size();
+    if (t1 > INT32_MAX || t2 > INT32_MAX || h1 > INT32_MAX || h2 > INT32_MAX || s1 > INT32_MAX || s2 > INT32_MAX)
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
+    Lo.ns1 = (int32_t)s1;
+    Lo.ns2 = (int32_t)s2;
     Lo.ng1 = (int32_t)t1;
     Lo.ng2 = (int32_t)t2;
     Lo.nh1 = (int32_t)h1;
@@ -299,6 +326,10 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_h1t = take(sizeof(GemmTile) * Lo.nh1);
     Lo.off_h2l = take(sizeof(HgLayer) * n);
     Lo.off_h2t = take(sizeof(GemmTile) * Lo.nh2);
+    Lo.off_s1l = take(sizeof(HgLayer) * n);
+    Lo.off_s1t = take(sizeof(GemmTile) * Lo.ns1);
+    Lo.off_s2l = take(sizeof(HgLayer) * n);
+    Lo.off_s2t = take(sizeof(GemmTile) * Lo.ns2);
     Lo.off_rsl = take(sizeof(RescaleLayer) * n);
     Lo.off_rsb = take(sizeof(RescaleBlock) * Lo.nrsblocks);
     Lo.off_mmat = take(sizeof(MeanMat) * Lo.nmeanmat);
@@ -328,7 +359,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     }
     for (int32_t i = 0; i < n; ++i) {
         if (!layers[i].second_order) continue;
-        // X^T (fp32) of fp32-factor layers, Y^T (bf16) of bf16-factor layers
+        // X^T or Y^T (fp32) of fp32-factor layers, Y^T (bf16) of bf16-factor layers
         Lo.x_off[i] = take((is_half(layers[i]) ? 2 : 4) * (size_t)layers[i].d_in * layers[i].d_out);
     }
     Lo.gh_off.assign(n, 0);
@@ -434,6 +465,10 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     HgLayer* h2l = reinterpret_cast<HgLayer*>(host.data() + lo.off_h2l);
     GemmTile* h1t = reinterpret_cast<GemmTile*>(host.data() + lo.off_h1t);
     GemmTile* h2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_h2t);
+    HgLayer* s1l = reinterpret_cast<HgLayer*>(host.data() + lo.off_s1l);
+    HgLayer* s2l = reinterpret_cast<HgLayer*>(host.data() + lo.off_s2l);
+    GemmTile* s1t = reinterpret_cast<GemmTile*>(host.data() + lo.off_s1t);
+    GemmTile* s2t = reinterpret_cast<GemmTile*>(host.data() + lo.off_s2t);
     CvtItem* cvi = reinterpret_cast<CvtItem*>(host.data() + lo.off_cvti);
     CvtBlock* cvb = reinterpret_cast<CvtBlock*>(host.data() + lo.off_cvtb);
     int32_t nci = 0, ncb = 0;
@@ -542,6 +577,27 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             dp += ndp;
             continue;
         }
+        if (is_split(L)) {
+            // Y^T = R G^T (fp32 in the workspace), then dW_hat = L Y, both on
+            // the bf16 split of the fp32 operands
+            void* Yt = base + lo.x_off[i];
+            const StageGeom s1 = stage_geom(L, 1), s2 = stage_geom(L, 2);
+            HgLayer& A = s1l[i];
+            A.P = L.Rinv; A.Q = L.G; A.C = Yt;
+            A.pend = fR.pend; A.w = fR.w;
+            A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
+            A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
+            A.qf32 = bf16 ? 0 : 1;
+            HgLayer& B = s2l[i];
+            B.P = L.Linv; B.Q = Yt; B.C = L.dW;
+            B.pend = fL.pend; B.w = fL.w;
+            B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
+            B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
+            B.qf32 = 1;
+            gp += ngp;
+            dp += ndp;
+            continue;
+        }
         float* X = reinterpret_cast<float*>(base + lo.x_off[i]);
         const int32_t tn1 = ceil_div(L.d_out, GEMM_SHAPE[0].bn);
         const int32_t tn2 = ceil_div(L.d_out, GEMM_SHAPE[1].bn);
@@ -562,12 +618,15 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         gp += ngp;
         dp += ndp;
     }
-    const std::vector<GemmTile> t1 = schedule_tiles(layers, n, 1, false), t2 = schedule_tiles(layers, n, 2, false);
+    const std::vector<GemmTile> t1 = schedule_tiles(layers, n, 1, FAM_FP32), t2 = schedule_tiles(layers, n, 2, FAM_FP32);
     std::copy(t1.begin(), t1.end(), g1t);
     std::copy(t2.begin(), t2.end(), g2t);
-    const std::vector<GemmTile> u1 = schedule_tiles(layers, n, 1, true), u2 = schedule_tiles(layers, n, 2, true);
+    const std::vector<GemmTile> u1 = schedule_tiles(layers, n, 1, FAM_HALF), u2 = schedule_tiles(layers, n, 2, FAM_HALF);
     std::copy(u1.begin(), u1.end(), h1t);
     std::copy(u2.begin(), u2.end(), h2t);
+    const std::vector<GemmTile> v1 = schedule_tiles(layers, n, 1, FAM_SPLIT), v2 = schedule_tiles(layers, n, 2, FAM_SPLIT);
+    std::copy(v1.begin(), v1.end(), s1t);
+    std::copy(v2.begin(), v2.end(), s2t);
 
     mkor_plan* plan = new (std::nothrow) mkor_plan;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "out of host memory");
@@ -630,6 +689,9 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             e = launch_hgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_h1l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_h1t), lo.nh1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "bf16 gemm (R G^T) launch");
+            e = launch_sgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_s1l),
+                             reinterpret_cast<const GemmTile*>(ws + lo.off_s1t), lo.ns1, gpart, s);
+            if (e != hipSuccess) return hip_fail(e, "split gemm (R G^T) launch");
             return MKOR_OK;
         case MKOR_STAGE_GEMM_DW:
             e = launch_gemm_dw(reinterpret_cast<const GemmLayer*>(ws + lo.off_g2l),
@@ -638,6 +700,9 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             e = launch_hgemm(2, reinterpret_cast<const HgLayer*>(ws + lo.off_h2l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_h2t), lo.nh2, dpart, s);
             if (e != hipSuccess) return hip_fail(e, "bf16 gemm (L Y) launch");
+            e = launch_sgemm(2, reinterpret_cast<const HgLayer*>(ws + lo.off_s2l),
+                             reinterpret_cast<const GemmTile*>(ws + lo.off_s2t), lo.ns2, dpart, s);
+            if (e != hipSuccess) return hip_fail(e, "split gemm (L Y) launch");
             return MKOR_OK;
         case MKOR_STAGE_RESCALE:
             e = launch_rescale(reinterpret_cast<const RescaleLayer*>(ws + lo.off_rsl),

@@ -166,16 +166,19 @@ constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
 constexpr int HG_BK = MKOR_HG_BK;                       // k per stage
 
+// Layer descriptor of the bf16-MFMA preconditioning stages (C = P_eff Q^T):
+// bf16 factors (hgemm: P, Q bf16; C bf16 in stage 1) and fp32 factors on the
+// three-way bf16 split (sgemm: P fp32, Q fp32 or bf16, C fp32).
 struct HgLayer {
-    const void*    P;      // factor S (bf16, I x K)
-    const void*    Q;      // bf16 J x K
-    void*          C;      // I x J: bf16 (stage 1) or fp32 (stage 2)
+    const void*    P;      // factor S (I x K)
+    const void*    Q;      // J x K
+    void*          C;      // I x J
     const Pending* pend;   // pending term of the factor
     const float*   w;      // its w vector (K = I entries)
     int32_t        I, J, K;
     int32_t        part0;  // first partial slot of this layer
     int32_t        ntj;    // number of column tiles
-    int32_t        _pad;
+    int32_t        qf32;   // sgemm: Q is fp32 (else bf16)
 };
 
 // fp32 -> bf16 copy of fp32 gradients of bf16-factor layers (the stage-1 Q)
@@ -190,6 +193,8 @@ struct CvtBlock {
 };
 constexpr int CVT_ELEMS = 1 << 16;   // elements per workgroup of the conversion
 
+hipError_t launch_sgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
+                        float* partials, hipStream_t stream);
 hipError_t launch_hgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream);
 hipError_t launch_cvt_bf16(const CvtItem* items, const CvtBlock* blocks, int32_t nblocks, hipStream_t stream);

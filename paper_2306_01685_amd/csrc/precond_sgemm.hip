@@ -1,0 +1,338 @@
+// Preconditioning of fp32-factor layers on the bf16 matrix cores, to fp32
+// accuracy (Algorithm 1, precondition line; Eq. 2).  Every fp32 operand value
+// x is carried as the sum of three bf16 values,
+//
+//   x = h + m + l,   h = bf16(x),  m = bf16(x - h),  l = bf16(x - h - m)
+//
+// (round to nearest even).  Both differences are exact in fp32 (Sterbenz), and
+// x - h - m is a multiple of ulp(x) no larger than 2^-16 |x|, i.e. it has at
+// most 8 significant bits, so l holds it exactly: the split is exact for
+// 2^-110 <= |x| < 3.39e38 (below, l loses bits under bf16's subnormal floor;
+// above, h overflows).  A product of two split values is the sum of nine bf16
+// products; the three smallest (m l', l m', l l') are below 2^-23 |x x'| and are
+// left out, the same order as one fp32 rounding.  Each bf16 x bf16 product is
+// exact in the fp32 accumulator of v_mfma_f32_32x32x16_bf16, so the result
+// carries fp32 accumulation error, like the fp32 MFMA path, at six (or, for a
+// bf16 operand, which needs no split, three) bf16 MFMAs per product.  The
+// bf16 matrix cores run sixteen times the fp32 rate.
+//
+// Association and operands as in the bf16-factor path, C = P_eff Q^T with the
+// factor as P:
+//   stage 1:  Y^T = R G^T     P = S_R (d_out x d_out, fp32), Q = G (d_in x
+//                             d_out, bf16 or fp32), C = Y^T in fp32 (d_out x
+//                             d_in), plus ||G||^2 partials;
+//   stage 2:  dW_hat = L Y    P = S_L (d_in x d_in, fp32), Q = Y^T (fp32),
+//                             C = dW_hat in fp32, plus ||dW_hat||^2 partials.
+// The pending rank-1 term of the SM update enters in the epilogue,
+//   C[i][j] = c1 (S Q^T)[i][j] + c2 Q[j][i] + sgn w[i] (Q w)[j],
+// with (Q w) summed from the staged Q values in fp32.
+//
+// Tiles of 256 x 256 outputs, eight waves of 128 x 64 (4 x 2 MFMA blocks), two
+// per SIMD.  K runs in slabs of 16 (one MFMA deep): each thread loads 8
+// consecutive k of one P row and one Q row into registers one slab ahead,
+// splits them and writes the planes into a two-stage LDS ring (16-byte
+// writes).  A plane row is 32 bytes; its two 16-byte halves are swapped in
+// rows 8..15 of every 16 (slot h ^ ((r >> 3) & 1)), so the 16 rows of an MFMA
+// operand read, and the 8 rows x 2 halves of a staging write, fall on 16
+// distinct 16-byte bank groups.  d_in and d_out are multiples of 64 (checked
+// by the plan); rows past a tile edge are loaded clamped to the last row and
+// never stored.
+#include "gmem.h"
+#include "mkor_internal.h"
+
+namespace mkor {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) mk_u4 lds_u4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
+typedef __attribute__((address_space(3))) float lds_float;
+
+constexpr int BI = 256, BJ = 256, NT = 512;
+constexpr int WI = 2, WJ = 4;                 // wave grid
+constexpr int TI = BI / WI, TJ = BJ / WJ;     // 128 x 64 per wave
+constexpr int FI = TI / 32, FJ = TJ / 32;     // 4 x 2 MFMA blocks
+constexpr int NW = NT / 64;
+static_assert(NT == WI * WJ * 64 && TI == 128 && TJ == 64, "wave layout");
+constexpr int BK = 16;                        // slab depth = one MFMA
+constexpr int ROWB = BK * 2;                  // bytes per plane row
+constexpr int PLANE = BI * ROWB;              // 8 KB
+static_assert(BI == BJ && 2 * BI == NT, "one half row of P and of Q per thread");
+constexpr int STB = 6 * PLANE;                // 3 planes of P, up to 3 of Q
+constexpr int RING = 2 * STB;                 // 96 KB
+constexpr int SMEM = RING + 4 * (BJ + NW);
+
+__device__ __forceinline__ int slot(int r, int h) { return r * ROWB + ((h ^ ((r >> 3) & 1)) << 4); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// 8 values -> their three bf16 planes (packed pairs, element 2e in the low half)
+__device__ __forceinline__ void split8(const float (&v)[8], mk_u4& hi, mk_u4& mi, mk_u4& lo) {
+    unsigned h[4], m[4], l[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float x0 = v[2 * e], x1 = v[2 * e + 1];
+        h[e] = f2bf2(x0, x1);
+        const float r0 = __fsub_rn(x0, __uint_as_float(h[e] << 16));
+        const float r1 = __fsub_rn(x1, __uint_as_float(h[e] & 0xffff0000u));
+        m[e] = f2bf2(r0, r1);
+        const float s0 = __fsub_rn(r0, __uint_as_float(m[e] << 16));
+        const float s1 = __fsub_rn(r1, __uint_as_float(m[e] & 0xffff0000u));
+        l[e] = f2bf2(s0, s1);
+    }
+    hi = mk_u4{h[0], h[1], h[2], h[3]};
+    mi = mk_u4{m[0], m[1], m[2], m[3]};
+    lo = mk_u4{l[0], l[1], l[2], l[3]};
+}
+
+struct SgArgs {
+    const HgLayer* layers;
+    const GemmTile* tiles;
+    float* partials;
+};
+
+// QF: Q is fp32 (three planes) or bf16 (one plane, exact as it is)
+template <int STAGE, bool QF, bool PEND>
+__device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
+                           lds_char* smem) {
+    constexpr int NQ = QF ? 3 : 1;
+    const int i0 = tile.tm * BI, j0 = tile.tn * BJ;
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int wi = wave % WI, wj = wave / WI;
+    const int li = lane & 31, lk = lane >> 5;
+    const int I = L.I, J = L.J, K = L.K;
+    const bool want_gsq = STAGE == 1 && tile.tm == 0;   // ||G||^2: each Q row once
+    lds_float* rvec = (lds_float*)(smem + RING);
+    lds_float* red = rvec + BJ;
+
+    floatx16 acc[FI][FJ];
+#pragma unroll
+    for (int a = 0; a < FI; ++a)
+#pragma unroll
+        for (int b = 0; b < FJ; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    // staging: thread t owns row sr of the P tile and of the Q tile, k half sh
+    const int sr = t >> 1, sh = t & 1;
+    const float* Pp = static_cast<const float*>(L.P) + (size_t)min(i0 + sr, I - 1) * K + 8 * sh;
+    const size_t qoff = (size_t)min(j0 + sr, J - 1) * K + 8 * sh;
+    const float* Qf = static_cast<const float*>(L.Q) + qoff;
+    const unsigned short* Qh = static_cast<const unsigned short*>(L.Q) + qoff;
+    const float* Wp = L.w + 8 * sh;
+    const bool gsq_row = want_gsq && j0 + sr < J;
+
+    float4 pr0, pr1, qr0, qr1, wr0, wr1;
+    mk_u4 qh;
+    auto load = [&](int s) {
+        const int k0 = s * BK;
+        pr0 = gld4(Pp + k0);
+        pr1 = gld4(Pp + k0 + 4);
+        if constexpr (QF) {
+            qr0 = gld4(Qf + k0);
+            qr1 = gld4(Qf + k0 + 4);
+        } else {
+            const uint4 u = gld_u4(Qh + k0);
+            qh = mk_u4{u.x, u.y, u.z, u.w};
+        }
+        if constexpr (PEND) {
+            wr0 = gld4(Wp + k0);
+            wr1 = gld4(Wp + k0 + 4);
+        }
+    };
+    float rdot = 0.f, gsq = 0.f;
+    // split the registers of slab s into ring stage s & 1; (Q w) and ||G||^2
+    // partial sums in a fixed order
+    auto stage = [&](int s) {
+        lds_char* buf = smem + (s & 1) * STB;
+        const int o = slot(sr, sh);
+        {
+            const float v[8] = {pr0.x, pr0.y, pr0.z, pr0.w, pr1.x, pr1.y, pr1.z, pr1.w};
+            mk_u4 hi, mi, lo;
+            split8(v, hi, mi, lo);
+            *(lds_u4*)(buf + o) = hi;
+            *(lds_u4*)(buf + PLANE + o) = mi;
+            *(lds_u4*)(buf + 2 * PLANE + o) = lo;
+        }
+        float v[8];
+        if constexpr (QF) {
+            const float f[8] = {qr0.x, qr0.y, qr0.z, qr0.w, qr1.x, qr1.y, qr1.z, qr1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = f[e];
+            mk_u4 hi, mi, lo;
+            split8(v, hi, mi, lo);
+            *(lds_u4*)(buf + 3 * PLANE + o) = hi;
+            *(lds_u4*)(buf + 4 * PLANE + o) = mi;
+            *(lds_u4*)(buf + 5 * PLANE + o) = lo;
+        } else {
+            const unsigned u[4] = {qh.x, qh.y, qh.z, qh.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[2 * e] = __uint_as_float(u[e] << 16);
+                v[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+            }
+            *(lds_u4*)(buf + 3 * PLANE + o) = qh;
+        }
+        if constexpr (PEND) {
+            const float w[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) rdot = fmaf(v[e], w[e], rdot);
+        }
+        if (STAGE == 1 && gsq_row) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) gsq = fmaf(v[e], v[e], gsq);
+        }
+    };
+    auto compute = [&](int s) {
+        const lds_char* buf = smem + (s & 1) * STB;
+        bf16x8 a[3][FI], b[NQ][FJ];
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+#pragma unroll
+            for (int x = 0; x < FI; ++x) a[p][x] = *(const lds_bf8*)(buf + p * PLANE + slot(wi * TI + x * 32 + li, lk));
+#pragma unroll
+        for (int p = 0; p < NQ; ++p)
+#pragma unroll
+            for (int y = 0; y < FJ; ++y)
+                b[p][y] = *(const lds_bf8*)(buf + (3 + p) * PLANE + slot(wj * TJ + y * 32 + li, lk));
+        // plane pairs with p + q <= 2, the small terms first
+        constexpr int NTERM = QF ? 6 : 3;
+        constexpr int TP[6] = {2, 1, 0, 1, 0, 0}, TQ[6] = {0, 1, 2, 0, 1, 0};
+        constexpr int UP[3] = {2, 1, 0};
+#pragma unroll
+        for (int u = 0; u < NTERM; ++u) {
+            const int pp = QF ? TP[u] : UP[u], qq = QF ? TQ[u] : 0;
+#pragma unroll
+            for (int x = 0; x < FI; ++x)
+#pragma unroll
+                for (int y = 0; y < FJ; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pp][x], b[qq][y], acc[x][y], 0, 0, 0);
+        }
+    };
+
+    const int nst = K / BK;
+    load(0);
+    stage(0);
+    if (nst > 1) load(1);
+    __syncthreads();
+    for (int s = 0; s < nst; ++s) {
+        if (s + 1 < nst) stage(s + 1);   // the other ring stage: its last reader finished before the barrier
+        if (s + 2 < nst) load(s + 2);
+        compute(s);
+        __syncthreads();
+    }
+
+    if (PEND) {
+        const float v = rdot + __shfl_xor(rdot, 1, 64);
+        if (sh == 0) rvec[sr] = v;
+    }
+    __syncthreads();
+
+    const float c1 = PEND ? q.c1 : 1.f, c2 = PEND ? q.c2 : 0.f, sg = PEND ? q.sgn : 0.f;
+    float csq = 0.f;
+    float* Cp = static_cast<float*>(L.C);
+    // One MFMA row block (x) at a time: the loads its output groups need
+    // (rows past the edge clamped), then C[i][j] = c1 acc + c2 Q[j][i] +
+    // sgn w[i] (Q w)[j], stored as 128-byte row segments.
+#pragma unroll
+    for (int x = 0; x < FI; ++x) {
+        float qv[FJ][4][4];
+        float4 wv[4];
+        if (PEND) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
+                wv[g] = gld4(L.w + i);
+#pragma unroll
+                for (int y = 0; y < FJ; ++y) {
+                    const size_t e0 = (size_t)min(j0 + wj * TJ + y * 32 + li, J - 1) * K + i;
+                    if constexpr (QF) {
+                        const float4 f = gld4(static_cast<const float*>(L.Q) + e0);
+                        qv[y][g][0] = f.x; qv[y][g][1] = f.y; qv[y][g][2] = f.z; qv[y][g][3] = f.w;
+                    } else {
+                        const uint2 h = gld_u2(static_cast<const unsigned short*>(L.Q) + e0);
+                        qv[y][g][0] = __uint_as_float(h.x << 16);
+                        qv[y][g][1] = __uint_as_float(h.x & 0xffff0000u);
+                        qv[y][g][2] = __uint_as_float(h.y << 16);
+                        qv[y][g][3] = __uint_as_float(h.y & 0xffff0000u);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int y = 0; y < FJ; ++y) {
+            const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
+            const float rq = PEND ? rvec[jl] : 0.f;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int i = i0 + wi * TI + x * 32 + 8 * g + 4 * lk;
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = acc[x][y][4 * g + e];
+                if (PEND) {
+                    const float wa[4] = {wv[g].x, wv[g].y, wv[g].z, wv[g].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wa[e] * rq));
+                }
+                if (i < I && j < J) {   // I, J multiples of 64: 4 rows all in or all out
+                    float* dst = Cp + (size_t)i * J + j;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        gst(dst + (size_t)e * J, v[e]);
+                        if (STAGE == 2) csq = fmaf(v[e], v[e], csq);
+                    }
+                }
+            }
+        }
+    }
+
+    // partials: block-wide fixed-order sums
+    const float part = STAGE == 1 ? gsq : csq;
+    const float ws = wave_sum(part);
+    if (lane == 0) red[wave] = ws;
+    __syncthreads();
+    if (t == 0 && (STAGE == 2 || want_gsq)) {
+        float s = 0.f;
+        for (int w = 0; w < NW; ++w) s += red[w];
+        if (STAGE == 1) gst(partials + L.part0 + tile.tn, s);
+        else            gst(partials + L.part0 + tile.tm * L.ntj + tile.tn, s);
+    }
+}
+
+// 8 waves per CU (2 per SIMD): at most 256 VGPRs per lane.
+template <int STAGE>
+__global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
+    __shared__ __attribute__((aligned(16))) char smem_[SMEM];
+    lds_char* smem = (lds_char*)smem_;
+    const GemmTile tile = args.tiles[blockIdx.x];
+    if (tile.layer < 0) return;   // padding of the XCD interleave
+    const HgLayer L = args.layers[tile.layer];
+    const Pending q = *L.pend;
+    if (L.qf32) {
+        if (q.has) sgemm_tile<STAGE, true, true>(L, tile, q, args.partials, smem);
+        else       sgemm_tile<STAGE, true, false>(L, tile, q, args.partials, smem);
+    } else {
+        if (q.has) sgemm_tile<STAGE, false, true>(L, tile, q, args.partials, smem);
+        else       sgemm_tile<STAGE, false, false>(L, tile, q, args.partials, smem);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_sgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
+                        float* partials, hipStream_t stream) {
+    if (ntiles <= 0) return hipSuccess;
+    SgArgs a{layers, tiles, partials};
+    if (stage == 1) hipLaunchKernelGGL(sgemm_kernel<1>, dim3(ntiles), dim3(NT), 0, stream, a);
+    else            hipLaunchKernelGGL(sgemm_kernel<2>, dim3(ntiles), dim3(NT), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace mkor

@@ -12,14 +12,15 @@ from .binding import STATS_BYTES, MkorPlan, read_stats
 
 
 def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True,
-                    rows=0, act_dtype="fp32", factor_dtype="fp32", rank=1, optimizer=None):
+                    rows=0, act_dtype="fp32", factor_dtype="fp32", rank=1, optimizer=None, gemm_path=None):
     """One dict of device tensors per (d_in, d_out); factors start as I.  With
     rows > 0 each second-order layer also gets token-row buffers A (rows x d_in)
     and Gout (rows x d_out), from which the library forms a and g.
     factor_dtype "bf16" stores Linv and Rinv in bf16 (half-precision factors).
     rank > 1 gives a and g the shapes (rank, d_in) and (rank, d_out): r vectors
     per factor (rank-r update).  optimizer "sgd" or "lamb" adds the weights W
-    (zeros) and the optimizer state (opt_m, and opt_v for LAMB)."""
+    (zeros) and the optimizer state (opt_m, and opt_v for LAMB).  gemm_path
+    ("auto", "fp32", "split") is set on the second-order layers when given."""
     fdt = torch.bfloat16 if factor_dtype == "bf16" else torch.float32
     gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
     layers = []
@@ -35,6 +36,8 @@ def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None,
             vg = (rank, d_out) if rank > 1 else (d_out,)
             L["a"] = torch.zeros(va, dtype=torch.float32, device=device)
             L["g"] = torch.zeros(vg, dtype=torch.float32, device=device)
+        if so and gemm_path is not None:
+            L["gemm_path"] = gemm_path
         if stats:
             L["stats"] = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=device)
         if optimizer is not None:

@@ -60,11 +60,11 @@ class FreeRun:
     checked output, layers being independent).
     """
 
-    def __init__(self, w: W.Workload, params: Params, sample, explicit=False, bulk_seed=1234):
+    def __init__(self, w: W.Workload, params: Params, sample, explicit=False, bulk_seed=1234, gemm_path=None):
         self.w, self.p, self.op = w, params, oparams(params)
         self.sample = list(sample)
         self.explicit = explicit
-        self.layers = H.allocate_layers(w.shapes, w.grad_dtype)
+        self.layers = H.allocate_layers(w.shapes, w.grad_dtype, gemm_path=gemm_path)
         self.gen = torch.Generator(device="cuda")
         self.gen.manual_seed(bulk_seed)
         self.state = {}

@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 6
+    assert lib.mkor_abi_version() == 7
 
 
 def test_status_strings(lib):
@@ -46,7 +46,7 @@ def test_status_strings(lib):
 
 def test_struct_sizes():
     assert ctypes.sizeof(B.mkor_params) == 28
-    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8 + 8 + 3 * 8
+    assert ctypes.sizeof(B.mkor_layer) == 16 + 7 * 8 + 8 + 2 * 8 + 8 + 3 * 8 + 8
     assert ctypes.sizeof(B.mkor_opt_params) == 40
     assert M.STATS_BYTES == 48
 
@@ -282,6 +282,25 @@ def test_workspace_bf16_factors(lib):
     # mixed lists plan both GEMM kinds
     st, _ = ws_status([layer(fk, 1024, 4096, fdt=1), layer(fk, 4096, 1024), layer(fk, 37, 100)])
     assert st == M.MKOR_OK
+
+
+def test_gemm_path_validation(lib):
+    fk = Fake()
+    for path in (M.GEMM_AUTO, M.GEMM_FP32, M.GEMM_SPLIT):
+        assert ws_status([dict(layer(fk, 64, 128), gemm_path=path)])[0] == M.MKOR_OK
+    for path in (-1, 3):
+        assert ws_status([dict(layer(fk, 64, 128), gemm_path=path)])[0] == M.MKOR_INVALID_ARG
+    # the split needs multiples of 64; AUTO and FP32 take any shape
+    assert ws_status([dict(layer(fk, 64, 96), gemm_path=M.GEMM_SPLIT)])[0] == M.MKOR_UNSUPPORTED
+    assert ws_status([dict(layer(fk, 37, 100), gemm_path=M.GEMM_AUTO)])[0] == M.MKOR_OK
+    assert ws_status([dict(layer(fk, 37, 100), gemm_path=M.GEMM_FP32)])[0] == M.MKOR_OK
+    # only for second-order layers with fp32 factors
+    assert ws_status([dict(layer(fk, 64, 128, fdt=1), gemm_path=M.GEMM_SPLIT)])[0] == M.MKOR_INVALID_ARG
+    assert ws_status([dict(layer(fk, 64, 128, so=0), gemm_path=M.GEMM_FP32)])[0] == M.MKOR_INVALID_ARG
+    assert ws_status([dict(layer(fk, 64, 128), reserved0=1)])[0] == M.MKOR_INVALID_ARG
+    # both paths keep a d_in x d_out fp32 intermediate
+    sizes = [ws_status([dict(layer(fk, 1024, 4096, dt=1), gemm_path=p)])[1] for p in (M.GEMM_FP32, M.GEMM_SPLIT)]
+    assert min(sizes) >= 4 * 1024 * 4096 and abs(sizes[0] - sizes[1]) < (1 << 20)
 
 
 def test_rank_r_layers(lib):

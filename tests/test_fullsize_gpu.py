@@ -21,9 +21,9 @@ from tests.parity import TOL_FREE, TOL_STEP, FreeRun, rel
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 
-def _free_run(cfg, steps, eps, sample, check_steps):
+def _free_run(cfg, steps, eps, sample, check_steps, gemm_path=None):
     w = W.CONFIGS[cfg]
-    fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=eps), sample=sample)
+    fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=eps), sample=sample, gemm_path=gemm_path)
     worst = {}
     for t in range(steps):
         check = (t + 1) in check_steps
@@ -41,9 +41,12 @@ def test_bert_base_72_layers_50_steps():
     assert fired > 0
 
 
-def test_bert_large_144_layers_50_steps():
-    fr, worst, fired = _free_run(3, 50, 100.0, sample=[0, 4, 5, 138], check_steps={1, 50})
-    print("bert-large worst errors", worst, "stabiliser fired", fired)
+@pytest.mark.parametrize("gemm_path", ["auto", "fp32"])
+def test_bert_large_144_layers_50_steps(gemm_path):
+    """auto: the split path (every shape is a multiple of 64), as timed by the
+    bench; fp32: the fp32 MFMA path."""
+    fr, worst, fired = _free_run(3, 50, 100.0, sample=[0, 4, 5, 138], check_steps={1, 50}, gemm_path=gemm_path)
+    print("bert-large", gemm_path, "worst errors", worst, "stabiliser fired", fired)
     assert fired > 0
 
 
