@@ -7,8 +7,10 @@ A step is one full pass of the hot path (stabiliser + SM update of both
 factors of every layer, preconditioning, rescale) over the whole grouped layer
 list, launched through the C ABI (mkor_step).  The default workload is the
 BERT-Large-shaped set: 24 blocks x {4 x 1024x1024, 1024x4096, 4096x1024},
-fp32 factors, bf16 gradients.  Inputs are synthetic, seeded, and resident in
-HBM before the timed region starts.
+fp32 factors, bf16 gradients, preconditioned on the layers' default GEMM path
+(the exact three-way bf16 split on the bf16 matrix cores for these shapes;
+the fp32 MFMA path is measured beside it, "fp32_mfma_path").  Inputs are
+synthetic, seeded, and resident in HBM before the timed region starts.
 
 Prints one JSON line: layer-updates/s, per-kernel times measured with HIP
 events on the launch stream, the roofline of the dominant kernel, and the
@@ -102,6 +104,10 @@ def parse():
                     help="skip the measurement of the step with the fused LAMB optimizer")
     ap.add_argument("--no-half", action="store_true",
                     help="skip the extra measurement with bf16 factors")
+    ap.add_argument("--gemm-path", choices=["auto", "fp32", "split"], default="auto",
+                    help="preconditioning GEMMs of fp32 factors (auto: the split where the shape allows)")
+    ap.add_argument("--no-fp32-path", action="store_true",
+                    help="skip the extra measurement on the fp32 MFMA GEMM path")
     return ap.parse_args()
 
 
@@ -134,6 +140,13 @@ def workload_desc(w, factor_dtype="fp32"):
         counts[s] = counts.get(s, 0) + 1
     inner = ", ".join(f"{c}x {i}x{o}" if c > 1 else f"{i}x{o}" for (i, o), c in counts.items())
     return f"{w.name}: {w.blocks} x {{{inner}}}, {factor_dtype} factors, {w.grad_dtype} G"
+
+
+def split_eligible(w, gemm_path):
+    """True when every layer of the workload runs on the split GEMMs."""
+    if gemm_path == "fp32":
+        return False
+    return all(i % 64 == 0 and o % 64 == 0 for i, o in w.shapes)
 
 
 def fill_rows(layers, seed=2307):
@@ -208,17 +221,20 @@ def cpu_baseline(w, budget_s):
                        f"float64 steps in {el:.1f} s; host has {len(os.sched_getaffinity(0))} cpus")
 
 
-def measure(w, args, factor_dtype):
-    """Times mkor_step over the workload with the given factor storage type.
-    Returns (ms_per_step, kernels, roofline, schedule)."""
+def measure(w, args, factor_dtype, gemm_path="auto"):
+    """Times mkor_step over the workload with the given factor storage type
+    (and, for fp32 factors, GEMM path).  Returns (ms_per_step, kernels,
+    roofline, schedule)."""
     import torch
 
     from paper_2306_01685_amd import NUM_STAGES, STAGE_NAMES, Params, harness as H
 
     half = factor_dtype == "bf16"
     rank = args.rank if not half else 1
+    split = not half and split_eligible(w, gemm_path)
     layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=args.rows, act_dtype="bf16",
-                               factor_dtype=factor_dtype, rank=rank)
+                               factor_dtype=factor_dtype, rank=rank,
+                               gemm_path=None if half else gemm_path)
     if w.init != "identity":
         for i, L in enumerate(layers):
             H.set_factors(L, *initial_factors_stored(w, i, half))
@@ -260,14 +276,23 @@ def measure(w, args, factor_dtype):
                 acc[s] += ev[s].elapsed_time(ev[s + 1])
         ms = [a / args.steps for a in acc]
         sq = w.factor_elems
-        # stage 1 contracts over d_in (fp32: Linv G) or d_out (bf16: G Rinv)
-        f1 = sum(2 * i * o * (o if half else i) for i, o in w.shapes)
-        f2 = sum(2 * i * o * (i if half else o) for i, o in w.shapes)
+        # stage 1 contracts over d_in (fp32 MFMA: Linv G; split with a bf16 G
+        # and d_in > d_out: Linv G) or d_out (G Rinv)
+        def k1(i, o):
+            if half:
+                return o
+            if split:
+                return i if (w.grad_dtype == "bf16" and i > o) else o
+            return i
+        f1 = sum(2 * i * o * k1(i, o) for i, o in w.shapes)
+        f2 = sum(2 * i * o * (i + o - k1(i, o)) for i, o in w.shapes)
+        # bf16 MFMA products per fp32 product on the split: 3 (bf16 G) or 6
+        terms = ((3 if w.grad_dtype == "bf16" else 6), 6) if split else (1, 1)
         nel = sum(i * o for i, o in w.shapes)
         gb = 1e-9
         sd = sum(i + o for i, o in w.shapes)
         means_ms, ms = ms[0], ms[1:]   # stage 0: rank-1 means (no work when a and g are given)
-        g1, g2 = ("gemm_gr", "gemm_ly") if half else ("gemm_xt", "gemm_dw")
+        g1, g2 = ("gemm_gr", "gemm_ly") if half else ("sgemm_gr", "sgemm_ly") if split else ("gemm_xt", "gemm_dw")
         # steady state, rank 1: every factor has a pending term, so the pass reads
         # and writes each element once, and the finalize moves O(sum d) (partials,
         # u_raw and x read, w written).  Rank r > 1: the pass only reads (the
@@ -292,23 +317,34 @@ def measure(w, args, factor_dtype):
         kernels["sm_total"] = dict(ms=sm_ms, alg_bytes=sm_b, gbs=sm_b * gb / (sm_ms / 1e3),
                                    frac_hbm=sm_b * gb / (sm_ms / 1e3) / HBM_PEAK_GBS)
         pre_ms = ms[2] + ms[3]
+        # the split's peak in fp32 products: the bf16 MFMA peak over the bf16
+        # products each one takes
+        peaks = (BF16_MFMA_PEAK_TF / terms[0], BF16_MFMA_PEAK_TF / terms[1]) if split else (mfma_peak, mfma_peak)
+        mfma_ms = (f1 / peaks[0] + f2 / peaks[1]) / 1e12 * 1e3   # both GEMMs at their peaks
         kernels["gemm_total"] = dict(ms=pre_ms, flops=f1 + f2,
                                      tflops=(f1 + f2) / (pre_ms / 1e3) / 1e12,
-                                     frac_mfma=(f1 + f2) / (pre_ms / 1e3) / 1e12 / mfma_peak)
+                                     frac_mfma=mfma_ms / pre_ms)
         for k in ("sm_pass", "sm_finalize", "rescale"):
             kernels[k]["frac_hbm"] = kernels[k]["gbs"] / HBM_PEAK_GBS
-        for k in (g1, g2):
-            kernels[k]["frac_mfma"] = kernels[k]["tflops"] / mfma_peak
+        for k, pk, tm in ((g1, peaks[0], terms[0]), (g2, peaks[1], terms[1])):
+            kernels[k]["peak"] = pk
+            kernels[k]["frac_mfma"] = kernels[k]["tflops"] / pk
+            if split:
+                kernels[k]["bf16_mfma_terms"] = tm
+                kernels[k]["bf16_mfma_tflops"] = kernels[k]["tflops"] * tm
         names = ["sm_pass", "sm_finalize", g1, g2, "rescale"]
         dom = max(range(NUM_STAGES - 1), key=lambda s: ms[s])
         name = names[dom]
         k = kernels[name]
         traffic = profiled_traffic(name, args.config, half)
         if "flops" in k:
-            roof = dict(kernel=name, bound="mfma", achieved=k["tflops"], peak=mfma_peak,
-                        unit="TFLOP/s", frac=k["tflops"] / mfma_peak,
+            roof = dict(kernel=name, bound="mfma", achieved=k["tflops"], peak=k["peak"],
+                        unit="TFLOP/s", frac=k["frac_mfma"],
                         traffic=None if traffic is None else traffic["total_bytes"],
                         per_launch=f"{k['flops']:.4e} flop (sum of 2*M*N*K over the layers)")
+            if split:
+                roof["peak_basis"] = (f"fp32 products on the three-way bf16 split: the {BF16_MFMA_PEAK_TF:.0f} "
+                                      f"TFLOP/s bf16 MFMA peak / {k['bf16_mfma_terms']} bf16 products each")
         else:
             roof = dict(kernel=name, bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
                         frac=k["gbs"] / HBM_PEAK_GBS,
@@ -418,8 +454,16 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     w = W.CONFIGS[args.config]
-    ms_step, kernels, roof, schedule = measure(w, args, args.factor_dtype)
+    ms_step, kernels, roof, schedule = measure(w, args, args.factor_dtype, args.gemm_path)
     value = w.n_layers / (ms_step / 1e3)
+    fp32_path = None
+    if (args.factor_dtype == "fp32" and not args.no_fp32_path and args.rank == 1
+            and split_eligible(w, args.gemm_path)):
+        # the same workload on the fp32 MFMA GEMMs, reported beside
+        f_ms, f_k, f_roof, _ = measure(w, argparse.Namespace(**{**vars(args), "no_schedule": True}),
+                                       "fp32", "fp32")
+        fp32_path = dict(value=w.n_layers / (f_ms / 1e3), unit="layer-updates/s", ms_per_step=f_ms,
+                         gemm="fp32 MFMA (v_mfma_f32_32x32x2_f32)", roofline=f_roof, kernels=f_k)
     half = None
     if args.factor_dtype == "fp32" and not args.no_half and args.rank == 1:
         # the same workload with half-precision (bf16) factors, reported beside
@@ -441,10 +485,14 @@ def main():
         "config": {"workload": workload_desc(w, args.factor_dtype), "n_layers": w.n_layers,
                    "factor_elems": w.factor_elems, "precond_flops": w.precond_flops,
                    "gamma": w.gamma, "zeta": 0.5, "eps": args.eps, "grad_dtype": w.grad_dtype,
-                   "factor_dtype": args.factor_dtype, "token_rows": args.rows, "rank": args.rank},
+                   "factor_dtype": args.factor_dtype, "token_rows": args.rows, "rank": args.rank,
+                   "gemm": ("bf16 factors, bf16 MFMA" if args.factor_dtype == "bf16" else
+                            "fp32 operands as exact three-way bf16 splits on bf16 MFMA, fp32 accumulation"
+                            if split_eligible(w, args.gemm_path) else "fp32 MFMA")},
         "roofline": roof,
         "schedule_f10": schedule,
         "kernels": kernels,
+        "fp32_mfma_path": fp32_path,
         "half_factors": half,
         "fused_optimizer": opt,
         "device": torch.cuda.get_device_name(0),

@@ -148,6 +148,7 @@ struct Layout {
     size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
     size_t off_s1l = 0, off_s1t = 0, off_s2l = 0, off_s2t = 0;   // fp32 factors on the bf16 split
     size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
+    size_t off_tri = 0, off_trb = 0;                             // G^T of swapped split layers
     size_t off_gram = 0;                                         // rank-r Gram partials
     size_t off_lpart = 0, off_trust = 0;                         // LAMB block sums, per-layer ratios
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
@@ -156,12 +157,14 @@ struct Layout {
     int32_t nh1 = 0, nh2 = 0;
     int32_t ns1 = 0, ns2 = 0;
     int32_t ncvt = 0, ncvtblk = 0;
+    int32_t ntr = 0, ntrblk = 0;
     int32_t nsecond = 0;
     int32_t nranked = 0;      // second-order layers with rank > 1
     int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
     int64_t nmeanpart = 0;   // doubles
     std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
     std::vector<size_t> gh_off;                // per layer: bf16 copy of an fp32 G (bf16 factors)
+    std::vector<size_t> gt_off;                // per layer: G^T (bf16) of swapped split layers
 };
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
@@ -174,6 +177,14 @@ bool is_split(const mkor_layer& L) {
     if (L.second_order != 1 || L.factor_dtype != MKOR_DTYPE_F32) return false;
     if (L.gemm_path == MKOR_GEMM_SPLIT) return true;
     return L.gemm_path == MKOR_GEMM_AUTO && L.d_in % 64 == 0 && L.d_out % 64 == 0;
+}
+
+// split layers with a bf16 G and d_in > d_out take the other association,
+// dW_hat = (Linv G) Rinv, so that the longer contraction (over d_in) is the
+// one whose Q operand (G^T) is bf16 and needs three bf16 products per product
+// instead of six
+bool is_swapped(const mkor_layer& L) {
+    return is_split(L) && L.grad_dtype == MKOR_DTYPE_BF16 && L.d_in > L.d_out;
 }
 
 // GEMM kernel family of a second-order layer
@@ -191,6 +202,10 @@ struct StageGeom {
     int32_t K;
 };
 StageGeom stage_geom(const mkor_layer& L, int stage) {
+    if (is_swapped(L)) {   // stage 1 X = Linv G (K = d_in), stage 2 dW_hat^T = Rinv X^T (K = d_out)
+        if (stage == 1) return StageGeom{HG_BI, HG_BJ, L.d_in, L.d_out, L.d_in};
+        return StageGeom{HG_BI, HG_BJ, L.d_out, L.d_in, L.d_out};
+    }
     if (gemm_family(L) != FAM_FP32) {   // hgemm and sgemm tiles are both 256 x 256
         if (stage == 1) return StageGeom{HG_BI, HG_BJ, L.d_out, L.d_in, L.d_out};
         return StageGeom{HG_BI, HG_BJ, L.d_in, L.d_out, L.d_in};
@@ -259,13 +274,17 @@ int64_t dpart_count(const mkor_layer& L) {
 bool needs_cvt(const mkor_layer& L) { return is_half(L) && L.grad_dtype == MKOR_DTYPE_F32; }
 
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
-    int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0, ncvt = 0, ncvtblk = 0;
+    int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0, ncvt = 0, ncvtblk = 0, ntr = 0, ntrblk = 0;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         rsb += ceil_div((int64_t)L.d_in * L.d_out, RS_ELEMS);
         if (needs_cvt(L)) {
             ncvt += 1;
             ncvtblk += ceil_div((int64_t)L.d_in * L.d_out, CVT_ELEMS);
+        }
+        if (is_swapped(L)) {
+            ntr += 1;
+            ntrblk += (int64_t)(L.d_in / 64) * (L.d_out / 64);
         }
         if (!L.second_order) continue;
         Lo.nsecond++;
@@ -289,7 +308,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
             mpart += nch * nrb * MEAN_COLS;
         }
     }
-    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX || mitems > INT32_MAX || ncvtblk > INT32_MAX)
+    if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX || mitems > INT32_MAX || ncvtblk > INT32_MAX ||
+        ntrblk > INT32_MAX)
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
     Lo.nmeanmat = (int32_t)mmats;
     Lo.nmeanitem = (int32_t)mitems;
@@ -313,6 +333,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.nrsblocks = (int32_t)rsb;
     Lo.ncvt = (int32_t)ncvt;
     Lo.ncvtblk = (int32_t)ncvtblk;
+    Lo.ntr = (int32_t)ntr;
+    Lo.ntrblk = (int32_t)ntrblk;
 
     size_t o = 0;
     auto take = [&](size_t bytes) { o = align_up(o, 256); size_t r = o; o += bytes; return r; };
@@ -337,6 +359,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_mchunk = take(sizeof(MeanItem) * Lo.nmeanchunk);
     Lo.off_cvti = take(sizeof(CvtItem) * Lo.ncvt);
     Lo.off_cvtb = take(sizeof(CvtBlock) * Lo.ncvtblk);
+    Lo.off_tri = take(sizeof(TrItem) * Lo.ntr);
+    Lo.off_trb = take(sizeof(TrBlock) * Lo.ntrblk);
     // pending terms start out empty (has = 0): the upload initialises them
     Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
     Lo.table_bytes = align_up(o, 256);
@@ -365,6 +389,9 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.gh_off.assign(n, 0);
     for (int32_t i = 0; i < n; ++i)
         if (needs_cvt(layers[i])) Lo.gh_off[i] = take(2 * (size_t)layers[i].d_in * layers[i].d_out);
+    Lo.gt_off.assign(n, 0);
+    for (int32_t i = 0; i < n; ++i)
+        if (is_swapped(layers[i])) Lo.gt_off[i] = take(2 * (size_t)layers[i].d_in * layers[i].d_out);
     Lo.total = align_up(o, 256);
     (void)usum;
     return MKOR_OK;
@@ -472,6 +499,9 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     CvtItem* cvi = reinterpret_cast<CvtItem*>(host.data() + lo.off_cvti);
     CvtBlock* cvb = reinterpret_cast<CvtBlock*>(host.data() + lo.off_cvtb);
     int32_t nci = 0, ncb = 0;
+    TrItem* tri = reinterpret_cast<TrItem*>(host.data() + lo.off_tri);
+    TrBlock* trb = reinterpret_cast<TrBlock*>(host.data() + lo.off_trb);
+    int32_t nti = 0, ntb = 0;
     RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
     RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
     Pending* pend_h = reinterpret_cast<Pending*>(host.data() + lo.off_pend);
@@ -577,6 +607,32 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             dp += ndp;
             continue;
         }
+        if (is_swapped(L)) {
+            // X = L G with Q = G^T (bf16, transposed into the workspace), then
+            // dW_hat^T = R X^T, stored transposed into dW
+            void* X = base + lo.x_off[i];
+            unsigned short* Gt = reinterpret_cast<unsigned short*>(base + lo.gt_off[i]);
+            tri[nti] = TrItem{static_cast<const unsigned short*>(L.G), Gt, L.d_in, L.d_out};
+            for (int32_t r0 = 0; r0 < L.d_in; r0 += 64)
+                for (int32_t c0 = 0; c0 < L.d_out; c0 += 64) trb[ntb++] = TrBlock{nti, r0, c0, 0};
+            ++nti;
+            const StageGeom s1 = stage_geom(L, 1), s2 = stage_geom(L, 2);
+            HgLayer& A = s1l[i];
+            A.P = L.Linv; A.Q = Gt; A.C = X;
+            A.pend = fL.pend; A.w = fL.w;
+            A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
+            A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
+            A.qf32 = 0; A.ct = 0;
+            HgLayer& B = s2l[i];
+            B.P = L.Rinv; B.Q = X; B.C = L.dW;
+            B.pend = fR.pend; B.w = fR.w;
+            B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
+            B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
+            B.qf32 = 1; B.ct = 1;
+            gp += ngp;
+            dp += ndp;
+            continue;
+        }
         if (is_split(L)) {
             // Y^T = R G^T (fp32 in the workspace), then dW_hat = L Y, both on
             // the bf16 split of the fp32 operands
@@ -587,13 +643,13 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.pend = fR.pend; A.w = fR.w;
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
-            A.qf32 = bf16 ? 0 : 1;
+            A.qf32 = bf16 ? 0 : 1; A.ct = 0;
             HgLayer& B = s2l[i];
             B.P = L.Linv; B.Q = Yt; B.C = L.dW;
             B.pend = fL.pend; B.w = fL.w;
             B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
             B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
-            B.qf32 = 1;
+            B.qf32 = 1; B.ct = 0;
             gp += ngp;
             dp += ndp;
             continue;
@@ -689,6 +745,9 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             e = launch_hgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_h1l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_h1t), lo.nh1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "bf16 gemm (R G^T) launch");
+            e = launch_transpose_bf16(reinterpret_cast<const TrItem*>(ws + lo.off_tri),
+                                      reinterpret_cast<const TrBlock*>(ws + lo.off_trb), lo.ntrblk, s);
+            if (e != hipSuccess) return hip_fail(e, "bf16 gradient transpose launch");
             e = launch_sgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_s1l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_s1t), lo.ns1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "split gemm (R G^T) launch");

@@ -179,6 +179,18 @@ struct HgLayer {
     int32_t        part0;  // first partial slot of this layer
     int32_t        ntj;    // number of column tiles
     int32_t        qf32;   // sgemm: Q is fp32 (else bf16)
+    int32_t        ct;     // sgemm: C is stored transposed (C[i][j] at C + j I + i)
+    int32_t        _pad;
+};
+
+// bf16 transposes (G^T for the split GEMMs that contract over d_in)
+struct TrItem {
+    const unsigned short* src;   // rows x cols
+    unsigned short*       dst;   // cols x rows
+    int32_t               rows, cols;   // multiples of 64
+};
+struct TrBlock {
+    int32_t item, r0, c0, _pad;  // 64 x 64 tile at (r0, c0) of src
 };
 
 // fp32 -> bf16 copy of fp32 gradients of bf16-factor layers (the stage-1 Q)
@@ -195,6 +207,7 @@ constexpr int CVT_ELEMS = 1 << 16;   // elements per workgroup of the conversion
 
 hipError_t launch_sgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream);
+hipError_t launch_transpose_bf16(const TrItem* items, const TrBlock* blocks, int32_t nblocks, hipStream_t stream);
 hipError_t launch_hgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream);
 hipError_t launch_cvt_bf16(const CvtItem* items, const CvtBlock* blocks, int32_t nblocks, hipStream_t stream);

@@ -28,15 +28,16 @@
 // with (Q w) summed from the staged Q values in fp32.
 //
 // Tiles of 256 x 256 outputs, eight waves of 128 x 64 (4 x 2 MFMA blocks), two
-// per SIMD.  K runs in slabs of 16 (one MFMA deep): each thread loads 8
-// consecutive k of one P row and one Q row into registers one slab ahead,
-// splits them and writes the planes into a two-stage LDS ring (16-byte
-// writes).  A plane row is 32 bytes; its two 16-byte halves are swapped in
-// rows 8..15 of every 16 (slot h ^ ((r >> 3) & 1)), so the 16 rows of an MFMA
-// operand read, and the 8 rows x 2 halves of a staging write, fall on 16
-// distinct 16-byte bank groups.  d_in and d_out are multiples of 64 (checked
-// by the plan); rows past a tile edge are loaded clamped to the last row and
-// never stored.
+// per SIMD.  K runs in slabs (16 deep when Q is fp32, 32 when it is bf16, so
+// that both ring stages fit in LDS): each thread loads one half slab row of
+// P and of Q into registers one slab ahead, splits them and writes the planes
+// into a two-stage LDS ring with 16-byte writes.  A plane row is BK * 2 bytes
+// in 16-byte chunks; chunk c of row r sits in slot c ^ f(r), f(r) = (r >> 3) & 1
+// for 32-byte rows and (r >> 2) & 3 for 64-byte rows, so the 16 rows of an
+// MFMA operand read, and the rows of a staging write, fall on 16 distinct
+// 16-byte bank groups.  d_in and d_out are multiples of 64 (checked by the
+// plan); rows past a tile edge are loaded clamped to the last row and never
+// stored.
 #include "gmem.h"
 #include "mkor_internal.h"
 
@@ -51,20 +52,41 @@ typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
 typedef __attribute__((address_space(3))) float lds_float;
 
 constexpr int BI = 256, BJ = 256, NT = 512;
-constexpr int WI = 2, WJ = 4;                 // wave grid
-constexpr int TI = BI / WI, TJ = BJ / WJ;     // 128 x 64 per wave
-constexpr int FI = TI / 32, FJ = TJ / 32;     // 4 x 2 MFMA blocks
 constexpr int NW = NT / 64;
-static_assert(NT == WI * WJ * 64 && TI == 128 && TJ == 64, "wave layout");
-constexpr int BK = 16;                        // slab depth = one MFMA
-constexpr int ROWB = BK * 2;                  // bytes per plane row
-constexpr int PLANE = BI * ROWB;              // 8 KB
 static_assert(BI == BJ && 2 * BI == NT, "one half row of P and of Q per thread");
-constexpr int STB = 6 * PLANE;                // 3 planes of P, up to 3 of Q
-constexpr int RING = 2 * STB;                 // 96 KB
+
+// wave layout and ring geometry for Q in fp32 (QF) or bf16.  With three P
+// planes and one Q plane a wave reads fewer operand bytes per MFMA when it
+// covers fewer P rows and more Q rows (64 x 128 instead of 128 x 64).
+#ifndef MKOR_SG_PFD
+#define MKOR_SG_PFD 1
+#endif
+#ifndef MKOR_SG_WI1
+#define MKOR_SG_WI1 4
+#endif
+#ifndef MKOR_SG_BK1
+#define MKOR_SG_BK1 16
+#endif
+template <bool QF> struct Geo {
+    static constexpr int WI = QF ? 2 : MKOR_SG_WI1, WJ = NW / WI;   // wave grid
+    static constexpr int TI = BI / WI, TJ = BJ / WJ;      // outputs per wave
+    static constexpr int FI = TI / 32, FJ = TJ / 32;      // MFMA blocks per wave
+    static constexpr int NQ = QF ? 3 : 1;          // Q planes
+    static constexpr int BK = QF ? 16 : MKOR_SG_BK1;   // slab depth
+    static constexpr int KS = BK / 16;             // MFMA k-steps per slab
+    static constexpr int HK = BK / 2;              // k per thread and slab
+    static constexpr int ROWB = BK * 2;            // bytes per plane row
+    static constexpr int PLANE = BI * ROWB;
+    static constexpr int STB = (3 + NQ) * PLANE;   // one ring stage
+    static constexpr int RING = 2 * STB;
+};
+constexpr int RING = Geo<true>::RING > Geo<false>::RING ? Geo<true>::RING : Geo<false>::RING;   // 128 KB
 constexpr int SMEM = RING + 4 * (BJ + NW);
 
-__device__ __forceinline__ int slot(int r, int h) { return r * ROWB + ((h ^ ((r >> 3) & 1)) << 4); }
+template <int ROWB>
+__device__ __forceinline__ int slot(int r, int c) {
+    return ROWB == 32 ? r * 32 + ((c ^ ((r >> 3) & 1)) << 4) : r * 64 + ((c ^ ((r >> 2) & 3)) << 4);
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -73,7 +95,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // 8 values -> their three bf16 planes (packed pairs, element 2e in the low half)
-__device__ __forceinline__ void split8(const float (&v)[8], mk_u4& hi, mk_u4& mi, mk_u4& lo) {
+__device__ __forceinline__ void split8(const float* v, mk_u4& hi, mk_u4& mi, mk_u4& lo) {
     unsigned h[4], m[4], l[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -101,7 +123,11 @@ struct SgArgs {
 template <int STAGE, bool QF, bool PEND>
 __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
                            lds_char* smem) {
-    constexpr int NQ = QF ? 3 : 1;
+    using G = Geo<QF>;
+    constexpr int WI = G::WI, TI = G::TI, TJ = G::TJ, FI = G::FI, FJ = G::FJ;
+    static_assert(NT == WI * G::WJ * 64, "wave layout");
+    constexpr int NQ = G::NQ, BK = G::BK, KS = G::KS, HK = G::HK, ROWB = G::ROWB, PLANE = G::PLANE;
+    constexpr int NC = HK / 8;                     // 16-byte chunks per thread and plane
     const int i0 = tile.tm * BI, j0 = tile.tn * BJ;
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -122,88 +148,115 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 
     // staging: thread t owns row sr of the P tile and of the Q tile, k half sh
     const int sr = t >> 1, sh = t & 1;
-    const float* Pp = static_cast<const float*>(L.P) + (size_t)min(i0 + sr, I - 1) * K + 8 * sh;
-    const size_t qoff = (size_t)min(j0 + sr, J - 1) * K + 8 * sh;
+    const float* Pp = static_cast<const float*>(L.P) + (size_t)min(i0 + sr, I - 1) * K + HK * sh;
+    const size_t qoff = (size_t)min(j0 + sr, J - 1) * K + HK * sh;
     const float* Qf = static_cast<const float*>(L.Q) + qoff;
     const unsigned short* Qh = static_cast<const unsigned short*>(L.Q) + qoff;
-    const float* Wp = L.w + 8 * sh;
+    const float* Wp = L.w + HK * sh;
     const bool gsq_row = want_gsq && j0 + sr < J;
 
-    float4 pr0, pr1, qr0, qr1, wr0, wr1;
-    mk_u4 qh;
-    auto load = [&](int s) {
-        const int k0 = s * BK;
-        pr0 = gld4(Pp + k0);
-        pr1 = gld4(Pp + k0 + 4);
-        if constexpr (QF) {
-            qr0 = gld4(Qf + k0);
-            qr1 = gld4(Qf + k0 + 4);
-        } else {
-            const uint4 u = gld_u4(Qh + k0);
-            qh = mk_u4{u.x, u.y, u.z, u.w};
-        }
+    // one slab's staged operands (P fp32, Q fp32 or packed bf16), and the w
+    // slice of a slab (cached: every thread of a tile reads the same one)
+    struct Regs {
+        float p[HK], q[QF ? HK : 1];
+        mk_u4 qh[QF ? 1 : NC];
+    };
+    float wr[PEND ? HK : 1];
+    auto load_w = [&](int s) {
         if constexpr (PEND) {
-            wr0 = gld4(Wp + k0);
-            wr1 = gld4(Wp + k0 + 4);
+            const int k0 = s * BK;
+#pragma unroll
+            for (int c = 0; c < HK / 4; ++c) {
+                const float4 v = gld4(Wp + k0 + 4 * c);
+                wr[4 * c] = v.x; wr[4 * c + 1] = v.y; wr[4 * c + 2] = v.z; wr[4 * c + 3] = v.w;
+            }
+        }
+    };
+    auto load = [&](Regs& R, int s) {
+        const int k0 = s * BK;
+#pragma unroll
+        for (int c = 0; c < HK / 4; ++c) {
+            const float4 v = gld4(Pp + k0 + 4 * c);
+            R.p[4 * c] = v.x; R.p[4 * c + 1] = v.y; R.p[4 * c + 2] = v.z; R.p[4 * c + 3] = v.w;
+        }
+        if constexpr (QF) {
+#pragma unroll
+            for (int c = 0; c < HK / 4; ++c) {
+                const float4 v = gld4(Qf + k0 + 4 * c);
+                R.q[4 * c] = v.x; R.q[4 * c + 1] = v.y; R.q[4 * c + 2] = v.z; R.q[4 * c + 3] = v.w;
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const uint4 u = gld_u4(Qh + k0 + 8 * c);
+                R.qh[c] = mk_u4{u.x, u.y, u.z, u.w};
+            }
         }
     };
     float rdot = 0.f, gsq = 0.f;
-    // split the registers of slab s into ring stage s & 1; (Q w) and ||G||^2
+    // split the registers of a slab into ring stage st; (Q w) and ||G||^2
     // partial sums in a fixed order
-    auto stage = [&](int s) {
-        lds_char* buf = smem + (s & 1) * STB;
-        const int o = slot(sr, sh);
-        {
-            const float v[8] = {pr0.x, pr0.y, pr0.z, pr0.w, pr1.x, pr1.y, pr1.z, pr1.w};
+    auto stage = [&](const Regs& R, int st) {
+        lds_char* buf = smem + st * G::STB;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int o = slot<ROWB>(sr, NC * sh + c);
             mk_u4 hi, mi, lo;
-            split8(v, hi, mi, lo);
+            split8(R.p + 8 * c, hi, mi, lo);
             *(lds_u4*)(buf + o) = hi;
             *(lds_u4*)(buf + PLANE + o) = mi;
             *(lds_u4*)(buf + 2 * PLANE + o) = lo;
         }
-        float v[8];
+        float v[HK];
         if constexpr (QF) {
-            const float f[8] = {qr0.x, qr0.y, qr0.z, qr0.w, qr1.x, qr1.y, qr1.z, qr1.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = f[e];
-            mk_u4 hi, mi, lo;
-            split8(v, hi, mi, lo);
-            *(lds_u4*)(buf + 3 * PLANE + o) = hi;
-            *(lds_u4*)(buf + 4 * PLANE + o) = mi;
-            *(lds_u4*)(buf + 5 * PLANE + o) = lo;
-        } else {
-            const unsigned u[4] = {qh.x, qh.y, qh.z, qh.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                v[2 * e] = __uint_as_float(u[e] << 16);
-                v[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+            for (int c = 0; c < NC; ++c) {
+                const int o = slot<ROWB>(sr, NC * sh + c);
+                mk_u4 hi, mi, lo;
+                split8(R.q + 8 * c, hi, mi, lo);
+                *(lds_u4*)(buf + 3 * PLANE + o) = hi;
+                *(lds_u4*)(buf + 4 * PLANE + o) = mi;
+                *(lds_u4*)(buf + 5 * PLANE + o) = lo;
             }
-            *(lds_u4*)(buf + 3 * PLANE + o) = qh;
+#pragma unroll
+            for (int e = 0; e < HK; ++e) v[e] = R.q[e];
+        } else {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                *(lds_u4*)(buf + 3 * PLANE + slot<ROWB>(sr, NC * sh + c)) = R.qh[c];
+                const unsigned u[4] = {R.qh[c].x, R.qh[c].y, R.qh[c].z, R.qh[c].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    v[8 * c + 2 * e] = __uint_as_float(u[e] << 16);
+                    v[8 * c + 2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+                }
+            }
         }
         if constexpr (PEND) {
-            const float w[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) rdot = fmaf(v[e], w[e], rdot);
+            for (int e = 0; e < HK; ++e) rdot = fmaf(v[e], wr[e], rdot);
         }
         if (STAGE == 1 && gsq_row) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) gsq = fmaf(v[e], v[e], gsq);
+            for (int e = 0; e < HK; ++e) gsq = fmaf(v[e], v[e], gsq);
         }
     };
-    auto compute = [&](int s) {
-        const lds_char* buf = smem + (s & 1) * STB;
+    constexpr int NTERM = QF ? 6 : 3;
+    // MFMA k-step ks of ring stage st: plane pairs with p + q <= 2, the small
+    // terms first
+    auto compute = [&](int st, int ks) {
+        const lds_char* buf = smem + st * G::STB;
+        const int c = 2 * ks + lk;
         bf16x8 a[3][FI], b[NQ][FJ];
 #pragma unroll
         for (int p = 0; p < 3; ++p)
 #pragma unroll
-            for (int x = 0; x < FI; ++x) a[p][x] = *(const lds_bf8*)(buf + p * PLANE + slot(wi * TI + x * 32 + li, lk));
+            for (int x = 0; x < FI; ++x) a[p][x] = *(const lds_bf8*)(buf + p * PLANE + slot<ROWB>(wi * TI + x * 32 + li, c));
 #pragma unroll
         for (int p = 0; p < NQ; ++p)
 #pragma unroll
             for (int y = 0; y < FJ; ++y)
-                b[p][y] = *(const lds_bf8*)(buf + (3 + p) * PLANE + slot(wj * TJ + y * 32 + li, lk));
-        // plane pairs with p + q <= 2, the small terms first
-        constexpr int NTERM = QF ? 6 : 3;
+                b[p][y] = *(const lds_bf8*)(buf + (3 + p) * PLANE + slot<ROWB>(wj * TJ + y * 32 + li, c));
         constexpr int TP[6] = {2, 1, 0, 1, 0, 0}, TQ[6] = {0, 1, 2, 0, 1, 0};
         constexpr int UP[3] = {2, 1, 0};
 #pragma unroll
@@ -217,17 +270,54 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         }
     };
 
-    const int nst = K / BK;
-    load(0);
-    stage(0);
-    if (nst > 1) load(1);
+    const int nst = K / BK;   // even: K is a multiple of 64
+#if MKOR_SG_PFD == 2
+    // Two register sets: the loads of slab s + 3 go out in iteration s, into
+    // the set that slab s + 1 has just been staged from, and have two slabs
+    // of MFMAs to land.
+    Regs R0, R1;
+    load(R0, 0);
+    load_w(0);
+    stage(R0, 0);
+    load(R1, 1);
+    load_w(1);
+    if (nst > 2) load(R0, 2);
+    __syncthreads();
+    auto iter = [&](int s, Regs& Rn) {   // Rn: the set holding slab s + 1
+        if (s + 1 < nst) stage(Rn, (s + 1) & 1);
+        if (s + 3 < nst) load(Rn, s + 3);
+        if (s + 2 < nst) load_w(s + 2);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) compute(s & 1, ks);
+        __syncthreads();
+    };
+    for (int s = 0; s < nst; s += 2) {
+        iter(s, R1);
+        iter(s + 1, R0);
+    }
+#else
+    Regs R;
+    load(R, 0);
+    load_w(0);
+    stage(R, 0);
+    if (nst > 1) {
+        load(R, 1);
+        load_w(1);
+    }
     __syncthreads();
     for (int s = 0; s < nst; ++s) {
-        if (s + 1 < nst) stage(s + 1);   // the other ring stage: its last reader finished before the barrier
-        if (s + 2 < nst) load(s + 2);
-        compute(s);
+        // slab s + 1 into the other ring stage (its last reader finished
+        // before the barrier), then the loads of slab s + 2
+        if (s + 1 < nst) stage(R, (s + 1) & 1);
+        if (s + 2 < nst) {
+            load(R, s + 2);
+            load_w(s + 2);
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) compute(s & 1, ks);
         __syncthreads();
     }
+#endif
 
     if (PEND) {
         const float v = rdot + __shfl_xor(rdot, 1, 64);
@@ -282,22 +372,30 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                     for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wa[e] * rq));
                 }
                 if (i < I && j < J) {   // I, J multiples of 64: 4 rows all in or all out
-                    float* dst = Cp + (size_t)i * J + j;
+                    if (L.ct) {
+                        // transposed: the 4 rows i .. i + 3 are contiguous in row j of C^T
+                        gst4(Cp + (size_t)j * I + i, make_float4(v[0], v[1], v[2], v[3]));
+                    } else {
+                        float* dst = Cp + (size_t)i * J + j;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        gst(dst + (size_t)e * J, v[e]);
-                        if (STAGE == 2) csq = fmaf(v[e], v[e], csq);
+                        for (int e = 0; e < 4; ++e) gst(dst + (size_t)e * J, v[e]);
+                    }
+                    if (STAGE == 2) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) csq = fmaf(v[e], v[e], csq);
                     }
                 }
             }
         }
     }
 
-    // partials: block-wide fixed-order sums
+    // partials: block-wide fixed-order sums.  The barrier waits for the LDS
+    // writes only (a bare s_barrier): the compiler's barrier would also wait
+    // until every output store of the tile has completed.
     const float part = STAGE == 1 ? gsq : csq;
     const float ws = wave_sum(part);
     if (lane == 0) red[wave] = ws;
-    __syncthreads();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (t == 0 && (STAGE == 2 || want_gsq)) {
         float s = 0.f;
         for (int w = 0; w < NW; ++w) s += red[w];
@@ -324,7 +422,40 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
     }
 }
 
+// G^T of bf16 gradients, 64 x 64 tiles through LDS (rows of 64 + 2 elements,
+// so the column reads of the transposed pass spread over the banks).
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const TrItem* __restrict__ items,
+                                                            const TrBlock* __restrict__ blocks) {
+    __shared__ unsigned short tile[64][66];
+    const TrBlock b = blocks[blockIdx.x];
+    const TrItem it = items[b.item];
+    const int t = threadIdx.x, r = t >> 2, c = 16 * (t & 3);
+    // 16 consecutive elements of source row r0 + r, as two 16-byte loads
+    const unsigned short* s = it.src + (size_t)(b.r0 + r) * it.cols + b.c0 + c;
+    const uint4 u0 = gld_u4(s), u1 = gld_u4(s + 8);
+    const unsigned w[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        tile[r][c + 2 * e] = (unsigned short)(w[e] & 0xffffu);
+        tile[r][c + 2 * e + 1] = (unsigned short)(w[e] >> 16);
+    }
+    __syncthreads();
+    // destination row c0 + r holds source column c0 + r: elements r0 + c .. + 15
+    unsigned o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (unsigned)tile[c + 2 * e][r] | ((unsigned)tile[c + 2 * e + 1][r] << 16);
+    unsigned short* d = it.dst + (size_t)(b.c0 + r) * it.rows + b.r0 + c;
+    gst_u4(d, make_uint4(o[0], o[1], o[2], o[3]));
+    gst_u4(d + 8, make_uint4(o[4], o[5], o[6], o[7]));
+}
+
 }  // namespace
+
+hipError_t launch_transpose_bf16(const TrItem* items, const TrBlock* blocks, int32_t nblocks, hipStream_t stream) {
+    if (nblocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(transpose_bf16_kernel, dim3(nblocks), dim3(256), 0, stream, items, blocks);
+    return hipGetLastError();
+}
 
 hipError_t launch_sgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream) {
