@@ -58,21 +58,12 @@ static_assert(BI == BJ && 2 * BI == NT, "one half row of P and of Q per thread")
 // wave layout and ring geometry for Q in fp32 (QF) or bf16.  With three P
 // planes and one Q plane a wave reads fewer operand bytes per MFMA when it
 // covers fewer P rows and more Q rows (64 x 128 instead of 128 x 64).
-#ifndef MKOR_SG_PFD
-#define MKOR_SG_PFD 1
-#endif
-#ifndef MKOR_SG_WI1
-#define MKOR_SG_WI1 4
-#endif
-#ifndef MKOR_SG_BK1
-#define MKOR_SG_BK1 16
-#endif
 template <bool QF> struct Geo {
-    static constexpr int WI = QF ? 2 : MKOR_SG_WI1, WJ = NW / WI;   // wave grid
+    static constexpr int WI = QF ? 2 : 4, WJ = NW / WI;   // wave grid
     static constexpr int TI = BI / WI, TJ = BJ / WJ;      // outputs per wave
     static constexpr int FI = TI / 32, FJ = TJ / 32;      // MFMA blocks per wave
     static constexpr int NQ = QF ? 3 : 1;          // Q planes
-    static constexpr int BK = QF ? 16 : MKOR_SG_BK1;   // slab depth
+    static constexpr int BK = QF ? 16 : 32;        // slab depth
     static constexpr int KS = BK / 16;             // MFMA k-steps per slab
     static constexpr int HK = BK / 2;              // k per thread and slab
     static constexpr int ROWB = BK * 2;            // bytes per plane row
@@ -172,6 +163,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             }
         }
     };
+    auto wsel = [&](int e) { return wr[e]; };
     auto load = [&](Regs& R, int s) {
         const int k0 = s * BK;
 #pragma unroll
@@ -196,7 +188,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     float rdot = 0.f, gsq = 0.f;
     // split the registers of a slab into ring stage st; (Q w) and ||G||^2
     // partial sums in a fixed order
-    auto stage = [&](const Regs& R, int st) {
+    auto stage = [&](const Regs& R, int st, bool count) {
         lds_char* buf = smem + st * G::STB;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -233,12 +225,16 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             }
         }
         if constexpr (PEND) {
+            float r = rdot;
 #pragma unroll
-            for (int e = 0; e < HK; ++e) rdot = fmaf(v[e], wr[e], rdot);
+            for (int e = 0; e < HK; ++e) r = fmaf(v[e], wsel(e), r);
+            rdot = count ? r : rdot;
         }
-        if (STAGE == 1 && gsq_row) {
+        if constexpr (STAGE == 1) {
+            float r = gsq;
 #pragma unroll
-            for (int e = 0; e < HK; ++e) gsq = fmaf(v[e], v[e], gsq);
+            for (int e = 0; e < HK; ++e) r = fmaf(v[e], v[e], r);
+            gsq = (count && gsq_row) ? r : gsq;
         }
     };
     constexpr int NTERM = QF ? 6 : 3;
@@ -271,53 +267,39 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     };
 
     const int nst = K / BK;   // even: K is a multiple of 64
-#if MKOR_SG_PFD == 2
-    // Two register sets: the loads of slab s + 3 go out in iteration s, into
-    // the set that slab s + 1 has just been staged from, and have two slabs
-    // of MFMAs to land.
-    Regs R0, R1;
-    load(R0, 0);
-    load_w(0);
-    stage(R0, 0);
-    load(R1, 1);
-    load_w(1);
-    if (nst > 2) load(R0, 2);
-    __syncthreads();
-    auto iter = [&](int s, Regs& Rn) {   // Rn: the set holding slab s + 1
-        if (s + 1 < nst) stage(Rn, (s + 1) & 1);
-        if (s + 3 < nst) load(Rn, s + 3);
-        if (s + 2 < nst) load_w(s + 2);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) compute(s & 1, ks);
-        __syncthreads();
-    };
-    for (int s = 0; s < nst; s += 2) {
-        iter(s, R1);
-        iter(s + 1, R0);
-    }
-#else
+    // One basic block per slab, so that the scheduler can interleave the
+    // split and LDS writes of slab s + 1 (into the other ring stage, whose
+    // last reader finished before the barrier) and the loads of slab s + 2
+    // with the MFMAs of slab s.  Past the end the loads are clamped to the
+    // last slab, which is then re-staged into the stage nobody reads again,
+    // without counting towards (Q w) and ||G||^2.
     Regs R;
     load(R, 0);
     load_w(0);
-    stage(R, 0);
-    if (nst > 1) {
-        load(R, 1);
-        load_w(1);
-    }
+    stage(R, 0, true);
+    load(R, 1);
+    load_w(1);
     __syncthreads();
+    constexpr int NMF = FI * FJ * NTERM * KS;
     for (int s = 0; s < nst; ++s) {
-        // slab s + 1 into the other ring stage (its last reader finished
-        // before the barrier), then the loads of slab s + 2
-        if (s + 1 < nst) stage(R, (s + 1) & 1);
-        if (s + 2 < nst) {
-            load(R, s + 2);
-            load_w(s + 2);
-        }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) compute(s & 1, ks);
+        stage(R, (s + 1) & 1, s + 1 < nst);
+        const int sl = min(s + 2, nst - 1);
+        load(R, sl);
+        load_w(sl);
+        __builtin_amdgcn_sched_group_barrier(0x100, 3 * FI + NQ * FJ, 0);   // operand reads
+#pragma unroll
+        for (int i = 0; i < NMF; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);              // VALU
+            if (i >= NMF / 2 && i < NMF / 2 + 3 + NQ)
+                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);          // LDS write
+            if (i >= NMF / 2 + 3 + NQ && i < NMF / 2 + 9 + NQ)
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);          // global load
+        }
         __syncthreads();
     }
-#endif
 
     if (PEND) {
         const float v = rdot + __shfl_xor(rdot, 1, 64);
