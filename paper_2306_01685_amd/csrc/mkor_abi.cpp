@@ -203,12 +203,14 @@ struct StageGeom {
 };
 StageGeom stage_geom(const mkor_layer& L, int stage) {
     if (is_swapped(L)) {   // stage 1 X = Linv G (K = d_in), stage 2 dW_hat^T = Rinv X^T (K = d_out)
-        if (stage == 1) return StageGeom{HG_BI, HG_BJ, L.d_in, L.d_out, L.d_in};
-        return StageGeom{HG_BI, HG_BJ, L.d_out, L.d_in, L.d_out};
+        if (stage == 1) return StageGeom{SG_BI, SG_BJ, L.d_in, L.d_out, L.d_in};
+        return StageGeom{SG_BI, SG_BJ, L.d_out, L.d_in, L.d_out};
     }
-    if (gemm_family(L) != FAM_FP32) {   // hgemm and sgemm tiles are both 256 x 256
-        if (stage == 1) return StageGeom{HG_BI, HG_BJ, L.d_out, L.d_in, L.d_out};
-        return StageGeom{HG_BI, HG_BJ, L.d_in, L.d_out, L.d_in};
+    const int fam = gemm_family(L);
+    if (fam != FAM_FP32) {
+        const int32_t bm = fam == FAM_HALF ? HG_BI : SG_BI, bn = fam == FAM_HALF ? HG_BJ : SG_BJ;
+        if (stage == 1) return StageGeom{bm, bn, L.d_out, L.d_in, L.d_out};
+        return StageGeom{bm, bn, L.d_in, L.d_out, L.d_in};
     }
     const GemmShape& sh = GEMM_SHAPE[stage - 1];
     return StageGeom{sh.bm, sh.bn, L.d_in, L.d_out, stage == 1 ? L.d_in : L.d_out};

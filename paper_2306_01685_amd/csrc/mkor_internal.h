@@ -164,6 +164,7 @@ constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 constexpr int HG_BI = MKOR_HG_BI, HG_BJ = MKOR_HG_BJ;   // tile of C (rows i x columns j)
 constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 x 64
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
+constexpr int SG_BI = 256, SG_BJ = 256;                  // tile of C of the split GEMMs (sgemm)
 constexpr int HG_BK = MKOR_HG_BK;                       // k per stage
 
 // Layer descriptor of the bf16-MFMA preconditioning stages (C = P_eff Q^T):

@@ -51,7 +51,7 @@ typedef __attribute__((address_space(3))) mk_u4 lds_u4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
 typedef __attribute__((address_space(3))) float lds_float;
 
-constexpr int BI = 256, BJ = 256, NT = 512;
+constexpr int BI = SG_BI, BJ = SG_BJ, NT = 512;
 constexpr int NW = NT / 64;
 static_assert(BI == BJ && 2 * BI == NT, "one half row of P and of Q per thread");
 
