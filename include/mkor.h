@@ -130,7 +130,7 @@ extern "C" {
                                   operand (x = h + m + l), the three smallest of the nine
                                   partial products (below 2^-23 |x x'|) left out; needs
                                   d_in and d_out multiples of 64; exact for operand
-                                  magnitudes in [2^-110, 3.38e38] */
+                                  magnitudes in [2^-110, 3.396e38) */
 
 /* largest supported d_in / d_out, and token rows of A / Gout */
 #define MKOR_MAX_DIM       32768

@@ -7,7 +7,7 @@
 // (round to nearest even).  Both differences are exact in fp32 (Sterbenz), and
 // x - h - m is a multiple of ulp(x) no larger than 2^-16 |x|, i.e. it has at
 // most 8 significant bits, so l holds it exactly: the split is exact for
-// 2^-110 <= |x| < 3.39e38 (below, l loses bits under bf16's subnormal floor;
+// 2^-110 <= |x| < 3.396e38 (below, l loses bits under bf16's subnormal floor;
 // above, h overflows).  A product of two split values is the sum of nine bf16
 // products; the three smallest (m l', l m', l l') are below 2^-23 |x x'| and are
 // left out, the same order as one fp32 rounding.  Each bf16 x bf16 product is

@@ -90,7 +90,7 @@ def test_split_precondition_only(grad_dtype):
 
 
 def test_split_small_and_large_magnitudes():
-    """The split is exact for operand magnitudes in [2^-110, 3.38e38]: factors
+    """The split is exact for operand magnitudes in [2^-110, 3.396e38): factors
     scaled by 1e-6 and 1e6 (and G with them; every partial product stays a
     normal fp32 number) keep the fp32-level error."""
     for fscale, gscale in ((1e-6, 1e-6), (1e6, 1e3)):
