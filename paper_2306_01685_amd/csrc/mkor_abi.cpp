@@ -202,9 +202,9 @@ struct StageGeom {
     int32_t K;
 };
 StageGeom stage_geom(const mkor_layer& L, int stage) {
-    if (is_swapped(L)) {   // stage 1 X = Linv G (K = d_in), stage 2 dW_hat^T = Rinv X^T (K = d_out)
+    if (is_swapped(L)) {   // stage 1 X = Linv G (K = d_in), stage 2 dW_hat = X Rinv (K = d_out)
         if (stage == 1) return StageGeom{SG_BI, SG_BJ, L.d_in, L.d_out, L.d_in};
-        return StageGeom{SG_BI, SG_BJ, L.d_out, L.d_in, L.d_out};
+        return StageGeom{SG_BI, SG_BJ, L.d_in, L.d_out, L.d_out};
     }
     const int fam = gemm_family(L);
     if (fam != FAM_FP32) {
@@ -611,7 +611,7 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
         }
         if (is_swapped(L)) {
             // X = L G with Q = G^T (bf16, transposed into the workspace), then
-            // dW_hat^T = R X^T, stored transposed into dW
+            // dW_hat = X R with the factor R as the Q operand
             void* X = base + lo.x_off[i];
             unsigned short* Gt = reinterpret_cast<unsigned short*>(base + lo.gt_off[i]);
             tri[nti] = TrItem{static_cast<const unsigned short*>(L.G), Gt, L.d_in, L.d_out};
@@ -624,13 +624,13 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.pend = fL.pend; A.w = fL.w;
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
-            A.qf32 = 0; A.ct = 0;
+            A.qf32 = 0; A.fq = 0;
             HgLayer& B = s2l[i];
-            B.P = L.Rinv; B.Q = X; B.C = L.dW;
+            B.P = X; B.Q = L.Rinv; B.C = L.dW;
             B.pend = fR.pend; B.w = fR.w;
             B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
             B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
-            B.qf32 = 1; B.ct = 1;
+            B.qf32 = 1; B.fq = 1;
             gp += ngp;
             dp += ndp;
             continue;
@@ -645,13 +645,13 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.pend = fR.pend; A.w = fR.w;
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
-            A.qf32 = bf16 ? 0 : 1; A.ct = 0;
+            A.qf32 = bf16 ? 0 : 1; A.fq = 0;
             HgLayer& B = s2l[i];
             B.P = L.Linv; B.Q = Yt; B.C = L.dW;
             B.pend = fL.pend; B.w = fL.w;
             B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
             B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
-            B.qf32 = 1; B.ct = 0;
+            B.qf32 = 1; B.fq = 0;
             gp += ngp;
             dp += ndp;
             continue;

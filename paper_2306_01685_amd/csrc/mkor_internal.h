@@ -180,7 +180,7 @@ struct HgLayer {
     int32_t        part0;  // first partial slot of this layer
     int32_t        ntj;    // number of column tiles
     int32_t        qf32;   // sgemm: Q is fp32 (else bf16)
-    int32_t        ct;     // sgemm: C is stored transposed (C[i][j] at C + j I + i)
+    int32_t        fq;     // sgemm: the factor is the Q operand, C = P Q_eff^T (else C = P_eff Q^T)
     int32_t        _pad;
 };
 

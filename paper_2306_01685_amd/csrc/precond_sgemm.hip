@@ -23,9 +23,13 @@
 //                             d_in), plus ||G||^2 partials;
 //   stage 2:  dW_hat = L Y    P = S_L (d_in x d_in, fp32), Q = Y^T (fp32),
 //                             C = dW_hat in fp32, plus ||dW_hat||^2 partials.
-// The pending rank-1 term of the SM update enters in the epilogue,
-//   C[i][j] = c1 (S Q^T)[i][j] + c2 Q[j][i] + sgn w[i] (Q w)[j],
-// with (Q w) summed from the staged Q values in fp32.
+// Layers with a bf16 G and d_in > d_out take the other association, so that
+// their longer contraction has the bf16 operand: stage 1 X = L G (P = S_L,
+// Q = G^T), stage 2 dW_hat = X R with the factor as the Q operand (P = X,
+// Q = S_R).  The pending rank-1 term of the SM update enters in the epilogue,
+//   C[i][j] = c1 (S Q^T)[i][j] + c2 Q[j][i] + sgn w[i] (Q w)[j]
+// (factor as Q: c1 (P S^T)[i][j] + c2 P[i][j] + sgn w[j] (P w)[i]), with the
+// matrix-vector product summed from the staged rows in fp32.
 //
 // Tiles of 256 x 256 outputs, eight waves of 128 x 64 (4 x 2 MFMA blocks), two
 // per SIMD.  K runs in slabs (16 deep when Q is fp32, 32 when it is bf16, so
@@ -110,8 +114,10 @@ struct SgArgs {
     float* partials;
 };
 
-// QF: Q is fp32 (three planes) or bf16 (one plane, exact as it is)
-template <int STAGE, bool QF, bool PEND>
+// QF: Q is fp32 (three planes) or bf16 (one plane, exact as it is).  FQ: the
+// factor is the Q operand (C = P Q_eff^T; the epilogue adds c2 P[i][j] +
+// sgn w[j] (P w)[i], with (P w) summed from the staged P rows).
+template <int STAGE, bool QF, bool PEND, bool FQ>
 __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
                            lds_char* smem) {
     using G = Geo<QF>;
@@ -227,7 +233,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         if constexpr (PEND) {
             float r = rdot;
 #pragma unroll
-            for (int e = 0; e < HK; ++e) r = fmaf(v[e], wsel(e), r);
+            for (int e = 0; e < HK; ++e) r = fmaf(FQ ? R.p[e] : v[e], wsel(e), r);
             rdot = count ? r : rdot;
         }
         if constexpr (STAGE == 1) {
@@ -312,28 +318,45 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     float* Cp = static_cast<float*>(L.C);
     // One MFMA row block (x) at a time: the loads its output groups need
     // (rows past the edge clamped), then C[i][j] = c1 acc + c2 Q[j][i] +
-    // sgn w[i] (Q w)[j], stored as 128-byte row segments.
+    // sgn w[i] (Q w)[j] (FQ: c1 acc + c2 P[i][j] + sgn w[j] (P w)[i]), stored
+    // as 128-byte row segments.
 #pragma unroll
     for (int x = 0; x < FI; ++x) {
         float qv[FJ][4][4];
         float4 wv[4];
+        float wcol[FJ];
         if (PEND) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
-                wv[g] = gld4(L.w + i);
+            if constexpr (FQ) {
 #pragma unroll
                 for (int y = 0; y < FJ; ++y) {
-                    const size_t e0 = (size_t)min(j0 + wj * TJ + y * 32 + li, J - 1) * K + i;
-                    if constexpr (QF) {
-                        const float4 f = gld4(static_cast<const float*>(L.Q) + e0);
-                        qv[y][g][0] = f.x; qv[y][g][1] = f.y; qv[y][g][2] = f.z; qv[y][g][3] = f.w;
-                    } else {
-                        const uint2 h = gld_u2(static_cast<const unsigned short*>(L.Q) + e0);
-                        qv[y][g][0] = __uint_as_float(h.x << 16);
-                        qv[y][g][1] = __uint_as_float(h.x & 0xffff0000u);
-                        qv[y][g][2] = __uint_as_float(h.y << 16);
-                        qv[y][g][3] = __uint_as_float(h.y & 0xffff0000u);
+                    const int j = min(j0 + wj * TJ + y * 32 + li, J - 1);
+                    wcol[y] = gld(L.w + j);
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            qv[y][g][e] = gld(static_cast<const float*>(L.P) + (size_t)(i + e) * K + j);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
+                    wv[g] = gld4(L.w + i);
+#pragma unroll
+                    for (int y = 0; y < FJ; ++y) {
+                        const size_t e0 = (size_t)min(j0 + wj * TJ + y * 32 + li, J - 1) * K + i;
+                        if constexpr (QF) {
+                            const float4 f = gld4(static_cast<const float*>(L.Q) + e0);
+                            qv[y][g][0] = f.x; qv[y][g][1] = f.y; qv[y][g][2] = f.z; qv[y][g][3] = f.w;
+                        } else {
+                            const uint2 h = gld_u2(static_cast<const unsigned short*>(L.Q) + e0);
+                            qv[y][g][0] = __uint_as_float(h.x << 16);
+                            qv[y][g][1] = __uint_as_float(h.x & 0xffff0000u);
+                            qv[y][g][2] = __uint_as_float(h.y << 16);
+                            qv[y][g][3] = __uint_as_float(h.y & 0xffff0000u);
+                        }
                     }
                 }
             }
@@ -341,27 +364,28 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
         for (int y = 0; y < FJ; ++y) {
             const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
-            const float rq = PEND ? rvec[jl] : 0.f;
+            const float rq = (PEND && !FQ) ? rvec[jl] : 0.f;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int i = i0 + wi * TI + x * 32 + 8 * g + 4 * lk;
+                const int il = wi * TI + x * 32 + 8 * g + 4 * lk, i = i0 + il;
                 float v[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = acc[x][y][4 * g + e];
                 if (PEND) {
-                    const float wa[4] = {wv[g].x, wv[g].y, wv[g].z, wv[g].w};
+                    if constexpr (FQ) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wa[e] * rq));
+                        for (int e = 0; e < 4; ++e)
+                            v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wcol[y] * rvec[il + e]));
+                    } else {
+                        const float wa[4] = {wv[g].x, wv[g].y, wv[g].z, wv[g].w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wa[e] * rq));
+                    }
                 }
                 if (i < I && j < J) {   // I, J multiples of 64: 4 rows all in or all out
-                    if (L.ct) {
-                        // transposed: the 4 rows i .. i + 3 are contiguous in row j of C^T
-                        gst4(Cp + (size_t)j * I + i, make_float4(v[0], v[1], v[2], v[3]));
-                    } else {
-                        float* dst = Cp + (size_t)i * J + j;
+                    float* dst = Cp + (size_t)i * J + j;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) gst(dst + (size_t)e * J, v[e]);
-                    }
+                    for (int e = 0; e < 4; ++e) gst(dst + (size_t)e * J, v[e]);
                     if (STAGE == 2) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e) csq = fmaf(v[e], v[e], csq);
@@ -391,16 +415,21 @@ template <int STAGE>
 __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
     __shared__ __attribute__((aligned(16))) char smem_[SMEM];
     lds_char* smem = (lds_char*)smem_;
-    const GemmTile tile = args.tiles[blockIdx.x];
-    if (tile.layer < 0) return;   // padding of the XCD interleave
-    const HgLayer L = args.layers[tile.layer];
-    const Pending q = *L.pend;
-    if (L.qf32) {
-        if (q.has) sgemm_tile<STAGE, true, true>(L, tile, q, args.partials, smem);
-        else       sgemm_tile<STAGE, true, false>(L, tile, q, args.partials, smem);
-    } else {
-        if (q.has) sgemm_tile<STAGE, false, true>(L, tile, q, args.partials, smem);
-        else       sgemm_tile<STAGE, false, false>(L, tile, q, args.partials, smem);
+    {
+        const GemmTile tile = args.tiles[blockIdx.x];
+        if (tile.layer < 0) return;   // padding of the XCD interleave
+        const HgLayer L = args.layers[tile.layer];
+        const Pending q = *L.pend;
+        if (STAGE == 2 && L.fq) {   // the second GEMM of a layer computed as X Rinv
+            if (q.has) sgemm_tile<STAGE, true, true, true>(L, tile, q, args.partials, smem);
+            else       sgemm_tile<STAGE, true, false, true>(L, tile, q, args.partials, smem);
+        } else if (L.qf32) {
+            if (q.has) sgemm_tile<STAGE, true, true, false>(L, tile, q, args.partials, smem);
+            else       sgemm_tile<STAGE, true, false, false>(L, tile, q, args.partials, smem);
+        } else {
+            if (q.has) sgemm_tile<STAGE, false, true, false>(L, tile, q, args.partials, smem);
+            else       sgemm_tile<STAGE, false, false, false>(L, tile, q, args.partials, smem);
+        }
     }
 }
 
@@ -443,8 +472,9 @@ hipError_t launch_sgemm(int stage, const HgLayer* layers, const GemmTile* tiles,
                         float* partials, hipStream_t stream) {
     if (ntiles <= 0) return hipSuccess;
     SgArgs a{layers, tiles, partials};
-    if (stage == 1) hipLaunchKernelGGL(sgemm_kernel<1>, dim3(ntiles), dim3(NT), 0, stream, a);
-    else            hipLaunchKernelGGL(sgemm_kernel<2>, dim3(ntiles), dim3(NT), 0, stream, a);
+    const int grid = ntiles;
+    if (stage == 1) hipLaunchKernelGGL(sgemm_kernel<1>, dim3(grid), dim3(NT), 0, stream, a);
+    else            hipLaunchKernelGGL(sgemm_kernel<2>, dim3(grid), dim3(NT), 0, stream, a);
     return hipGetLastError();
 }
 
