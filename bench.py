@@ -323,7 +323,8 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
         mfma_ms = (f1 / peaks[0] + f2 / peaks[1]) / 1e12 * 1e3   # both GEMMs at their peaks
         kernels["gemm_total"] = dict(ms=pre_ms, flops=f1 + f2,
                                      tflops=(f1 + f2) / (pre_ms / 1e3) / 1e12,
-                                     frac_mfma=mfma_ms / pre_ms)
+                                     frac_mfma=mfma_ms / pre_ms,
+                                     frac_of_fp32_mfma_peak=(f1 + f2) / (pre_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TF)
         for k in ("sm_pass", "sm_finalize", "rescale"):
             kernels[k]["frac_hbm"] = kernels[k]["gbs"] / HBM_PEAK_GBS
         for k, pk, tm in ((g1, peaks[0], terms[0]), (g2, peaks[1], terms[1])):
@@ -345,6 +346,7 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
             if split:
                 roof["peak_basis"] = (f"fp32 products on the three-way bf16 split: the {BF16_MFMA_PEAK_TF:.0f} "
                                       f"TFLOP/s bf16 MFMA peak / {k['bf16_mfma_terms']} bf16 products each")
+                roof["frac_of_fp32_mfma_peak"] = k["tflops"] / FP32_MFMA_PEAK_TF
         else:
             roof = dict(kernel=name, bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
                         frac=k["gbs"] / HBM_PEAK_GBS,
