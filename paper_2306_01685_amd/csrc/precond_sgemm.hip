@@ -36,10 +36,13 @@
 // that both ring stages fit in LDS): each thread loads one half slab row of
 // P and of Q into registers one slab ahead, splits them and writes the planes
 // into a two-stage LDS ring with 16-byte writes.  A plane row is BK * 2 bytes
-// in 16-byte chunks; chunk c of row r sits in slot c ^ f(r), f(r) = (r >> 3) & 1
-// for 32-byte rows and (r >> 2) & 3 for 64-byte rows, so the 16 rows of an
-// MFMA operand read, and the rows of a staging write, fall on 16 distinct
-// 16-byte bank groups.  d_in and d_out are multiples of 64 (checked by the
+// in 16-byte chunks; chunk c of row r sits in slot c ^ f(r).  A 16-byte LDS
+// read is served 16 lanes at a time from 16 bank groups of 16 bytes, a 16-byte
+// write 8 lanes at a time from 8 (address / 16 mod 8; measured with the bank
+// conflict counter), so f(r) = (r >> 3) & 1 for 32-byte rows and
+// ((r >> 2) & 3) ^ ((r >> 1) & 1) for 64-byte rows put the 16 rows of an MFMA
+// operand read on 16 groups and the 8 lanes of a staging write on 8: no bank
+// conflicts in either direction.  d_in and d_out are multiples of 64 (checked by the
 // plan); rows past a tile edge are loaded clamped to the last row and never
 // stored.
 #include "gmem.h"
@@ -80,7 +83,8 @@ constexpr int SMEM = RING + 4 * (BJ + NW);
 
 template <int ROWB>
 __device__ __forceinline__ int slot(int r, int c) {
-    return ROWB == 32 ? r * 32 + ((c ^ ((r >> 3) & 1)) << 4) : r * 64 + ((c ^ ((r >> 2) & 3)) << 4);
+    return ROWB == 32 ? r * 32 + ((c ^ ((r >> 3) & 1)) << 4)
+                      : r * 64 + ((c ^ ((r >> 2) & 3) ^ ((r >> 1) & 1)) << 4);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
