@@ -108,6 +108,9 @@ def parse():
                     help="preconditioning GEMMs of fp32 factors (auto: the split where the shape allows)")
     ap.add_argument("--no-fp32-path", action="store_true",
                     help="skip the extra measurement on the fp32 MFMA GEMM path")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured once in a HIP graph and replayed K times "
+                         "(saves the launch gaps of launch-bound workloads)")
     return ap.parse_args()
 
 
@@ -361,6 +364,32 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                                  traffic=None if t is None else t["total_bytes"],
                                  per_launch=f"{k['alg_bytes']:.4e} B")
 
+    # The same step captured in a HIP graph (kernel launches only) and replayed.
+    graph = None
+    if getattr(args, "graph", False):
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                plan.step(params)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        g_ms = e0.elapsed_time(e1) / args.steps
+        graph = dict(ms_per_step=g_ms, value=w.n_layers / (g_ms / 1e3), unit="layer-updates/s",
+                     note="one mkor_step captured in a HIP graph, replayed")
+        del g
+
     # The paper's schedule: factors updated every 10 iterations (stale factors
     # precondition the other nine); per-step rate averaged over whole cycles.
     schedule = None
@@ -380,6 +409,8 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                         value=w.n_layers / (f_ms / 1e3), unit="layer-updates/s")
     del plan, layers
     torch.cuda.empty_cache()
+    if graph is not None:
+        kernels["graph_replay"] = graph
     return ms_step, kernels, roof, schedule
 
 
