@@ -116,8 +116,9 @@ extern "C" {
 #define MKOR_STAGE_MEANS      0   /* a, g = row means of A, Gout (layers with rows > 0) */
 #define MKOR_STAGE_SM_PASS    1   /* write pending term into S; u_raw = P x, norm and s partials */
 #define MKOR_STAGE_SM_FINALIZE 2  /* stabiliser decision, new pending rank-1 term */
-#define MKOR_STAGE_GEMM_XT    3   /* first GEMM: X^T = (Linv G)^T (fp32 MFMA) or Y^T = Rinv G^T
-                                     (bf16 MFMA paths), ||G||^2 partials */
+#define MKOR_STAGE_GEMM_XT    3   /* first GEMM: X^T = (Linv G)^T (fp32 MFMA), Y^T = Rinv G^T
+                                     (bf16 MFMA paths) or X = Linv G (split path, bf16 G,
+                                     d_in > d_out; G^T formed first), ||G||^2 partials */
 #define MKOR_STAGE_GEMM_DW    4   /* second GEMM: dW_hat = X Rinv or Linv Y, ||dW_hat||^2 partials */
 #define MKOR_STAGE_RESCALE    5   /* rescale / first-order pass-through */
 #define MKOR_NUM_STAGES       6
