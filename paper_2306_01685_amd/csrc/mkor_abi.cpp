@@ -149,6 +149,7 @@ struct Layout {
     size_t off_s1l = 0, off_s1t = 0, off_s2l = 0, off_s2t = 0;   // fp32 factors on the bf16 split
     size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
     size_t off_tri = 0, off_trb = 0;                             // G^T of swapped split layers
+    size_t off_qdb = 0;                                          // stage-1 (Q w) row blocks (split)
     size_t off_gram = 0;                                         // rank-r Gram partials
     size_t off_lpart = 0, off_trust = 0;                         // LAMB block sums, per-layer ratios
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
@@ -158,6 +159,7 @@ struct Layout {
     int32_t ns1 = 0, ns2 = 0;
     int32_t ncvt = 0, ncvtblk = 0;
     int32_t ntr = 0, ntrblk = 0;
+    int32_t nqdb = 0;
     int32_t nsecond = 0;
     int32_t nranked = 0;      // second-order layers with rank > 1
     int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
@@ -165,6 +167,7 @@ struct Layout {
     std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
     std::vector<size_t> gh_off;                // per layer: bf16 copy of an fp32 G (bf16 factors)
     std::vector<size_t> gt_off;                // per layer: G^T (bf16) of swapped split layers
+    std::vector<size_t> rq_off;                // per layer: stage-1 (Q w) of split layers
 };
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
@@ -277,6 +280,7 @@ bool needs_cvt(const mkor_layer& L) { return is_half(L) && L.grad_dtype == MKOR_
 
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0, ncvt = 0, ncvtblk = 0, ntr = 0, ntrblk = 0;
+    int64_t nqdb = 0;
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         rsb += ceil_div((int64_t)L.d_in * L.d_out, RS_ELEMS);
@@ -288,6 +292,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
             ntr += 1;
             ntrblk += (int64_t)(L.d_in / 64) * (L.d_out / 64);
         }
+        if (is_split(L)) nqdb += gpart_count(L);
         if (!L.second_order) continue;
         Lo.nsecond++;
         if (layer_rank(L) > 1) Lo.nranked++;
@@ -311,7 +316,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         }
     }
     if (rowblocks > INT32_MAX || g1 > INT32_MAX || rsb > INT32_MAX || mitems > INT32_MAX || ncvtblk > INT32_MAX ||
-        ntrblk > INT32_MAX)
+        ntrblk > INT32_MAX || nqdb > INT32_MAX)
         return fail(MKOR_UNSUPPORTED, "layer list too large for one grouped launch");
     Lo.nmeanmat = (int32_t)mmats;
     Lo.nmeanitem = (int32_t)mitems;
@@ -337,6 +342,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.ncvtblk = (int32_t)ncvtblk;
     Lo.ntr = (int32_t)ntr;
     Lo.ntrblk = (int32_t)ntrblk;
+    Lo.nqdb = (int32_t)nqdb;
 
     size_t o = 0;
     auto take = [&](size_t bytes) { o = align_up(o, 256); size_t r = o; o += bytes; return r; };
@@ -363,6 +369,7 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_cvtb = take(sizeof(CvtBlock) * Lo.ncvtblk);
     Lo.off_tri = take(sizeof(TrItem) * Lo.ntr);
     Lo.off_trb = take(sizeof(TrBlock) * Lo.ntrblk);
+    Lo.off_qdb = take(sizeof(QdBlock) * Lo.nqdb);
     // pending terms start out empty (has = 0): the upload initialises them
     Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
     Lo.table_bytes = align_up(o, 256);
@@ -394,6 +401,9 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.gt_off.assign(n, 0);
     for (int32_t i = 0; i < n; ++i)
         if (is_swapped(layers[i])) Lo.gt_off[i] = take(2 * (size_t)layers[i].d_in * layers[i].d_out);
+    Lo.rq_off.assign(n, 0);
+    for (int32_t i = 0; i < n; ++i)
+        if (is_split(layers[i])) Lo.rq_off[i] = take(sizeof(float) * (size_t)stage_geom(layers[i], 1).cols);
     Lo.total = align_up(o, 256);
     (void)usum;
     return MKOR_OK;
@@ -504,6 +514,8 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     TrItem* tri = reinterpret_cast<TrItem*>(host.data() + lo.off_tri);
     TrBlock* trb = reinterpret_cast<TrBlock*>(host.data() + lo.off_trb);
     int32_t nti = 0, ntb = 0;
+    QdBlock* qdb = reinterpret_cast<QdBlock*>(host.data() + lo.off_qdb);
+    int32_t nqb = 0;
     RescaleLayer* rsl = reinterpret_cast<RescaleLayer*>(host.data() + lo.off_rsl);
     RescaleBlock* rsb = reinterpret_cast<RescaleBlock*>(host.data() + lo.off_rsb);
     Pending* pend_h = reinterpret_cast<Pending*>(host.data() + lo.off_pend);
@@ -625,6 +637,8 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
             A.qf32 = 0; A.fq = 0;
+            A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
+            for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
             HgLayer& B = s2l[i];
             B.P = X; B.Q = L.Rinv; B.C = L.dW;
             B.pend = fR.pend; B.w = fR.w;
@@ -646,6 +660,8 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
             A.qf32 = bf16 ? 0 : 1; A.fq = 0;
+            A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
+            for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
             HgLayer& B = s2l[i];
             B.P = L.Linv; B.Q = Yt; B.C = L.dW;
             B.pend = fL.pend; B.w = fL.w;
@@ -750,6 +766,9 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             e = launch_transpose_bf16(reinterpret_cast<const TrItem*>(ws + lo.off_tri),
                                       reinterpret_cast<const TrBlock*>(ws + lo.off_trb), lo.ntrblk, s);
             if (e != hipSuccess) return hip_fail(e, "bf16 gradient transpose launch");
+            e = launch_qdot(reinterpret_cast<const HgLayer*>(ws + lo.off_s1l),
+                            reinterpret_cast<const QdBlock*>(ws + lo.off_qdb), lo.nqdb, gpart, s);
+            if (e != hipSuccess) return hip_fail(e, "split gemm row pass launch");
             e = launch_sgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_s1l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_s1t), lo.ns1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "split gemm (R G^T) launch");

@@ -182,6 +182,13 @@ struct HgLayer {
     int32_t        qf32;   // sgemm: Q is fp32 (else bf16)
     int32_t        fq;     // sgemm: the factor is the Q operand, C = P Q_eff^T (else C = P_eff Q^T)
     int32_t        _pad;
+    float*         rq;     // sgemm stage 1: (Q w) per Q row, formed by qdot_kernel before the GEMM
+};
+
+// Rows of the stage-1 Q operand of the split GEMMs, one block of SG_BJ rows
+// per workgroup: (Q w) for the pending term and the ||G||^2 partial
+struct QdBlock {
+    int32_t layer, rb;     // index into the stage-1 layer table, row block
 };
 
 // bf16 transposes (G^T for the split GEMMs that contract over d_in)
@@ -208,6 +215,8 @@ constexpr int CVT_ELEMS = 1 << 16;   // elements per workgroup of the conversion
 
 hipError_t launch_sgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream);
+hipError_t launch_qdot(const HgLayer* layers, const QdBlock* blocks, int32_t nblocks, float* partials,
+                       hipStream_t stream);
 hipError_t launch_transpose_bf16(const TrItem* items, const TrBlock* blocks, int32_t nblocks, hipStream_t stream);
 hipError_t launch_hgemm(int stage, const HgLayer* layers, const GemmTile* tiles, int32_t ntiles,
                         float* partials, hipStream_t stream);

@@ -33,9 +33,11 @@
 //
 // Tiles of 256 x 256 outputs, eight waves of 128 x 64 (4 x 2 MFMA blocks), two
 // per SIMD.  K runs in slabs (16 deep when Q is fp32, 32 when it is bf16, so
-// that both ring stages fit in LDS): each thread loads one half slab row of
-// P and of Q into registers one slab ahead, splits them and writes the planes
-// into a two-stage LDS ring with 16-byte writes.  A plane row is BK * 2 bytes
+// that the rings fit in LDS): each thread loads one half slab row of P (and
+// of an fp32 Q) into registers one slab ahead, splits them and writes the
+// planes into a two-stage LDS ring with 16-byte writes.  A bf16 Q needs no
+// split: its slab goes from global memory straight into a three-slot LDS ring
+// (global_load_lds_dwordx4), in the same swizzle.  A plane row is BK * 2 bytes
 // in 16-byte chunks; chunk c of row r sits in slot c ^ f(r).  A 16-byte LDS
 // read is served 16 lanes at a time from 16 bank groups of 16 bytes, a 16-byte
 // write 8 lanes at a time from 8 (address / 16 mod 8; measured with the bank
@@ -65,6 +67,8 @@ static_assert(BI == BJ && 2 * BI == NT, "one half row of P and of Q per thread")
 // wave layout and ring geometry for Q in fp32 (QF) or bf16.  With three P
 // planes and one Q plane a wave reads fewer operand bytes per MFMA when it
 // covers fewer P rows and more Q rows (64 x 128 instead of 128 x 64).
+// A bf16 Q has a ring of its own, three slots of one plane after the P
+// stages.
 template <bool QF> struct Geo {
     static constexpr int WI = QF ? 2 : 4, WJ = NW / WI;   // wave grid
     static constexpr int TI = BI / WI, TJ = BJ / WJ;      // outputs per wave
@@ -75,11 +79,17 @@ template <bool QF> struct Geo {
     static constexpr int HK = BK / 2;              // k per thread and slab
     static constexpr int ROWB = BK * 2;            // bytes per plane row
     static constexpr int PLANE = BI * ROWB;
-    static constexpr int STB = (3 + NQ) * PLANE;   // one ring stage
-    static constexpr int RING = 2 * STB;
+    static constexpr int STB = (QF ? 6 : 3) * PLANE;   // one ring stage (P and, for an fp32 Q, Q)
+    static constexpr int QRING = 2 * STB;              // bf16 Q: three slots of one plane
+    static constexpr int RING = QF ? 2 * STB : QRING + 3 * PLANE;
 };
-constexpr int RING = Geo<true>::RING > Geo<false>::RING ? Geo<true>::RING : Geo<false>::RING;   // 128 KB
+constexpr int RING = Geo<true>::RING > Geo<false>::RING ? Geo<true>::RING : Geo<false>::RING;   // 144 KB
 constexpr int SMEM = RING + 4 * (BJ + NW);
+
+__device__ __forceinline__ void dma16(unsigned lds, unsigned voff, const void* base) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
+                 : "memory");
+}
 
 template <int ROWB>
 __device__ __forceinline__ int slot(int r, int c) {
@@ -125,6 +135,8 @@ template <int STAGE, bool QF, bool PEND, bool FQ>
 __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
                            lds_char* smem) {
     using G = Geo<QF>;
+    constexpr bool QDMA = !QF;   // bf16 Q (first GEMM only)
+    static_assert(!QDMA || STAGE == 1, "a bf16 Q operand is the first GEMM's");
     constexpr int WI = G::WI, TI = G::TI, TJ = G::TJ, FI = G::FI, FJ = G::FJ;
     static_assert(NT == WI * G::WJ * 64, "wave layout");
     constexpr int NQ = G::NQ, BK = G::BK, KS = G::KS, HK = G::HK, ROWB = G::ROWB, PLANE = G::PLANE;
@@ -135,7 +147,6 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     const int wi = wave % WI, wj = wave / WI;
     const int li = lane & 31, lk = lane >> 5;
     const int I = L.I, J = L.J, K = L.K;
-    const bool want_gsq = STAGE == 1 && tile.tm == 0;   // ||G||^2: each Q row once
     lds_float* rvec = (lds_float*)(smem + RING);
     lds_float* red = rvec + BJ;
 
@@ -152,19 +163,19 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     const float* Pp = static_cast<const float*>(L.P) + (size_t)min(i0 + sr, I - 1) * K + HK * sh;
     const size_t qoff = (size_t)min(j0 + sr, J - 1) * K + HK * sh;
     const float* Qf = static_cast<const float*>(L.Q) + qoff;
-    const unsigned short* Qh = static_cast<const unsigned short*>(L.Q) + qoff;
     const float* Wp = L.w + HK * sh;
-    const bool gsq_row = want_gsq && j0 + sr < J;
 
-    // one slab's staged operands (P fp32, Q fp32 or packed bf16), and the w
-    // slice of a slab (cached: every thread of a tile reads the same one)
+    // one slab's operands staged through registers (P, and Q when it is
+    // fp32), and the w slice of a slab (cached: every thread of a tile reads
+    // the same one)
     struct Regs {
         float p[HK], q[QF ? HK : 1];
-        mk_u4 qh[QF ? 1 : NC];
     };
-    float wr[PEND ? HK : 1];
+    // stage 1 takes (Q w) from qdot_kernel: its loop stages no w slice
+    constexpr bool RDOT = PEND && STAGE == 2;
+    float wr[RDOT ? HK : 1];
     auto load_w = [&](int s) {
-        if constexpr (PEND) {
+        if constexpr (RDOT) {
             const int k0 = s * BK;
 #pragma unroll
             for (int c = 0; c < HK / 4; ++c) {
@@ -187,16 +198,29 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                 const float4 v = gld4(Qf + k0 + 4 * c);
                 R.q[4 * c] = v.x; R.q[4 * c + 1] = v.y; R.q[4 * c + 2] = v.z; R.q[4 * c + 3] = v.w;
             }
-        } else {
-#pragma unroll
-            for (int c = 0; c < NC; ++c) {
-                const uint4 u = gld_u4(Qh + k0 + 8 * c);
-                R.qh[c] = mk_u4{u.x, u.y, u.z, u.w};
-            }
         }
     };
-    float rdot = 0.f, gsq = 0.f;
-    // split the registers of a slab into ring stage st; (Q w) and ||G||^2
+    // bf16 Q of slab s into slot qs of the Q ring: wave w fills rows 32 w ..
+    // 32 w + 31 as two 1-KB blocks; lane l of a block lands at byte 16 l, so
+    // it loads the chunk that the swizzle puts there (row r = l / 4 of the
+    // block, chunk (l % 4) ^ f(r))
+    unsigned qoffs[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int r = 16 * (2 * wave + b) + (lane >> 2);
+        const int c = (lane & 3) ^ ((r >> 2) & 3) ^ ((r >> 1) & 1);
+        qoffs[b] = ((unsigned)min(j0 + r, J - 1) * (unsigned)K) * 2u + 16u * c;
+    }
+    const unsigned lds_q = (unsigned)(size_t)smem + G::QRING;
+    auto dma_q = [&](int s, int qs) {
+        if constexpr (QDMA) {
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                dma16(lds_q + qs * PLANE + 1024u * (2 * wave + b), qoffs[b] + 2u * s * BK, L.Q);
+        }
+    };
+    float rdot = 0.f;
+    // split the registers of a slab into ring stage st; (Q w) (or, FQ, (P w))
     // partial sums in a fixed order
     auto stage = [&](const Regs& R, int st, bool count) {
         lds_char* buf = smem + st * G::STB;
@@ -209,7 +233,6 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             *(lds_u4*)(buf + PLANE + o) = mi;
             *(lds_u4*)(buf + 2 * PLANE + o) = lo;
         }
-        float v[HK];
         if constexpr (QF) {
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
@@ -220,38 +243,20 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                 *(lds_u4*)(buf + 4 * PLANE + o) = mi;
                 *(lds_u4*)(buf + 5 * PLANE + o) = lo;
             }
-#pragma unroll
-            for (int e = 0; e < HK; ++e) v[e] = R.q[e];
-        } else {
-#pragma unroll
-            for (int c = 0; c < NC; ++c) {
-                *(lds_u4*)(buf + 3 * PLANE + slot<ROWB>(sr, NC * sh + c)) = R.qh[c];
-                const unsigned u[4] = {R.qh[c].x, R.qh[c].y, R.qh[c].z, R.qh[c].w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    v[8 * c + 2 * e] = __uint_as_float(u[e] << 16);
-                    v[8 * c + 2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
-                }
-            }
         }
-        if constexpr (PEND) {
+        if constexpr (RDOT) {   // the second GEMM only, whose Q is fp32
             float r = rdot;
 #pragma unroll
-            for (int e = 0; e < HK; ++e) r = fmaf(FQ ? R.p[e] : v[e], wsel(e), r);
+            for (int e = 0; e < HK; ++e) r = fmaf(FQ ? R.p[e] : R.q[e], wsel(e), r);
             rdot = count ? r : rdot;
-        }
-        if constexpr (STAGE == 1) {
-            float r = gsq;
-#pragma unroll
-            for (int e = 0; e < HK; ++e) r = fmaf(v[e], v[e], r);
-            gsq = (count && gsq_row) ? r : gsq;
         }
     };
     constexpr int NTERM = QF ? 6 : 3;
     // MFMA k-step ks of ring stage st: plane pairs with p + q <= 2, the small
     // terms first
-    auto compute = [&](int st, int ks) {
+    auto compute = [&](int st, int qs, int ks) {
         const lds_char* buf = smem + st * G::STB;
+        const lds_char* qbuf = QDMA ? smem + G::QRING + qs * PLANE : buf + 3 * PLANE;
         const int c = 2 * ks + lk;
         bf16x8 a[3][FI], b[NQ][FJ];
 #pragma unroll
@@ -262,7 +267,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         for (int p = 0; p < NQ; ++p)
 #pragma unroll
             for (int y = 0; y < FJ; ++y)
-                b[p][y] = *(const lds_bf8*)(buf + (3 + p) * PLANE + slot<ROWB>(wj * TJ + y * 32 + li, c));
+                b[p][y] = *(const lds_bf8*)(qbuf + p * PLANE + slot<ROWB>(wj * TJ + y * 32 + li, c));
         constexpr int TP[6] = {2, 1, 0, 1, 0, 0}, TQ[6] = {0, 1, 2, 0, 1, 0};
         constexpr int UP[3] = {2, 1, 0};
 #pragma unroll
@@ -283,21 +288,32 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     // with the MFMAs of slab s.  Past the end the loads are clamped to the
     // last slab, which is then re-staged into the stage nobody reads again,
     // without counting towards (Q w) and ||G||^2.
+    // A bf16 Q slab goes into its slot with the loads of the P slab it pairs
+    // with, one slab ahead of the split and two ahead of the MFMAs; the slot
+    // is the one slab s - 1 used, whose readers finished before the last
+    // barrier, and the wait ahead of the split (which also covers these DMA
+    // loads, issued after the register loads it waits for) completes it one
+    // barrier before compute reads it.
     Regs R;
     load(R, 0);
     load_w(0);
+    dma_q(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     stage(R, 0, true);
     load(R, 1);
     load_w(1);
+    dma_q(1, 1);
     __syncthreads();
     constexpr int NMF = FI * FJ * NTERM * KS;
     for (int s = 0; s < nst; ++s) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) compute(s & 1, ks);
+        for (int ks = 0; ks < KS; ++ks) compute(s & 1, s % 3, ks);
+        if constexpr (QDMA) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         stage(R, (s + 1) & 1, s + 1 < nst);
         const int sl = min(s + 2, nst - 1);
         load(R, sl);
         load_w(sl);
+        dma_q(sl, (s + 2) % 3);
         __builtin_amdgcn_sched_group_barrier(0x100, 3 * FI + NQ * FJ, 0);   // operand reads
 #pragma unroll
         for (int i = 0; i < NMF; ++i) {
@@ -311,7 +327,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         __syncthreads();
     }
 
-    if (PEND) {
+    if (RDOT) {
         const float v = rdot + __shfl_xor(rdot, 1, 64);
         if (sh == 0) rvec[sr] = v;
     }
@@ -368,7 +384,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
         for (int y = 0; y < FJ; ++y) {
             const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
-            const float rq = (PEND && !FQ) ? rvec[jl] : 0.f;
+            const float rq = (PEND && !FQ) ? (STAGE == 1 ? gld(L.rq + min(j, J - 1)) : rvec[jl]) : 0.f;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int il = wi * TI + x * 32 + 8 * g + 4 * lk, i = i0 + il;
@@ -399,18 +415,19 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         }
     }
 
-    // partials: block-wide fixed-order sums.  The barrier waits for the LDS
-    // writes only (a bare s_barrier): the compiler's barrier would also wait
-    // until every output store of the tile has completed.
-    const float part = STAGE == 1 ? gsq : csq;
-    const float ws = wave_sum(part);
-    if (lane == 0) red[wave] = ws;
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (t == 0 && (STAGE == 2 || want_gsq)) {
-        float s = 0.f;
-        for (int w = 0; w < NW; ++w) s += red[w];
-        if (STAGE == 1) gst(partials + L.part0 + tile.tn, s);
-        else            gst(partials + L.part0 + tile.tm * L.ntj + tile.tn, s);
+    // ||dW_hat||^2 partial: block-wide fixed-order sum (stage 1's ||G||^2
+    // partials come from qdot_kernel).  The barrier waits for the LDS writes
+    // only (a bare s_barrier): the compiler's barrier would also wait until
+    // every output store of the tile has completed.
+    if constexpr (STAGE == 2) {
+        const float ws = wave_sum(csq);
+        if (lane == 0) red[wave] = ws;
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (t == 0) {
+            float s = 0.f;
+            for (int w = 0; w < NW; ++w) s += red[w];
+            gst(partials + L.part0 + tile.tm * L.ntj + tile.tn, s);
+        }
     }
 }
 
@@ -427,14 +444,80 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
         if (STAGE == 2 && L.fq) {   // the second GEMM of a layer computed as X Rinv
             if (q.has) sgemm_tile<STAGE, true, true, true>(L, tile, q, args.partials, smem);
             else       sgemm_tile<STAGE, true, false, true>(L, tile, q, args.partials, smem);
-        } else if (L.qf32) {
+        } else if (STAGE == 2 || L.qf32) {   // the second GEMM's Q (Y^T or X) is fp32
             if (q.has) sgemm_tile<STAGE, true, true, false>(L, tile, q, args.partials, smem);
             else       sgemm_tile<STAGE, true, false, false>(L, tile, q, args.partials, smem);
-        } else {
+        } else if constexpr (STAGE == 1) {
             if (q.has) sgemm_tile<STAGE, false, true, false>(L, tile, q, args.partials, smem);
             else       sgemm_tile<STAGE, false, false, false>(L, tile, q, args.partials, smem);
         }
     }
+}
+
+// Stage-1 Q rows ahead of the first split GEMM: (Q w)[j] for the pending term
+// of the factor (when there is one) and the ||G||^2 partial of the block of
+// SG_BJ rows (Q is G, or G^T: the same elements).  Four waves take 8 rows
+// at a time (8 loads in flight per lane); lanes take 16-byte chunks with a
+// stride of 64 chunks, then fixed-order wave sums: deterministic.
+__global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ layers,
+                                                  const QdBlock* __restrict__ blocks, float* __restrict__ partials) {
+    constexpr int RB = 8;   // rows in flight per wave
+    __shared__ float red[4];
+    const QdBlock b = blocks[blockIdx.x];
+    const HgLayer L = layers[b.layer];
+    const Pending q = *L.pend;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int K = L.K, J = L.J;
+    float gsq = 0.f;
+    for (int r0 = wave * RB; r0 < SG_BJ; r0 += 4 * RB) {
+        const int jb = b.rb * SG_BJ + r0;
+        if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
+        float dot[RB], sq[RB];
+#pragma unroll
+        for (int i = 0; i < RB; ++i) dot[i] = sq[i] = 0.f;
+        if (L.qf32) {
+            const float* row = static_cast<const float*>(L.Q) + (size_t)jb * K;
+            for (int k = 4 * lane; k < K; k += 256) {
+                const float4 wv = q.has ? gld4(L.w + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int i = 0; i < RB; ++i) {
+                    const float4 v = gld4(row + (size_t)i * K + k);
+                    sq[i] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sq[i]))));
+                    dot[i] = fmaf(v.x, wv.x, fmaf(v.y, wv.y, fmaf(v.z, wv.z, fmaf(v.w, wv.w, dot[i]))));
+                }
+            }
+        } else {
+            const unsigned short* row = static_cast<const unsigned short*>(L.Q) + (size_t)jb * K;
+            for (int k = 8 * lane; k < K; k += 512) {
+                float wv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                if (q.has) {
+                    const float4 w0 = gld4(L.w + k), w1 = gld4(L.w + k + 4);
+                    wv[0] = w0.x; wv[1] = w0.y; wv[2] = w0.z; wv[3] = w0.w;
+                    wv[4] = w1.x; wv[5] = w1.y; wv[6] = w1.z; wv[7] = w1.w;
+                }
+#pragma unroll
+                for (int i = 0; i < RB; ++i) {
+                    const uint4 u = gld_u4(row + (size_t)i * K + k);
+                    const unsigned h[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float v0 = __uint_as_float(h[e] << 16), v1 = __uint_as_float(h[e] & 0xffff0000u);
+                        sq[i] = fmaf(v1, v1, fmaf(v0, v0, sq[i]));
+                        dot[i] = fmaf(v1, wv[2 * e + 1], fmaf(v0, wv[2 * e], dot[i]));
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            const float d = wave_sum(dot[i]);
+            if (lane == 0 && q.has) gst(L.rq + jb + i, d);
+            gsq += wave_sum(sq[i]);   // the same value in every lane
+        }
+    }
+    if (lane == 0) red[wave] = gsq;
+    __syncthreads();
+    if (t == 0) gst(partials + L.part0 + b.rb, (red[0] + red[1]) + (red[2] + red[3]));
 }
 
 // G^T of bf16 gradients, 64 x 64 tiles through LDS (rows of 64 + 2 elements,
@@ -465,6 +548,13 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const TrItem* __res
 }
 
 }  // namespace
+
+hipError_t launch_qdot(const HgLayer* layers, const QdBlock* blocks, int32_t nblocks, float* partials,
+                       hipStream_t stream) {
+    if (nblocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(qdot_kernel, dim3(nblocks), dim3(256), 0, stream, layers, blocks, partials);
+    return hipGetLastError();
+}
 
 hipError_t launch_transpose_bf16(const TrItem* items, const TrBlock* blocks, int32_t nblocks, hipStream_t stream) {
     if (nblocks <= 0) return hipSuccess;
