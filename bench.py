@@ -295,6 +295,7 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
         gb = 1e-9
         sd = sum(i + o for i, o in w.shapes)
         means_ms, ms = ms[0], ms[1:]   # stage 0: rank-1 means (no work when a and g are given)
+        prep_ms, ms = ms[2], ms[:2] + ms[3:]   # operand preparation of the bf16 MFMA paths
         g1, g2 = ("gemm_gr", "gemm_ly") if half else ("sgemm_gr", "sgemm_ly") if split else ("gemm_xt", "gemm_dw")
         # steady state, rank 1: every factor has a pending term, so the pass reads
         # and writes each element once, and the finalize moves O(sum d) (partials,
@@ -303,7 +304,19 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
         # writes the new update into the factor (a read and a write).
         pass_b = 2 * esz * sq if rank == 1 else esz * sq
         fin_b = 12 * sd if rank == 1 else 2 * esz * sq + 12 * rank * sd
+        # preparation bytes: the bf16 copy of an fp32 G (bf16 factors), G^T of the
+        # split layers with d_in > d_out, the split's row pass over its first
+        # GEMM's Q (G or G^T, bf16, min(d_in, d_out) rows of max(d_in, d_out))
+        # and w, with (Q w) written per row
+        if half:
+            prep_b = 6 * nel if w.grad_dtype == "fp32" else 0
+        elif split and w.grad_dtype == "bf16":
+            prep_b = (sum(4 * i * o for i, o in w.shapes if i > o) + 2 * nel
+                      + sum(4 * (i + o) for i, o in w.shapes))
+        else:
+            prep_b = 0
         kernels = {
+            "gemm_prep": dict(ms=prep_ms, alg_bytes=prep_b, gbs=prep_b * gb / (prep_ms / 1e3) if prep_ms > 0 else 0.0),
             "sm_pass": dict(ms=ms[0], alg_bytes=pass_b, gbs=pass_b * gb / (ms[0] / 1e3)),
             "sm_finalize": dict(ms=ms[1], alg_bytes=fin_b, gbs=fin_b * gb / (ms[1] / 1e3)),
             g1: dict(ms=ms[2], flops=f1, tflops=f1 / (ms[2] / 1e3) / 1e12),
@@ -337,7 +350,7 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                 kernels[k]["bf16_mfma_terms"] = tm
                 kernels[k]["bf16_mfma_tflops"] = kernels[k]["tflops"] * tm
         names = ["sm_pass", "sm_finalize", g1, g2, "rescale"]
-        dom = max(range(NUM_STAGES - 1), key=lambda s: ms[s])
+        dom = max(range(len(names)), key=lambda s: ms[s])
         name = names[dom]
         k = kernels[name]
         traffic = profiled_traffic(name, args.config, half)

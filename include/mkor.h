@@ -93,7 +93,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 7
+#define MKOR_ABI_VERSION 8
 
 /* status codes */
 #define MKOR_OK                   0
@@ -116,12 +116,15 @@ extern "C" {
 #define MKOR_STAGE_MEANS      0   /* a, g = row means of A, Gout (layers with rows > 0) */
 #define MKOR_STAGE_SM_PASS    1   /* write pending term into S; u_raw = P x, norm and s partials */
 #define MKOR_STAGE_SM_FINALIZE 2  /* stabiliser decision, new pending rank-1 term */
-#define MKOR_STAGE_GEMM_XT    3   /* first GEMM: X^T = (Linv G)^T (fp32 MFMA), Y^T = Rinv G^T
+#define MKOR_STAGE_GEMM_PREP  3   /* operands of the bf16 MFMA paths: bf16 copy of an fp32 G
+                                     (bf16 factors), G^T (split path, bf16 G, d_in > d_out),
+                                     (Q w) and ||G||^2 partials of the split path's first GEMM */
+#define MKOR_STAGE_GEMM_XT    4   /* first GEMM: X^T = (Linv G)^T (fp32 MFMA), Y^T = Rinv G^T
                                      (bf16 MFMA paths) or X = Linv G (split path, bf16 G,
-                                     d_in > d_out; G^T formed first), ||G||^2 partials */
-#define MKOR_STAGE_GEMM_DW    4   /* second GEMM: dW_hat = X Rinv or Linv Y, ||dW_hat||^2 partials */
-#define MKOR_STAGE_RESCALE    5   /* rescale / first-order pass-through */
-#define MKOR_NUM_STAGES       6
+                                     d_in > d_out), ||G||^2 partials (the other paths) */
+#define MKOR_STAGE_GEMM_DW    5   /* second GEMM: dW_hat = X Rinv or Linv Y, ||dW_hat||^2 partials */
+#define MKOR_STAGE_RESCALE    6   /* rescale / first-order pass-through */
+#define MKOR_NUM_STAGES       7
 
 /* mkor_layer.gemm_path: how the preconditioning GEMMs of a layer with fp32
  * factors multiply.  Both paths give fp32 results to fp32 accuracy. */

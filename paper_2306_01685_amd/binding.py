@@ -35,7 +35,7 @@ DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
 MAX_RANK = 4
-ABI_VERSION = 7
+ABI_VERSION = 8
 GEMM_AUTO = 0
 GEMM_FP32 = 1
 GEMM_SPLIT = 2
@@ -88,8 +88,8 @@ EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_p
             "mkor_opt_params_check", "mkor_step_opt", "mkor_precondition_opt", "mkor_plan_destroy"]
 
 STAGE_MEANS, STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(6)
-NUM_STAGES = 6
-STAGE_NAMES = ["means", "sm_pass", "sm_finalize", "gemm_xt", "gemm_dw", "rescale"]
+NUM_STAGES = 7
+STAGE_NAMES = ["means", "sm_pass", "sm_finalize", "gemm_prep", "gemm_xt", "gemm_dw", "rescale"]
 
 
 class MkorError(RuntimeError):

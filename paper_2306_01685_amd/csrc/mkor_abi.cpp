@@ -753,22 +753,24 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
             if (lo.nranked > 0) e = launch_sm_apply_rank(fd, rb, lo.nrowblocks, lo.nfactors, s);
             if (e != hipSuccess) return hip_fail(e, "rank-r apply launch");
             return MKOR_OK;
-        case MKOR_STAGE_GEMM_XT:
-            e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
-                               reinterpret_cast<const GemmTile*>(ws + lo.off_g1t), lo.ng1, gpart, s);
-            if (e != hipSuccess) return hip_fail(e, "gemm_xt launch");
+        case MKOR_STAGE_GEMM_PREP:
             e = launch_cvt_bf16(reinterpret_cast<const CvtItem*>(ws + lo.off_cvti),
                                 reinterpret_cast<const CvtBlock*>(ws + lo.off_cvtb), lo.ncvtblk, s);
             if (e != hipSuccess) return hip_fail(e, "bf16 gradient copy launch");
-            e = launch_hgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_h1l),
-                             reinterpret_cast<const GemmTile*>(ws + lo.off_h1t), lo.nh1, gpart, s);
-            if (e != hipSuccess) return hip_fail(e, "bf16 gemm (R G^T) launch");
             e = launch_transpose_bf16(reinterpret_cast<const TrItem*>(ws + lo.off_tri),
                                       reinterpret_cast<const TrBlock*>(ws + lo.off_trb), lo.ntrblk, s);
             if (e != hipSuccess) return hip_fail(e, "bf16 gradient transpose launch");
             e = launch_qdot(reinterpret_cast<const HgLayer*>(ws + lo.off_s1l),
                             reinterpret_cast<const QdBlock*>(ws + lo.off_qdb), lo.nqdb, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "split gemm row pass launch");
+            return MKOR_OK;
+        case MKOR_STAGE_GEMM_XT:
+            e = launch_gemm_xt(reinterpret_cast<const GemmLayer*>(ws + lo.off_g1l),
+                               reinterpret_cast<const GemmTile*>(ws + lo.off_g1t), lo.ng1, gpart, s);
+            if (e != hipSuccess) return hip_fail(e, "gemm_xt launch");
+            e = launch_hgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_h1l),
+                             reinterpret_cast<const GemmTile*>(ws + lo.off_h1t), lo.nh1, gpart, s);
+            if (e != hipSuccess) return hip_fail(e, "bf16 gemm (R G^T) launch");
             e = launch_sgemm(1, reinterpret_cast<const HgLayer*>(ws + lo.off_s1l),
                              reinterpret_cast<const GemmTile*>(ws + lo.off_s1t), lo.ns1, gpart, s);
             if (e != hipSuccess) return hip_fail(e, "split gemm (R G^T) launch");
@@ -880,7 +882,7 @@ int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream) 
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_plan_params(plan, params);
     if (st != MKOR_OK) return st;
-    return run_range(plan, params, MKOR_STAGE_GEMM_XT, MKOR_STAGE_RESCALE,
+    return run_range(plan, params, MKOR_STAGE_GEMM_PREP, MKOR_STAGE_RESCALE,
                      static_cast<hipStream_t>(stream));
 }
 
@@ -922,7 +924,7 @@ int mkor_precondition_opt(mkor_plan* plan, const mkor_params* params, const mkor
     if (st != MKOR_OK) return st;
     if (plan->n == 0) return MKOR_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    st = run_range(plan, params, MKOR_STAGE_GEMM_XT, MKOR_STAGE_GEMM_DW, s);
+    st = run_range(plan, params, MKOR_STAGE_GEMM_PREP, MKOR_STAGE_GEMM_DW, s);
     if (st != MKOR_OK) return st;
     return run_rescale_opt(plan, params, opt, s);
 }
