@@ -206,13 +206,16 @@ struct StageGeom {
 };
 StageGeom stage_geom(const mkor_layer& L, int stage) {
     if (is_swapped(L)) {   // stage 1 X = Linv G (K = d_in), stage 2 dW_hat = X Rinv (K = d_out)
-        if (stage == 1) return StageGeom{SG_BI, SG_BJ, L.d_in, L.d_out, L.d_in};
+        if (stage == 1) return StageGeom{SG_BI1H, SG_BJ1H, L.d_in, L.d_out, L.d_in};
         return StageGeom{SG_BI, SG_BJ, L.d_in, L.d_out, L.d_out};
     }
     const int fam = gemm_family(L);
     if (fam != FAM_FP32) {
         const int32_t bm = fam == FAM_HALF ? HG_BI : SG_BI, bn = fam == FAM_HALF ? HG_BJ : SG_BJ;
-        if (stage == 1) return StageGeom{bm, bn, L.d_out, L.d_in, L.d_out};
+        // the split's first GEMM with a bf16 Q (G) has tiles of fewer P rows
+        // and more Q rows: half the fp32 factor bytes per output
+        const bool h1 = fam == FAM_SPLIT && L.grad_dtype == MKOR_DTYPE_BF16;
+        if (stage == 1) return StageGeom{h1 ? SG_BI1H : bm, h1 ? SG_BJ1H : bn, L.d_out, L.d_in, L.d_out};
         return StageGeom{bm, bn, L.d_in, L.d_out, L.d_in};
     }
     const GemmShape& sh = GEMM_SHAPE[stage - 1];
@@ -268,6 +271,7 @@ std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int st
 // ||dW_hat||^2 partials (one per tile of the stage that writes dW_hat).
 int64_t gpart_count(const mkor_layer& L) {
     const StageGeom g = stage_geom(L, 1);
+    if (is_split(L)) return ceil_div(g.cols, QD_ROWS);   // one per qdot_kernel block
     return ceil_div(g.cols, g.bn);
 }
 int64_t dpart_count(const mkor_layer& L) {

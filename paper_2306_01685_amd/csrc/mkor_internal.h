@@ -165,6 +165,8 @@ constexpr int HG_BI = MKOR_HG_BI, HG_BJ = MKOR_HG_BJ;   // tile of C (rows i x c
 constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 x 64
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
 constexpr int SG_BI = 256, SG_BJ = 256;                  // tile of C of the split GEMMs (sgemm)
+constexpr int SG_BI1H = 128, SG_BJ1H = 512;              // ... of the first one when Q is bf16
+constexpr int QD_ROWS = 256;                             // Q rows per qdot_kernel block
 constexpr int HG_BK = MKOR_HG_BK;                       // k per stage
 
 // Layer descriptor of the bf16-MFMA preconditioning stages (C = P_eff Q^T):
@@ -185,7 +187,7 @@ struct HgLayer {
     float*         rq;     // sgemm stage 1: (Q w) per Q row, formed by qdot_kernel before the GEMM
 };
 
-// Rows of the stage-1 Q operand of the split GEMMs, one block of SG_BJ rows
+// Rows of the stage-1 Q operand of the split GEMMs, one block of QD_ROWS rows
 // per workgroup: (Q w) for the pending term and the ||G||^2 partial
 struct QdBlock {
     int32_t layer, rb;     // index into the stage-1 layer table, row block

@@ -60,31 +60,38 @@ typedef __attribute__((address_space(3))) mk_u4 lds_u4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
 typedef __attribute__((address_space(3))) float lds_float;
 
-constexpr int BI = SG_BI, BJ = SG_BJ, NT = 512;
+constexpr int NT = 512;
 constexpr int NW = NT / 64;
-static_assert(BI == BJ && 2 * BI == NT, "one half row of P and of Q per thread");
 
-// wave layout and ring geometry for Q in fp32 (QF) or bf16.  With three P
-// planes and one Q plane a wave reads fewer operand bytes per MFMA when it
-// covers fewer P rows and more Q rows (64 x 128 instead of 128 x 64).
-// A bf16 Q has a ring of its own, three slots of one plane after the P
-// stages.
+// Tile, wave layout and ring geometry for Q in fp32 (QF) or bf16.  An fp32
+// Q: 256 x 256 tiles, waves of 128 x 64, six planes per slab.  A bf16 Q
+// (three P planes, one Q plane): 128 x 512 tiles, which halve the fp32 P
+// bytes per output against 256 x 256 for the same accumulators (the P rows
+// pass through registers and the split; the Q rows go straight into LDS),
+// and waves of 64 x 128, which read fewer operand bytes per MFMA.  A bf16 Q
+// has a ring of its own, three slots of one plane after the P stages.
 template <bool QF> struct Geo {
-    static constexpr int WI = QF ? 2 : 4, WJ = NW / WI;   // wave grid
+    static constexpr int BI = QF ? SG_BI : SG_BI1H, BJ = QF ? SG_BJ : SG_BJ1H;   // tile
+    static constexpr int WI = 2, WJ = NW / WI;            // wave grid
     static constexpr int TI = BI / WI, TJ = BJ / WJ;      // outputs per wave
     static constexpr int FI = TI / 32, FJ = TJ / 32;      // MFMA blocks per wave
     static constexpr int NQ = QF ? 3 : 1;          // Q planes
     static constexpr int BK = QF ? 16 : 32;        // slab depth
     static constexpr int KS = BK / 16;             // MFMA k-steps per slab
-    static constexpr int HK = BK / 2;              // k per thread and slab
+    static constexpr int TPR = NT / BI;            // staging threads per P row
+    static constexpr int HK = BK / TPR;            // k per thread and slab
     static constexpr int ROWB = BK * 2;            // bytes per plane row
-    static constexpr int PLANE = BI * ROWB;
+    static constexpr int PLANE = BI * ROWB;        // a P plane (an fp32 Q's too: BJ == BI)
+    static constexpr int QPLANE = BJ * ROWB;       // a Q plane
     static constexpr int STB = (QF ? 6 : 3) * PLANE;   // one ring stage (P and, for an fp32 Q, Q)
     static constexpr int QRING = 2 * STB;              // bf16 Q: three slots of one plane
-    static constexpr int RING = QF ? 2 * STB : QRING + 3 * PLANE;
+    static constexpr int RING = QF ? 2 * STB : QRING + 3 * QPLANE;
+    static_assert(!QF || BI == BJ, "an fp32 Q is staged by the threads that stage P");
+    static_assert(HK == 8, "one 16-byte chunk per thread, row and plane");
 };
 constexpr int RING = Geo<true>::RING > Geo<false>::RING ? Geo<true>::RING : Geo<false>::RING;   // 144 KB
-constexpr int SMEM = RING + 4 * (BJ + NW);
+constexpr int BJMAX = SG_BJ > SG_BJ1H ? SG_BJ : SG_BJ1H;
+constexpr int SMEM = RING + 4 * (BJMAX + NW);
 
 __device__ __forceinline__ void dma16(unsigned lds, unsigned voff, const void* base) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
@@ -137,7 +144,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     using G = Geo<QF>;
     constexpr bool QDMA = !QF;   // bf16 Q (first GEMM only)
     static_assert(!QDMA || STAGE == 1, "a bf16 Q operand is the first GEMM's");
-    constexpr int WI = G::WI, TI = G::TI, TJ = G::TJ, FI = G::FI, FJ = G::FJ;
+    constexpr int BI = G::BI, BJ = G::BJ, WI = G::WI, TI = G::TI, TJ = G::TJ, FI = G::FI, FJ = G::FJ;
     static_assert(NT == WI * G::WJ * 64, "wave layout");
     constexpr int NQ = G::NQ, BK = G::BK, KS = G::KS, HK = G::HK, ROWB = G::ROWB, PLANE = G::PLANE;
     constexpr int NC = HK / 8;                     // 16-byte chunks per thread and plane
@@ -148,7 +155,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     const int li = lane & 31, lk = lane >> 5;
     const int I = L.I, J = L.J, K = L.K;
     lds_float* rvec = (lds_float*)(smem + RING);
-    lds_float* red = rvec + BJ;
+    lds_float* red = rvec + BJMAX;
 
     floatx16 acc[FI][FJ];
 #pragma unroll
@@ -158,8 +165,9 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-    // staging: thread t owns row sr of the P tile and of the Q tile, k half sh
-    const int sr = t >> 1, sh = t & 1;
+    // staging: thread t owns row sr of the P tile (and of an fp32 Q tile),
+    // k part sh
+    const int sr = t / G::TPR, sh = t % G::TPR;
     const float* Pp = static_cast<const float*>(L.P) + (size_t)min(i0 + sr, I - 1) * K + HK * sh;
     const size_t qoff = (size_t)min(j0 + sr, J - 1) * K + HK * sh;
     const float* Qf = static_cast<const float*>(L.Q) + qoff;
@@ -200,14 +208,15 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             }
         }
     };
-    // bf16 Q of slab s into slot qs of the Q ring: wave w fills rows 32 w ..
-    // 32 w + 31 as two 1-KB blocks; lane l of a block lands at byte 16 l, so
-    // it loads the chunk that the swizzle puts there (row r = l / 4 of the
-    // block, chunk (l % 4) ^ f(r))
-    unsigned qoffs[2];
+    // bf16 Q of slab s into slot qs of the Q ring: wave w fills NQB 1-KB
+    // blocks of 16 rows; lane l of a block lands at byte 16 l, so it loads
+    // the chunk that the swizzle puts there (row r = l / 4 of the block,
+    // chunk (l % 4) ^ f(r))
+    constexpr int NQB = QDMA ? G::QPLANE / 1024 / NW : 1;
+    unsigned qoffs[NQB];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        const int r = 16 * (2 * wave + b) + (lane >> 2);
+    for (int b = 0; b < NQB; ++b) {
+        const int r = 16 * (NQB * wave + b) + (lane >> 2);
         const int c = (lane & 3) ^ ((r >> 2) & 3) ^ ((r >> 1) & 1);
         qoffs[b] = ((unsigned)min(j0 + r, J - 1) * (unsigned)K) * 2u + 16u * c;
     }
@@ -215,8 +224,8 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     auto dma_q = [&](int s, int qs) {
         if constexpr (QDMA) {
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-                dma16(lds_q + qs * PLANE + 1024u * (2 * wave + b), qoffs[b] + 2u * s * BK, L.Q);
+            for (int b = 0; b < NQB; ++b)
+                dma16(lds_q + qs * G::QPLANE + 1024u * (NQB * wave + b), qoffs[b] + 2u * s * BK, L.Q);
         }
     };
     float rdot = 0.f;
@@ -256,7 +265,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     // terms first
     auto compute = [&](int st, int qs, int ks) {
         const lds_char* buf = smem + st * G::STB;
-        const lds_char* qbuf = QDMA ? smem + G::QRING + qs * PLANE : buf + 3 * PLANE;
+        const lds_char* qbuf = QDMA ? smem + G::QRING + qs * G::QPLANE : buf + 3 * PLANE;
         const int c = 2 * ks + lk;
         bf16x8 a[3][FI], b[NQ][FJ];
 #pragma unroll
@@ -327,6 +336,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         __syncthreads();
     }
 
+    static_assert(!RDOT || G::TPR == 2, "two threads per staged row");
     if (RDOT) {
         const float v = rdot + __shfl_xor(rdot, 1, 64);
         if (sh == 0) rvec[sr] = v;
@@ -469,8 +479,8 @@ __global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ l
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int K = L.K, J = L.J;
     float gsq = 0.f;
-    for (int r0 = wave * RB; r0 < SG_BJ; r0 += 4 * RB) {
-        const int jb = b.rb * SG_BJ + r0;
+    for (int r0 = wave * RB; r0 < QD_ROWS; r0 += 4 * RB) {
+        const int jb = b.rb * QD_ROWS + r0;
         if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
         float dot[RB], sq[RB];
 #pragma unroll
