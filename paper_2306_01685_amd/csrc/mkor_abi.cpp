@@ -204,18 +204,26 @@ struct StageGeom {
     int32_t rows, cols;  // output rows, columns
     int32_t K;
 };
+// The split's first GEMM with a bf16 Q (G or G^T) takes SG_BI1H x SG_BJ1H
+// tiles (half the fp32 factor bytes per output) unless they pad the layer's
+// output more than SG_BI x SG_BJ tiles do (rows: the factor's, columns: Q's).
+bool split_wide(int64_t rows, int64_t cols) {
+    auto padded = [&](int64_t bm, int64_t bn) { return ceil_div(rows, bm) * bm * ceil_div(cols, bn) * bn; };
+    return padded(SG_BI1H, SG_BJ1H) <= padded(SG_BI, SG_BJ);
+}
 StageGeom stage_geom(const mkor_layer& L, int stage) {
     if (is_swapped(L)) {   // stage 1 X = Linv G (K = d_in), stage 2 dW_hat = X Rinv (K = d_out)
-        if (stage == 1) return StageGeom{SG_BI1H, SG_BJ1H, L.d_in, L.d_out, L.d_in};
+        if (stage == 1) {
+            const bool w = split_wide(L.d_in, L.d_out);
+            return StageGeom{w ? SG_BI1H : SG_BI, w ? SG_BJ1H : SG_BJ, L.d_in, L.d_out, L.d_in};
+        }
         return StageGeom{SG_BI, SG_BJ, L.d_in, L.d_out, L.d_out};
     }
     const int fam = gemm_family(L);
     if (fam != FAM_FP32) {
         const int32_t bm = fam == FAM_HALF ? HG_BI : SG_BI, bn = fam == FAM_HALF ? HG_BJ : SG_BJ;
-        // the split's first GEMM with a bf16 Q (G) has tiles of fewer P rows
-        // and more Q rows: half the fp32 factor bytes per output
-        const bool h1 = fam == FAM_SPLIT && L.grad_dtype == MKOR_DTYPE_BF16;
-        if (stage == 1) return StageGeom{h1 ? SG_BI1H : bm, h1 ? SG_BJ1H : bn, L.d_out, L.d_in, L.d_out};
+        const bool w = fam == FAM_SPLIT && L.grad_dtype == MKOR_DTYPE_BF16 && split_wide(L.d_out, L.d_in);
+        if (stage == 1) return StageGeom{w ? SG_BI1H : bm, w ? SG_BJ1H : bn, L.d_out, L.d_in, L.d_out};
         return StageGeom{bm, bn, L.d_in, L.d_out, L.d_in};
     }
     const GemmShape& sh = GEMM_SHAPE[stage - 1];
@@ -640,7 +648,7 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.pend = fL.pend; A.w = fL.w;
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
-            A.qf32 = 0; A.fq = 0;
+            A.qf32 = 0; A.fq = 0; A.wide = s1.bm == SG_BI1H;
             A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
             for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
             HgLayer& B = s2l[i];
@@ -663,7 +671,7 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             A.pend = fR.pend; A.w = fR.w;
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
-            A.qf32 = bf16 ? 0 : 1; A.fq = 0;
+            A.qf32 = bf16 ? 0 : 1; A.fq = 0; A.wide = s1.bm == SG_BI1H;
             A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
             for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
             HgLayer& B = s2l[i];

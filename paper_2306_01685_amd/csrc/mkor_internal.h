@@ -166,7 +166,10 @@ constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
 constexpr int SG_BI = 256, SG_BJ = 256;                  // tile of C of the split GEMMs (sgemm)
 constexpr int SG_BI1H = 128, SG_BJ1H = 512;              // ... of the first one when Q is bf16
-constexpr int QD_ROWS = 256;                             // Q rows per qdot_kernel block
+#ifndef MKOR_QD_ROWS
+#define MKOR_QD_ROWS 256
+#endif
+constexpr int QD_ROWS = MKOR_QD_ROWS;                    // Q rows per qdot_kernel block
 constexpr int HG_BK = MKOR_HG_BK;                       // k per stage
 
 // Layer descriptor of the bf16-MFMA preconditioning stages (C = P_eff Q^T):
@@ -183,7 +186,7 @@ struct HgLayer {
     int32_t        ntj;    // number of column tiles
     int32_t        qf32;   // sgemm: Q is fp32 (else bf16)
     int32_t        fq;     // sgemm: the factor is the Q operand, C = P Q_eff^T (else C = P_eff Q^T)
-    int32_t        _pad;
+    int32_t        wide;   // sgemm stage 1, bf16 Q: SG_BI1H x SG_BJ1H tiles (else SG_BI x SG_BJ)
     float*         rq;     // sgemm stage 1: (Q w) per Q row, formed by qdot_kernel before the GEMM
 };
 

@@ -63,16 +63,19 @@ typedef __attribute__((address_space(3))) float lds_float;
 constexpr int NT = 512;
 constexpr int NW = NT / 64;
 
-// Tile, wave layout and ring geometry for Q in fp32 (QF) or bf16.  An fp32
-// Q: 256 x 256 tiles, waves of 128 x 64, six planes per slab.  A bf16 Q
-// (three P planes, one Q plane): 128 x 512 tiles, which halve the fp32 P
-// bytes per output against 256 x 256 for the same accumulators (the P rows
-// pass through registers and the split; the Q rows go straight into LDS),
-// and waves of 64 x 128, which read fewer operand bytes per MFMA.  A bf16 Q
-// has a ring of its own, three slots of one plane after the P stages.
-template <bool QF> struct Geo {
-    static constexpr int BI = QF ? SG_BI : SG_BI1H, BJ = QF ? SG_BJ : SG_BJ1H;   // tile
-    static constexpr int WI = 2, WJ = NW / WI;            // wave grid
+// Tile, wave layout and ring geometry (GV): an fp32 Q (GV_F32): 256 x 256
+// tiles, waves of 128 x 64, six planes per slab.  A bf16 Q (three P planes,
+// one Q plane) with waves of 64 x 128, which read fewer operand bytes per
+// MFMA: 256 x 256 tiles (GV_H) or 128 x 512 (GV_HW), which halve the fp32 P
+// bytes per output for the same accumulators (the P rows pass through
+// registers and the split, the Q rows go straight into LDS) where the layer
+// fills them as well.  A bf16 Q has a ring of its own, three slots of one
+// plane after the P stages.
+enum { GV_F32 = 0, GV_H = 1, GV_HW = 2 };
+template <int GV> struct Geo {
+    static constexpr bool QF = GV == GV_F32;
+    static constexpr int BI = GV == GV_HW ? SG_BI1H : SG_BI, BJ = GV == GV_HW ? SG_BJ1H : SG_BJ;   // tile
+    static constexpr int WI = GV == GV_H ? 4 : 2, WJ = NW / WI;   // wave grid
     static constexpr int TI = BI / WI, TJ = BJ / WJ;      // outputs per wave
     static constexpr int FI = TI / 32, FJ = TJ / 32;      // MFMA blocks per wave
     static constexpr int NQ = QF ? 3 : 1;          // Q planes
@@ -87,9 +90,10 @@ template <bool QF> struct Geo {
     static constexpr int QRING = 2 * STB;              // bf16 Q: three slots of one plane
     static constexpr int RING = QF ? 2 * STB : QRING + 3 * QPLANE;
     static_assert(!QF || BI == BJ, "an fp32 Q is staged by the threads that stage P");
-    static_assert(HK == 8, "one 16-byte chunk per thread, row and plane");
+    static_assert(HK % 8 == 0, "whole 16-byte chunks per thread, row and plane");
 };
-constexpr int RING = Geo<true>::RING > Geo<false>::RING ? Geo<true>::RING : Geo<false>::RING;   // 144 KB
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int RING = cmax(Geo<GV_F32>::RING, cmax(Geo<GV_H>::RING, Geo<GV_HW>::RING));   // 144 KB
 constexpr int BJMAX = SG_BJ > SG_BJ1H ? SG_BJ : SG_BJ1H;
 constexpr int SMEM = RING + 4 * (BJMAX + NW);
 
@@ -138,10 +142,11 @@ struct SgArgs {
 // QF: Q is fp32 (three planes) or bf16 (one plane, exact as it is).  FQ: the
 // factor is the Q operand (C = P Q_eff^T; the epilogue adds c2 P[i][j] +
 // sgn w[j] (P w)[i], with (P w) summed from the staged P rows).
-template <int STAGE, bool QF, bool PEND, bool FQ>
+template <int STAGE, int GV, bool PEND, bool FQ>
 __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
                            lds_char* smem) {
-    using G = Geo<QF>;
+    using G = Geo<GV>;
+    constexpr bool QF = G::QF;
     constexpr bool QDMA = !QF;   // bf16 Q (first GEMM only)
     static_assert(!QDMA || STAGE == 1, "a bf16 Q operand is the first GEMM's");
     constexpr int BI = G::BI, BJ = G::BJ, WI = G::WI, TI = G::TI, TJ = G::TJ, FI = G::FI, FJ = G::FJ;
@@ -452,14 +457,19 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
         const HgLayer L = args.layers[tile.layer];
         const Pending q = *L.pend;
         if (STAGE == 2 && L.fq) {   // the second GEMM of a layer computed as X Rinv
-            if (q.has) sgemm_tile<STAGE, true, true, true>(L, tile, q, args.partials, smem);
-            else       sgemm_tile<STAGE, true, false, true>(L, tile, q, args.partials, smem);
+            if (q.has) sgemm_tile<STAGE, GV_F32, true, true>(L, tile, q, args.partials, smem);
+            else       sgemm_tile<STAGE, GV_F32, false, true>(L, tile, q, args.partials, smem);
         } else if (STAGE == 2 || L.qf32) {   // the second GEMM's Q (Y^T or X) is fp32
-            if (q.has) sgemm_tile<STAGE, true, true, false>(L, tile, q, args.partials, smem);
-            else       sgemm_tile<STAGE, true, false, false>(L, tile, q, args.partials, smem);
+            if (q.has) sgemm_tile<STAGE, GV_F32, true, false>(L, tile, q, args.partials, smem);
+            else       sgemm_tile<STAGE, GV_F32, false, false>(L, tile, q, args.partials, smem);
         } else if constexpr (STAGE == 1) {
-            if (q.has) sgemm_tile<STAGE, false, true, false>(L, tile, q, args.partials, smem);
-            else       sgemm_tile<STAGE, false, false, false>(L, tile, q, args.partials, smem);
+            if (L.wide) {
+                if (q.has) sgemm_tile<STAGE, GV_HW, true, false>(L, tile, q, args.partials, smem);
+                else       sgemm_tile<STAGE, GV_HW, false, false>(L, tile, q, args.partials, smem);
+            } else {
+                if (q.has) sgemm_tile<STAGE, GV_H, true, false>(L, tile, q, args.partials, smem);
+                else       sgemm_tile<STAGE, GV_H, false, false>(L, tile, q, args.partials, smem);
+            }
         }
     }
 }
