@@ -26,10 +26,14 @@
 // Layers with a bf16 G and d_in > d_out take the other association, so that
 // their longer contraction has the bf16 operand: stage 1 X = L G (P = S_L,
 // Q = G^T), stage 2 dW_hat = X R with the factor as the Q operand (P = X,
-// Q = S_R).  The pending rank-1 term of the SM update enters in the epilogue,
-//   C[i][j] = c1 (S Q^T)[i][j] + c2 Q[j][i] + sgn w[i] (Q w)[j]
-// (factor as Q: c1 (P S^T)[i][j] + c2 P[i][j] + sgn w[j] (P w)[i]), with the
-// matrix-vector product summed from the staged rows in fp32.
+// Q = S_R).  The pending term of the SM update, P_eff = c1 S + c2 I +
+// sgn w w^T, enters as
+//   C[i][j] = c1 ((S + (c2 / c1) I) Q^T)[i][j] + sgn w[i] (Q w)[j]
+// (factor as Q: c1 (P (S + (c2 / c1) I)^T)[i][j] + sgn w[j] (P w)[i]): the
+// diagonal shift is added to the factor as it is staged (one fp32 rounding
+// of each diagonal entry), c1 and the rank-1 term in the epilogue, with the
+// matrix-vector product summed in fp32 from the staged rows (second GEMM)
+// or by a row pass ahead of the first.
 //
 // Tiles of 256 x 256 outputs, eight waves of 128 x 64 (4 x 2 MFMA blocks), two
 // per SIMD.  K runs in slabs (16 deep when Q is fp32, 32 when it is bf16, so
@@ -139,8 +143,8 @@ struct SgArgs {
     float* partials;
 };
 
-// QF: Q is fp32 (three planes) or bf16 (one plane, exact as it is).  FQ: the
-// factor is the Q operand (C = P Q_eff^T; the epilogue adds c2 P[i][j] +
+// GV: tile geometry (Q fp32 in three planes, or bf16 in one, exact as it
+// is).  FQ: the factor is the Q operand (C = P Q_eff^T; the epilogue adds
 // sgn w[j] (P w)[i], with (P w) summed from the staged P rows).
 template <int STAGE, int GV, bool PEND, bool FQ>
 __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
@@ -236,13 +240,31 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     float rdot = 0.f;
     // split the registers of a slab into ring stage st; (Q w) (or, FQ, (P w))
     // partial sums in a fixed order
-    auto stage = [&](const Regs& R, int st, bool count) {
+    // The pending term's c2 I enters through the staged factor (P, or Q when
+    // FQ): its diagonal entry is staged as S_ii + c2 / c1, rounded once in
+    // fp32 like the c1 scaling of the output, so the epilogue reads no second
+    // copy of the other operand.  frow: the factor row this thread stages.
+    const int frow = FQ ? min(j0 + sr, J - 1) : min(i0 + sr, I - 1);
+    const float dd = PEND ? q.c2 / q.c1 : 0.f;
+    auto stage = [&](const Regs& R, int st, bool count, int sl) {
         lds_char* buf = smem + st * G::STB;
+        float pv[HK], qv[QF ? HK : 1];
+#pragma unroll
+        for (int e = 0; e < HK; ++e) {
+            pv[e] = R.p[e];
+            if constexpr (QF) qv[e] = R.q[e];
+        }
+        if constexpr (PEND) {   // selects, not a branch: the slab stays one basic block
+            const int dk = frow - (sl * BK + HK * sh);   // the diagonal's place in this thread's part
+            float* f = FQ ? qv : pv;
+#pragma unroll
+            for (int e = 0; e < HK; ++e) f[e] = e == dk ? __fadd_rn(f[e], dd) : f[e];
+        }
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             const int o = slot<ROWB>(sr, NC * sh + c);
             mk_u4 hi, mi, lo;
-            split8(R.p + 8 * c, hi, mi, lo);
+            split8(pv + 8 * c, hi, mi, lo);
             *(lds_u4*)(buf + o) = hi;
             *(lds_u4*)(buf + PLANE + o) = mi;
             *(lds_u4*)(buf + 2 * PLANE + o) = lo;
@@ -252,7 +274,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             for (int c = 0; c < NC; ++c) {
                 const int o = slot<ROWB>(sr, NC * sh + c);
                 mk_u4 hi, mi, lo;
-                split8(R.q + 8 * c, hi, mi, lo);
+                split8(qv + 8 * c, hi, mi, lo);
                 *(lds_u4*)(buf + 3 * PLANE + o) = hi;
                 *(lds_u4*)(buf + 4 * PLANE + o) = mi;
                 *(lds_u4*)(buf + 5 * PLANE + o) = lo;
@@ -313,7 +335,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     load_w(0);
     dma_q(0, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    stage(R, 0, true);
+    stage(R, 0, true, 0);
     load(R, 1);
     load_w(1);
     dma_q(1, 1);
@@ -323,7 +345,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) compute(s & 1, s % 3, ks);
         if constexpr (QDMA) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        stage(R, (s + 1) & 1, s + 1 < nst);
+        stage(R, (s + 1) & 1, s + 1 < nst, min(s + 1, nst - 1));
         const int sl = min(s + 2, nst - 1);
         load(R, sl);
         load_w(sl);
@@ -348,52 +370,24 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     }
     __syncthreads();
 
-    const float c1 = PEND ? q.c1 : 1.f, c2 = PEND ? q.c2 : 0.f, sg = PEND ? q.sgn : 0.f;
+    const float c1 = PEND ? q.c1 : 1.f, sg = PEND ? q.sgn : 0.f;
     float csq = 0.f;
     float* Cp = static_cast<float*>(L.C);
-    // One MFMA row block (x) at a time: the loads its output groups need
-    // (rows past the edge clamped), then C[i][j] = c1 acc + c2 Q[j][i] +
-    // sgn w[i] (Q w)[j] (FQ: c1 acc + c2 P[i][j] + sgn w[j] (P w)[i]), stored
-    // as 128-byte row segments.
+    // One MFMA row block (x) at a time: the w values its output groups need
+    // (rows past the edge clamped), then C[i][j] = c1 acc + sgn w[i] (Q w)[j]
+    // (FQ: c1 acc + sgn w[j] (P w)[i]), c2 I having entered acc through the
+    // staged factor, stored as 128-byte row segments.
 #pragma unroll
     for (int x = 0; x < FI; ++x) {
-        float qv[FJ][4][4];
         float4 wv[4];
         float wcol[FJ];
         if (PEND) {
             if constexpr (FQ) {
 #pragma unroll
-                for (int y = 0; y < FJ; ++y) {
-                    const int j = min(j0 + wj * TJ + y * 32 + li, J - 1);
-                    wcol[y] = gld(L.w + j);
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            qv[y][g][e] = gld(static_cast<const float*>(L.P) + (size_t)(i + e) * K + j);
-                    }
-                }
+                for (int y = 0; y < FJ; ++y) wcol[y] = gld(L.w + min(j0 + wj * TJ + y * 32 + li, J - 1));
             } else {
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
-                    wv[g] = gld4(L.w + i);
-#pragma unroll
-                    for (int y = 0; y < FJ; ++y) {
-                        const size_t e0 = (size_t)min(j0 + wj * TJ + y * 32 + li, J - 1) * K + i;
-                        if constexpr (QF) {
-                            const float4 f = gld4(static_cast<const float*>(L.Q) + e0);
-                            qv[y][g][0] = f.x; qv[y][g][1] = f.y; qv[y][g][2] = f.z; qv[y][g][3] = f.w;
-                        } else {
-                            const uint2 h = gld_u2(static_cast<const unsigned short*>(L.Q) + e0);
-                            qv[y][g][0] = __uint_as_float(h.x << 16);
-                            qv[y][g][1] = __uint_as_float(h.x & 0xffff0000u);
-                            qv[y][g][2] = __uint_as_float(h.y << 16);
-                            qv[y][g][3] = __uint_as_float(h.y & 0xffff0000u);
-                        }
-                    }
-                }
+                for (int g = 0; g < 4; ++g) wv[g] = gld4(L.w + min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4));
             }
         }
 #pragma unroll
@@ -410,11 +404,11 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                     if constexpr (FQ) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wcol[y] * rvec[il + e]));
+                            v[e] = fmaf(c1, v[e], sg * wcol[y] * rvec[il + e]);
                     } else {
                         const float wa[4] = {wv[g].x, wv[g].y, wv[g].z, wv[g].w};
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(c2, qv[y][g][e], sg * wa[e] * rq));
+                        for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], sg * wa[e] * rq);
                     }
                 }
                 if (i < I && j < J) {   // I, J multiples of 64: 4 rows all in or all out
