@@ -35,11 +35,12 @@
 // matrix-vector product summed in fp32 from the staged rows (second GEMM)
 // or by a row pass ahead of the first.
 //
-// Tiles of 256 x 256 outputs, eight waves of 128 x 64 (4 x 2 MFMA blocks), two
-// per SIMD.  K runs in slabs (16 deep when Q is fp32, 32 when it is bf16, so
-// that the rings fit in LDS): each thread loads one half slab row of P (and
-// of an fp32 Q) into registers one slab ahead, splits them and writes the
-// planes into a two-stage LDS ring with 16-byte writes.  A bf16 Q needs no
+// Eight waves, two per SIMD, each with 128 accumulator registers (Geo: 256 x
+// 256 tiles, or 128 x 512 for a bf16 Q where the layer fills them).  K runs
+// in slabs (16 deep when Q is fp32, 32 when it is bf16, so that the rings fit
+// in LDS): each thread loads its part of a slab row of P (and of an fp32 Q)
+// into registers one slab ahead, splits it and writes the planes into a
+// two-stage LDS ring with 16-byte writes.  A bf16 Q needs no
 // split: its slab goes from global memory straight into a three-slot LDS ring
 // (global_load_lds_dwordx4), in the same swizzle.  A plane row is BK * 2 bytes
 // in 16-byte chunks; chunk c of row r sits in slot c ^ f(r).  A 16-byte LDS
