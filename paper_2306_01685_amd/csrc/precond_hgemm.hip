@@ -274,7 +274,10 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     float csq = 0.f;
     // One MFMA row block (x) at a time: first every load its output groups
     // need (rows past the edge clamped, so the loads go out together without
-    // branches), then C[i][j] = c1 acc + c2 Q[j][i] + sgn w[i] (Q w)[j].
+    // branches), then C[i][j] = c1 acc + c2 Q[j][i] + sgn w[i] (Q w)[j].  c2 is
+    // zero unless the stabiliser blended the factor (Alg. 1): Q[j][i] is only
+    // read when it counts (a branch on a value uniform over the tile).
+    const bool qterm = PEND && c2 != 0.f;
 #pragma unroll
     for (int x = 0; x < FI; ++x) {
         uint2 qh[FJ][4];
@@ -287,7 +290,8 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
                 for (int y = 0; y < FJ; ++y) {
                     const int j = min(j0 + wj * TJ + y * 32 + li, J - 1);
-                    qh[y][g] = gld_u2(static_cast<const unsigned short*>(L.Q) + (size_t)j * K + i);
+                    qh[y][g] = qterm ? gld_u2(static_cast<const unsigned short*>(L.Q) + (size_t)j * K + i)
+                                     : make_uint2(0u, 0u);
                 }
             }
         }
