@@ -147,10 +147,13 @@ struct SgArgs {
 // GV: tile geometry (Q fp32 in three planes, or bf16 in one, exact as it
 // is).  FQ: the factor is the Q operand (C = P Q_eff^T; the epilogue adds
 // sgn w[j] (P w)[i], with (P w) summed from the staged P rows).
-template <int STAGE, int GV, bool PEND, bool FQ>
+// PM: pending term of the factor: none (0), c2 = 0 (1: no stabiliser blend,
+// no diagonal shift), or c2 != 0 (2).
+template <int STAGE, int GV, int PM, bool FQ>
 __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending& q, float* partials,
                            lds_char* smem) {
     using G = Geo<GV>;
+    constexpr bool PEND = PM != 0, DIAG = PM == 2;
     constexpr bool QF = G::QF;
     constexpr bool QDMA = !QF;   // bf16 Q (first GEMM only)
     static_assert(!QDMA || STAGE == 1, "a bf16 Q operand is the first GEMM's");
@@ -255,7 +258,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             pv[e] = R.p[e];
             if constexpr (QF) qv[e] = R.q[e];
         }
-        if constexpr (PEND) {   // selects, not a branch: the slab stays one basic block
+        if constexpr (DIAG) {   // selects, not a branch: the slab stays one basic block
             const int dk = frow - (sl * BK + HK * sh);   // the diagonal's place in this thread's part
             float* f = FQ ? qv : pv;
 #pragma unroll
@@ -441,6 +444,14 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     }
 }
 
+template <int STAGE, int GV, bool FQ>
+__device__ __forceinline__ void sgemm_pm(int pm, const HgLayer& L, const GemmTile& tile, const Pending& q,
+                                         float* partials, lds_char* smem) {
+    if (pm == 2)      sgemm_tile<STAGE, GV, 2, FQ>(L, tile, q, partials, smem);
+    else if (pm == 1) sgemm_tile<STAGE, GV, 1, FQ>(L, tile, q, partials, smem);
+    else              sgemm_tile<STAGE, GV, 0, FQ>(L, tile, q, partials, smem);
+}
+
 // 8 waves per CU (2 per SIMD): at most 256 VGPRs per lane.
 template <int STAGE>
 __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
@@ -451,20 +462,14 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
         if (tile.layer < 0) return;   // padding of the XCD interleave
         const HgLayer L = args.layers[tile.layer];
         const Pending q = *L.pend;
+        const int pm = !q.has ? 0 : q.c2 != 0.f ? 2 : 1;
         if (STAGE == 2 && L.fq) {   // the second GEMM of a layer computed as X Rinv
-            if (q.has) sgemm_tile<STAGE, GV_F32, true, true>(L, tile, q, args.partials, smem);
-            else       sgemm_tile<STAGE, GV_F32, false, true>(L, tile, q, args.partials, smem);
+            sgemm_pm<STAGE, GV_F32, true>(pm, L, tile, q, args.partials, smem);
         } else if (STAGE == 2 || L.qf32) {   // the second GEMM's Q (Y^T or X) is fp32
-            if (q.has) sgemm_tile<STAGE, GV_F32, true, false>(L, tile, q, args.partials, smem);
-            else       sgemm_tile<STAGE, GV_F32, false, false>(L, tile, q, args.partials, smem);
+            sgemm_pm<STAGE, GV_F32, false>(pm, L, tile, q, args.partials, smem);
         } else if constexpr (STAGE == 1) {
-            if (L.wide) {
-                if (q.has) sgemm_tile<STAGE, GV_HW, true, false>(L, tile, q, args.partials, smem);
-                else       sgemm_tile<STAGE, GV_HW, false, false>(L, tile, q, args.partials, smem);
-            } else {
-                if (q.has) sgemm_tile<STAGE, GV_H, true, false>(L, tile, q, args.partials, smem);
-                else       sgemm_tile<STAGE, GV_H, false, false>(L, tile, q, args.partials, smem);
-            }
+            if (L.wide) sgemm_pm<STAGE, GV_HW, false>(pm, L, tile, q, args.partials, smem);
+            else        sgemm_pm<STAGE, GV_H, false>(pm, L, tile, q, args.partials, smem);
         }
     }
 }
