@@ -358,7 +358,7 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 #pragma unroll
         for (int i = 0; i < NMF; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, QDMA ? 4 : 3, 0);   // VALU (measured best)
+            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);              // VALU (measured best)
             if (i >= NMF / 2 && i < NMF / 2 + 3 + NQ)
                 __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);          // LDS write
             if (i >= NMF / 2 + 3 + NQ && i < NMF / 2 + 9 + NQ)
