@@ -302,7 +302,10 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
         # u_raw and x read, w written).  Rank r > 1: the pass only reads (the
         # previous update is already in the factor) and the finalize stage also
         # writes the new update into the factor (a read and a write).
-        pass_b = 2 * esz * sq if rank == 1 else esz * sq
+        # the factor of a split layer's first GEMM is written back every other
+        # step (two pending terms), so its pass moves 6 B per element on average
+        lazy_sq = sum((i * i if (w.grad_dtype == "bf16" and i > o) else o * o) for i, o in w.shapes) if split else 0
+        pass_b = (2 * esz * sq - 2 * lazy_sq) if rank == 1 else esz * sq
         fin_b = 12 * sd if rank == 1 else 2 * esz * sq + 12 * rank * sd
         # preparation bytes: the bf16 copy of an fp32 G (bf16 factors), G^T of the
         # split layers with d_in > d_out, the split's row pass over its first

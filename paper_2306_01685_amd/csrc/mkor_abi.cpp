@@ -190,6 +190,15 @@ bool is_swapped(const mkor_layer& L) {
     return is_split(L) && L.grad_dtype == MKOR_DTYPE_BF16 && L.d_in > L.d_out;
 }
 
+// The factor of a split layer's first GEMM (Rinv, or Linv for the other
+// association) keeps up to two pending terms, so the SM pass writes it only
+// every other step; that GEMM applies both terms in its epilogue, with (Q w)
+// of each from the row pass ahead of it.  Side 0: Linv, 1: Rinv.
+bool lazy_factor(const mkor_layer& L, int side) {
+    if (!is_split(L) || layer_rank(L) != 1) return false;
+    return side == (is_swapped(L) ? 0 : 1);
+}
+
 // GEMM kernel family of a second-order layer
 enum { FAM_FP32 = 0, FAM_HALF = 1, FAM_SPLIT = 2 };
 int gemm_family(const mkor_layer& L) { return is_half(L) ? FAM_HALF : is_split(L) ? FAM_SPLIT : FAM_FP32; }
@@ -397,9 +406,10 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.x_off.assign(n, 0);
     for (int32_t i = 0; i < n; ++i) {
         if (!layers[i].second_order) continue;
-        for (const int32_t d : {layers[i].d_in, layers[i].d_out}) {
+        for (int side = 0; side < 2; ++side) {
+            const int32_t d = side == 0 ? layers[i].d_in : layers[i].d_out;
             Lo.u_off.push_back(take(sizeof(float) * d * layer_rank(layers[i])));
-            Lo.w_off.push_back(take(sizeof(float) * d * layer_rank(layers[i])));
+            Lo.w_off.push_back(take(sizeof(float) * d * (lazy_factor(layers[i], side) ? 2 : layer_rank(layers[i]))));
         }
     }
     for (int32_t i = 0; i < n; ++i) {
@@ -415,7 +425,8 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         if (is_swapped(layers[i])) Lo.gt_off[i] = take(2 * (size_t)layers[i].d_in * layers[i].d_out);
     Lo.rq_off.assign(n, 0);
     for (int32_t i = 0; i < n; ++i)
-        if (is_split(layers[i])) Lo.rq_off[i] = take(sizeof(float) * (size_t)stage_geom(layers[i], 1).cols);
+        if (is_split(layers[i]))   // (Q w) of the first GEMM's factor, one row per pending term
+            Lo.rq_off[i] = take(sizeof(float) * 2 * (size_t)stage_geom(layers[i], 1).cols);
     Lo.total = align_up(o, 256);
     (void)usum;
     return MKOR_OK;
@@ -596,6 +607,7 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
             f.side = side;
             f.half = half ? 1 : 0;
             f.rank = layer_rank(L);
+            f.lazy = lazy_factor(L, side) ? 1 : 0;
             for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * rows};
             ++fi;
         }

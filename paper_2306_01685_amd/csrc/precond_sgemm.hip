@@ -381,9 +381,14 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     // (rows past the edge clamped), then C[i][j] = c1 acc + sgn w[i] (Q w)[j]
     // (FQ: c1 acc + sgn w[j] (P w)[i]), c2 I having entered acc through the
     // staged factor, stored as 128-byte row segments.
+    // a lazy factor (the first GEMM's) may carry a second term: w2 = w + K,
+    // (Q w2) at rq + J, coefficient sgnb (q holds the composed c1, c2 and
+    // the first term's c1b sgn: see sgemm_kernel)
+    const bool two = STAGE == 1 && PEND && !FQ && q.has == 2;
+    const float sg2 = two ? q.sgnb : 0.f;
 #pragma unroll
     for (int x = 0; x < FI; ++x) {
-        float4 wv[4];
+        float4 wv[4], wv2[4];
         float wcol[FJ];
         if (PEND) {
             if constexpr (FQ) {
@@ -391,13 +396,18 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                 for (int y = 0; y < FJ; ++y) wcol[y] = gld(L.w + min(j0 + wj * TJ + y * 32 + li, J - 1));
             } else {
 #pragma unroll
-                for (int g = 0; g < 4; ++g) wv[g] = gld4(L.w + min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4));
+                for (int g = 0; g < 4; ++g) {
+                    const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
+                    wv[g] = gld4(L.w + i);
+                    wv2[g] = two ? gld4(L.w + K + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
             }
         }
 #pragma unroll
         for (int y = 0; y < FJ; ++y) {
             const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
             const float rq = (PEND && !FQ) ? (STAGE == 1 ? gld(L.rq + min(j, J - 1)) : rvec[jl]) : 0.f;
+            const float rq2 = two ? gld(L.rq + J + min(j, J - 1)) : 0.f;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int il = wi * TI + x * 32 + 8 * g + 4 * lk, i = i0 + il;
@@ -411,8 +421,9 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                             v[e] = fmaf(c1, v[e], sg * wcol[y] * rvec[il + e]);
                     } else {
                         const float wa[4] = {wv[g].x, wv[g].y, wv[g].z, wv[g].w};
+                        const float wb[4] = {wv2[g].x, wv2[g].y, wv2[g].z, wv2[g].w};
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], sg * wa[e] * rq);
+                        for (int e = 0; e < 4; ++e) v[e] = fmaf(c1, v[e], fmaf(sg2 * wb[e], rq2, sg * wa[e] * rq));
                     }
                 }
                 if (i < I && j < J) {   // I, J multiples of 64: 4 rows all in or all out
@@ -461,7 +472,12 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
         const GemmTile tile = args.tiles[blockIdx.x];
         if (tile.layer < 0) return;   // padding of the XCD interleave
         const HgLayer L = args.layers[tile.layer];
-        const Pending q = *L.pend;
+        Pending q = *L.pend;
+        if (q.has == 2) {   // two terms: c1b (c1 S + c2 I + sgn w w^T) + c2b I + sgnb w2 w2^T
+            q.sgn = q.c1b * q.sgn;
+            q.c2 = fmaf(q.c1b, q.c2, q.c2b);
+            q.c1 = q.c1b * q.c1;
+        }
         const int pm = !q.has ? 0 : q.c2 != 0.f ? 2 : 1;
         if (STAGE == 2 && L.fq) {   // the second GEMM of a layer computed as X Rinv
             sgemm_pm<STAGE, GV_F32, true>(pm, L, tile, q, args.partials, smem);
@@ -474,46 +490,46 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
     }
 }
 
-// Stage-1 Q rows ahead of the first split GEMM: (Q w)[j] for the pending term
-// of the factor (when there is one) and the ||G||^2 partial of the block of
-// SG_BJ rows (Q is G, or G^T: the same elements).  Four waves take 8 rows
-// at a time (8 loads in flight per lane); lanes take 16-byte chunks with a
-// stride of 64 chunks, then fixed-order wave sums: deterministic.
-__global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ layers,
-                                                  const QdBlock* __restrict__ blocks, float* __restrict__ partials) {
+template <bool TWO>
+__device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, const Pending& q, float* partials,
+                                           float* red) {
     constexpr int RB = 8;   // rows in flight per wave
-    __shared__ float red[4];
-    const QdBlock b = blocks[blockIdx.x];
-    const HgLayer L = layers[b.layer];
-    const Pending q = *L.pend;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int K = L.K, J = L.J;
+    const float* w2 = L.w + K;
     float gsq = 0.f;
     for (int r0 = wave * RB; r0 < QD_ROWS; r0 += 4 * RB) {
         const int jb = b.rb * QD_ROWS + r0;
         if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
-        float dot[RB], sq[RB];
+        float dot[RB], dot2[RB], sq[RB];
 #pragma unroll
-        for (int i = 0; i < RB; ++i) dot[i] = sq[i] = 0.f;
+        for (int i = 0; i < RB; ++i) dot[i] = dot2[i] = sq[i] = 0.f;
         if (L.qf32) {
             const float* row = static_cast<const float*>(L.Q) + (size_t)jb * K;
             for (int k = 4 * lane; k < K; k += 256) {
                 const float4 wv = q.has ? gld4(L.w + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+                const float4 wv2 = TWO ? gld4(w2 + k) : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
                     const float4 v = gld4(row + (size_t)i * K + k);
                     sq[i] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sq[i]))));
                     dot[i] = fmaf(v.x, wv.x, fmaf(v.y, wv.y, fmaf(v.z, wv.z, fmaf(v.w, wv.w, dot[i]))));
+                    if (TWO) dot2[i] = fmaf(v.x, wv2.x, fmaf(v.y, wv2.y, fmaf(v.z, wv2.z, fmaf(v.w, wv2.w, dot2[i]))));
                 }
             }
         } else {
             const unsigned short* row = static_cast<const unsigned short*>(L.Q) + (size_t)jb * K;
             for (int k = 8 * lane; k < K; k += 512) {
-                float wv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                float wv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, wv2[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
                 if (q.has) {
                     const float4 w0 = gld4(L.w + k), w1 = gld4(L.w + k + 4);
                     wv[0] = w0.x; wv[1] = w0.y; wv[2] = w0.z; wv[3] = w0.w;
                     wv[4] = w1.x; wv[5] = w1.y; wv[6] = w1.z; wv[7] = w1.w;
+                }
+                if (TWO) {
+                    const float4 w0 = gld4(w2 + k), w1 = gld4(w2 + k + 4);
+                    wv2[0] = w0.x; wv2[1] = w0.y; wv2[2] = w0.z; wv2[3] = w0.w;
+                    wv2[4] = w1.x; wv2[5] = w1.y; wv2[6] = w1.z; wv2[7] = w1.w;
                 }
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
@@ -524,6 +540,7 @@ __global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ l
                         const float v0 = __uint_as_float(h[e] << 16), v1 = __uint_as_float(h[e] & 0xffff0000u);
                         sq[i] = fmaf(v1, v1, fmaf(v0, v0, sq[i]));
                         dot[i] = fmaf(v1, wv[2 * e + 1], fmaf(v0, wv[2 * e], dot[i]));
+                        if (TWO) dot2[i] = fmaf(v1, wv2[2 * e + 1], fmaf(v0, wv2[2 * e], dot2[i]));
                     }
                 }
             }
@@ -532,12 +549,32 @@ __global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ l
         for (int i = 0; i < RB; ++i) {
             const float d = wave_sum(dot[i]);
             if (lane == 0 && q.has) gst(L.rq + jb + i, d);
+            if (TWO) {
+                const float d2 = wave_sum(dot2[i]);
+                if (lane == 0) gst(L.rq + J + jb + i, d2);
+            }
             gsq += wave_sum(sq[i]);   // the same value in every lane
         }
     }
     if (lane == 0) red[wave] = gsq;
     __syncthreads();
     if (t == 0) gst(partials + L.part0 + b.rb, (red[0] + red[1]) + (red[2] + red[3]));
+}
+
+// Stage-1 Q rows ahead of the first split GEMM: (Q w)[j] for each pending
+// term of the factor (one, or two for a lazy factor) and the ||G||^2 partial
+// of the block of QD_ROWS rows (Q is G, or G^T: the same elements).  Four
+// waves take 8 rows at a time (8 loads in flight per lane); lanes take
+// 16-byte chunks with a stride of 64 chunks, then fixed-order wave sums:
+// deterministic.
+__global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ layers,
+                                                  const QdBlock* __restrict__ blocks, float* __restrict__ partials) {
+    __shared__ float red[4];
+    const QdBlock b = blocks[blockIdx.x];
+    const HgLayer L = layers[b.layer];
+    const Pending q = *L.pend;
+    if (q.has == 2) qdot_block<true>(L, b, q, partials, red);
+    else            qdot_block<false>(L, b, q, partials, red);
 }
 
 // G^T of bf16 gradients, 64 x 64 tiles through LDS (rows of 64 + 2 elements,

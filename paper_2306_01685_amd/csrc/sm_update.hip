@@ -59,17 +59,27 @@ __device__ __forceinline__ float absacc(float acc, float v, int maxabs) {
 __device__ __forceinline__ float apply(const Pending& q, float s, float wi, float wj) {
     return __fmaf_rn(q.c1, s, q.sgn * __fmul_rn(wi, wj));
 }
+// The second of two terms, applied to the value after the first (with its
+// diagonal c2 added): the same operations as the pass that would have
+// written the first term back.
+__device__ __forceinline__ float apply_b(const Pending& q, float v, float wi, float wj) {
+    return __fmaf_rn(q.c1b, v, q.sgnb * __fmul_rn(wi, wj));
+}
 
 // ------------------------------------------------------------------ pass
 // Rows rbase .. rbase + nr - 1 of one fp32 factor, d a multiple of 4.  FULL: nr = R.
-template <int RW, bool HAS, bool MV, bool FULL>
+// ST: write the current values into S; T2: the pending term has two parts.
+template <int RW, bool HAS, bool MV, bool FULL, bool ST = HAS, bool T2 = false>
 __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q, int rbase, int nr,
                                            int lane, int maxabs, float (&dot)[RW], float (&nrm)[RW]) {
     const int d = f.d, d4 = d >> 2;
     float* __restrict__ P = static_cast<float*>(f.P) + (size_t)rbase * d;
-    float wi[RW];
+    float wi[RW], wi2[RW];
 #pragma unroll
-    for (int r = 0; r < RW; ++r) wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
+    for (int r = 0; r < RW; ++r) {
+        wi[r] = (HAS && (FULL || r < nr)) ? gld(f.w + rbase + r) : 0.f;
+        wi2[r] = (T2 && (FULL || r < nr)) ? gld(f.w + d + rbase + r) : 0.f;
+    }
 
     for (int j = lane; j < d4; j += 64) {
         float4 p[RW];
@@ -78,9 +88,10 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
             if (!FULL && r >= nr) continue;
             p[r] = MKOR_SM_NT ? gld4_nt(P + (size_t)r * d + 4 * j) : gld4(P + (size_t)r * d + 4 * j);
         }
-        float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), wv = xv;
+        float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), wv = xv, wv2 = xv;
         if constexpr (MV) xv = gld4(f.x + 4 * j);
         if constexpr (HAS) wv = gld4(f.w + 4 * j);
+        if constexpr (T2) wv2 = gld4(f.w + d + 4 * j);
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
             if (!FULL && r >= nr) break;
@@ -90,17 +101,32 @@ __device__ __forceinline__ void pass_rows4(const FactorDesc& f, const Pending& q
                 p[r].z = apply(q, p[r].z, wi[r], wv.z);
                 p[r].w = apply(q, p[r].w, wi[r], wv.w);
                 const int row = rbase + r;
-                if ((row >> 2) == j) {
-                    const int c = row & 3;
+                const bool diag = (row >> 2) == j;
+                const int c = row & 3;
+                if (diag) {
                     if (c == 0) p[r].x = __fadd_rn(p[r].x, q.c2);
                     else if (c == 1) p[r].y = __fadd_rn(p[r].y, q.c2);
                     else if (c == 2) p[r].z = __fadd_rn(p[r].z, q.c2);
                     else p[r].w = __fadd_rn(p[r].w, q.c2);
                 }
-                if (MKOR_SM_NT) {
-                    gst4_nt(P + (size_t)r * d + 4 * j, p[r]);
-                } else {
-                    gst4(P + (size_t)r * d + 4 * j, p[r]);
+                if constexpr (T2) {
+                    p[r].x = apply_b(q, p[r].x, wi2[r], wv2.x);
+                    p[r].y = apply_b(q, p[r].y, wi2[r], wv2.y);
+                    p[r].z = apply_b(q, p[r].z, wi2[r], wv2.z);
+                    p[r].w = apply_b(q, p[r].w, wi2[r], wv2.w);
+                    if (diag) {
+                        if (c == 0) p[r].x = __fadd_rn(p[r].x, q.c2b);
+                        else if (c == 1) p[r].y = __fadd_rn(p[r].y, q.c2b);
+                        else if (c == 2) p[r].z = __fadd_rn(p[r].z, q.c2b);
+                        else p[r].w = __fadd_rn(p[r].w, q.c2b);
+                    }
+                }
+                if constexpr (ST) {
+                    if (MKOR_SM_NT) {
+                        gst4_nt(P + (size_t)r * d + 4 * j, p[r]);
+                    } else {
+                        gst4(P + (size_t)r * d + 4 * j, p[r]);
+                    }
                 }
             }
             if constexpr (MV) {
@@ -219,11 +245,18 @@ __device__ __forceinline__ void pass_rows1(const FactorDesc& f, const Pending& q
     }
 }
 
-// HALF (bf16 factor, d a multiple of 64) or fp32; RW rows per wave.
-template <int RW, bool HALF, bool HAS, bool MV>
+// HALF (bf16 factor, d a multiple of 64) or fp32; RW rows per wave.  A
+// factor that skips the write (ST = false with HAS) or has two terms (T2) is
+// lazy: fp32 with d a multiple of 64.
+template <int RW, bool HALF, bool HAS, bool MV, bool ST = HAS, bool T2 = false>
 __device__ __forceinline__ void pass_rows(const FactorDesc& f, const Pending& q, int rbase, int nr,
                                           int lane, int maxabs, float (&dot)[RW], float (&nrm)[RW]) {
-    if constexpr (HALF) {
+    if constexpr (T2 || ST != HAS) {
+        if constexpr (!HALF) {
+            if (nr == RW) pass_rows4<RW, HAS, MV, true, ST, T2>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else          pass_rows4<RW, HAS, MV, false, ST, T2>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+        }
+    } else if constexpr (HALF) {
         if (nr == RW) pass_rows8h<RW, HAS, MV, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
         else          pass_rows8h<RW, HAS, MV, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
     } else if ((f.d & 3) == 0) {
@@ -252,12 +285,18 @@ __device__ __forceinline__ void pass_block(const FactorDesc& f, const RowBlock& 
     float dot[RW], nrm[RW];
 #pragma unroll
     for (int r = 0; r < RW; ++r) { dot[r] = 0.f; nrm[r] = 0.f; }
+    // a lazy factor with one pending term is only read: the next term joins
+    // it (finalize), and the pass of the step after writes both
+    const bool two = q.has == 2, store = has && (!matvec || !f.lazy || two);
     if (nr > 0) {
         if (matvec) {
-            if (has) pass_rows<RW, HALF, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-            else     pass_rows<RW, HALF, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            if (!has)       pass_rows<RW, HALF, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else if (two)   pass_rows<RW, HALF, true, true, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else if (store) pass_rows<RW, HALF, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else            pass_rows<RW, HALF, true, true, false, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
         } else {
-            pass_rows<RW, HALF, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            if (two) pass_rows<RW, HALF, true, false, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+            else     pass_rows<RW, HALF, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
         }
     }
     if (!matvec) return;
@@ -509,6 +548,7 @@ struct SmScalars {
     float zp, zq;             // u = zp * u_raw + zq * x
     int   stab, skip;
     float nu, s;
+    int   comp;               // lazy factor whose pass left its term pending: two terms
 };
 
 // Rank-r factor: the r sequential Sherman-Morrison updates of P^(0) = P_hat /
@@ -658,6 +698,8 @@ __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
             c1 = g * zp; c2 = g * zq; c3 = k;
         }
         c.skip = (isfinite(nu) && isfinite(s) && isfinite(c3)) ? 0 : 1;
+        const Pending qp = *f.pend;   // the term the pass applied (and wrote, unless comp)
+        c.comp = (f.lazy && qp.has == 1) ? 1 : 0;
         c.c1 = (float)c1; c.c2 = (float)c2;
         c.sgn = c3 < 0.0 ? -1.f : 1.f;
         c.sqc = (float)sqrt(fabs(c3));
@@ -669,9 +711,13 @@ __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
             if (f.side == 0) { st->nu_L = c.nu; st->s_L = c.s; st->stab_L = c.stab; st->skip_L = c.skip; }
             else             { st->nu_R = c.nu; st->s_R = c.s; st->stab_R = c.stab; st->skip_R = c.skip; }
         }
-        Pending q;
+        Pending q{};
         if (c.skip && a.guard) {   // leave the factor unchanged
-            q.c1 = 1.f; q.c2 = 0.f; q.sgn = 0.f; q.has = 0;
+            if (c.comp) q = qp;
+            else { q.c1 = 1.f; q.c2 = 0.f; q.sgn = 0.f; q.has = 0; }
+        } else if (c.comp) {   // the new term after the pending one
+            q = qp;
+            q.c1b = c.c1; q.c2b = c.c2; q.sgnb = c.sgn; q.has = 2;
         } else {
             q.c1 = c.c1; q.c2 = c.c2; q.sgn = c.sgn; q.has = 1;
         }
@@ -680,9 +726,10 @@ __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
     __syncthreads();
     const SmScalars c = s_c;
     if (c.skip && a.guard) return;
-    // w = sqc * (zp * u_raw + zq * x), each rounding pinned
+    // w = sqc * (zp * u_raw + zq * x), each rounding pinned (w2 when comp)
+    float* wn = f.w + (c.comp ? f.d : 0);
     for (int i = t; i < f.d; i += SM_THREADS)
-        gst(f.w + i, __fmul_rn(c.sqc, __fmaf_rn(c.zp, gld(f.u + i), __fmul_rn(c.zq, gld(f.x + i)))));
+        gst(wn + i, __fmul_rn(c.sqc, __fmaf_rn(c.zp, gld(f.u + i), __fmul_rn(c.zq, gld(f.x + i)))));
 }
 
 __global__ void sm_reset_kernel(const FactorDesc* __restrict__ factors, int32_t nfactors, int ranked_only) {

@@ -156,7 +156,8 @@ def test_guard_nonfinite():
     assert H.get_stats(layers[0])["skip_L"] == 1
 
 
-def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0, sync_every=False, gemm_path=None):
+def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0, sync_every=False, gemm_path=None,
+               sync_at=None):
     if layers is None:
         layers = H.allocate_layers(shapes, dt, gemm_path=gemm_path)
     plan = H.make_plan(layers)
@@ -166,7 +167,7 @@ def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0, sync_every=
             a, g, G = _random_inputs(seed + 1000 * t + i, L["d_in"], L["d_out"], dt)
             H.set_inputs(L, a, g, G)
         plan.step(p)
-        if sync_every:
+        if sync_every or t + 1 == sync_at:
             plan.sync_factors()
     plan.sync_factors()
     torch.cuda.synchronize()
@@ -180,23 +181,33 @@ def test_determinism_and_checkpoint_resume():
     for x, y in zip(A, B):
         for k in ("Linv", "Rinv", "dW"):
             assert torch.equal(x[k], y[k]), k
-    # 5 steps, save the state, fresh buffers and plan, 5 more steps
+    # 5 steps, save the state (a sync: the buffers then hold the factors and
+    # nothing is pending), fresh buffers and plan, 5 more steps: the same bits
+    # as syncing after step 5 and going on in the same plan.  Without that
+    # sync the factors are the same bits too; dW, whose split-path epilogue
+    # applies one or two pending terms algebraically, differs by rounding.
     C = _run_steps(shapes, 5, seed=7)
     saved = [(H.get_factors(L)) for L in C]
     D = H.allocate_layers(shapes, "bf16")
     for L, (Li, Ri) in zip(D, saved):
         H.set_factors(L, Li, Ri)
     D = _run_steps(shapes, 5, seed=7, layers=D, start=5)
-    for x, y in zip(A, D):
+    E = _run_steps(shapes, 10, seed=7, sync_at=5)
+    for x, y, z in zip(A, D, E):
         for k in ("Linv", "Rinv", "dW"):
+            assert torch.equal(z[k], y[k]), k
+        for k in ("Linv", "Rinv"):
             assert torch.equal(x[k], y[k]), k
+        assert rel(x["dW"].cpu().numpy(), y["dW"].cpu().numpy()) <= 1e-6
 
 
 def test_pending_term_matches_write_back_every_step():
     """Keeping each update pending (applied in the fp32 GEMM's loads and
     written by the next pass) gives the same bits as writing it back after
     every step.  On the split path the pending term enters the epilogue
-    algebraically: the factors still agree bit for bit, dW to rounding."""
+    algebraically, and the first GEMM's factor carries two terms every other
+    step (the pass writes it back only then, evaluating them one after the
+    other): the factors still agree bit for bit, dW to rounding."""
     shapes = [(128, 256), (37, 100), (256, 128), (64, 64)]
     A = _run_steps(shapes, 8, seed=11, dt="fp32", gemm_path="fp32")
     B = _run_steps(shapes, 8, seed=11, dt="fp32", sync_every=True, gemm_path="fp32")
