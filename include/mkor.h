@@ -47,8 +47,14 @@
  * the new pending term; the preconditioning applies that term while it loads
  * the factor, so it multiplies with the updated factor.  Results are the same
  * values a write-back after every update would give (element for element the
- * same roundings).  Consequently, after mkor_step or mkor_update_factors the
- * buffers Linv and Rinv hold the factors as of the previous update;
+ * same roundings).  The factor of a split-path layer's first GEMM (Rinv, or
+ * Linv when G is bf16 and d_in > d_out) is written only every other step: the
+ * step in between leaves it in S with two pending terms, evaluated one after
+ * the other with the same roundings, so the factor values are unchanged; the
+ * preconditioning applies both algebraically, so dW matches a write-back
+ * after every step to rounding, and bit for bit after mkor_sync_factors.
+ * Consequently, after mkor_step or mkor_update_factors the buffers Linv and
+ * Rinv hold the factors as of the previous update or the one before;
  * mkor_sync_factors writes the current factors into them.  Call it before
  * reading, saving or modifying Linv / Rinv, and before mkor_plan_destroy if
  * the factors are to be kept.  A new plan starts with no pending term.
