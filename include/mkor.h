@@ -120,7 +120,8 @@ extern "C" {
 
 /* kernels of one step, in launch order (mkor_run_stage) */
 #define MKOR_STAGE_MEANS      0   /* a, g = row means of A, Gout (layers with rows > 0) */
-#define MKOR_STAGE_SM_PASS    1   /* write pending term into S; u_raw = P x, norm and s partials */
+#define MKOR_STAGE_SM_PASS    1   /* write pending term(s) into S (a lazy factor's: every other
+                                     step); u_raw = P x, norm and s partials */
 #define MKOR_STAGE_SM_FINALIZE 2  /* stabiliser decision, new pending rank-1 term */
 #define MKOR_STAGE_GEMM_PREP  3   /* operands of the bf16 MFMA paths: bf16 copy of an fp32 G
                                      (bf16 factors), G^T (split path, bf16 G, d_in > d_out),
