@@ -156,6 +156,30 @@ def test_guard_nonfinite():
     assert H.get_stats(layers[0])["skip_L"] == 1
 
 
+def test_guard_nonfinite_keeps_lazy_pending_term():
+    """The split path writes the first GEMM's factor (Rinv here) back only
+    every other step; an update skipped while the previous one is still
+    pending keeps that one: after a good step and a skipped one the factor is
+    the good step's."""
+    layers, host = _setup([(64, 64)], "fp32", seed=410)
+    Li, Ri, a, g, G = host[0]
+    plan = H.make_plan(layers)
+    p = Params(eps=math.inf, guard_nonfinite=True)
+    plan.step(p)
+    g_bad = g.copy()
+    g_bad[5] = np.nan
+    H.set_inputs(layers[0], g=g_bad)
+    plan.step(p)
+    torch.cuda.synchronize()
+    s = H.get_stats(layers[0])
+    assert s["skip_R"] == 1 and s["skip_L"] == 0
+    assert np.isfinite(H.get_dW(layers[0])).all()
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    Ro, _ = O.update_factor(Ri, g, oparams(p))
+    assert rel(H.get_factors(layers[0])[1], Ro) <= TOL_STEP
+
+
 def _run_steps(shapes, steps, seed, dt="bf16", layers=None, start=0, sync_every=False, gemm_path=None,
                sync_at=None):
     if layers is None:
