@@ -156,6 +156,39 @@ def test_guard_nonfinite():
     assert H.get_stats(layers[0])["skip_L"] == 1
 
 
+def test_stages_in_order_equal_step():
+    """Launching the stages one by one (mkor_run_stage 0 .. NUM_STAGES - 1, as
+    bench.py does for per-kernel times) is mkor_step: the same bits, over
+    several steps, on the split, fp32 MFMA and first-order paths."""
+    from paper_2306_01685_amd import NUM_STAGES
+    shapes = [(128, 256), (256, 128), (37, 100), (64, 64)]
+    second = [1, 1, 1, 0]
+    A, _ = _setup(shapes, "bf16", seed=500, second_order=second)
+    B, _ = _setup(shapes, "bf16", seed=500, second_order=second)
+    pa, pb = H.make_plan(A), H.make_plan(B)
+    p = Params(eps=3.0)
+    for t in range(5):
+        for i, (LA, LB) in enumerate(zip(A, B)):
+            a, g, G = _random_inputs(900 + 10 * t + i, LA["d_in"], LA["d_out"], "bf16")
+            for L in (LA, LB):
+                if L["second_order"]:
+                    H.set_inputs(L, a, g, G)
+                else:
+                    H.set_inputs(L, G=G)
+        pa.step(p)
+        for st in range(NUM_STAGES):
+            pb.run_stage(p, st)
+        torch.cuda.synchronize()
+        for x, y in zip(A, B):
+            assert torch.equal(x["dW"], y["dW"]), t
+    pa.sync_factors()
+    pb.sync_factors()
+    torch.cuda.synchronize()
+    for x, y in zip(A, B):
+        if x["second_order"]:
+            assert torch.equal(x["Linv"], y["Linv"]) and torch.equal(x["Rinv"], y["Rinv"])
+
+
 def test_guard_nonfinite_keeps_lazy_pending_term():
     """The split path writes the first GEMM's factor (Rinv here) back only
     every other step; an update skipped while the previous one is still
