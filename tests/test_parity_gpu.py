@@ -189,6 +189,33 @@ def test_stages_in_order_equal_step():
             assert torch.equal(x["Linv"], y["Linv"]) and torch.equal(x["Rinv"], y["Rinv"])
 
 
+def test_lazy_write_back_cadence():
+    """On the split path Rinv (the first GEMM's factor here) is written back
+    every other step and Linv every step: after two steps the Rinv buffer
+    still holds the initial factor and the Linv buffer P_1; after three, Rinv
+    holds P_2 (both pending terms, evaluated in order) and Linv P_2."""
+    layers, host = _setup([(128, 192)], "fp32", seed=420)
+    Li, Ri, a, g, G = host[0]
+    L = layers[0]
+    plan = H.make_plan(layers)
+    p = Params(eps=math.inf)
+    op = oparams(p)
+    L1, _ = O.update_factor(Li, a, op)
+    R1, _ = O.update_factor(Ri, g, op)
+    L2, _ = O.update_factor(L1, a, op)
+    R2, _ = O.update_factor(R1, g, op)
+    plan.step(p)
+    plan.step(p)
+    torch.cuda.synchronize()
+    Lg, Rg = H.get_factors(L)
+    np.testing.assert_array_equal(Rg, Ri.astype(np.float32))
+    assert rel(Lg, L1) <= TOL_STEP
+    plan.step(p)
+    torch.cuda.synchronize()
+    Lg, Rg = H.get_factors(L)
+    assert rel(Lg, L2) <= TOL_STEP and rel(Rg, R2) <= TOL_STEP
+
+
 def test_guard_nonfinite_keeps_lazy_pending_term():
     """The split path writes the first GEMM's factor (Rinv here) back only
     every other step; an update skipped while the previous one is still
