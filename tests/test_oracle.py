@@ -364,3 +364,57 @@ def test_layer_step_rows_uses_row_means():
     np.testing.assert_allclose(dW, dWj, rtol=1e-12)
     with pytest.raises(ValueError):
         O.rank1_means(np.zeros((0, 3)))
+
+
+# ---------------------------------------------------------------- the grouped step
+
+def test_oracle_step_grouped_against_brute_force():
+    """oracle_step over a list (Algorithm 1, "for each layer"): a mixed
+    second_order list, a stabiliser override on one factor of one layer, and
+    the update / precondition halves run separately, each layer checked
+    against the explicit inverse of its explicitly accumulated factors (and a
+    first-order layer against its gradient), over two steps."""
+    rng = np.random.default_rng(2306)
+    gamma, zeta = 0.9, 0.5
+    p = O.Params(gamma=gamma, zeta=zeta, eps=math.inf)
+    shapes = [(5, 3), (4, 6), (3, 7)]
+    so = [True, False, True]
+    layers = []
+    M = []   # explicit factors (inverses of the inverse factors)
+    for (i, o), s in zip(shapes, so):
+        P0L, P0R = np.eye(i), np.linalg.inv(_spd(rng, o, 0.5))
+        layers.append(dict(Linv=P0L, Rinv=P0R, second_order=s))
+        M.append([np.linalg.inv(P0L), np.linalg.inv(P0R)])
+    for step in range(2):
+        for L, (i, o) in zip(layers, shapes):
+            L["a"], L["g"] = rng.standard_normal(i), rng.standard_normal(o) * 0.3
+            L["G"] = rng.standard_normal((i, o))
+        # only layer 2's right factor is blended on step 0
+        ov = [(None, None), (None, None), (None, step == 0)]
+        half = O.oracle_step(layers, p, update=True, precond=False, stab_overrides=ov)
+        mid = [dict(L, Linv=h["Linv"], Rinv=h["Rinv"]) for L, h in zip(layers, half)]
+        pre = O.oracle_step(mid, p, update=False, precond=True)
+        full = O.oracle_step(layers, p, stab_overrides=ov)
+        for k, ((i, o), L) in enumerate(zip(shapes, layers)):
+            assert half[k]["dW"] is None
+            np.testing.assert_array_equal(pre[k]["dW"], full[k]["dW"])
+            if not so[k]:
+                np.testing.assert_array_equal(full[k]["dW"], L["G"])
+                np.testing.assert_array_equal(full[k]["Linv"], L["Linv"])
+                np.testing.assert_array_equal(full[k]["Rinv"], L["Rinv"])
+                continue
+            new = []
+            for side, x in ((0, L["a"]), (1, L["g"])):
+                Mh = M[k][side]
+                if ov[k][side]:
+                    Mh = np.linalg.inv(zeta * np.linalg.inv(Mh) + (1 - zeta) * np.eye(len(x)))
+                M[k][side] = gamma * Mh + (1 - gamma) * np.outer(x, x)
+                new.append(np.linalg.inv(M[k][side]))
+            assert full[k]["stats"].R.stab == bool(ov[k][1])
+            np.testing.assert_allclose(full[k]["Linv"], new[0], rtol=0, atol=1e-12)
+            np.testing.assert_allclose(full[k]["Rinv"], new[1], rtol=0, atol=1e-12)
+            dW_hat = new[0] @ L["G"] @ new[1]
+            ref = np.linalg.norm(L["G"]) / np.linalg.norm(dW_hat) * dW_hat
+            np.testing.assert_allclose(full[k]["dW"], ref, rtol=0, atol=1e-12)
+        for L, f in zip(layers, full):
+            L["Linv"], L["Rinv"] = f["Linv"], f["Rinv"]
