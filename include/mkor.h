@@ -99,7 +99,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 8
+#define MKOR_ABI_VERSION 9
 
 /* status codes */
 #define MKOR_OK                   0
@@ -147,6 +147,8 @@ extern "C" {
 #define MKOR_MAX_DIM       32768
 #define MKOR_MAX_ROWS      (1 << 26)
 #define MKOR_MAX_RANK      4
+/* device workspace bytes mkor_step_noalloc can use (one array per GPU) */
+#define MKOR_NOALLOC_MAX_BYTES (64u << 20)
 
 typedef struct mkor_params {
     float   gamma;            /* momentum of Eq. 4/5, 0 < gamma < 1 */
@@ -319,6 +321,29 @@ int mkor_step_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_par
  * factor updates of an update-every-f schedule). */
 int mkor_precondition_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt,
                           void* stream);
+
+/* One full step for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * The same as creating a plan over layers[0..n) (a fresh one: no pending
+ * term), mkor_step, mkor_sync_factors and mkor_plan_destroy, with the same
+ * kernels and results, but with no workspace argument: the workspace lives in
+ * a device array of MKOR_NOALLOC_MAX_BYTES that the library holds on each GPU
+ * it runs on until the process ends.  The call allocates no device or pinned
+ * memory.
+ *   - Factors: Linv / Rinv are read, updated and written back within the
+ *     call; afterwards they hold the updated factors (nothing is pending).
+ *   - Size: a layer list whose mkor_workspace_size exceeds
+ *     MKOR_NOALLOC_MAX_BYTES is rejected with MKOR_WORKSPACE_TOO_SMALL
+ *     before any device work; use a plan for it.
+ *   - Device and stream: the array of the current device (hipGetDevice) is
+ *     used; `stream` must belong to that device.  The descriptor tables reach
+ *     the array through small stream-ordered kernel launches (1 KiB each).
+ *   - Concurrency: every call on one GPU shares that GPU's array and leaves
+ *     it holding its own tables and partials.  Calls whose executions overlap
+ *     on one GPU (other streams, other host threads) race and give undefined
+ *     results: order them on one stream or with events.
+ * Validation and errors as for mkor_plan_create and mkor_step. */
+int mkor_step_noalloc(const mkor_layer* layers, int32_t n, const mkor_params* params, void* stream);
 
 /* Frees the host-side plan (NULL is allowed).  The workspace stays the
  * caller's. */

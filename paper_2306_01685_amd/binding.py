@@ -35,7 +35,8 @@ DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
 MAX_RANK = 4
-ABI_VERSION = 8
+ABI_VERSION = 9
+NOALLOC_MAX_BYTES = 64 << 20
 GEMM_AUTO = 0
 GEMM_FP32 = 1
 GEMM_SPLIT = 2
@@ -85,7 +86,8 @@ STATS_FIELDS = [f for f, _ in mkor_layer_stats._fields_]
 EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_params_check",
             "mkor_workspace_size", "mkor_plan_create", "mkor_update_factors",
             "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_sync_factors",
-            "mkor_opt_params_check", "mkor_step_opt", "mkor_precondition_opt", "mkor_plan_destroy"]
+            "mkor_opt_params_check", "mkor_step_opt", "mkor_precondition_opt", "mkor_step_noalloc",
+            "mkor_plan_destroy"]
 
 STAGE_MEANS, STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(6)
 NUM_STAGES = 7
@@ -137,6 +139,8 @@ def load_library(path: str = LIB_PATH):
         fn = getattr(lib, name)
         fn.restype = ctypes.c_int
         fn.argtypes = [P, ctypes.POINTER(mkor_params), ctypes.POINTER(mkor_opt_params), P]
+    lib.mkor_step_noalloc.restype = ctypes.c_int
+    lib.mkor_step_noalloc.argtypes = [ctypes.POINTER(mkor_layer), I32, ctypes.POINTER(mkor_params), P]
     lib.mkor_plan_destroy.restype = None
     lib.mkor_plan_destroy.argtypes = [P]
     if lib.mkor_abi_version() != ABI_VERSION:
@@ -233,6 +237,48 @@ def _stream_handle(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def layer_descs(layers):
+    """mkor_layer field values (raw device pointers) of a list of layer dicts
+    holding torch tensors (see MkorPlan)."""
+    descs = []
+    for L in layers:
+        so = int(bool(L.get("second_order", True)))
+        G = L["G"]
+        if G.dtype == torch.bfloat16:
+            gdt = DTYPE_BF16
+        elif G.dtype == torch.float32:
+            gdt = DTYPE_F32
+        else:
+            raise TypeError(f"unsupported gradient dtype {G.dtype}")
+        for k in ("Linv", "Rinv", "a", "g", "G", "dW", "A", "Gout", "W", "opt_m", "opt_v"):
+            t = L.get(k)
+            if t is not None and not t.is_contiguous():
+                raise ValueError(f"{k} must be contiguous")
+        fdt = DTYPE_F32
+        if so:
+            dts = {L["Linv"].dtype, L["Rinv"].dtype}
+            if dts == {torch.bfloat16}:
+                fdt = DTYPE_BF16
+            elif dts != {torch.float32}:
+                raise TypeError("Linv and Rinv must both be fp32 or both bf16")
+        A = L.get("A")
+        rows, adt = 0, DTYPE_F32
+        if A is not None:
+            rows = int(A.shape[0])
+            adt = DTYPE_BF16 if A.dtype == torch.bfloat16 else DTYPE_F32
+            if A.dtype not in (torch.bfloat16, torch.float32) or L["Gout"].dtype != A.dtype:
+                raise TypeError("A and Gout must both be fp32 or both bf16")
+        descs.append(dict(d_in=int(L["d_in"]), d_out=int(L["d_out"]), second_order=so,
+                          grad_dtype=gdt, Linv=_ptr(L.get("Linv")), Rinv=_ptr(L.get("Rinv")),
+                          a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
+                          stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
+                          Gout=_ptr(L.get("Gout")), factor_dtype=fdt,
+                          rank=int(L["a"].shape[0]) if so and L["a"].dim() == 2 else 0,
+                          W=_ptr(L.get("W")), opt_m=_ptr(L.get("opt_m")), opt_v=_ptr(L.get("opt_v")),
+                          gemm_path=GEMM_PATHS[L.get("gemm_path", "auto")]))
+    return descs
+
+
 class MkorPlan:
     """A plan over a grouped list of layers, holding torch device tensors.
 
@@ -256,42 +302,7 @@ class MkorPlan:
     def __init__(self, layers, device=None):
         self._lib = load_library()
         self.layers = layers
-        descs = []
-        for L in layers:
-            so = int(bool(L.get("second_order", True)))
-            G = L["G"]
-            if G.dtype == torch.bfloat16:
-                gdt = DTYPE_BF16
-            elif G.dtype == torch.float32:
-                gdt = DTYPE_F32
-            else:
-                raise TypeError(f"unsupported gradient dtype {G.dtype}")
-            for k in ("Linv", "Rinv", "a", "g", "G", "dW", "A", "Gout", "W", "opt_m", "opt_v"):
-                t = L.get(k)
-                if t is not None and not t.is_contiguous():
-                    raise ValueError(f"{k} must be contiguous")
-            fdt = DTYPE_F32
-            if so:
-                dts = {L["Linv"].dtype, L["Rinv"].dtype}
-                if dts == {torch.bfloat16}:
-                    fdt = DTYPE_BF16
-                elif dts != {torch.float32}:
-                    raise TypeError("Linv and Rinv must both be fp32 or both bf16")
-            A = L.get("A")
-            rows, adt = 0, DTYPE_F32
-            if A is not None:
-                rows = int(A.shape[0])
-                adt = DTYPE_BF16 if A.dtype == torch.bfloat16 else DTYPE_F32
-                if A.dtype not in (torch.bfloat16, torch.float32) or L["Gout"].dtype != A.dtype:
-                    raise TypeError("A and Gout must both be fp32 or both bf16")
-            descs.append(dict(d_in=int(L["d_in"]), d_out=int(L["d_out"]), second_order=so,
-                              grad_dtype=gdt, Linv=_ptr(L.get("Linv")), Rinv=_ptr(L.get("Rinv")),
-                              a=_ptr(L.get("a")), g=_ptr(L.get("g")), G=_ptr(G), dW=_ptr(L["dW"]),
-                              stats=_ptr(L.get("stats")), rows=rows, act_dtype=adt, A=_ptr(A),
-                              Gout=_ptr(L.get("Gout")), factor_dtype=fdt,
-                              rank=int(L["a"].shape[0]) if so and L["a"].dim() == 2 else 0,
-                              W=_ptr(L.get("W")), opt_m=_ptr(L.get("opt_m")), opt_v=_ptr(L.get("opt_v")),
-                              gemm_path=GEMM_PATHS[L.get("gemm_path", "auto")]))
+        descs = layer_descs(layers)
         self._arr = make_layer_array(descs)
         n = len(descs)
         size = ctypes.c_size_t(0)
@@ -352,6 +363,17 @@ class MkorPlan:
             self.close()
         except Exception:
             pass
+
+
+def step_noalloc(layers, params: Params, stream=None):
+    """One full step over `layers` (dicts of torch tensors, as for MkorPlan)
+    through mkor_step_noalloc: no workspace, no device allocation; the
+    factors are updated in place."""
+    descs = layer_descs(layers)
+    arr = make_layer_array(descs)
+    p = params.to_c() if isinstance(params, Params) else params
+    _check(load_library().mkor_step_noalloc(arr, len(descs), ctypes.byref(p), _stream_handle(stream)),
+           "mkor_step_noalloc")
 
 
 def read_stats(stats_tensor) -> dict:

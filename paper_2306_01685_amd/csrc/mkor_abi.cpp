@@ -2,7 +2,7 @@
 //
 // All validation runs on the host before the first HIP call of an entry
 // point, so every error path can be exercised without a GPU.
-#include "mkor_internal.h"
+#include "plan.h"
 
 #include <algorithm>
 #include <cmath>
@@ -16,8 +16,10 @@
 using namespace mkor;
 
 namespace {
-
 thread_local char g_err[512] = "";
+}  // namespace
+
+namespace mkor {
 
 int fail(int status, const char* fmt, ...) {
     va_list ap;
@@ -30,6 +32,10 @@ int fail(int status, const char* fmt, ...) {
 int hip_fail(hipError_t e, const char* what) {
     return fail(MKOR_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
 }
+
+void clear_error() { g_err[0] = 0; }
+
+namespace {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -44,6 +50,8 @@ struct Interval {
 
 // vectors per factor update: rank 0 means 1; first-order layers have none
 int32_t layer_rank(const mkor_layer& L) { return L.second_order == 1 ? std::max(1, L.rank) : 1; }
+
+}  // namespace
 
 int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_bytes) {
     if (n < 0) return fail(MKOR_INVALID_ARG, "n = %d is negative", n);
@@ -139,36 +147,9 @@ int check_layers(const mkor_layer* layers, int32_t n, const void* ws, size_t ws_
     return MKOR_OK;
 }
 
+namespace {
+
 // ------------------------------------------------------------------ layout
-struct Layout {
-    size_t off_factors = 0, off_rowblocks = 0, off_pend = 0, off_smpart = 0;
-    size_t off_g1l = 0, off_g1t = 0, off_g2l = 0, off_g2t = 0, off_gpart = 0, off_dpart = 0;
-    size_t off_rsl = 0, off_rsb = 0, off_x = 0;
-    size_t off_mmat = 0, off_mitem = 0, off_mchunk = 0, off_mpart = 0;
-    size_t off_h1l = 0, off_h1t = 0, off_h2l = 0, off_h2t = 0;   // bf16-factor GEMMs
-    size_t off_s1l = 0, off_s1t = 0, off_s2l = 0, off_s2t = 0;   // fp32 factors on the bf16 split
-    size_t off_cvti = 0, off_cvtb = 0;                           // fp32 -> bf16 gradient copies
-    size_t off_tri = 0, off_trb = 0;                             // G^T of swapped split layers
-    size_t off_qdb = 0;                                          // stage-1 (Q w) row blocks (split)
-    size_t off_gram = 0;                                         // rank-r Gram partials
-    size_t off_lpart = 0, off_trust = 0;                         // LAMB block sums, per-layer ratios
-    size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
-    size_t total = 0;
-    int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;
-    int32_t nh1 = 0, nh2 = 0;
-    int32_t ns1 = 0, ns2 = 0;
-    int32_t ncvt = 0, ncvtblk = 0;
-    int32_t ntr = 0, ntrblk = 0;
-    int32_t nqdb = 0;
-    int32_t nsecond = 0;
-    int32_t nranked = 0;      // second-order layers with rank > 1
-    int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
-    int64_t nmeanpart = 0;   // doubles
-    std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
-    std::vector<size_t> gh_off;                // per layer: bf16 copy of an fp32 G (bf16 factors)
-    std::vector<size_t> gt_off;                // per layer: G^T (bf16) of swapped split layers
-    std::vector<size_t> rq_off;                // per layer: stage-1 (Q w) of split layers
-};
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
@@ -298,6 +279,8 @@ int64_t dpart_count(const mkor_layer& L) {
 
 // bf16-factor layer whose gradient is fp32: the GEMMs read a bf16 copy
 bool needs_cvt(const mkor_layer& L) { return is_half(L) && L.grad_dtype == MKOR_DTYPE_F32; }
+
+}  // namespace
 
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     int64_t rowblocks = 0, g1 = 0, gpart = 0, rsb = 0, usum = 0, ncvt = 0, ncvtblk = 0, ntr = 0, ntrblk = 0;
@@ -451,72 +434,11 @@ int check_params(const mkor_params* p) {
     return MKOR_OK;
 }
 
-}  // namespace
 
-struct mkor_plan {
-    int32_t n = 0;
-    char* ws = nullptr;
-    Layout lo;
-    std::vector<uint8_t> optbuf;   // per layer: 1 W, 2 opt_m, 4 opt_v
-};
-
-extern "C" {
-
-int mkor_abi_version(void) { return MKOR_ABI_VERSION; }
-
-const char* mkor_status_string(int status) {
-    switch (status) {
-        case MKOR_OK: return "MKOR_OK";
-        case MKOR_INVALID_ARG: return "MKOR_INVALID_ARG";
-        case MKOR_WORKSPACE_TOO_SMALL: return "MKOR_WORKSPACE_TOO_SMALL";
-        case MKOR_UNSUPPORTED: return "MKOR_UNSUPPORTED";
-        case MKOR_HIP_ERROR: return "MKOR_HIP_ERROR";
-        default: return "MKOR_UNKNOWN_STATUS";
-    }
-}
-
-const char* mkor_last_error(void) { return g_err; }
-
-int mkor_params_check(const mkor_params* params) {
-    g_err[0] = 0;
-    return check_params(params);
-}
-
-int mkor_workspace_size(const mkor_layer* layers, int32_t n, size_t* bytes) {
-    g_err[0] = 0;
-    if (bytes == nullptr) return fail(MKOR_INVALID_ARG, "bytes is NULL");
-    int st = check_layers(layers, n, nullptr, 0);
-    if (st != MKOR_OK) return st;
-    Layout lo;
-    st = compute_layout(layers, n, lo);
-    if (st != MKOR_OK) return st;
-    *bytes = lo.total;
-    return MKOR_OK;
-}
-
-int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, size_t ws_bytes,
-                     mkor_plan** out) {
-    g_err[0] = 0;
-    if (out == nullptr) return fail(MKOR_INVALID_ARG, "out is NULL");
-    *out = nullptr;
-    int st = check_layers(layers, n, nullptr, 0);
-    if (st != MKOR_OK) return st;
-    Layout lo;
-    st = compute_layout(layers, n, lo);
-    if (st != MKOR_OK) return st;
-    if (lo.total > 0) {
-        if (d_workspace == nullptr) return fail(MKOR_INVALID_ARG, "workspace is NULL");
-        if (!aligned(d_workspace, 256)) return fail(MKOR_INVALID_ARG, "workspace is not 256-byte aligned");
-        if (ws_bytes < lo.total)
-            return fail(MKOR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, the plan needs %zu", ws_bytes,
-                        lo.total);
-        st = check_layers(layers, n, d_workspace, lo.total);
-        if (st != MKOR_OK) return st;
-    }
-
-    // ---- host-side descriptor tables
-    char* base = static_cast<char*>(d_workspace);
-    std::vector<char> host(lo.table_bytes, 0);
+// Descriptor tables of a plan whose workspace starts at device address
+// `base`: the bytes [0, lo.table_bytes) of that workspace, built on the host.
+void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout& lo, std::vector<char>& host) {
+    host.assign(lo.table_bytes, 0);
     FactorDesc* fd = reinterpret_cast<FactorDesc*>(host.data() + lo.off_factors);
     RowBlock* rb = reinterpret_cast<RowBlock*>(host.data() + lo.off_rowblocks);
     GemmLayer* g1l = reinterpret_cast<GemmLayer*>(host.data() + lo.off_g1l);
@@ -726,28 +648,11 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     std::copy(v1.begin(), v1.end(), s1t);
     std::copy(v2.begin(), v2.end(), s2t);
 
-    mkor_plan* plan = new (std::nothrow) mkor_plan;
-    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "out of host memory");
-    plan->n = n;
-    plan->ws = base;
-    plan->lo = lo;
-    plan->optbuf.resize(n);
-    for (int32_t i = 0; i < n; ++i)
-        plan->optbuf[i] = (uint8_t)((layers[i].W ? 1 : 0) | (layers[i].opt_m ? 2 : 0) | (layers[i].opt_v ? 4 : 0));
-    if (lo.table_bytes > 0) {
-        hipError_t e = hipMemcpy(base, host.data(), lo.table_bytes, hipMemcpyHostToDevice);
-        if (e != hipSuccess) {
-            delete plan;
-            return hip_fail(e, "uploading plan descriptors");
-        }
-    }
-    *out = plan;
-    return MKOR_OK;
 }
 
-static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStream_t s) {
-    const Layout& lo = p->lo;
-    char* ws = p->ws;
+int run_stage(const WsView& v, const mkor_params* prm, int32_t stage, hipStream_t s) {
+    const Layout& lo = *v.lo;
+    char* ws = v.ws;
     const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(ws + lo.off_factors);
     const RowBlock* rb = reinterpret_cast<const RowBlock*>(ws + lo.off_rowblocks);
     float4* smpart = reinterpret_cast<float4*>(ws + lo.off_smpart);
@@ -821,23 +726,133 @@ static int run_stage(mkor_plan* p, const mkor_params* prm, int32_t stage, hipStr
     }
 }
 
-static int run_range(mkor_plan* p, const mkor_params* prm, int32_t first, int32_t last, hipStream_t s) {
-    if (p->n == 0) return MKOR_OK;
+int run_range(const WsView& v, const mkor_params* prm, int32_t first, int32_t last, hipStream_t s) {
+    if (v.n == 0) return MKOR_OK;
     for (int32_t st = first; st <= last; ++st) {
-        const int r = run_stage(p, prm, st, s);
+        const int r = run_stage(v, prm, st, s);
         if (r != MKOR_OK) return r;
     }
     return MKOR_OK;
 }
 
-// Parameters valid, and valid for this plan: rank-r layers exist for the
-// EXACT variant only.
-static int check_plan_params(const mkor_plan* plan, const mkor_params* params) {
+// Writes every pending term into its factor buffer and clears the terms.
+int sync_factors(const WsView& v, hipStream_t s) {
+    const Layout& lo = *v.lo;
+    if (v.n == 0 || lo.nfactors == 0) return MKOR_OK;
+    const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(v.ws + lo.off_factors);
+    const RowBlock* rb = reinterpret_cast<const RowBlock*>(v.ws + lo.off_rowblocks);
+    float4* smpart = reinterpret_cast<float4*>(v.ws + lo.off_smpart);
+    hipError_t e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, nullptr, MKOR_NORM_INF, 0, lo.nranked > 0, s);
+    if (e != hipSuccess) return hip_fail(e, "sm_pass launch");
+    e = launch_sm_reset(fd, lo.nfactors, s);
+    if (e != hipSuccess) return hip_fail(e, "sm_reset launch");
+    return MKOR_OK;
+}
+
+// Parameters valid, and valid for a layer list with `nranked` rank-r layers:
+// those exist for the EXACT variant only.
+int check_run_params(const mkor_params* params, int32_t nranked) {
     const int st = check_params(params);
     if (st != MKOR_OK) return st;
-    if (plan->lo.nranked > 0 && params->sm_variant != MKOR_SM_EXACT)
+    if (nranked > 0 && params->sm_variant != MKOR_SM_EXACT)
         return fail(MKOR_UNSUPPORTED, "rank-r layers need sm_variant = MKOR_SM_EXACT");
     return MKOR_OK;
+}
+
+}  // namespace mkor
+
+struct mkor_plan {
+    int32_t n = 0;
+    char* ws = nullptr;
+    Layout lo;
+    std::vector<uint8_t> optbuf;   // per layer: 1 W, 2 opt_m, 4 opt_v
+};
+
+extern "C" {
+
+int mkor_abi_version(void) { return MKOR_ABI_VERSION; }
+
+const char* mkor_status_string(int status) {
+    switch (status) {
+        case MKOR_OK: return "MKOR_OK";
+        case MKOR_INVALID_ARG: return "MKOR_INVALID_ARG";
+        case MKOR_WORKSPACE_TOO_SMALL: return "MKOR_WORKSPACE_TOO_SMALL";
+        case MKOR_UNSUPPORTED: return "MKOR_UNSUPPORTED";
+        case MKOR_HIP_ERROR: return "MKOR_HIP_ERROR";
+        default: return "MKOR_UNKNOWN_STATUS";
+    }
+}
+
+const char* mkor_last_error(void) { return g_err; }
+
+int mkor_params_check(const mkor_params* params) {
+    g_err[0] = 0;
+    return check_params(params);
+}
+
+int mkor_workspace_size(const mkor_layer* layers, int32_t n, size_t* bytes) {
+    g_err[0] = 0;
+    if (bytes == nullptr) return fail(MKOR_INVALID_ARG, "bytes is NULL");
+    int st = check_layers(layers, n, nullptr, 0);
+    if (st != MKOR_OK) return st;
+    Layout lo;
+    st = compute_layout(layers, n, lo);
+    if (st != MKOR_OK) return st;
+    *bytes = lo.total;
+    return MKOR_OK;
+}
+
+int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, size_t ws_bytes,
+                     mkor_plan** out) {
+    g_err[0] = 0;
+    if (out == nullptr) return fail(MKOR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    int st = check_layers(layers, n, nullptr, 0);
+    if (st != MKOR_OK) return st;
+    Layout lo;
+    st = compute_layout(layers, n, lo);
+    if (st != MKOR_OK) return st;
+    if (lo.total > 0) {
+        if (d_workspace == nullptr) return fail(MKOR_INVALID_ARG, "workspace is NULL");
+        if (!aligned(d_workspace, 256)) return fail(MKOR_INVALID_ARG, "workspace is not 256-byte aligned");
+        if (ws_bytes < lo.total)
+            return fail(MKOR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, the plan needs %zu", ws_bytes,
+                        lo.total);
+        st = check_layers(layers, n, d_workspace, lo.total);
+        if (st != MKOR_OK) return st;
+    }
+
+    std::vector<char> host;
+    build_tables(layers, n, static_cast<char*>(d_workspace), lo, host);
+    char* base = static_cast<char*>(d_workspace);
+
+    mkor_plan* plan = new (std::nothrow) mkor_plan;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "out of host memory");
+    plan->n = n;
+    plan->ws = base;
+    plan->lo = lo;
+    plan->optbuf.resize(n);
+    for (int32_t i = 0; i < n; ++i)
+        plan->optbuf[i] = (uint8_t)((layers[i].W ? 1 : 0) | (layers[i].opt_m ? 2 : 0) | (layers[i].opt_v ? 4 : 0));
+    if (lo.table_bytes > 0) {
+        hipError_t e = hipMemcpy(base, host.data(), lo.table_bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            delete plan;
+            return hip_fail(e, "uploading plan descriptors");
+        }
+    }
+    *out = plan;
+    return MKOR_OK;
+}
+
+static WsView view(const mkor_plan* p) { return WsView{p->ws, &p->lo, p->n}; }
+
+static int check_plan_params(const mkor_plan* plan, const mkor_params* params) {
+    return check_run_params(params, plan->lo.nranked);
+}
+
+static int run_range(mkor_plan* p, const mkor_params* prm, int32_t first, int32_t last, hipStream_t s) {
+    return run_range(view(p), prm, first, last, s);
 }
 
 static int check_opt(const mkor_opt_params* o) {
@@ -960,23 +975,13 @@ int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, vo
     if (st != MKOR_OK) return st;
     if (stage < 0 || stage >= MKOR_NUM_STAGES) return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
     if (plan->n == 0) return MKOR_OK;
-    return run_stage(plan, params, stage, static_cast<hipStream_t>(stream));
+    return run_stage(view(plan), params, stage, static_cast<hipStream_t>(stream));
 }
 
 int mkor_sync_factors(mkor_plan* plan, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
-    const Layout& lo = plan->lo;
-    if (plan->n == 0 || lo.nfactors == 0) return MKOR_OK;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const FactorDesc* fd = reinterpret_cast<const FactorDesc*>(plan->ws + lo.off_factors);
-    const RowBlock* rb = reinterpret_cast<const RowBlock*>(plan->ws + lo.off_rowblocks);
-    float4* smpart = reinterpret_cast<float4*>(plan->ws + lo.off_smpart);
-    hipError_t e = launch_sm_pass(fd, rb, lo.nrowblocks, smpart, nullptr, MKOR_NORM_INF, 0, lo.nranked > 0, s);
-    if (e != hipSuccess) return hip_fail(e, "sm_pass launch");
-    e = launch_sm_reset(fd, lo.nfactors, s);
-    if (e != hipSuccess) return hip_fail(e, "sm_reset launch");
-    return MKOR_OK;
+    return sync_factors(view(plan), static_cast<hipStream_t>(stream));
 }
 
 void mkor_plan_destroy(mkor_plan* plan) { delete plan; }

@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(M.EXPORTED), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.mkor_abi_version() == 8
+    assert lib.mkor_abi_version() == M.binding.ABI_VERSION
 
 
 def test_status_strings(lib):
@@ -347,3 +347,25 @@ def test_opt_buffers_validated(lib):
     L4 = dict(L)
     L4["opt_v"] = L["opt_v"] + 4              # misaligned
     assert ws_status([L4])[0] == M.MKOR_INVALID_ARG
+
+
+def test_noalloc_rejects_before_device(lib):
+    """mkor_step_noalloc validates on the host and refuses a layer list larger
+    than its device array before any HIP call."""
+    fk = Fake()
+    p = M.Params().to_c()
+    assert lib.mkor_step_noalloc(None, 0, ctypes.byref(p), None) == M.MKOR_OK
+    assert lib.mkor_step_noalloc(None, 0, None, None) == M.MKOR_INVALID_ARG
+    big = B.make_layer_array([layer(fk, 4096, 4096)])   # its X alone is 64 MiB
+    st, need = ws_status([layer(fk, 4096, 4096)])
+    assert st == M.MKOR_OK and need > B.NOALLOC_MAX_BYTES
+    assert lib.mkor_step_noalloc(big, 1, ctypes.byref(p), None) == M.MKOR_WORKSPACE_TOO_SMALL
+    assert "mkor_step_noalloc" in M.last_error()
+    bad = M.Params(gamma=2.0).to_c()
+    small = [layer(fk, 64, 64)]
+    assert lib.mkor_step_noalloc(B.make_layer_array(small), 1, ctypes.byref(bad), None) == M.MKOR_INVALID_ARG
+    small[0]["dW"] = small[0]["G"]   # output aliases an input
+    assert lib.mkor_step_noalloc(B.make_layer_array(small), 1, ctypes.byref(p), None) == M.MKOR_INVALID_ARG
+    rk = [layer(fk, 64, 64, rank=2)]   # rank-r layers need the EXACT variant
+    eq6 = M.Params(variant=M.SM_PAPER_EQ6).to_c()
+    assert lib.mkor_step_noalloc(B.make_layer_array(rk), 1, ctypes.byref(eq6), None) == M.MKOR_UNSUPPORTED
