@@ -99,7 +99,7 @@
 extern "C" {
 #endif
 
-#define MKOR_ABI_VERSION 9
+#define MKOR_ABI_VERSION 10
 
 /* status codes */
 #define MKOR_OK                   0
@@ -321,6 +321,68 @@ int mkor_step_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_par
  * factor updates of an update-every-f schedule). */
 int mkor_precondition_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt,
                           void* stream);
+
+/* ---- MKOR-H (the paper's "Hybrid MKOR" subsection): the second-order
+ * branch early in training, the first-order one once the second-order
+ * updates no longer speed up the decrease of the loss. */
+
+/* Chooses each layer's branch of Algorithm 1 for the calls that follow on
+ * the plan, without a new plan: flags[i] = 1 second-order (stabiliser, factor
+ * update, preconditioning, rescale), 0 first-order (dW = G, and with
+ * mkor_step_opt the optimizer steps with G; the layer's means, factor update
+ * and GEMMs are skipped).  `flags` is a host array of the plan's n entries,
+ * read before the call returns.  The mode words reach the workspace by a
+ * small kernel launch on `stream`: calls enqueued after it on that stream see
+ * them; the caller orders calls on other streams after it.  A layer planned
+ * with second_order = 0 has no factors and must stay 0 (MKOR_INVALID_ARG,
+ * nothing changed).  While a layer is first-order its factors (buffers and
+ * pending terms) and its stats stay as they are; switching it back resumes
+ * the updates from those factors.  mkor_sync_factors writes the pending terms
+ * of every layer, whatever its mode.  A plan starts with every layer as
+ * planned. */
+int mkor_set_second_order(mkor_plan* plan, const int32_t* flags, void* stream);
+
+/* *pending = 1 when a factor update ran on the plan since its creation or
+ * its last mkor_sync_factors: the Linv / Rinv buffers of rank-1 layers may
+ * then lag the current factors (see "Factor state"), and mkor_sync_factors is
+ * needed before reading, saving or modifying them; else 0.  Host-side. */
+int mkor_factors_pending(const mkor_plan* plan, int32_t* pending);
+
+/* The switching rule (host-side).  The paper bases it on the rate at which
+ * the loss decreases and gives no formula; this reading averages the loss
+ * over consecutive windows of `window` iterations and, after each closed
+ * window k >= max(1, warmup), forms the relative decrease of the window means
+ *     r_k = (m_{k-1} - m_k) / |m_{k-1}|      (0 when m_{k-1} = 0);
+ * after `patience` consecutive evaluated windows with r_k < threshold the
+ * decision turns to first-order for the rest of training (the fallback the
+ * paper describes; it never turns back). */
+typedef struct mkor_hybrid_params {
+    int32_t window;      /* iterations per window, >= 1 (e.g. the factor-update period) */
+    int32_t patience;    /* consecutive slow windows before the switch, >= 1 */
+    int32_t warmup;      /* closed windows before the first evaluation, >= 1 */
+    float   threshold;   /* relative decrease per window below which a window is slow, finite, >= 0 */
+} mkor_hybrid_params;
+
+typedef struct mkor_hybrid_state {   /* caller-owned; fields are read-only outside the calls */
+    mkor_hybrid_params params;
+    double  sum;             /* losses of the open window */
+    double  prev_mean;       /* mean loss of the last closed window */
+    double  last_rate;       /* r_k of the last closed window (NaN before the second) */
+    int64_t observed;        /* losses observed */
+    int64_t switched_at;     /* value of `observed` when the decision turned to 0, or -1 */
+    int32_t count;           /* losses in the open window */
+    int32_t windows;         /* closed windows */
+    int32_t slow;            /* consecutive evaluated windows below the threshold */
+    int32_t second_order;    /* the decision: 1, then 0 after the switch */
+} mkor_hybrid_state;
+
+/* Validates `params` and starts a state (decision 1). */
+int mkor_hybrid_init(const mkor_hybrid_params* params, mkor_hybrid_state* state);
+
+/* Adds the loss of one iteration and writes the decision after it to
+ * *second_order (may be NULL).  A non-finite loss is rejected
+ * (MKOR_INVALID_ARG) and leaves the state unchanged. */
+int mkor_hybrid_observe(mkor_hybrid_state* state, float loss, int32_t* second_order);
 
 /* One full step for callers that cannot allocate device memory: code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.

@@ -35,7 +35,7 @@ DTYPE_BF16 = 1
 MAX_DIM = 32768
 MAX_ROWS = 1 << 26
 MAX_RANK = 4
-ABI_VERSION = 9
+ABI_VERSION = 10
 NOALLOC_MAX_BYTES = 64 << 20
 GEMM_AUTO = 0
 GEMM_FP32 = 1
@@ -80,6 +80,18 @@ class mkor_layer_stats(ctypes.Structure):
                 ("nonfinite_scale", ctypes.c_int32)]
 
 
+class mkor_hybrid_params(ctypes.Structure):
+    _fields_ = [("window", ctypes.c_int32), ("patience", ctypes.c_int32), ("warmup", ctypes.c_int32),
+                ("threshold", ctypes.c_float)]
+
+
+class mkor_hybrid_state(ctypes.Structure):
+    _fields_ = [("params", mkor_hybrid_params), ("sum", ctypes.c_double), ("prev_mean", ctypes.c_double),
+                ("last_rate", ctypes.c_double), ("observed", ctypes.c_int64), ("switched_at", ctypes.c_int64),
+                ("count", ctypes.c_int32), ("windows", ctypes.c_int32), ("slow", ctypes.c_int32),
+                ("second_order", ctypes.c_int32)]
+
+
 STATS_BYTES = ctypes.sizeof(mkor_layer_stats)
 STATS_FIELDS = [f for f, _ in mkor_layer_stats._fields_]
 
@@ -87,11 +99,14 @@ EXPORTED = ["mkor_abi_version", "mkor_status_string", "mkor_last_error", "mkor_p
             "mkor_workspace_size", "mkor_plan_create", "mkor_update_factors",
             "mkor_precondition", "mkor_step", "mkor_run_stage", "mkor_sync_factors",
             "mkor_opt_params_check", "mkor_step_opt", "mkor_precondition_opt", "mkor_step_noalloc",
+            "mkor_set_second_order", "mkor_factors_pending", "mkor_hybrid_init", "mkor_hybrid_observe",
             "mkor_plan_destroy"]
 
-STAGE_MEANS, STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_XT, STAGE_GEMM_DW, STAGE_RESCALE = range(6)
-NUM_STAGES = 7
+# MKOR_STAGE_*, in launch order
 STAGE_NAMES = ["means", "sm_pass", "sm_finalize", "gemm_prep", "gemm_xt", "gemm_dw", "rescale"]
+(STAGE_MEANS, STAGE_SM_PASS, STAGE_SM_FINALIZE, STAGE_GEMM_PREP, STAGE_GEMM_XT, STAGE_GEMM_DW,
+ STAGE_RESCALE) = range(len(STAGE_NAMES))
+NUM_STAGES = len(STAGE_NAMES)
 
 
 class MkorError(RuntimeError):
@@ -141,6 +156,14 @@ def load_library(path: str = LIB_PATH):
         fn.argtypes = [P, ctypes.POINTER(mkor_params), ctypes.POINTER(mkor_opt_params), P]
     lib.mkor_step_noalloc.restype = ctypes.c_int
     lib.mkor_step_noalloc.argtypes = [ctypes.POINTER(mkor_layer), I32, ctypes.POINTER(mkor_params), P]
+    lib.mkor_set_second_order.restype = ctypes.c_int
+    lib.mkor_set_second_order.argtypes = [P, ctypes.POINTER(I32), P]
+    lib.mkor_factors_pending.restype = ctypes.c_int
+    lib.mkor_factors_pending.argtypes = [P, ctypes.POINTER(I32)]
+    lib.mkor_hybrid_init.restype = ctypes.c_int
+    lib.mkor_hybrid_init.argtypes = [ctypes.POINTER(mkor_hybrid_params), ctypes.POINTER(mkor_hybrid_state)]
+    lib.mkor_hybrid_observe.restype = ctypes.c_int
+    lib.mkor_hybrid_observe.argtypes = [ctypes.POINTER(mkor_hybrid_state), ctypes.c_float, ctypes.POINTER(I32)]
     lib.mkor_plan_destroy.restype = None
     lib.mkor_plan_destroy.argtypes = [P]
     if lib.mkor_abi_version() != ABI_VERSION:
@@ -353,6 +376,21 @@ class MkorPlan:
     def sync_factors(self, stream=None):
         _check(self._lib.mkor_sync_factors(self._plan, _stream_handle(stream)), "mkor_sync_factors")
 
+    def set_second_order(self, flags, stream=None):
+        """MKOR-H: the branch of each layer for the following calls (1
+        second-order, 0 first-order), one entry per layer of the plan."""
+        n = len(self.layers)
+        if len(flags) != n:
+            raise ValueError(f"{len(flags)} flags for {n} layers")
+        arr = (ctypes.c_int32 * max(1, n))(*[int(f) for f in flags])
+        _check(self._lib.mkor_set_second_order(self._plan, arr, _stream_handle(stream)), "mkor_set_second_order")
+
+    def factors_pending(self) -> bool:
+        """True when Linv / Rinv may lag the current factors (sync_factors needed)."""
+        out = ctypes.c_int32(0)
+        _check(self._lib.mkor_factors_pending(self._plan, ctypes.byref(out)), "mkor_factors_pending")
+        return bool(out.value)
+
     def close(self):
         if getattr(self, "_plan", None) is not None and self._plan.value:
             self._lib.mkor_plan_destroy(self._plan)
@@ -363,6 +401,32 @@ class MkorPlan:
             self.close()
         except Exception:
             pass
+
+
+class Hybrid:
+    """MKOR-H's switching rule (mkor_hybrid_init / mkor_hybrid_observe): feed
+    one loss per iteration; `second_order` turns False once the windowed loss
+    decrease has stayed below `threshold` for `patience` windows."""
+
+    def __init__(self, window=10, patience=2, warmup=1, threshold=0.01):
+        self._lib = load_library()
+        self.params = mkor_hybrid_params(int(window), int(patience), int(warmup), float(threshold))
+        self.state = mkor_hybrid_state()
+        _check(self._lib.mkor_hybrid_init(ctypes.byref(self.params), ctypes.byref(self.state)), "mkor_hybrid_init")
+
+    def observe(self, loss: float) -> bool:
+        out = ctypes.c_int32(1)
+        _check(self._lib.mkor_hybrid_observe(ctypes.byref(self.state), float(loss), ctypes.byref(out)),
+               "mkor_hybrid_observe")
+        return bool(out.value)
+
+    @property
+    def second_order(self) -> bool:
+        return bool(self.state.second_order)
+
+    @property
+    def switched_at(self):
+        return None if self.state.switched_at < 0 else int(self.state.switched_at)
 
 
 def step_noalloc(layers, params: Params, stream=None):

@@ -21,6 +21,8 @@ typedef unsigned int mk_u2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float gld(const float* p) { return *(const MKOR_GLOBAL float*)p; }
 
+__device__ __forceinline__ int gld_i32(const int32_t* p) { return *(const MKOR_GLOBAL int32_t*)p; }
+
 __device__ __forceinline__ unsigned short gld_u16(const unsigned short* p) {
     return *(const MKOR_GLOBAL unsigned short*)p;
 }

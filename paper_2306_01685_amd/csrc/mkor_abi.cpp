@@ -374,8 +374,10 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
     Lo.off_tri = take(sizeof(TrItem) * Lo.ntr);
     Lo.off_trb = take(sizeof(TrBlock) * Lo.ntrblk);
     Lo.off_qdb = take(sizeof(QdBlock) * Lo.nqdb);
-    // pending terms start out empty (has = 0): the upload initialises them
+    // pending terms start out empty (has = 0), the mode words as planned:
+    // the upload initialises them
     Lo.off_pend = take(sizeof(Pending) * Lo.nfactors);
+    Lo.off_mode = take(sizeof(int32_t) * (size_t)n);
     Lo.table_bytes = align_up(o, 256);
     Lo.off_smpart = take(sizeof(float4) * Lo.nrowblocks);
     Lo.off_gram = take(Lo.nranked > 0 ? sizeof(float) * GRAM * (size_t)Lo.nrowblocks : 0);
@@ -467,6 +469,9 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
     MeanMat* mm = reinterpret_cast<MeanMat*>(host.data() + lo.off_mmat);
     MeanItem* mi = reinterpret_cast<MeanItem*>(host.data() + lo.off_mitem);
     MeanItem* mc = reinterpret_cast<MeanItem*>(host.data() + lo.off_mchunk);
+    int32_t* mode_h = reinterpret_cast<int32_t*>(host.data() + lo.off_mode);
+    const int32_t* mode_d = reinterpret_cast<const int32_t*>(base + lo.off_mode);
+    for (int32_t i = 0; i < n; ++i) mode_h[i] = layers[i].second_order;
     {
         int32_t k = 0, ki = 0, kc = 0;
         int64_t p0 = 0;
@@ -484,6 +489,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
                 M.nchunk = ceil_div(M.cols, MEAN_COLS);
                 M.nrb = ceil_div(M.rows, MEAN_ROWS);
                 M.part0 = p0;
+                M.mode = mode_d + i;
                 p0 += (int64_t)M.nchunk * M.nrb * MEAN_COLS;
                 for (int32_t rb = 0; rb < M.nrb; ++rb)
                     for (int32_t c = 0; c < M.nchunk; ++c) mi[ki++] = MeanItem{k, c, rb, 0};
@@ -511,6 +517,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
         R.W = L.W;
         R.m = L.opt_m;
         R.v = L.opt_v;
+        R.mode = mode_d + i;
         if (!L.second_order) continue;
         const bool half = is_half(L);
         for (int side = 0; side < 2; ++side) {
@@ -530,6 +537,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             f.half = half ? 1 : 0;
             f.rank = layer_rank(L);
             f.lazy = lazy_factor(L, side) ? 1 : 0;
+            f.mode = mode_d + i;
             for (int32_t r = 0; r < f.nblk; ++r) rb[bi++] = RowBlock{fi, r * rows};
             ++fi;
         }
@@ -547,7 +555,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             if (needs_cvt(L)) {
                 unsigned short* gh = reinterpret_cast<unsigned short*>(base + lo.gh_off[i]);
                 const int64_t ne = (int64_t)L.d_in * L.d_out;
-                cvi[nci] = CvtItem{static_cast<const float*>(L.G), gh, ne};
+                cvi[nci] = CvtItem{static_cast<const float*>(L.G), gh, ne, mode_d + i};
                 for (int64_t o = 0; o < ne; o += CVT_ELEMS) cvb[ncb++] = CvtBlock{nci, 0, o};
                 ++nci;
                 Gq = gh;
@@ -558,11 +566,13 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             A.pend = fR.pend; A.w = fR.w;
             A.I = s1.rows; A.J = s1.cols; A.K = s1.K;
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
+            A.mode = mode_d + i;
             HgLayer& B = h2l[i];
             B.P = L.Linv; B.Q = Yt; B.C = L.dW;
             B.pend = fL.pend; B.w = fL.w;
             B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
             B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
+            B.mode = mode_d + i;
             gp += ngp;
             dp += ndp;
             continue;
@@ -572,7 +582,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             // dW_hat = X R with the factor R as the Q operand
             void* X = base + lo.x_off[i];
             unsigned short* Gt = reinterpret_cast<unsigned short*>(base + lo.gt_off[i]);
-            tri[nti] = TrItem{static_cast<const unsigned short*>(L.G), Gt, L.d_in, L.d_out};
+            tri[nti] = TrItem{static_cast<const unsigned short*>(L.G), Gt, L.d_in, L.d_out, mode_d + i};
             for (int32_t r0 = 0; r0 < L.d_in; r0 += 64)
                 for (int32_t c0 = 0; c0 < L.d_out; c0 += 64) trb[ntb++] = TrBlock{nti, r0, c0, 0};
             ++nti;
@@ -584,6 +594,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
             A.qf32 = 0; A.fq = 0; A.wide = s1.bm == SG_BI1H;
             A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
+            A.mode = mode_d + i;
             for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
             HgLayer& B = s2l[i];
             B.P = X; B.Q = L.Rinv; B.C = L.dW;
@@ -591,6 +602,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
             B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
             B.qf32 = 1; B.fq = 1;
+            B.mode = mode_d + i;
             gp += ngp;
             dp += ndp;
             continue;
@@ -607,6 +619,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             A.part0 = gp; A.ntj = ceil_div(s1.cols, s1.bn);
             A.qf32 = bf16 ? 0 : 1; A.fq = 0; A.wide = s1.bm == SG_BI1H;
             A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
+            A.mode = mode_d + i;
             for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
             HgLayer& B = s2l[i];
             B.P = L.Linv; B.Q = Yt; B.C = L.dW;
@@ -614,6 +627,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             B.I = s2.rows; B.J = s2.cols; B.K = s2.K;
             B.part0 = dp; B.ntj = ceil_div(s2.cols, s2.bn);
             B.qf32 = 1; B.fq = 0;
+            B.mode = mode_d + i;
             gp += ngp;
             dp += ndp;
             continue;
@@ -628,6 +642,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
         A.b_bf16 = bf16;
         A.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
         A.part0 = gp; A.ntn = tn1;
+        A.mode = mode_d + i;
         GemmLayer& B = g2l[i];
         B.At = X; B.B = L.Rinv; B.C = L.dW;
         B.pend = fR.pend; B.w = fR.w;
@@ -635,6 +650,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
         B.b_bf16 = 0;
         B.vec = (L.d_in % 4 == 0) && (L.d_out % 4 == 0);
         B.part0 = dp; B.ntn = tn2;
+        B.mode = mode_d + i;
         gp += ngp;
         dp += ndp;
     }
@@ -766,6 +782,10 @@ struct mkor_plan {
     char* ws = nullptr;
     Layout lo;
     std::vector<uint8_t> optbuf;   // per layer: 1 W, 2 opt_m, 4 opt_v
+    std::vector<uint8_t> planned;  // per layer: 1 second-order at creation (has factors)
+    std::vector<uint8_t> rank1;    // per layer: second-order with a rank-1 update (leaves pending terms)
+    std::vector<int32_t> mode;     // per layer: the mode word as the calls on the plan set it
+    int32_t pending = 0;           // a factor update ran since creation or the last sync
 };
 
 extern "C" {
@@ -832,8 +852,16 @@ int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, siz
     plan->ws = base;
     plan->lo = lo;
     plan->optbuf.resize(n);
-    for (int32_t i = 0; i < n; ++i)
-        plan->optbuf[i] = (uint8_t)((layers[i].W ? 1 : 0) | (layers[i].opt_m ? 2 : 0) | (layers[i].opt_v ? 4 : 0));
+    plan->planned.resize(n);
+    plan->rank1.resize(n);
+    plan->mode.resize(n);
+    for (int32_t i = 0; i < n; ++i) {
+        const mkor_layer& L = layers[i];
+        plan->optbuf[i] = (uint8_t)((L.W ? 1 : 0) | (L.opt_m ? 2 : 0) | (L.opt_v ? 4 : 0));
+        plan->planned[i] = (uint8_t)L.second_order;
+        plan->rank1[i] = (uint8_t)(L.second_order == 1 && L.rank <= 1);
+        plan->mode[i] = L.second_order;
+    }
     if (lo.table_bytes > 0) {
         hipError_t e = hipMemcpy(base, host.data(), lo.table_bytes, hipMemcpyHostToDevice);
         if (e != hipSuccess) {
@@ -851,8 +879,18 @@ static int check_plan_params(const mkor_plan* plan, const mkor_params* params) {
     return check_run_params(params, plan->lo.nranked);
 }
 
+// A range that includes the factor update leaves pending terms on the
+// rank-1 factors of the layers whose mode is second-order.
+static void note_update(mkor_plan* p, int32_t first, int32_t last) {
+    if (first > MKOR_STAGE_SM_FINALIZE || last < MKOR_STAGE_SM_FINALIZE) return;
+    for (int32_t i = 0; i < p->n; ++i)
+        if (p->rank1[i] && p->mode[i]) p->pending = 1;
+}
+
 static int run_range(mkor_plan* p, const mkor_params* prm, int32_t first, int32_t last, hipStream_t s) {
-    return run_range(view(p), prm, first, last, s);
+    const int st = run_range(view(p), prm, first, last, s);
+    if (st == MKOR_OK) note_update(p, first, last);
+    return st;
 }
 
 static int check_opt(const mkor_opt_params* o) {
@@ -975,13 +1013,48 @@ int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, vo
     if (st != MKOR_OK) return st;
     if (stage < 0 || stage >= MKOR_NUM_STAGES) return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
     if (plan->n == 0) return MKOR_OK;
-    return run_stage(view(plan), params, stage, static_cast<hipStream_t>(stream));
+    st = run_stage(view(plan), params, stage, static_cast<hipStream_t>(stream));
+    if (st == MKOR_OK) note_update(plan, stage, stage);
+    return st;
 }
 
 int mkor_sync_factors(mkor_plan* plan, void* stream) {
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
-    return sync_factors(view(plan), static_cast<hipStream_t>(stream));
+    const int st = sync_factors(view(plan), static_cast<hipStream_t>(stream));
+    if (st == MKOR_OK) plan->pending = 0;
+    return st;
+}
+
+int mkor_factors_pending(const mkor_plan* plan, int32_t* pending) {
+    g_err[0] = 0;
+    if (plan == nullptr || pending == nullptr) return fail(MKOR_INVALID_ARG, "plan or pending is NULL");
+    *pending = plan->pending;
+    return MKOR_OK;
+}
+
+int mkor_set_second_order(mkor_plan* plan, const int32_t* flags, void* stream) {
+    g_err[0] = 0;
+    if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
+    if (plan->n == 0) return MKOR_OK;
+    if (flags == nullptr) return fail(MKOR_INVALID_ARG, "flags is NULL");
+    for (int32_t i = 0; i < plan->n; ++i) {
+        if (flags[i] != 0 && flags[i] != 1)
+            return fail(MKOR_INVALID_ARG, "flags[%d] = %d is not 0 or 1", i, flags[i]);
+        if (flags[i] == 1 && !plan->planned[i])
+            return fail(MKOR_INVALID_ARG, "layer %d was planned first-order (it has no factors)", i);
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int32_t* mode_d = reinterpret_cast<int32_t*>(plan->ws + plan->lo.off_mode);
+    for (int32_t first = 0; first < plan->n; first += MODE_CHUNK) {
+        const int32_t count = std::min<int32_t>(MODE_CHUNK, plan->n - first);
+        uint32_t bits[MODE_CHUNK / 32] = {};
+        for (int32_t k = 0; k < count; ++k) bits[k >> 5] |= (uint32_t)flags[first + k] << (k & 31);
+        const hipError_t e = launch_set_modes(mode_d, first, count, bits, s);
+        if (e != hipSuccess) return hip_fail(e, "mode word launch");
+    }
+    std::copy(flags, flags + plan->n, plan->mode.begin());
+    return MKOR_OK;
 }
 
 void mkor_plan_destroy(mkor_plan* plan) { delete plan; }

@@ -12,6 +12,15 @@
 
 namespace mkor {
 
+// ---------------------------------------------------------------- layer modes
+// Every layer has a mode word in the workspace: 1 while it takes the
+// second-order branch of Algorithm 1, 0 while it takes the first-order one
+// (dW = G; its factors are neither read nor updated).  A layer planned
+// first-order always has 0; mkor_set_second_order rewrites the words of the
+// others on the stream.  Each descriptor below carries a pointer to its
+// layer's word, and every kernel of a step skips the work of a layer whose
+// word is 0, except the rescale, which then copies G into dW.
+
 // ---------------------------------------------------------------- rank-1 means
 // Column means of the rows x cols activation / output-gradient matrices.
 constexpr int MEAN_COLS = 512;      // columns per chunk: 8 per lane of one wave
@@ -27,6 +36,7 @@ struct MeanMat {
     int32_t     nchunk;   // column chunks of MEAN_COLS
     int32_t     nrb;      // row blocks of MEAN_ROWS
     int64_t     part0;    // first partial (double) of this matrix
+    const int32_t* mode;  // the layer's mode word (see LayerMode)
 };
 
 struct MeanItem {
@@ -76,6 +86,7 @@ struct FactorDesc {
     int32_t           rank;    // r vectors: x, u and w are d x r (vector l at + l * d)
     int32_t           lazy;    // rank 1, fp32: up to two pending terms (w holds 2 d floats)
     int32_t           _pad;
+    const int32_t*    mode;    // the layer's mode word
 };
 
 // Rank-r factors (rank > 1): per row block, the Gram partials
@@ -123,6 +134,7 @@ struct GemmLayer {
     int32_t        part0;     // first partial-sum slot of this layer
     int32_t        ntn;       // number of N tiles
     int32_t        _pad;
+    const int32_t* mode;      // the layer's mode word
 };
 
 struct GemmTile {
@@ -202,6 +214,7 @@ struct HgLayer {
     int32_t        fq;     // sgemm: the factor is the Q operand, C = P Q_eff^T (else C = P_eff Q^T)
     int32_t        wide;   // sgemm stage 1, bf16 Q: SG_BI1H x SG_BJ1H tiles (else SG_BI x SG_BJ)
     float*         rq;     // sgemm stage 1: (Q w) per Q row, formed by qdot_kernel before the GEMM
+    const int32_t* mode;   // the layer's mode word
 };
 
 // Rows of the stage-1 Q operand of the split GEMMs, one block of QD_ROWS rows
@@ -215,6 +228,7 @@ struct TrItem {
     const unsigned short* src;   // rows x cols
     unsigned short*       dst;   // cols x rows
     int32_t               rows, cols;   // multiples of 64
+    const int32_t*        mode;         // the layer's mode word
 };
 struct TrBlock {
     int32_t item, r0, c0, _pad;  // 64 x 64 tile at (r0, c0) of src
@@ -225,6 +239,7 @@ struct CvtItem {
     const float*    src;
     unsigned short* dst;
     int64_t         n;      // elements (a multiple of 8)
+    const int32_t*  mode;   // the layer's mode word
 };
 struct CvtBlock {
     int32_t item, _pad;
@@ -256,6 +271,7 @@ struct RescaleLayer {
     float*            W;                // backend optimizer state (null when unused)
     float*            m;
     float*            v;
+    const int32_t*    mode;             // the layer's mode word
 };
 
 // Backend optimizer fused with the rescale (host-computed scalars).
@@ -308,6 +324,12 @@ hipError_t launch_sm_finalize(const FactorDesc* factors, int32_t nfactors, const
 
 // Marks every pending term applied (after a materialising pass).
 hipError_t launch_sm_reset(const FactorDesc* factors, int32_t nfactors, hipStream_t stream);
+
+// Sets the mode words mode[first .. first + count) from bit i of `bits`
+// (count <= MODE_CHUNK), stream-ordered.
+constexpr int MODE_CHUNK = 1024;
+hipError_t launch_set_modes(int32_t* mode, int32_t first, int32_t count, const uint32_t* bits,
+                            hipStream_t stream);
 
 // GEMM 1: X^T = (Linv G)^T, plus ||G||^2 partials from the tiles of the first M row.
 hipError_t launch_gemm_xt(const GemmLayer* layers, const GemmTile* tiles, int32_t ntiles,

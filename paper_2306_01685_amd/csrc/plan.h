@@ -31,6 +31,7 @@ struct Layout {
     size_t off_qdb = 0;                                          // stage-1 (Q w) row blocks (split)
     size_t off_gram = 0;                                         // rank-r Gram partials
     size_t off_lpart = 0, off_trust = 0;                         // LAMB block sums, per-layer ratios
+    size_t off_mode = 0;                                         // per-layer mode words (int32)
     size_t table_bytes = 0;   // descriptor tables [0, table_bytes) are uploaded
     size_t total = 0;
     int32_t nfactors = 0, nrowblocks = 0, ng1 = 0, ng2 = 0, ngpart = 0, ndpart = 0, nrsblocks = 0;

@@ -540,6 +540,7 @@ __global__ __launch_bounds__(NT, SHP.minb) void gemm_kernel(
     const GemmTile tile = tiles[blockIdx.x];
     if (tile.layer < 0) return;   // padding of the XCD interleave
     const GemmLayer L = layers[tile.layer];
+    if (!gld_i32(L.mode)) return;   // first-order layer this step
     const Pending q = *L.pend;
     // the factor operand is At in stage 1 and B in stage 2
     if (q.has) run_tile<STAGE, STAGE>(L, tile, q, partials, smem);

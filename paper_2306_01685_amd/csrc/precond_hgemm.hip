@@ -364,6 +364,7 @@ __global__ __launch_bounds__(NT, 512 / NT) void hgemm_kernel(HgArgs args) {
     const GemmTile tile = args.tiles[blockIdx.x];
     if (tile.layer < 0) return;   // padding of the XCD interleave
     const HgLayer L = args.layers[tile.layer];
+    if (!gld_i32(L.mode)) return;   // first-order layer this step
     const Pending q = *L.pend;
     if (q.has) hgemm_tile<STAGE, true>(L, tile, q, args.partials, smem);
     else       hgemm_tile<STAGE, false>(L, tile, q, args.partials, smem);
@@ -374,6 +375,7 @@ __global__ __launch_bounds__(256) void cvt_bf16_kernel(const CvtItem* __restrict
                                                       const CvtBlock* __restrict__ blocks) {
     const CvtBlock b = blocks[blockIdx.x];
     const CvtItem it = items[b.item];
+    if (!gld_i32(it.mode)) return;
     const int64_t end = min(b.off + (int64_t)CVT_ELEMS, it.n);
     for (int64_t e = b.off + 8 * (int64_t)threadIdx.x; e < end; e += 8 * 256) {
         const float4 x0 = gld4_nt(it.src + e), x1 = gld4_nt(it.src + e + 4);

@@ -472,6 +472,7 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
         const GemmTile tile = args.tiles[blockIdx.x];
         if (tile.layer < 0) return;   // padding of the XCD interleave
         const HgLayer L = args.layers[tile.layer];
+        if (!gld_i32(L.mode)) return;   // first-order layer this step
         Pending q = *L.pend;
         if (q.has == 2) {   // two terms: c1b (c1 S + c2 I + sgn w w^T) + c2b I + sgnb w2 w2^T
             q.sgn = q.c1b * q.sgn;
@@ -572,6 +573,7 @@ __global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ l
     __shared__ float red[4];
     const QdBlock b = blocks[blockIdx.x];
     const HgLayer L = layers[b.layer];
+    if (!gld_i32(L.mode)) return;   // block-uniform
     const Pending q = *L.pend;
     if (q.has == 2) qdot_block<true>(L, b, q, partials, red);
     else            qdot_block<false>(L, b, q, partials, red);
@@ -584,6 +586,7 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const TrItem* __res
     __shared__ unsigned short tile[64][66];
     const TrBlock b = blocks[blockIdx.x];
     const TrItem it = items[b.item];
+    if (!gld_i32(it.mode)) return;   // block-uniform
     const int t = threadIdx.x, r = t >> 2, c = 16 * (t & 3);
     // 16 consecutive elements of source row r0 + r, as two 16-byte loads
     const unsigned short* s = it.src + (size_t)(b.r0 + r) * it.cols + b.c0 + c;

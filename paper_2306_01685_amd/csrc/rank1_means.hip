@@ -37,6 +37,7 @@ __global__ __launch_bounds__(MT) void colmean_partial_kernel(const MeanMat* __re
                                                              double* __restrict__ part) {
     const MeanItem it = items[blockIdx.x];
     const MeanMat m = mats[it.mat];
+    if (!gld_i32(m.mode)) return;   // first-order layer: no means (block-uniform)
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     constexpr int CPT = MEAN_COLS / 64;                // columns per thread (8)
     const int c0 = it.chunk * MEAN_COLS + CPT * lane;  // this thread's columns
@@ -101,6 +102,7 @@ __global__ __launch_bounds__(MEAN_COLS) void colmean_final_kernel(const MeanMat*
                                                                   const double* __restrict__ part) {
     const MeanItem ch = chunks[blockIdx.x];
     const MeanMat m = mats[ch.mat];
+    if (!gld_i32(m.mode)) return;
     const int c = ch.chunk * MEAN_COLS + threadIdx.x;
     if (c >= m.cols) return;
     const double* p = part + m.part0 + (size_t)ch.chunk * MEAN_COLS + threadIdx.x;

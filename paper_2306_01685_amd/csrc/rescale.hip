@@ -58,7 +58,7 @@ __device__ __forceinline__ void rescale_block(const RescaleLayer* __restrict__ l
     const int t = threadIdx.x;
     const int64_t end = min(b.start + (int64_t)RS_ELEMS, L.numel);
 
-    if (!L.second_order) {
+    if (!L.second_order || !gld_i32(L.mode)) {   // planned or switched first-order: dW = G
         if (L.g_bf16) {
             const unsigned short* G = static_cast<const unsigned short*>(L.G);
             for (int64_t i = b.start + t; i < end; i += RS_THREADS)
@@ -172,12 +172,13 @@ __global__ __launch_bounds__(RS_THREADS) void opt_pass_a_kernel(
         const RescaleBlock b = blocks[bi];
         const RescaleLayer L = layers[b.layer];
         const int64_t end = min(b.start + (int64_t)RS_ELEMS, L.numel);
-        const float sc = L.second_order ? layer_scale(L, bi, gpart, dpart, rescale, s_g, s_d, &s_scale) : 1.f;
+        const bool so = L.second_order && gld_i32(L.mode);   // block-uniform
+        const float sc = so ? layer_scale(L, bi, gpart, dpart, rescale, s_g, s_d, &s_scale) : 1.f;
         float w2 = 0.f, r2 = 0.f;
         if ((L.numel & 3) == 0) {   // blocks start at multiples of RS_ELEMS: 16-byte groups
             for (int64_t i = b.start + 4 * t; i < end; i += 4 * RS_THREADS) {
                 float g[4];
-                if (L.second_order) {
+                if (so) {
                     const float4 d = gld4(L.dW + i);
                     g[0] = __fmul_rn(d.x, sc); g[1] = __fmul_rn(d.y, sc);
                     g[2] = __fmul_rn(d.z, sc); g[3] = __fmul_rn(d.w, sc);
@@ -194,7 +195,7 @@ __global__ __launch_bounds__(RS_THREADS) void opt_pass_a_kernel(
         } else {
             for (int64_t i = b.start + t; i < end; i += RS_THREADS) {
                 float g;
-                if (L.second_order)  g = __fmul_rn(gld(L.dW + i), sc);
+                if (so)              g = __fmul_rn(gld(L.dW + i), sc);
                 else if (L.g_bf16)   g = __uint_as_float(((unsigned)gld_u16(static_cast<const unsigned short*>(L.G) + i)) << 16);
                 else                 g = gld(static_cast<const float*>(L.G) + i);
                 opt_elem<KIND>(L, i, g, o, w2, r2);

@@ -345,6 +345,9 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_kernel(
         const RowBlock rb = blocks[b];
         const FactorDesc f = factors[rb.factor];
         if (f.rank > 1) continue;   // sm_pass_rank_kernel
+        // a first-order layer this step: its factor is neither read nor
+        // updated (a write-back pass, matvec = 0, still writes its terms)
+        if (matvec && !gld_i32(f.mode)) continue;
         if (f.half) pass_block<SM_ROWS_PER_WAVE_HALF, true>(f, rb, partials, b, maxabs, matvec, sred);
         else        pass_block<SM_ROWS_PER_WAVE, false>(f, rb, partials, b, maxabs, matvec, sred);
     }
@@ -458,6 +461,7 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_rank_kernel(
         const RowBlock rb = blocks[b];
         const FactorDesc f = factors[rb.factor];
         if (f.rank <= 1) continue;
+        if (matvec && !gld_i32(f.mode)) continue;   // first-order layer this step
         const Pending q = *f.pend;
         const bool has = q.has != 0;
         if (!has && !matvec) continue;
@@ -653,6 +657,7 @@ __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
     const FactorDesc* __restrict__ factors, const float4* __restrict__ partials, const float* __restrict__ gram,
     UpdateArgs a) {
     const FactorDesc f = factors[blockIdx.x];
+    if (!gld_i32(f.mode)) return;   // first-order layer this step: no update, no stats
     if (f.rank > 1) {
         finalize_rank(f, partials, gram, a);
         return;
@@ -732,6 +737,15 @@ __global__ __launch_bounds__(SM_THREADS) void sm_finalize_kernel(
         gst(wn + i, __fmul_rn(c.sqc, __fmaf_rn(c.zp, gld(f.u + i), __fmul_rn(c.zq, gld(f.x + i)))));
 }
 
+struct ModeBits {
+    uint32_t w[MODE_CHUNK / 32];
+};
+
+__global__ __launch_bounds__(256) void set_modes_kernel(int32_t* __restrict__ mode, int32_t count, ModeBits bits) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < count) mode[i] = (int32_t)((bits.w[i >> 5] >> (i & 31)) & 1u);
+}
+
 __global__ void sm_reset_kernel(const FactorDesc* __restrict__ factors, int32_t nfactors, int ranked_only) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < nfactors && (!ranked_only || factors[i].rank > 1)) *factors[i].pend = Pending{1.f, 0.f, 0.f, 0};
@@ -773,6 +787,16 @@ hipError_t launch_sm_finalize(const FactorDesc* factors, int32_t nfactors, const
     UpdateArgs a{p.gamma, p.zeta, p.stab_eps, p.sm_variant, p.guard_nonfinite};
     hipLaunchKernelGGL(sm_finalize_kernel, dim3(nfactors), dim3(SM_THREADS), 0, stream, factors,
                        partials, gram, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_set_modes(int32_t* mode, int32_t first, int32_t count, const uint32_t* bits,
+                            hipStream_t stream) {
+    if (count <= 0) return hipSuccess;
+    if (count > MODE_CHUNK) return hipErrorInvalidValue;
+    ModeBits b{};
+    for (int i = 0; i < (count + 31) / 32; ++i) b.w[i] = bits[i];
+    hipLaunchKernelGGL(set_modes_kernel, dim3((count + 255) / 256), dim3(256), 0, stream, mode + first, count, b);
     return hipGetLastError();
 }
 

@@ -369,3 +369,57 @@ def test_noalloc_rejects_before_device(lib):
     rk = [layer(fk, 64, 64, rank=2)]   # rank-r layers need the EXACT variant
     eq6 = M.Params(variant=M.SM_PAPER_EQ6).to_c()
     assert lib.mkor_step_noalloc(B.make_layer_array(rk), 1, ctypes.byref(eq6), None) == M.MKOR_UNSUPPORTED
+
+
+def header_defines():
+    """Integer #defines of include/mkor.h (name -> value)."""
+    src = open(os.path.join(ROOT, "include", "mkor.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    out = {}
+    for name, expr in re.findall(r"^#define\s+(MKOR_[A-Z0-9_]+)\s+(.+?)\s*$", src, flags=re.M):
+        expr = expr.replace("u", "") if re.fullmatch(r"[0-9u<() ]+", expr) else expr
+        try:
+            out[name] = int(eval(expr, {"__builtins__": {}}))
+        except Exception:
+            pass
+    return out
+
+
+def test_binding_constants_match_header():
+    d = header_defines()
+    pairs = {
+        "MKOR_ABI_VERSION": B.ABI_VERSION, "MKOR_OK": M.MKOR_OK, "MKOR_INVALID_ARG": M.MKOR_INVALID_ARG,
+        "MKOR_WORKSPACE_TOO_SMALL": M.MKOR_WORKSPACE_TOO_SMALL, "MKOR_UNSUPPORTED": M.MKOR_UNSUPPORTED,
+        "MKOR_HIP_ERROR": M.MKOR_HIP_ERROR, "MKOR_SM_EXACT": B.SM_EXACT, "MKOR_SM_PAPER_EQ6": B.SM_PAPER_EQ6,
+        "MKOR_NORM_INF": B.NORM_INF, "MKOR_NORM_MAXABS": B.NORM_MAXABS, "MKOR_DTYPE_F32": B.DTYPE_F32,
+        "MKOR_DTYPE_BF16": B.DTYPE_BF16, "MKOR_STAGE_MEANS": B.STAGE_MEANS, "MKOR_STAGE_SM_PASS": B.STAGE_SM_PASS,
+        "MKOR_STAGE_SM_FINALIZE": B.STAGE_SM_FINALIZE, "MKOR_STAGE_GEMM_PREP": B.STAGE_GEMM_PREP,
+        "MKOR_STAGE_GEMM_XT": B.STAGE_GEMM_XT, "MKOR_STAGE_GEMM_DW": B.STAGE_GEMM_DW,
+        "MKOR_STAGE_RESCALE": B.STAGE_RESCALE, "MKOR_NUM_STAGES": B.NUM_STAGES, "MKOR_GEMM_AUTO": B.GEMM_AUTO,
+        "MKOR_GEMM_FP32": B.GEMM_FP32, "MKOR_GEMM_SPLIT": B.GEMM_SPLIT, "MKOR_MAX_DIM": B.MAX_DIM,
+        "MKOR_MAX_ROWS": B.MAX_ROWS, "MKOR_MAX_RANK": B.MAX_RANK, "MKOR_OPT_SGD": B.OPT_SGD,
+        "MKOR_OPT_LAMB": B.OPT_LAMB, "MKOR_NOALLOC_MAX_BYTES": B.NOALLOC_MAX_BYTES,
+    }
+    assert set(d) == set(pairs), sorted(set(d) ^ set(pairs))
+    for name, value in pairs.items():
+        assert d[name] == value, (name, d[name], value)
+    stages = sorted((v, k) for k, v in d.items() if k.startswith("MKOR_STAGE_"))
+    assert [k[len("MKOR_STAGE_"):].lower() for _, k in stages] == B.STAGE_NAMES
+
+
+def test_hybrid_struct_sizes():
+    assert ctypes.sizeof(B.mkor_hybrid_params) == 16
+    assert ctypes.sizeof(B.mkor_hybrid_state) == 16 + 3 * 8 + 2 * 8 + 4 * 4
+
+
+def test_mode_and_pending_calls_on_host(lib):
+    flags = (ctypes.c_int32 * 1)(1)
+    out = ctypes.c_int32(5)
+    assert lib.mkor_set_second_order(None, flags, None) == M.MKOR_INVALID_ARG
+    assert lib.mkor_factors_pending(None, ctypes.byref(out)) == M.MKOR_INVALID_ARG
+    plan = ctypes.c_void_p(None)
+    assert lib.mkor_plan_create(None, 0, None, 0, ctypes.byref(plan)) == M.MKOR_OK
+    assert lib.mkor_set_second_order(plan, None, None) == M.MKOR_OK   # n = 0: nothing to set
+    assert lib.mkor_factors_pending(plan, None) == M.MKOR_INVALID_ARG
+    assert lib.mkor_factors_pending(plan, ctypes.byref(out)) == M.MKOR_OK and out.value == 0
+    lib.mkor_plan_destroy(plan)
