@@ -276,3 +276,93 @@ def test_half_bert_large_shapes_one_step():
         f = (check_stored(Lg, PL, update_error_bound(Li, a, op, st.L.stab), ("L", i)),
              check_stored(Rg, PR, update_error_bound(Ri, g, op, st.R.stab), ("R", i)))
         print("   flip fraction", f)
+
+
+# ------------------------------------------------------------------ against full precision
+
+def _trajectory(seed, d, steps=5, gamma=0.9):
+    """A factor after a few float64 updates from I: not bf16-representable."""
+    rng = np.random.default_rng(seed)
+    P = np.eye(d)
+    p = O.Params(gamma=gamma, eps=math.inf)
+    for _ in range(steps):
+        P, _ = O.update_factor(P, rng.standard_normal(d) / math.sqrt(d), p)
+    return P
+
+
+def first_order_update_error(P, E, x, gamma):
+    """Frobenius bound, to first order in E, on the change of the exact
+    Sherman-Morrison update P' = (P - k P x x^T P) / gamma,
+    k = (1 - gamma) / (gamma + (1 - gamma) x^T P x), when its input P moves
+    by E: dP' = (E - k (E x u^T + u x^T E) + k^2 (x^T E x) u u^T) / gamma with
+    u = P x (dk = -k^2 d(x^T P x))."""
+    u = P @ x
+    k = (1.0 - gamma) / (gamma + (1.0 - gamma) * float(x @ u))
+    Ex = E @ x
+    return (np.linalg.norm(E) + 2 * abs(k) * np.linalg.norm(Ex) * np.linalg.norm(u)
+            + k * k * abs(float(x @ Ex)) * float(u @ u)) / gamma
+
+
+@pytest.mark.parametrize("grad_dtype", ["fp32", "bf16"])
+def test_half_step_against_full_precision(grad_dtype):
+    """One bf16-factor step from stored factors Q = bf16(P) against the
+    fp32-reading oracle (Algorithm 1 in float64, nothing rounded).
+
+    Factors: the stored result against the update of the unquantised P, within
+    Lemma 2's bound (eps = max |Q - P|, m = the largest entry of P and x) plus
+    the rounding of the result to bf16; and, in Frobenius norm, within the
+    first-order change of the update under E = Q - P plus that rounding
+    (10 % margin for the higher-order terms and the fp32 evaluation).
+
+    dW: against the oracle's step from the same stored Q.  The kernel rounds
+    Y = G_h Rinv' to bf16 (and an fp32 G to G_h), each a relative error of at
+    most 2^-9 per element; through dW_hat = Linv' Y_h that is a relative error
+    of at most kappa(Linv') ((kappa(Rinv') + 1) 2^-9 (fp32 G) or 2^-9 (bf16 G)),
+    doubled by the normalisation of the rescale, plus 2^-9 for ||G_h|| in
+    place of ||G|| (fp32 G)."""
+    from oracle.half import lemma2_bound
+    shapes = [(192, 256), (512, 128), (1024, 1024)]
+    p = Params(eps=math.inf)
+    op = oparams(p)
+    layers = H.allocate_layers(shapes, grad_dtype, factor_dtype="bf16")
+    host = []
+    for i, (L, (d_in, d_out)) in enumerate(zip(layers, shapes)):
+        PL, PR = _trajectory(40 + i, d_in), _trajectory(50 + i, d_out)
+        QL, QR = round_bf16(PL), round_bf16(PR)
+        a, g, G = _inputs(60 + i, d_in, d_out, grad_dtype)
+        H.set_factors(L, QL, QR)
+        H.set_inputs(L, a, g, G)
+        host.append((PL, PR, QL, QR, a, g, G))
+    plan = H.make_plan(layers)
+    plan.step(p)
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    u9 = 2.0 ** -9
+    for i, (L, (PL, PR, QL, QR, a, g, G)) in enumerate(zip(layers, host)):
+        stored = H.get_factors(L)
+        updated = []
+        for P, Q, x, S in ((PL, QL, a, stored[0]), (PR, QR, g, stored[1])):
+            x = np.asarray(x, np.float64)
+            P_full, _ = O.update_factor(P, x, op)
+            Pq, _ = O.update_factor(Q, x, op)
+            updated.append(Pq)
+            S = S.astype(np.float64)
+            eps_q = float(np.max(np.abs(Q - P)))
+            m = float(max(np.max(np.abs(P)), np.max(np.abs(x))))
+            err = float(np.max(np.abs(S - P_full)))
+            bound = lemma2_bound(op.gamma, m, P.shape[0], eps_q) + u9 * float(np.max(np.abs(P_full)))
+            assert eps_q > 0.0 and err <= bound, (i, err, bound)
+            fo = 1.1 * first_order_update_error(P, Q - P, x, op.gamma) + u9 * np.linalg.norm(P_full)
+            ef = float(np.linalg.norm(S - P_full))
+            print(shapes[i], grad_dtype, "factor: max err", err, "Lemma 2 bound", bound,
+                  "Frobenius err", ef, "first-order bound", fo)
+            assert ef <= fo, (i, ef, fo)
+        _, _, dW_ref, _ = O.layer_step(QL, QR, a, g, G, op)
+        kL, kR = np.linalg.cond(updated[0]), np.linalg.cond(updated[1])
+        if grad_dtype == "bf16":
+            tol = 2 * kL * u9 + 1e-5
+        else:
+            tol = 2 * kL * (kR + 1) * u9 + u9 + 1e-5
+        e = rel(H.get_dW(L), dW_ref)
+        print(shapes[i], grad_dtype, "dW err", e, "bound", tol, "kappa", kL, kR)
+        assert e <= tol, (i, e, tol)

@@ -104,18 +104,23 @@ def test_split_small_and_large_magnitudes():
 
 def test_split_after_sync_and_over_steps():
     """Several steps (pending terms carried), a sync in between, then a
-    precondition-only step: each against the oracle."""
+    precondition-only step: dW of every step against the oracle.  With a bf16
+    G, (320, 64) and (576, 320) take the other association, whose lazily
+    written Linv carries two pending terms on every other step, so both forms
+    of the first GEMM's epilogue are checked, before and after the sync
+    shifts the write-back cadence."""
     p = Params(eps=3.0)
     op = oparams(p)
-    layers = H.allocate_layers(SHAPES[:3], "bf16", gemm_path="split")
+    shapes = SHAPES[:3] + [SHAPES[3], SHAPES[5]]
+    layers = H.allocate_layers(shapes, "bf16", gemm_path="split")
     state = []
-    for i, (L, (d_in, d_out)) in enumerate(zip(layers, SHAPES)):
+    for i, (L, (d_in, d_out)) in enumerate(zip(layers, shapes)):
         Li, Ri = spd(500 + i, d_in), spd(600 + i, d_out)
         H.set_factors(L, Li, Ri)
         state.append([Li.astype(np.float64), Ri.astype(np.float64)])
     plan = H.make_plan(layers)
-    for t in range(6):
-        update = t != 5
+    for t in range(9):
+        update = t != 8
         outs = []
         for i, L in enumerate(layers):
             a, g, G = _inputs(700 + 10 * t + i, L["d_in"], L["d_out"], "bf16")
