@@ -18,7 +18,9 @@ from dataclasses import dataclass
 import torch  # noqa: F401  (must precede loading libmkor, see module docstring)
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libmkor.so")
+# MKOR_LIBRARY selects another build of the same library (e.g. the
+# sanitizer-instrumented one the host tests run against)
+LIB_PATH = os.environ.get("MKOR_LIBRARY") or os.path.join(_PKG, "libmkor.so")
 
 MKOR_OK = 0
 MKOR_INVALID_ARG = -1
@@ -322,7 +324,7 @@ class MkorPlan:
     writes the current factors into them (include/mkor.h, "Factor state").
     """
 
-    def __init__(self, layers, device=None):
+    def __init__(self, layers, device=None, workspace=None):
         self._lib = load_library()
         self.layers = layers
         descs = layer_descs(layers)
@@ -331,15 +333,26 @@ class MkorPlan:
         size = ctypes.c_size_t(0)
         _check(self._lib.mkor_workspace_size(self._arr, n, ctypes.byref(size)), "mkor_workspace_size")
         self.ws_bytes = size.value
-        if device is None:
-            device = layers[0]["dW"].device if layers else torch.device("cuda")
-        # over-allocate by 256 bytes and align the base to 256
-        self._ws_raw = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
-        base = self._ws_raw.data_ptr()
-        off = (-base) % 256
-        self.workspace = self._ws_raw[off:off + self.ws_bytes]
+        if workspace is not None:
+            # the caller's workspace: a uint8 device tensor of at least ws_bytes,
+            # 256-byte aligned (checked by mkor_plan_create)
+            if workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+                raise TypeError("workspace must be a contiguous uint8 tensor")
+            self._ws_raw = workspace
+            self.workspace = workspace
+            base, off = workspace.data_ptr(), 0
+            ws_len = workspace.numel()
+        else:
+            if device is None:
+                device = layers[0]["dW"].device if layers else torch.device("cuda")
+            # over-allocate by 256 bytes and align the base to 256
+            self._ws_raw = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
+            base = self._ws_raw.data_ptr()
+            off = (-base) % 256
+            self.workspace = self._ws_raw[off:off + self.ws_bytes]
+            ws_len = self.ws_bytes
         plan = ctypes.c_void_p(None)
-        _check(self._lib.mkor_plan_create(self._arr, n, ctypes.c_void_p(base + off), self.ws_bytes,
+        _check(self._lib.mkor_plan_create(self._arr, n, ctypes.c_void_p(base + off), ws_len,
                                           ctypes.byref(plan)), "mkor_plan_create")
         self._plan = plan
 

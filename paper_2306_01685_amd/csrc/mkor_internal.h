@@ -187,8 +187,14 @@ constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 #ifndef MKOR_HG_BK
 #define MKOR_HG_BK 64
 #endif
+// Each wave computes 128 x HG_TJ outputs: 128 (four waves, one per SIMD,
+// 256 accumulators each) or 64 (eight waves, two per SIMD, 128 each).
+#ifndef MKOR_HG_TJ
+#define MKOR_HG_TJ 64
+#endif
 constexpr int HG_BI = MKOR_HG_BI, HG_BJ = MKOR_HG_BJ;   // tile of C (rows i x columns j)
-constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / 64);   // waves of 128 x 64
+constexpr int HG_TJ = MKOR_HG_TJ;
+constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / HG_TJ);
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
 constexpr int SG_BI = 256, SG_BJ = 256;                  // tile of C of the split GEMMs (sgemm)
 constexpr int SG_BI1H = 128, SG_BJ1H = 512;              // ... of the first one when Q is bf16

@@ -61,10 +61,10 @@ typedef __attribute__((address_space(3))) float lds_float;
 typedef __attribute__((address_space(3))) unsigned short lds_u16;
 
 constexpr int BI = HG_BI, BJ = HG_BJ, NT = HG_THREADS;
-constexpr int WI = BI / 128, WJ = BJ / 64;   // wave grid
-constexpr int TI = BI / WI, TJ = BJ / WJ;     // 128 x 64 per wave
-constexpr int FI = TI / 32, FJ = TJ / 32;     // 4 x 2 MFMA blocks
-static_assert(NT == WI * WJ * 64 && TI == 128 && TJ == 64, "wave layout");
+constexpr int WI = BI / 128, WJ = BJ / HG_TJ;   // wave grid
+constexpr int TI = BI / WI, TJ = BJ / WJ;        // 128 x HG_TJ per wave
+constexpr int FI = TI / 32, FJ = TJ / 32;        // 4 x 2 or 4 x 4 MFMA blocks
+static_assert(NT == WI * WJ * 64 && TI == 128 && (TJ == 64 || TJ == 128), "wave layout");
 
 constexpr int BK = HG_BK, NS = HG_NS;         // slab depth, ring stages
 static_assert(BK == 32 || BK == 64, "slab rows of 64 or 128 bytes");
@@ -77,7 +77,8 @@ constexpr int WSLOT = 256;                    // w[k0 .. k0 + 64) per stage (BK 
 constexpr int NW = NT / 64;
 constexpr int PBLK = PB / 1024 / NW, QBLK = QB / 1024 / NW;   // 1-KB load blocks per wave and slab
 static_assert(PB % (1024 * NW) == 0 && QB % (1024 * NW) == 0, "load blocks per wave");
-static_assert(2 * BJ == NT, "rank-1 reads: one half Q row per thread");
+constexpr int TPQ = NT / BJ;                  // threads per Q row in the rank-1 reads
+static_assert(TPQ * BJ == NT && (TPQ == 1 || TPQ == 2), "rank-1 reads: a whole or half Q row per thread");
 constexpr int RING = NS * STB;
 // Stage-1 output staging: the bf16 tile, rows of BJ * 2 bytes with the
 // 16-byte chunk index XORed with the row, in the ring once the K loop is done.
@@ -194,9 +195,10 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
             dma4(lds0 + RING + (unsigned)(st % NS) * WSLOT, (unsigned)min(st * BK + lane, K - 1) * 4u, L.w);
     };
 
-    // rank-1 dot (and ||G||^2) of this thread's half Q row: row t / 2, chunks
-    // h KC / 2 .. (h + 1) KC / 2 - 1, summed in a fixed order over the slabs
-    const int rr = t >> 1, rh = t & 1;
+    // rank-1 dot (and ||G||^2) of this thread's part of a Q row: row t / TPQ,
+    // chunks h KC / TPQ .. (h + 1) KC / TPQ - 1, summed in a fixed order over
+    // the slabs
+    const int rr = t / TPQ, rh = t % TPQ;
     float rdot = 0.f, gsq = 0.f;
     const bool gsq_row = want_gsq && j0 + rr < J;
 
@@ -247,8 +249,8 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         if (PEND || want_gsq) {
             const lds_float* wsl = (const lds_float*)(smem + RING + (s % NS) * WSLOT);
 #pragma unroll
-            for (int e = 0; e < KC / 2; ++e) {
-                const int c = (KC / 2) * rh + e;
+            for (int e = 0; e < KC / TPQ; ++e) {
+                const int c = (KC / TPQ) * rh + e;
                 float v[8];
                 const mk_u4 hv = *(const lds_u4*)(Qb + swz(rr, c));
                 unpack8(hv, v);
@@ -265,7 +267,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     }
 
     if (PEND) {
-        const float v = rdot + __shfl_xor(rdot, 1, 64);
+        const float v = TPQ == 2 ? rdot + __shfl_xor(rdot, 1, 64) : rdot;
         if (rh == 0) rvec[rr] = v;
     }
     __syncthreads();   // rvec complete; the ring is free for the output staging
@@ -358,7 +360,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 
 // 8 waves per CU (2 per SIMD): at most 256 VGPRs per lane.
 template <int STAGE>
-__global__ __launch_bounds__(NT, 512 / NT) void hgemm_kernel(HgArgs args) {
+__global__ __launch_bounds__(NT, 1) void hgemm_kernel(HgArgs args) {
     __shared__ __attribute__((aligned(16))) char smem_[SMEM];
     lds_char* smem = (lds_char*)smem_;
     const GemmTile tile = args.tiles[blockIdx.x];

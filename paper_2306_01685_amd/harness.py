@@ -11,8 +11,38 @@ import torch
 from .binding import STATS_BYTES, MkorPlan, read_stats
 
 
+class Guarded:
+    """Device tensors carved out of larger buffers with a guard region of
+    `guard` bytes on each side, filled with a byte pattern, so that a write
+    past either end of a tensor shows up in intact()."""
+
+    PATTERN = 0x7F   # 0x7F7F7F7F as fp32 is 3.39e38: finite, unlike anything a kernel writes here
+
+    def __init__(self, guard=4096):
+        assert guard % 256 == 0
+        self.guard = guard
+        self.raws = []
+
+    def empty(self, shape, dtype, device="cuda"):
+        nbytes = int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size()
+        body = (nbytes + 255) // 256 * 256
+        raw = torch.full((self.guard + body + self.guard,), self.PATTERN, dtype=torch.uint8, device=device)
+        self.raws.append((raw, nbytes))
+        return raw[self.guard:self.guard + nbytes].view(dtype).view(shape)
+
+    def intact(self):
+        """True when every guard region still holds the pattern (also the
+        padding between a tensor's end and its guard)."""
+        for raw, nbytes in self.raws:
+            g = self.guard
+            if not bool((raw[:g] == self.PATTERN).all()) or not bool((raw[g + nbytes:] == self.PATTERN).all()):
+                return False
+        return True
+
+
 def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None, stats=True,
-                    rows=0, act_dtype="fp32", factor_dtype="fp32", rank=1, optimizer=None, gemm_path=None):
+                    rows=0, act_dtype="fp32", factor_dtype="fp32", rank=1, optimizer=None, gemm_path=None,
+                    guards=None):
     """One dict of device tensors per (d_in, d_out); factors start as I.  With
     rows > 0 each second-order layer also gets token-row buffers A (rows x d_in)
     and Gout (rows x d_out), from which the library forms a and g.
@@ -20,33 +50,45 @@ def allocate_layers(shapes, grad_dtype="fp32", device="cuda", second_order=None,
     rank > 1 gives a and g the shapes (rank, d_in) and (rank, d_out): r vectors
     per factor (rank-r update).  optimizer "sgd" or "lamb" adds the weights W
     (zeros) and the optimizer state (opt_m, and opt_v for LAMB).  gemm_path
-    ("auto", "fp32", "split") is set on the second-order layers when given."""
+    ("auto", "fp32", "split") is set on the second-order layers when given.
+    With guards (a Guarded), every tensor is carved out of a guarded buffer."""
+    def new(shape, dtype):
+        if guards is None:
+            return torch.zeros(shape, dtype=dtype, device=device)
+        t = guards.empty(shape, dtype, device)
+        t.zero_()
+        return t
+
+    def eye(d, dtype):
+        t = new((d, d), dtype)
+        t.copy_(torch.eye(d, dtype=dtype, device=device))
+        return t
+
     fdt = torch.bfloat16 if factor_dtype == "bf16" else torch.float32
     gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
     layers = []
     for i, (d_in, d_out) in enumerate(shapes):
         so = True if second_order is None else bool(second_order[i])
         L = dict(d_in=d_in, d_out=d_out, second_order=so,
-                 G=torch.zeros((d_in, d_out), dtype=gdt, device=device),
-                 dW=torch.zeros((d_in, d_out), dtype=torch.float32, device=device))
+                 G=new((d_in, d_out), gdt), dW=new((d_in, d_out), torch.float32))
         if so:
-            L["Linv"] = torch.eye(d_in, dtype=fdt, device=device)
-            L["Rinv"] = torch.eye(d_out, dtype=fdt, device=device)
+            L["Linv"] = eye(d_in, fdt)
+            L["Rinv"] = eye(d_out, fdt)
             va = (rank, d_in) if rank > 1 else (d_in,)
             vg = (rank, d_out) if rank > 1 else (d_out,)
-            L["a"] = torch.zeros(va, dtype=torch.float32, device=device)
-            L["g"] = torch.zeros(vg, dtype=torch.float32, device=device)
+            L["a"] = new(va, torch.float32)
+            L["g"] = new(vg, torch.float32)
         if so and gemm_path is not None:
             L["gemm_path"] = gemm_path
         if stats:
-            L["stats"] = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=device)
+            L["stats"] = new((STATS_BYTES,), torch.uint8)
         if optimizer is not None:
             for k in ("W", "opt_m") + (("opt_v",) if optimizer == "lamb" else ()):
-                L[k] = torch.zeros((d_in, d_out), dtype=torch.float32, device=device)
+                L[k] = new((d_in, d_out), torch.float32)
         if so and rows:
             adt = torch.bfloat16 if act_dtype == "bf16" else torch.float32
-            L["A"] = torch.zeros((rows, d_in), dtype=adt, device=device)
-            L["Gout"] = torch.zeros((rows, d_out), dtype=adt, device=device)
+            L["A"] = new((rows, d_in), adt)
+            L["Gout"] = new((rows, d_out), adt)
         layers.append(L)
     return layers
 
@@ -98,5 +140,5 @@ def get_stats(L):
     return read_stats(L["stats"])
 
 
-def make_plan(layers) -> MkorPlan:
-    return MkorPlan(layers)
+def make_plan(layers, workspace=None) -> MkorPlan:
+    return MkorPlan(layers, workspace=workspace)
