@@ -27,6 +27,7 @@ import json
 import math
 import os
 import sys
+import statistics
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -36,6 +37,26 @@ METRIC = "layer-updates/sec (SM update + precondition), BERT-Large set; % HBM / 
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 FP32_MFMA_PEAK_TF = 157.3   # MI355X dense fp32 matrix
 BF16_MFMA_PEAK_TF = 2500.0  # MI355X dense bf16 matrix
+
+
+REPEATS = 5                 # timed windows per measurement; the median is reported
+
+
+def timed_windows(run, stream, steps, repeats):
+    """ms per step of `repeats` windows of `steps` calls of run(), each window
+    bracketed by HIP events on `stream` with the device idle before it."""
+    import torch
+    out = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) / steps)
+    return out
 
 
 PROFILE_TRAFFIC = {False: os.path.join(ROOT, "profiles", "traffic_bert_large_144.md"),
@@ -108,33 +129,79 @@ def parse():
                     help="preconditioning GEMMs of fp32 factors (auto: the split where the shape allows)")
     ap.add_argument("--no-fp32-path", action="store_true",
                     help="skip the extra measurement on the fp32 MFMA GEMM path")
+    ap.add_argument("--no-stabilised", action="store_true",
+                    help="skip the extra window with the stabiliser firing on every step (eps = 0)")
+    ap.add_argument("--no-references", action="store_true",
+                    help="skip the copy-kernel and torch.matmul reference measurements")
     ap.add_argument("--graph", action="store_true",
                     help="also time the step captured once in a HIP graph and replayed K times "
                          "(saves the launch gaps of launch-bound workloads)")
     return ap.parse_args()
 
 
-def copy_reference(args):
-    """A plain copy kernel of known size: reads and writes copy_mib MiB once."""
+def copy_measure(mib, steps, warmup):
+    """A plain device-to-device copy of `mib` MiB (torch's copy kernel): the
+    achievable-bandwidth reference for read + write traffic."""
     import torch
-    n = args.copy_mib * (1 << 20) // 4
+    n = mib * (1 << 20) // 4
     src = torch.ones(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     stream = torch.cuda.current_stream()
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         dst.copy_(src)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         dst.copy_(src)
     e1.record(stream)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = e0.elapsed_time(e1) / steps
     nbytes = 2 * n * 4
-    print(json.dumps({"mode": "copy", "bytes_read": n * 4, "bytes_written": n * 4, "ms": ms,
-                      "gbs": nbytes / (ms / 1e3) / 1e9, "frac_hbm": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}),
-          flush=True)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_read": n * 4, "bytes_written": n * 4, "ms": ms,
+            "gbs": nbytes / (ms / 1e3) / 1e9, "frac_hbm": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}
+
+
+def copy_reference(args):
+    """--mode copy: the copy kernel alone (its FETCH_SIZE / WRITE_SIZE
+    counters calibrate the traffic figures)."""
+    print(json.dumps({"mode": "copy", **copy_measure(args.copy_mib, args.steps, args.warmup)}), flush=True)
+
+
+def torch_matmul_reference(w, reps=3):
+    """torch.matmul in fp32 (the vendor GEMM library) on the workload's two
+    preconditioning products per layer, Linv @ G then X @ Rinv, one pair per
+    distinct shape timed and weighted by its count: an out-of-product
+    reference for the preconditioning GEMMs."""
+    import torch
+    counts = {}
+    for s in w.shapes:
+        counts[s] = counts.get(s, 0) + 1
+    stream = torch.cuda.current_stream()
+    total_ms, flops = 0.0, 0
+    for (d_in, d_out), c in counts.items():
+        L = torch.randn(d_in, d_in, device="cuda")
+        R = torch.randn(d_out, d_out, device="cuda")
+        G = torch.randn(d_in, d_out, device="cuda")
+        for _ in range(2):
+            torch.matmul(torch.matmul(L, G), R)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            torch.matmul(torch.matmul(L, G), R)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        total_ms += c * e0.elapsed_time(e1) / reps
+        flops += c * 2 * d_in * d_out * (d_in + d_out)
+        del L, R, G
+    torch.cuda.empty_cache()
+    return {"ms": total_ms, "tflops": flops / (total_ms / 1e3) / 1e12,
+            "frac_fp32_mfma_peak": flops / (total_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TF,
+            "allow_tf32": bool(torch.backends.cuda.matmul.allow_tf32),
+            "note": "torch.matmul fp32, Linv @ G @ Rinv per layer, shapes timed one pair at a time"}
 
 
 def workload_desc(w, factor_dtype="fp32"):
@@ -197,11 +264,12 @@ def cpu_baseline(w, budget_s):
 
     import oracle as O
     import workloads as W
+    affinity = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
         threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
+        threads = affinity
     nb = len(w.block_shapes)
     inputs = []
     for i in range(nb):
@@ -219,9 +287,32 @@ def cpu_baseline(w, budget_s):
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
+    # cores: the threads the oracle ran on (its GEMMs on the BLAS pool; its
+    # rank-1 updates are single-threaded NumPy elementwise work)
     return dict(value=nb * steps / el, unit="layer-updates/s", cores=int(threads), kind="oracle",
+                blas_threads=int(threads), affinity_cpus=affinity,
                 sample=f"first block of the workload ({nb} layers, one of each shape), {steps} full "
-                       f"float64 steps in {el:.1f} s; host has {len(os.sched_getaffinity(0))} cpus")
+                       f"float64 steps in {el:.1f} s")
+
+
+def stage_times(plan, params, stream, steps):
+    """Average ms of each kernel of a step (MKOR_STAGE_*), over `steps` steps
+    launched stage by stage with HIP events between consecutive kernels on the
+    launch stream."""
+    import torch
+
+    from paper_2306_01685_amd import NUM_STAGES
+    acc = [0.0] * NUM_STAGES
+    for _ in range(steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(NUM_STAGES + 1)]
+        ev[0].record(stream)
+        for s in range(NUM_STAGES):
+            plan.run_stage(params, s)
+            ev[s + 1].record(stream)
+        torch.cuda.synchronize()
+        for s in range(NUM_STAGES):
+            acc[s] += ev[s].elapsed_time(ev[s + 1])
+    return [a / steps for a in acc]
 
 
 def measure(w, args, factor_dtype, gemm_path="auto"):
@@ -252,14 +343,10 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
     for _ in range(args.warmup):
         plan.step(params)
     torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for _ in range(args.steps):
-        plan.step(params)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / args.steps
+    # the paper's protocol: the median of REPEATS timed windows, each of
+    # exactly args.steps steps
+    windows = timed_windows(lambda: plan.step(params), stream, args.steps, REPEATS)
+    ms_step = statistics.median(windows)
 
     # per-kernel times: the same steps launched stage by stage with HIP events
     # between consecutive kernels on the launch stream
@@ -267,17 +354,7 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
     esz = 2 if half else 4                                  # factor element bytes
     mfma_peak = BF16_MFMA_PEAK_TF if half else FP32_MFMA_PEAK_TF
     if not args.no_stage_timing:
-        acc = [0.0] * NUM_STAGES
-        for _ in range(args.steps):
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(NUM_STAGES + 1)]
-            ev[0].record(stream)
-            for s in range(NUM_STAGES):
-                plan.run_stage(params, s)
-                ev[s + 1].record(stream)
-            torch.cuda.synchronize()
-            for s in range(NUM_STAGES):
-                acc[s] += ev[s].elapsed_time(ev[s + 1])
-        ms = [a / args.steps for a in acc]
+        ms = stage_times(plan, params, stream, args.steps)
         sq = w.factor_elems
         # stage 1 contracts over d_in (fp32 MFMA: Linv G; split with a bf16 G
         # and d_in > d_out: Linv G) or d_out (G Rinv)
@@ -346,12 +423,21 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                                      frac_of_fp32_mfma_peak=(f1 + f2) / (pre_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TF)
         for k in ("sm_pass", "sm_finalize", "rescale"):
             kernels[k]["frac_hbm"] = kernels[k]["gbs"] / HBM_PEAK_GBS
+        # the SM update's algorithmic bytes per step (read every factor element
+        # once, write it once), whatever the write-back cadence actually moves
+        alg_sm = 2 * esz * sq
+        kernels["sm_pass"]["alg_basis_bytes"] = alg_sm
+        kernels["sm_pass"]["gbs_alg"] = alg_sm * gb / (ms[0] / 1e3)
+        kernels["sm_pass"]["frac_alg"] = kernels["sm_pass"]["gbs_alg"] / HBM_PEAK_GBS
         for k, pk, tm in ((g1, peaks[0], terms[0]), (g2, peaks[1], terms[1])):
             kernels[k]["peak"] = pk
             kernels[k]["frac_mfma"] = kernels[k]["tflops"] / pk
             if split:
                 kernels[k]["bf16_mfma_terms"] = tm
                 kernels[k]["bf16_mfma_tflops"] = kernels[k]["tflops"] * tm
+                # fp32 products per second against the raw bf16 peak (no credit
+                # for the split's extra bf16 products)
+                kernels[k]["frac_of_bf16_peak"] = kernels[k]["tflops"] / BF16_MFMA_PEAK_TF
         names = ["sm_pass", "sm_finalize", g1, g2, "rescale"]
         dom = max(range(len(names)), key=lambda s: ms[s])
         name = names[dom]
@@ -366,6 +452,7 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                 roof["peak_basis"] = (f"fp32 products on the three-way bf16 split: the {BF16_MFMA_PEAK_TF:.0f} "
                                       f"TFLOP/s bf16 MFMA peak / {k['bf16_mfma_terms']} bf16 products each")
                 roof["frac_of_fp32_mfma_peak"] = k["tflops"] / FP32_MFMA_PEAK_TF
+                roof["frac_of_bf16_peak"] = k["tflops"] / BF16_MFMA_PEAK_TF
         else:
             roof = dict(kernel=name, bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
                         frac=k["gbs"] / HBM_PEAK_GBS,
@@ -378,7 +465,10 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
         roof["sm_update"] = dict(kernel="sm_pass", bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS,
                                  unit="GB/s", frac=k["gbs"] / HBM_PEAK_GBS,
                                  traffic=None if t is None else t["total_bytes"],
-                                 per_launch=f"{k['alg_bytes']:.4e} B")
+                                 per_launch=f"{k['alg_bytes']:.4e} B",
+                                 achieved_alg=k["gbs_alg"], frac_alg=k["frac_alg"],
+                                 per_launch_alg=f"{k['alg_basis_bytes']:.4e} B (8 B per fp32 factor "
+                                                f"element: one read, one write)")
 
     # The same step captured in a HIP graph (kernel launches only) and replayed.
     graph = None
@@ -423,11 +513,28 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
         f_ms = e0.elapsed_time(e1) / (10 * cycles)
         schedule = dict(update_every=10, steps=10 * cycles, ms_per_step=f_ms,
                         value=w.n_layers / (f_ms / 1e3), unit="layer-updates/s")
+    # A window in which the stabiliser fires: eps = 0 blends every factor on
+    # every step, so the GEMMs run their variants with the diagonal shift
+    # (c2 != 0), which the eps = 100 windows above never reach.
+    stabilised = None
+    if not args.no_stabilised:
+        p0 = Params(gamma=w.gamma, zeta=0.5, eps=0.0)
+        for _ in range(2):
+            plan.step(p0)
+        sw = timed_windows(lambda: plan.step(p0), stream, args.steps, REPEATS)
+        s_ms = statistics.median(sw)
+        stabilised = dict(eps=0.0, ms_per_step=s_ms, value=w.n_layers / (s_ms / 1e3), unit="layer-updates/s",
+                          windows_ms_per_step=sw,
+                          note="stabiliser fires on every factor at every step (eps = 0)")
+        if not args.no_stage_timing:
+            st = stage_times(plan, p0, stream, args.steps)
+            stabilised["gemm_ms"] = [st[4], st[5]]
     del plan, layers
     torch.cuda.empty_cache()
     if graph is not None:
         kernels["graph_replay"] = graph
-    return ms_step, kernels, roof, schedule
+    extra = dict(windows_ms_per_step=windows, stabilised_step=stabilised)
+    return ms_step, kernels, roof, schedule, extra
 
 
 def measure_opt(w, args):
@@ -503,20 +610,21 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     w = W.CONFIGS[args.config]
-    ms_step, kernels, roof, schedule = measure(w, args, args.factor_dtype, args.gemm_path)
+    ms_step, kernels, roof, schedule, extra = measure(w, args, args.factor_dtype, args.gemm_path)
     value = w.n_layers / (ms_step / 1e3)
     fp32_path = None
     if (args.factor_dtype == "fp32" and not args.no_fp32_path and args.rank == 1
             and split_eligible(w, args.gemm_path)):
         # the same workload on the fp32 MFMA GEMMs, reported beside
-        f_ms, f_k, f_roof, _ = measure(w, argparse.Namespace(**{**vars(args), "no_schedule": True}),
-                                       "fp32", "fp32")
+        f_ms, f_k, f_roof, _, _ = measure(w, argparse.Namespace(**{**vars(args), "no_schedule": True,
+                                                                   "no_stabilised": True}), "fp32", "fp32")
         fp32_path = dict(value=w.n_layers / (f_ms / 1e3), unit="layer-updates/s", ms_per_step=f_ms,
                          gemm="fp32 MFMA (v_mfma_f32_32x32x2_f32)", roofline=f_roof, kernels=f_k)
     half = None
     if args.factor_dtype == "fp32" and not args.no_half and args.rank == 1:
         # the same workload with half-precision (bf16) factors, reported beside
-        h_ms, h_k, h_roof, h_sched = measure(w, args, "bf16")
+        h_ms, h_k, h_roof, h_sched, _ = measure(w, argparse.Namespace(**{**vars(args), "no_stabilised": True}),
+                                                "bf16")
         half = dict(value=w.n_layers / (h_ms / 1e3), unit="layer-updates/s", ms_per_step=h_ms,
                     dtype="bf16 factors, bf16 MFMA (fp32 accumulation)", roofline=h_roof,
                     schedule_f10=h_sched, kernels=h_k)
@@ -524,6 +632,10 @@ def main():
     opt = None
     if args.factor_dtype == "fp32" and not args.no_opt and args.rank == 1:
         opt = measure_opt(w, args)
+    refs = None
+    if not args.no_references:
+        refs = dict(copy_kernel=copy_measure(args.copy_mib, args.steps, args.warmup),
+                    torch_matmul_fp32=torch_matmul_reference(w))
 
     out = {
         "metric": METRIC, "value": value, "unit": "layer-updates/s", "n_gpus": 1,
@@ -539,6 +651,10 @@ def main():
                             "fp32 operands as exact three-way bf16 splits on bf16 MFMA, fp32 accumulation"
                             if split_eligible(w, args.gemm_path) else "fp32 MFMA")},
         "roofline": roof,
+        "timing": {"repeats": REPEATS, "windows_ms_per_step": extra["windows_ms_per_step"],
+                   "statistic": "median of the windows (the paper's median of 5 runs)"},
+        "stabilised_step": extra["stabilised_step"],
+        "references": refs,
         "schedule_f10": schedule,
         "kernels": kernels,
         "fp32_mfma_path": fp32_path,
