@@ -491,6 +491,26 @@ __global__ __launch_bounds__(NT, 1) void sgemm_kernel(SgArgs args) {
     }
 }
 
+// The sums over the wave of eight per-lane values, one per row: a butterfly
+// that halves the values each lane keeps at the xor-32, -16 and -8 steps and
+// sums the last over the remaining lane bits, so lanes 8 r .. 8 r + 7 end
+// with row r's total (r = lane >> 3), in a fixed order.
+__device__ __forceinline__ float row_sums8(const float (&v)[8], int lane) {
+    const bool h5 = (lane & 32) != 0, h4 = (lane & 16) != 0, h3 = (lane & 8) != 0;
+    float a[4], b[2];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)   // rows k + 4 h5
+        a[k] = (h5 ? v[k + 4] : v[k]) + __shfl_xor(h5 ? v[k] : v[k + 4], 32, 64);
+#pragma unroll
+    for (int k = 0; k < 2; ++k)   // rows 4 h5 + 2 h4 + k
+        b[k] = (h4 ? a[k + 2] : a[k]) + __shfl_xor(h4 ? a[k] : a[k + 2], 16, 64);
+    float c = (h3 ? b[1] : b[0]) + __shfl_xor(h3 ? b[0] : b[1], 8, 64);   // row 4 h5 + 2 h4 + h3
+    c += __shfl_xor(c, 4, 64);
+    c += __shfl_xor(c, 2, 64);
+    c += __shfl_xor(c, 1, 64);
+    return c;
+}
+
 template <bool TWO>
 __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, const Pending& q, float* partials,
                                            float* red) {
@@ -498,13 +518,13 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int K = L.K, J = L.J;
     const float* w2 = L.w + K;
-    float gsq = 0.f;
+    float sq = 0.f;   // this lane's part of ||Q||^2 over all its rows
     for (int r0 = wave * RB; r0 < QD_ROWS; r0 += 4 * RB) {
         const int jb = b.rb * QD_ROWS + r0;
         if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
-        float dot[RB], dot2[RB], sq[RB];
+        float dot[RB], dot2[RB];
 #pragma unroll
-        for (int i = 0; i < RB; ++i) dot[i] = dot2[i] = sq[i] = 0.f;
+        for (int i = 0; i < RB; ++i) dot[i] = dot2[i] = 0.f;
         if (L.qf32) {
             const float* row = static_cast<const float*>(L.Q) + (size_t)jb * K;
             for (int k = 4 * lane; k < K; k += 256) {
@@ -513,7 +533,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
                     const float4 v = gld4(row + (size_t)i * K + k);
-                    sq[i] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sq[i]))));
+                    sq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sq))));
                     dot[i] = fmaf(v.x, wv.x, fmaf(v.y, wv.y, fmaf(v.z, wv.z, fmaf(v.w, wv.w, dot[i]))));
                     if (TWO) dot2[i] = fmaf(v.x, wv2.x, fmaf(v.y, wv2.y, fmaf(v.z, wv2.z, fmaf(v.w, wv2.w, dot2[i]))));
                 }
@@ -539,24 +559,21 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float v0 = __uint_as_float(h[e] << 16), v1 = __uint_as_float(h[e] & 0xffff0000u);
-                        sq[i] = fmaf(v1, v1, fmaf(v0, v0, sq[i]));
+                        sq = fmaf(v1, v1, fmaf(v0, v0, sq));
                         dot[i] = fmaf(v1, wv[2 * e + 1], fmaf(v0, wv[2 * e], dot[i]));
                         if (TWO) dot2[i] = fmaf(v1, wv2[2 * e + 1], fmaf(v0, wv2[2 * e], dot2[i]));
                     }
                 }
             }
         }
-#pragma unroll
-        for (int i = 0; i < RB; ++i) {
-            const float d = wave_sum(dot[i]);
-            if (lane == 0 && q.has) gst(L.rq + jb + i, d);
-            if (TWO) {
-                const float d2 = wave_sum(dot2[i]);
-                if (lane == 0) gst(L.rq + J + jb + i, d2);
-            }
-            gsq += wave_sum(sq[i]);   // the same value in every lane
+        const float d = row_sums8(dot, lane);
+        if ((lane & 7) == 0 && q.has) gst(L.rq + jb + (lane >> 3), d);
+        if (TWO) {
+            const float d2 = row_sums8(dot2, lane);
+            if ((lane & 7) == 0) gst(L.rq + J + jb + (lane >> 3), d2);
         }
     }
+    const float gsq = wave_sum(sq);
     if (lane == 0) red[wave] = gsq;
     __syncthreads();
     if (t == 0) gst(partials + L.part0 + b.rb, (red[0] + red[1]) + (red[2] + red[3]));
