@@ -824,6 +824,7 @@ int mkor_workspace_size(const mkor_layer* layers, int32_t n, size_t* bytes) {
 
 int mkor_plan_create(const mkor_layer* layers, int32_t n, void* d_workspace, size_t ws_bytes,
                      mkor_plan** out) {
+    const TraceRange range("mkor_plan_create");
     g_err[0] = 0;
     if (out == nullptr) return fail(MKOR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -946,6 +947,7 @@ static int check_opt_plan(const mkor_plan* plan, const mkor_opt_params* o) {
 }
 
 int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream) {
+    const TraceRange range("mkor_update_factors");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_plan_params(plan, params);
@@ -955,6 +957,7 @@ int mkor_update_factors(mkor_plan* plan, const mkor_params* params, void* stream
 }
 
 int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream) {
+    const TraceRange range("mkor_precondition");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_plan_params(plan, params);
@@ -964,6 +967,7 @@ int mkor_precondition(mkor_plan* plan, const mkor_params* params, void* stream) 
 }
 
 int mkor_step(mkor_plan* plan, const mkor_params* params, void* stream) {
+    const TraceRange range("mkor_step");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_plan_params(plan, params);
@@ -978,6 +982,7 @@ int mkor_opt_params_check(const mkor_opt_params* opt) {
 }
 
 int mkor_step_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt, void* stream) {
+    const TraceRange range("mkor_step_opt");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_plan_params(plan, params);
@@ -993,6 +998,7 @@ int mkor_step_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_par
 
 int mkor_precondition_opt(mkor_plan* plan, const mkor_params* params, const mkor_opt_params* opt,
                           void* stream) {
+    const TraceRange range("mkor_precondition_opt");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     int st = check_plan_params(plan, params);
@@ -1013,12 +1019,17 @@ int mkor_run_stage(mkor_plan* plan, const mkor_params* params, int32_t stage, vo
     if (st != MKOR_OK) return st;
     if (stage < 0 || stage >= MKOR_NUM_STAGES) return fail(MKOR_INVALID_ARG, "stage = %d unknown", stage);
     if (plan->n == 0) return MKOR_OK;
+    static const char* const names[MKOR_NUM_STAGES] = {
+        "mkor_run_stage: means", "mkor_run_stage: sm_pass", "mkor_run_stage: sm_finalize", "mkor_run_stage: gemm_prep",
+        "mkor_run_stage: gemm_xt", "mkor_run_stage: gemm_dw", "mkor_run_stage: rescale"};
+    const TraceRange range(names[stage]);
     st = run_stage(view(plan), params, stage, static_cast<hipStream_t>(stream));
     if (st == MKOR_OK) note_update(plan, stage, stage);
     return st;
 }
 
 int mkor_sync_factors(mkor_plan* plan, void* stream) {
+    const TraceRange range("mkor_sync_factors");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     const int st = sync_factors(view(plan), static_cast<hipStream_t>(stream));
@@ -1034,6 +1045,7 @@ int mkor_factors_pending(const mkor_plan* plan, int32_t* pending) {
 }
 
 int mkor_set_second_order(mkor_plan* plan, const int32_t* flags, void* stream) {
+    const TraceRange range("mkor_set_second_order");
     g_err[0] = 0;
     if (plan == nullptr) return fail(MKOR_INVALID_ARG, "plan is NULL");
     if (plan->n == 0) return MKOR_OK;

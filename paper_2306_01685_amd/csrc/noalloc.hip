@@ -79,6 +79,7 @@ int upload(char* dst, const std::vector<char>& host, hipStream_t s) {
 using namespace mkor;
 
 extern "C" int mkor_step_noalloc(const mkor_layer* layers, int32_t n, const mkor_params* params, void* stream) {
+    const TraceRange range("mkor_step_noalloc");
     clear_error();
     int st = check_layers(layers, n, nullptr, 0);
     if (st != MKOR_OK) return st;

@@ -8,9 +8,21 @@
 
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "mkor_internal.h"
 
 namespace mkor {
+
+// A roctx range over the host-side span of an entry point (its launches), so
+// that a trace (rocprofv3 --marker-trace) groups each call's kernels under
+// its name.  Costs a function call when no tool is attached.
+struct TraceRange {
+    explicit TraceRange(const char* name) { roctxRangePush(name); }
+    ~TraceRange() { roctxRangePop(); }
+    TraceRange(const TraceRange&) = delete;
+    TraceRange& operator=(const TraceRange&) = delete;
+};
 
 // Records the thread-local error text (mkor_last_error) and returns `status`.
 int fail(int status, const char* fmt, ...);

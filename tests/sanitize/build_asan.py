@@ -48,7 +48,7 @@ def build() -> str:
         objs = list(ex.map(_compile, B.sources()))
     # the runtime is preloaded into the process, so the library leaves the
     # sanitizer symbols for the dynamic linker to resolve
-    cmd = [B.HIPCC, "-shared", "-fPIC", f"--offload-arch={B.ARCH}", *objs, "-o", LIB + ".tmp"]
+    cmd = [B.HIPCC, "-shared", "-fPIC", f"--offload-arch={B.ARCH}", *objs, *B.LINK_FLAGS, "-o", LIB + ".tmp"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"{' '.join(cmd)}\n{r.stderr[-4000:]}")

@@ -423,3 +423,11 @@ def test_mode_and_pending_calls_on_host(lib):
     assert lib.mkor_factors_pending(plan, None) == M.MKOR_INVALID_ARG
     assert lib.mkor_factors_pending(plan, ctypes.byref(out)) == M.MKOR_OK and out.value == 0
     lib.mkor_plan_destroy(plan)
+
+
+def test_entry_points_open_roctx_ranges(lib):
+    """The library imports roctx's range calls (each entry point opens a
+    named range for traces taken with rocprofv3 --marker-trace)."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", M.LIB_PATH], capture_output=True, text=True).stdout
+    assert "roctxRangePushA" in out and "roctxRangePop" in out
