@@ -459,9 +459,11 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                         traffic=None if traffic is None else traffic["total_bytes"],
                         per_launch=f"{k['alg_bytes']:.4e} B")
         roof["traffic_detail"] = traffic
-        # the SM update is the benchmark spec's other roofline: report it beside
+        # the SM update is the benchmark spec's other roofline: report it beside (its
+        # traffic differs with the GEMM path: only the split path writes some
+        # factors every other step)
         k = kernels["sm_pass"]
-        t = profiled_traffic("sm_pass", args.config, half)
+        t = profiled_traffic("sm_pass" if (half or split) else "sm_pass_fp32", args.config, half)
         roof["sm_update"] = dict(kernel="sm_pass", bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS,
                                  unit="GB/s", frac=k["gbs"] / HBM_PEAK_GBS,
                                  traffic=None if t is None else t["total_bytes"],
