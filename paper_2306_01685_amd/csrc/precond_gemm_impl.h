@@ -213,9 +213,10 @@ struct Loader {
     // diagonal elements of the factor operand.
     template <bool DIAG>
     __device__ static void store(const SlabRegs<BF16>& r, const GemmLayer& L, const Xform& xf,
-                                 int m0, int n0, int k0, float* As, float* Bs, float& gsq,
+                                 int m0, int n0, int k0, float* As, float* Bs, double& gsq,
                                  bool want_gsq) {
         const int t = threadIdx.x;
+        float part = 0.f;   // this slab's squares: a short fp32 chain, added to gsq in fp64
         const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
         if constexpr (VEC) {
             const int ca = 4 * (t % AC4);
@@ -241,7 +242,7 @@ struct Loader {
                     if constexpr (XF == 2) {
                         if (ok) v = xf4<DIAG>(xf, v, r.wk[i], k, n);
                     }
-                    if (want_gsq) sq4(gsq, v);
+                    if (want_gsq) sq4(part, v);
                     *reinterpret_cast<float4*>(Bs + row * BN + cb) = v;
                 }
             } else {
@@ -260,7 +261,7 @@ struct Loader {
                     const float4 v1 = make_float4(
                         __uint_as_float(h1.x << 16), __uint_as_float(h1.x & 0xffff0000u),
                         __uint_as_float(h1.y << 16), __uint_as_float(h1.y & 0xffff0000u));
-                    if (want_gsq) { sq4(gsq, v0); sq4(gsq, v1); }
+                    if (want_gsq) { sq4(part, v0); sq4(part, v1); }
                     *reinterpret_cast<float4*>(Bs + row * BN + cb) = v0;
                     *reinterpret_cast<float4*>(Bs + row * BN + cb + BN / 2) = v1;
                 }
@@ -290,10 +291,11 @@ struct Loader {
                              : gld(static_cast<const float*>(L.B) + off);
                     if constexpr (XF == 2) v = xf1<true>(xf, v, gld(xf.w + k), xf.sgn * gld(xf.w + n), k, n);
                 }
-                if (want_gsq) gsq = fmaf(v, v, gsq);
+                if (want_gsq) part = fmaf(v, v, part);
                 Bs[row * BN + col] = v;
             }
         }
+        if (want_gsq) gsq += (double)part;
     }
 };
 
@@ -475,7 +477,11 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pendin
         return k0 < c0 + cw && c0 < k0 + BK;
     };
 
-    float gsq = 0.f;
+    // ||G||^2 over this thread's share of the whole K range: per-slab fp32
+    // sums accumulated in fp64 (one fp32 chain over thousands of positive
+    // terms drifts low by several 1e-6 relative, a bias the rescale would
+    // carry into every element of dW)
+    double gsq = 0.0;
     const int nslab = (L.K + BK - 1) / BK;
 
     Regs regs;
@@ -502,7 +508,7 @@ __device__ void gemm_tile(const GemmLayer& L, const GemmTile& tile, const Pendin
         __syncthreads();
     }
 
-    tile_epilogue<VEC, STAGE>(L, tile, acc, gsq, want_gsq, partials, red);
+    tile_epilogue<VEC, STAGE>(L, tile, acc, (float)gsq, want_gsq, partials, red);
 }
 
 constexpr int SMEM_BYTES = 4 * (2 * BK * (BM + BN) + NT / 64);

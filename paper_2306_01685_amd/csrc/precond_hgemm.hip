@@ -197,9 +197,12 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
 
     // rank-1 dot (and ||G||^2) of this thread's part of a Q row: row t / TPQ,
     // chunks h KC / TPQ .. (h + 1) KC / TPQ - 1, summed in a fixed order over
-    // the slabs
+    // the slabs.  The squares go into a short fp32 sum per slab, accumulated
+    // in fp64: one fp32 chain of K / TPQ positive terms drifts low by several
+    // 1e-6 relative, a bias the rescale would carry into every element of dW.
     const int rr = t / TPQ, rh = t % TPQ;
-    float rdot = 0.f, gsq = 0.f;
+    float rdot = 0.f;
+    double gsq = 0.0;
     const bool gsq_row = want_gsq && j0 + rr < J;
 
     for (int st = 0; st < NS - 1 && st < nst; ++st) issue(st);
@@ -248,6 +251,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         }
         if (PEND || want_gsq) {
             const lds_float* wsl = (const lds_float*)(smem + RING + (s % NS) * WSLOT);
+            float part = 0.f;
 #pragma unroll
             for (int e = 0; e < KC / TPQ; ++e) {
                 const int c = (KC / TPQ) * rh + e;
@@ -260,9 +264,10 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
                 }
                 if (STAGE == 1 && gsq_row) {
 #pragma unroll
-                    for (int x = 0; x < 8; ++x) gsq = fmaf(v[x], v[x], gsq);
+                    for (int x = 0; x < 8; ++x) part = fmaf(v[x], v[x], part);
                 }
             }
+            if (STAGE == 1 && gsq_row) gsq += (double)part;
         }
     }
 
@@ -346,7 +351,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     }
 
     // partials: block-wide fixed-order sums
-    const float part = STAGE == 1 ? gsq : csq;
+    const float part = STAGE == 1 ? (float)gsq : csq;
     const float ws = wave_sum(part);
     if (lane == 0) red[wave] = ws;
     __syncthreads();

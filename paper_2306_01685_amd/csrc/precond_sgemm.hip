@@ -518,13 +518,17 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int K = L.K, J = L.J;
     const float* w2 = L.w + K;
-    float sq = 0.f;   // this lane's part of ||Q||^2 over all its rows
+    // this lane's part of ||Q||^2: a short chain per row (K / 64 terms), the
+    // rows of a pass added as a tree, the passes chained.  One fp32 chain over
+    // all the block's rows (thousands of positive terms) drifts low by several
+    // 1e-6 relative, which the rescale would carry into every element of dW.
+    float sq = 0.f;
     for (int r0 = wave * RB; r0 < QD_ROWS; r0 += 4 * RB) {
         const int jb = b.rb * QD_ROWS + r0;
         if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
-        float dot[RB], dot2[RB];
+        float dot[RB], dot2[RB], sqr[RB];
 #pragma unroll
-        for (int i = 0; i < RB; ++i) dot[i] = dot2[i] = 0.f;
+        for (int i = 0; i < RB; ++i) dot[i] = dot2[i] = sqr[i] = 0.f;
         if (L.qf32) {
             const float* row = static_cast<const float*>(L.Q) + (size_t)jb * K;
             for (int k = 4 * lane; k < K; k += 256) {
@@ -533,7 +537,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
                     const float4 v = gld4(row + (size_t)i * K + k);
-                    sq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sq))));
+                    sqr[i] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sqr[i]))));
                     dot[i] = fmaf(v.x, wv.x, fmaf(v.y, wv.y, fmaf(v.z, wv.z, fmaf(v.w, wv.w, dot[i]))));
                     if (TWO) dot2[i] = fmaf(v.x, wv2.x, fmaf(v.y, wv2.y, fmaf(v.z, wv2.z, fmaf(v.w, wv2.w, dot2[i]))));
                 }
@@ -559,13 +563,14 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float v0 = __uint_as_float(h[e] << 16), v1 = __uint_as_float(h[e] & 0xffff0000u);
-                        sq = fmaf(v1, v1, fmaf(v0, v0, sq));
+                        sqr[i] = fmaf(v1, v1, fmaf(v0, v0, sqr[i]));
                         dot[i] = fmaf(v1, wv[2 * e + 1], fmaf(v0, wv[2 * e], dot[i]));
                         if (TWO) dot2[i] = fmaf(v1, wv2[2 * e + 1], fmaf(v0, wv2[2 * e], dot2[i]));
                     }
                 }
             }
         }
+        sq += ((sqr[0] + sqr[1]) + (sqr[2] + sqr[3])) + ((sqr[4] + sqr[5]) + (sqr[6] + sqr[7]));
         const float d = row_sums8(dot, lane);
         if ((lane & 7) == 0 && q.has) gst(L.rq + jb + (lane >> 3), d);
         if (TWO) {
