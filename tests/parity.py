@@ -10,10 +10,16 @@ import torch
 
 import oracle as O
 import workloads as W
+from oracle.half import layer_step_half, round_bf16
+from oracle.optimizer import lamb_step
 from paper_2306_01685_amd import Params, harness as H
 
 TOL_STEP = 1e-4   # relative Frobenius error after one step from the same state
 TOL_FREE = 1e-3   # after up to 50 independently accumulated steps
+# bf16 factors (bars derived in tests/test_half_gpu.py): dW after one step
+# from the same stored factors, and factors and dW after up to 50 steps
+TOL_HALF_STEP = 2e-4
+TOL_HALF_FREE = 2e-2
 NEAR_TIE = 1e-4   # |nu - eps| / eps band in which either stabiliser decision is accepted
 
 
@@ -57,14 +63,27 @@ class FreeRun:
 
     Inputs of sampled layers come from the workload generator; the other
     layers get seeded values drawn on the GPU (their values never reach a
-    checked output, layers being independent).
+    checked output, layers being independent).  half: bf16 factors, followed
+    by the half-precision oracle (its state is the unrounded factor; the
+    stored one is its bf16 rounding).  optimizer "lamb": every layer carries
+    weights and moments for the fused LAMB step.
     """
 
-    def __init__(self, w: W.Workload, params: Params, sample, explicit=False, bulk_seed=1234, gemm_path=None):
+    def __init__(self, w: W.Workload, params: Params, sample, explicit=False, bulk_seed=1234, gemm_path=None,
+                 half=False, optimizer=None):
         self.w, self.p, self.op = w, params, oparams(params)
         self.sample = list(sample)
         self.explicit = explicit
-        self.layers = H.allocate_layers(w.shapes, w.grad_dtype, gemm_path=gemm_path)
+        self.half = half
+        self.layers = H.allocate_layers(w.shapes, w.grad_dtype, gemm_path=None if half else gemm_path,
+                                        factor_dtype="bf16" if half else "fp32", optimizer=optimizer)
+        self.opt_state = {}
+        if optimizer is not None:
+            for i in self.sample:
+                d_in, d_out = w.shapes[i]
+                W0 = (np.random.default_rng(777 + i).standard_normal((d_in, d_out)) * 0.02).astype(np.float32)
+                self.layers[i]["W"].copy_(torch.from_numpy(W0))
+                self.opt_state[i] = [W0.astype(np.float64), np.zeros((d_in, d_out)), np.zeros((d_in, d_out))]
         self.gen = torch.Generator(device="cuda")
         self.gen.manual_seed(bulk_seed)
         self.state = {}
@@ -101,36 +120,80 @@ class FreeRun:
                     L["G"].normal_(0.0, self.w.G_std, generator=self.gen)
         return host
 
-    def step(self, precond_oracle=False):
-        """One step on both sides; returns the oracle's dW per sampled layer
-        when precond_oracle is set (else None)."""
+    def step(self, precond_oracle=False, update=True, opt=None):
+        """One step on both sides (update=False: the precondition-only call of
+        an update-every-f schedule; opt: an OptParams for the fused optimizer
+        step, followed by the oracle for the sampled layers' weights and
+        moments); returns the oracle's dW per sampled layer when precond_oracle
+        is set (else None)."""
         host = self._inputs(self.t)
-        self.plan.step(self.p)
+        if opt is not None:
+            (self.plan.step_opt if update else self.plan.precondition_opt)(self.p, opt)
+        else:
+            (self.plan.step if update else self.plan.precondition)(self.p)
         torch.cuda.synchronize()
         out = {}
         for i in self.sample:
             st = H.get_stats(self.layers[i])
             a, g, G = host[i]
             Lp, Rp = self.state[i]
-            Ln, sL = oracle_factor_step(Lp, a, self.op, st["stab_L"])
-            Rn, sR = oracle_factor_step(Rp, g, self.op, st["stab_R"])
+            if update and self.half:
+                # the half oracle updates from the stored (rounded) factor; it
+                # adopts the GPU's stabiliser decision only in the near-tie band
+                pre = precond_oracle or opt is not None
+                Ln, Rn, dWh, ost = layer_step_half(Lp, Rp, a, g, G, self.op, precond=pre)
+                ov = tuple(bool(st[f"stab_{s}"]) if (near_tie(fs.nu, self.op.eps) and fs.stab != bool(st[f"stab_{s}"]))
+                           else None for s, fs in (("L", ost.L), ("R", ost.R)))
+                if ov != (None, None):
+                    Ln, Rn, dWh, ost = layer_step_half(Lp, Rp, a, g, G, self.op, ov, precond=pre)
+                self.flags[i].append(((ost.L.stab, st["stab_L"], ost.L.nu), (ost.R.stab, st["stab_R"], ost.R.nu)))
+            elif update:
+                Ln, sL = oracle_factor_step(Lp, a, self.op, st["stab_L"])
+                Rn, sR = oracle_factor_step(Rp, g, self.op, st["stab_R"])
+                self.flags[i].append(((sL.stab, st["stab_L"], sL.nu), (sR.stab, st["stab_R"], sR.nu)))
+            else:
+                Ln, Rn = Lp, Rp
             self.state[i] = [Ln, Rn]
-            self.flags[i].append(((sL.stab, st["stab_L"], sL.nu), (sR.stab, st["stab_R"], sR.nu)))
-            if precond_oracle:
-                _, _, dW, ost = O.layer_step(Ln, Rn, a, g, G, self.op, update=False)
+            if precond_oracle or opt is not None:
+                if self.half:
+                    if not update:
+                        _, _, dWh, ost = layer_step_half(Ln, Rn, a, g, G, self.op, update=False)
+                    dW = dWh
+                else:
+                    _, _, dW, ost = O.layer_step(Ln, Rn, a, g, G, self.op, update=False)
                 out[i] = (dW, ost)
+                if opt is not None and i in self.opt_state:
+                    Wo, mo, vo = self.opt_state[i]
+                    F = lambda x: float(np.float32(x))  # noqa: E731  (the ABI takes fp32 hyper-parameters)
+                    self.opt_state[i][:] = list(lamb_step(Wo, mo, vo, dW, opt.step, F(opt.lr), F(opt.beta1),
+                                                          F(opt.beta2), F(opt.eps), F(opt.weight_decay)))[:3]
         self.t += 1
         return out if precond_oracle else None
 
+    def check_optimizer(self, tol):
+        """Weights and moments of the sampled layers against the oracle's."""
+        worst = 0.0
+        for i, (Wo, mo, vo) in self.opt_state.items():
+            L = self.layers[i]
+            for name, x, y in (("W", L["W"], Wo), ("m", L["opt_m"], mo), ("v", L["opt_v"], vo)):
+                e = rel(x.cpu().numpy(), y)
+                worst = max(worst, e)
+                assert e <= tol, (self.w.name, i, self.t, name, e)
+        return worst
+
     def check_factors(self, tol):
         """Writes the current factors into their buffers (the plan keeps the
-        last update pending) and compares them with the oracle's."""
+        last update pending) and compares them with the oracle's (bf16
+        factors: with the bf16 rounding of the oracle's)."""
         self.plan.sync_factors()
         torch.cuda.synchronize()
         worst = 0.0
         for i in self.sample:
             Lg, Rg = H.get_factors(self.layers[i])
-            eL, eR = rel(Lg, self.state[i][0]), rel(Rg, self.state[i][1])
+            Lo, Ro = self.state[i]
+            if self.half:
+                Lo, Ro = round_bf16(Lo), round_bf16(Ro)
+            eL, eR = rel(Lg, Lo), rel(Rg, Ro)
             worst = max(worst, eL, eR)
             assert eL <= tol and eR <= tol, (self.w.name, i, self.t, eL, eR)
         return worst

@@ -19,8 +19,8 @@ import torch
 
 import oracle as O
 import workloads as W
-from paper_2306_01685_amd import Params, harness as H
-from tests.parity import TOL_FREE, TOL_STEP, FreeRun, rel
+from paper_2306_01685_amd import OPT_LAMB, OptParams, Params, harness as H
+from tests.parity import TOL_FREE, TOL_HALF_FREE, TOL_HALF_STEP, TOL_STEP, FreeRun, rel
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -75,6 +75,55 @@ def test_gpt2_xl_explicit_student_t_means_one_step():
     out = fr.step(precond_oracle=True)
     e = (fr.check_factors(TOL_STEP), fr.check_dW(out, TOL_STEP))
     print("gpt2-xl explicit Student-t means, step 1 worst errors (factors, dW)", e)
+
+
+def test_bert_large_bf16_factors_20_steps():
+    """The bench's half-precision leg: all 144 layers with bf16 factors in one
+    grouped launch per kernel, 20 steps; the half-precision oracle follows a
+    1024 x 1024 and a 4096 x 1024 layer (stored factors against the bf16
+    rounding of its factors)."""
+    w = W.CONFIGS[3]
+    fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 5], half=True)
+    worst = {}
+    for t in range(20):
+        check = (t + 1) in (1, 19, 20)
+        out = fr.step(precond_oracle=check)
+        if check:
+            tf, td = (1e-3, TOL_HALF_STEP) if t == 0 else (TOL_HALF_FREE, TOL_HALF_FREE)
+            worst[t + 1] = (fr.check_factors(tf), fr.check_dW(out, td))
+    fr.check_flags()
+    print("bert-large bf16 factors worst errors", worst)
+
+
+def test_bert_large_update_every_10_steps():
+    """The bench's schedule_f10 leg on the default path: factors updated on
+    steps 1 and 11, the steps between precondition with the stale factors
+    (pending terms held across them); dW of update and precondition-only steps
+    against the oracle, factors at the end."""
+    w = W.CONFIGS[3]
+    fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 4, 5])
+    worst = {}
+    for t in range(13):
+        update = t % 10 == 0
+        check = t in (0, 1, 9, 10, 12)
+        out = fr.step(precond_oracle=check, update=update)
+        if check:
+            worst[t + 1] = fr.check_dW(out, TOL_STEP if t <= 1 else TOL_FREE)
+    worst["factors"] = fr.check_factors(TOL_FREE)
+    print("bert-large update every 10 worst errors", worst)
+
+
+def test_bert_large_fused_lamb_3_steps():
+    """The bench's fused-optimizer leg: all 144 layers with weights and LAMB
+    moments, three mkor_step_opt calls; dW, weights and moments of two sampled
+    layers against the oracle."""
+    w = W.CONFIGS[3]
+    fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 5], optimizer="lamb")
+    worst = []
+    for t in range(3):
+        out = fr.step(precond_oracle=True, opt=OptParams(kind=OPT_LAMB, step=t + 1, lr=1e-3, store_dw=True))
+        worst.append((fr.check_dW(out, TOL_STEP), fr.check_optimizer(TOL_STEP)))
+    print("bert-large fused LAMB worst errors (dW, W/m/v)", worst)
 
 
 def _sampled_rows_check(L, Lo, Ro, G, rows, tol):

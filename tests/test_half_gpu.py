@@ -32,12 +32,10 @@ import oracle as O
 import workloads as W
 from oracle.half import layer_step_half, round_bf16
 from paper_2306_01685_amd import Params, harness as H, SM_PAPER_EQ6
-from tests.parity import oparams, rel, spd
+from tests.parity import TOL_HALF_FREE, TOL_HALF_STEP, oparams, rel, spd
 
 pytestmark = pytest.mark.gpu
 
-TOL_HALF_STEP = 2e-4
-TOL_HALF_FREE = 2e-2
 NEAR_MID_ULPS = 16   # fp32 ulps of the update's term magnitude
 
 # multiples of 64 (the bf16 path's requirement) that span several 256 x 128
