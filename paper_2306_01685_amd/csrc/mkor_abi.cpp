@@ -264,12 +264,18 @@ std::vector<GemmTile> schedule_tiles(const mkor_layer* layers, int32_t n, int st
     return table;
 }
 
+// Rows per qdot_kernel block of a split layer: its stage-1 Q is G or G^T, rows
+// of K elements in G's dtype.
+int32_t qd_rows_of(const mkor_layer& L) {
+    return qd_rows(stage_geom(L, 1).K, L.grad_dtype == MKOR_DTYPE_BF16 ? 2 : 4);
+}
+
 // ||G||^2 partials of a layer (one per stage-1 tile column for fp32 factors,
 // one per stage-1 tile column, i.e. per block of G rows, for bf16 factors) and
 // ||dW_hat||^2 partials (one per tile of the stage that writes dW_hat).
 int64_t gpart_count(const mkor_layer& L) {
     const StageGeom g = stage_geom(L, 1);
-    if (is_split(L)) return ceil_div(g.cols, QD_ROWS);   // one per qdot_kernel block
+    if (is_split(L)) return ceil_div(g.cols, qd_rows_of(L));   // one per qdot_kernel block
     return ceil_div(g.cols, g.bn);
 }
 int64_t dpart_count(const mkor_layer& L) {
@@ -595,7 +601,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             A.qf32 = 0; A.fq = 0; A.wide = s1.bm == SG_BI1H;
             A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
             A.mode = mode_d + i;
-            for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
+            for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r, qd_rows_of(L)};
             HgLayer& B = s2l[i];
             B.P = X; B.Q = L.Rinv; B.C = L.dW;
             B.pend = fR.pend; B.w = fR.w;
@@ -620,7 +626,7 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
             A.qf32 = bf16 ? 0 : 1; A.fq = 0; A.wide = s1.bm == SG_BI1H;
             A.rq = reinterpret_cast<float*>(base + lo.rq_off[i]);
             A.mode = mode_d + i;
-            for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r};
+            for (int32_t r = 0; r < ngp; ++r) qdb[nqb++] = QdBlock{i, r, qd_rows_of(L)};
             HgLayer& B = s2l[i];
             B.P = L.Linv; B.Q = Yt; B.C = L.dW;
             B.pend = fL.pend; B.w = fL.w;

@@ -161,10 +161,13 @@ constexpr GemmShape GEMM_SHAPE[2] = {GemmShape{MKOR_GEMM1_SHAPE}, GemmShape{MKOR
 // Tile scheduling: workgroup b of a launch runs on XCD b % GEMM_XCDS (the
 // hardware's round-robin dispatch), and each XCD takes super-tiles of one
 // layer covering up to GEMM_SUPER x GEMM_SUPER outputs, so the tiles that run
-// together on an XCD share their operand panels in that XCD's L2.
+// together on an XCD share their operand panels in that XCD's L2.  2048: a
+// 4096-row layer's first GEMM is two super-tiles of 32 tiles (one per CU of
+// an XCD) rather than four of 16, which halves the re-reads of its Q panel by
+// other XCDs (1024 and 4096 measured slower).
 constexpr int GEMM_XCDS = 8;
 #ifndef MKOR_GEMM_SUPER
-#define MKOR_GEMM_SUPER 1024
+#define MKOR_GEMM_SUPER 2048
 #endif
 constexpr int GEMM_SUPER = MKOR_GEMM_SUPER;
 
@@ -198,10 +201,18 @@ constexpr int HG_THREADS = 64 * (HG_BI / 128) * (HG_BJ / HG_TJ);
 constexpr int HG_NS = MKOR_HG_NS;                       // stages of the LDS ring
 constexpr int SG_BI = 256, SG_BJ = 256;                  // tile of C of the split GEMMs (sgemm)
 constexpr int SG_BI1H = 128, SG_BJ1H = 512;              // ... of the first one when Q is bf16
-#ifndef MKOR_QD_ROWS
-#define MKOR_QD_ROWS 256
+// qdot_kernel blocks: Q rows in multiples of 32 (4 waves x 8 rows per pass),
+// as many as make about QD_BYTES of Q, between 32 and QD_MAX_ROWS, so that a
+// layer with long rows does not form the tail
+#ifndef MKOR_QD_BYTES
+#define MKOR_QD_BYTES (512 << 10)
 #endif
-constexpr int QD_ROWS = MKOR_QD_ROWS;                    // Q rows per qdot_kernel block
+constexpr int QD_MAX_ROWS = 256;
+constexpr int64_t QD_BYTES = MKOR_QD_BYTES;
+constexpr int32_t qd_rows(int32_t K, int32_t elem_bytes) {
+    const int64_t r = QD_BYTES / ((int64_t)K * elem_bytes) / 32 * 32;
+    return r < 32 ? 32 : (r > QD_MAX_ROWS ? QD_MAX_ROWS : (int32_t)r);
+}
 constexpr int HG_BK = MKOR_HG_BK;                       // k per stage
 
 // Layer descriptor of the bf16-MFMA preconditioning stages (C = P_eff Q^T):
@@ -223,10 +234,12 @@ struct HgLayer {
     const int32_t* mode;   // the layer's mode word
 };
 
-// Rows of the stage-1 Q operand of the split GEMMs, one block of QD_ROWS rows
-// per workgroup: (Q w) for the pending term and the ||G||^2 partial
+// Rows of the stage-1 Q operand of the split GEMMs, one block of `rows` rows
+// per workgroup (qd_rows of the layer): (Q w) for the pending term and the
+// ||G||^2 partial
 struct QdBlock {
     int32_t layer, rb;     // index into the stage-1 layer table, row block
+    int32_t rows;          // rows per block of this layer (a multiple of 32)
 };
 
 // bf16 transposes (G^T for the split GEMMs that contract over d_in)

@@ -523,8 +523,8 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
     // all the block's rows (thousands of positive terms) drifts low by several
     // 1e-6 relative, which the rescale would carry into every element of dW.
     float sq = 0.f;
-    for (int r0 = wave * RB; r0 < QD_ROWS; r0 += 4 * RB) {
-        const int jb = b.rb * QD_ROWS + r0;
+    for (int r0 = wave * RB; r0 < b.rows; r0 += 4 * RB) {
+        const int jb = b.rb * b.rows + r0;
         if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
         float dot[RB], dot2[RB], sqr[RB];
 #pragma unroll
@@ -586,7 +586,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 
 // Stage-1 Q rows ahead of the first split GEMM: (Q w)[j] for each pending
 // term of the factor (one, or two for a lazy factor) and the ||G||^2 partial
-// of the block of QD_ROWS rows (Q is G, or G^T: the same elements).  Four
+// of the block of rows (Q is G, or G^T: the same elements).  Four
 // waves take 8 rows at a time (8 loads in flight per lane); lanes take
 // 16-byte chunks with a stride of 64 chunks, then fixed-order wave sums:
 // deterministic.
