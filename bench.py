@@ -112,9 +112,12 @@ def parse():
                          "headline metric")
     ap.add_argument("--no-schedule", action="store_true",
                     help="skip the update-every-10-steps measurement")
-    ap.add_argument("--mode", choices=["step", "copy"], default="step",
+    ap.add_argument("--mode", choices=["step", "copy", "power"], default="step",
                     help="copy: time a plain device-to-device copy of --copy-mib MiB (the reference "
-                         "kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures)")
+                         "kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures); "
+                         "power: run the step and single GEMM stages back to back, --power-seconds "
+                         "each, while sampling board power and clocks with amd-smi")
+    ap.add_argument("--power-seconds", type=float, default=6.0)
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--factor-dtype", choices=["fp32", "bf16"], default="fp32",
                     help="storage type of the inverse factors of the timed run (bf16: the "
@@ -593,6 +596,101 @@ def initial_factors_stored(w, i, half):
     return L0, R0
 
 
+def _smi_sample():
+    """One reading of socket power (W) and the mean graphics clock of the XCDs
+    (MHz) from `amd-smi metric` (read-only), or None."""
+    import subprocess
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-g", "0", "-p", "-c", "--json"],
+                           capture_output=True, text=True, timeout=15)
+        g = json.loads(r.stdout)["gpu_data"][0]
+        clks = [v["clk"]["value"] for k, v in g["clock"].items()
+                if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v["clk"]["value"], (int, float))]
+        return float(g["power"]["socket_power"]["value"]), statistics.mean(clks)
+    except Exception:  # noqa: BLE001  (tool missing, or a field not reported)
+        return None
+
+
+def power_profile(args):
+    """--mode power: the step and its GEMM stages (split, bf16 factors, fp32
+    MFMA) and the rescale, each launched back to back for --power-seconds,
+    with board power and graphics clock sampled by a background thread.  The
+    first 1.5 s of each phase are left out (the clock settles)."""
+    import threading
+
+    import torch
+
+    import workloads as W
+    from paper_2306_01685_amd import STAGE_NAMES, Params, harness as H
+
+    w = W.CONFIGS[args.config]
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            t, v = time.time(), _smi_sample()
+            if v is not None:
+                samples.append((t, *v))
+            time.sleep(0.1)
+
+    def make(factor_dtype, gemm_path):
+        layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, factor_dtype=factor_dtype,
+                                   gemm_path=None if factor_dtype == "bf16" else gemm_path)
+        fill_inputs(layers, w)
+        plan = H.make_plan(layers)
+        p = Params(gamma=w.gamma, zeta=0.5, eps=args.eps)
+        for _ in range(3):
+            plan.step(p)
+        torch.cuda.synchronize()
+        return layers, plan, p
+
+    phases = []
+
+    def phase(name, fn):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0, n = time.time(), 0
+        e0.record()
+        while time.time() - t0 < args.power_seconds:
+            for _ in range(5):
+                fn()
+            n += 5
+            torch.cuda.synchronize()
+        e1.record()
+        torch.cuda.synchronize()
+        phases.append(dict(name=name, t0=t0, t1=time.time(), calls=n, ms_per_call=e0.elapsed_time(e1) / n))
+
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    t_idle = time.time()
+    time.sleep(3.0)
+    phases.append(dict(name="idle", t0=t_idle - 1.5, t1=time.time(), calls=0, ms_per_call=0.0))
+    stage = {n: i for i, n in enumerate(STAGE_NAMES)}
+    if split_eligible(w, "auto"):
+        runs = [("fp32", "auto", "split"), ("bf16", None, "bf16_factors"), ("fp32", "fp32", "fp32_mfma")]
+    else:
+        runs = [("fp32", "fp32", "fp32_mfma"), ("bf16", None, "bf16_factors")]
+    for fdt, path, tag in runs:
+        layers, plan, p = make(fdt, path)
+        phase(f"{tag}: step", lambda: plan.step(p))
+        phase(f"{tag}: first GEMM", lambda: plan.run_stage(p, stage["gemm_xt"]))
+        phase(f"{tag}: second GEMM", lambda: plan.run_stage(p, stage["gemm_dw"]))
+        if tag == "split":
+            phase("rescale", lambda: plan.run_stage(p, stage["rescale"]))
+        del plan, layers
+        torch.cuda.empty_cache()
+    stop.set()
+    th.join(timeout=30)
+    out = []
+    for ph in phases:
+        xs = [x for x in samples if ph["t0"] + 1.5 <= x[0] <= ph["t1"]]
+        out.append(dict(name=ph["name"], ms_per_call=ph["ms_per_call"], samples=len(xs),
+                        power_w=statistics.median([x[1] for x in xs]) if xs else None,
+                        gfx_mhz=statistics.median([x[2] for x in xs]) if xs else None))
+    print(json.dumps({"mode": "power", "workload": workload_desc(w), "phases": out,
+                      "note": "board (socket) power and mean graphics clock of the 8 XCDs, medians"}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -602,6 +700,9 @@ def main():
 
     if args.mode == "copy":
         copy_reference(args)
+        return
+    if args.mode == "power":
+        power_profile(args)
         return
 
     import torch
