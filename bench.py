@@ -462,7 +462,7 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                         traffic=None if traffic is None else traffic["total_bytes"],
                         per_launch=f"{k['alg_bytes']:.4e} B")
         roof["traffic_detail"] = traffic
-        # the SM update is the benchmark spec's other roofline: report it beside (its
+        # the SM update, the step's bandwidth-bound half: its roofline beside (its
         # traffic differs with the GEMM path: only the split path writes some
         # factors every other step)
         k = kernels["sm_pass"]
@@ -623,7 +623,7 @@ def power_profile(args):
     import workloads as W
     from paper_2306_01685_amd import STAGE_NAMES, Params, harness as H
 
-    w = W.CONFIGS[args.config]
+    w = W.WORKLOADS[args.config]
     samples, stop = [], threading.Event()
 
     def sampler():
@@ -712,7 +712,7 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    w = W.CONFIGS[args.config]
+    w = W.WORKLOADS[args.config]
     ms_step, kernels, roof, schedule, extra = measure(w, args, args.factor_dtype, args.gemm_path)
     value = w.n_layers / (ms_step / 1e3)
     fp32_path = None

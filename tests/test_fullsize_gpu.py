@@ -25,8 +25,7 @@ from tests.parity import TOL_FREE, TOL_HALF_FREE, TOL_HALF_STEP, TOL_STEP, FreeR
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 
-def _free_run(cfg, steps, eps, sample, check_steps, gemm_path=None):
-    w = W.CONFIGS[cfg]
+def _free_run(w, steps, eps, sample, check_steps, gemm_path=None):
     fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=eps), sample=sample, gemm_path=gemm_path)
     worst = {}
     for t in range(steps):
@@ -40,7 +39,7 @@ def _free_run(cfg, steps, eps, sample, check_steps, gemm_path=None):
 
 
 def test_bert_base_72_layers_50_steps():
-    fr, worst, fired = _free_run(2, 50, 100.0, sample=[0, 4, 5], check_steps={1, 49, 50})
+    fr, worst, fired = _free_run(W.BERT_BASE, 50, 100.0, sample=[0, 4, 5], check_steps={1, 49, 50})
     print("bert-base worst errors", worst, "stabiliser fired", fired)
     assert fired > 0
 
@@ -49,7 +48,7 @@ def test_bert_base_72_layers_50_steps():
 def test_bert_large_144_layers_50_steps(gemm_path):
     """auto: the split path (every shape is a multiple of 64), as timed by the
     bench; fp32: the fp32 MFMA path."""
-    fr, worst, fired = _free_run(3, 50, 100.0, sample=[0, 4, 5, 138], check_steps={1, 49, 50},
+    fr, worst, fired = _free_run(W.BERT_LARGE, 50, 100.0, sample=[0, 4, 5, 138], check_steps={1, 49, 50},
                                  gemm_path=gemm_path)
     print("bert-large", gemm_path, "worst errors", worst, "stabiliser fired", fired)
     assert fired > 0
@@ -60,7 +59,7 @@ def test_gpt2_xl_192_layers_two_blocks_50_steps(gemm_path):
     """GPT-2-XL set: all 192 layers stepped 50 times; the oracle follows two
     blocks (8 layers, every shape twice: 1600x4800, 1600x1600, 1600x6400,
     6400x1600).  eps = 100 fires within the run."""
-    fr, worst, fired = _free_run(5, 50, 100.0, sample=list(range(8)), check_steps={1, 49, 50},
+    fr, worst, fired = _free_run(W.GPT2_XL, 50, 100.0, sample=list(range(8)), check_steps={1, 49, 50},
                                  gemm_path=gemm_path)
     print("gpt2-xl", gemm_path, "worst errors", worst, "stabiliser fired", fired)
     assert fired > 0
@@ -70,7 +69,7 @@ def test_gpt2_xl_explicit_student_t_means_one_step():
     """One step of the GPT-2-XL set with the rank-1 means of one block formed
     explicitly from 32768 Student-t(4) activation rows and 32768 N(0, 1e-6)
     gradient rows (the other tests draw the mean's distribution directly)."""
-    w = W.CONFIGS[5]
+    w = W.GPT2_XL
     fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 1, 2, 3], explicit=True)
     out = fr.step(precond_oracle=True)
     e = (fr.check_factors(TOL_STEP), fr.check_dW(out, TOL_STEP))
@@ -82,7 +81,7 @@ def test_bert_large_bf16_factors_20_steps():
     grouped launch per kernel, 20 steps; the half-precision oracle follows a
     1024 x 1024 and a 4096 x 1024 layer (stored factors against the bf16
     rounding of its factors)."""
-    w = W.CONFIGS[3]
+    w = W.BERT_LARGE
     fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 5], half=True)
     worst = {}
     for t in range(20):
@@ -100,7 +99,7 @@ def test_bert_large_update_every_10_steps():
     steps 1 and 11, the steps between precondition with the stale factors
     (pending terms held across them); dW of update and precondition-only steps
     against the oracle, factors at the end."""
-    w = W.CONFIGS[3]
+    w = W.BERT_LARGE
     fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 4, 5])
     worst = {}
     for t in range(13):
@@ -117,7 +116,7 @@ def test_bert_large_fused_lamb_3_steps():
     """The bench's fused-optimizer leg: all 144 layers with weights and LAMB
     moments, three mkor_step_opt calls; dW, weights and moments of two sampled
     layers against the oracle."""
-    w = W.CONFIGS[3]
+    w = W.BERT_LARGE
     fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=100.0), sample=[0, 5], optimizer="lamb")
     worst = []
     for t in range(3):
@@ -143,7 +142,7 @@ def _sampled_rows_check(L, Lo, Ro, G, rows, tol):
 def test_single_8192_layer_20_steps():
     """8192 x 8192, perturbed SPD init, gamma = 0.95, 20 steps; eps = 2 fires
     around step 13."""
-    w = W.CONFIGS[4]
+    w = W.SINGLE_8192
     fr = FreeRun(w, Params(gamma=w.gamma, zeta=0.5, eps=2.0), sample=[0])
     rows = np.random.default_rng(5).choice(8192, size=96, replace=False)
     G_last = None

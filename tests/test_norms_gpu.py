@@ -26,8 +26,9 @@ pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 TOL_NORM_G = 2e-7   # |recorded ||G|| / ||G||_fp64 - 1|
 TOL_RATIO = 2e-7    # | ||dW|| / ||G|| - 1 |
 
-CASES = [(3, dict(gemm_path="auto")), (3, dict(gemm_path="fp32")), (3, dict(factor_dtype="bf16")),
-         (5, dict(gemm_path="auto")), (5, dict(gemm_path="fp32"))]
+CASES = [(W.BERT_LARGE, dict(gemm_path="auto")), (W.BERT_LARGE, dict(gemm_path="fp32")),
+         (W.BERT_LARGE, dict(factor_dtype="bf16")), (W.GPT2_XL, dict(gemm_path="auto")),
+         (W.GPT2_XL, dict(gemm_path="fp32"))]
 
 
 def _fill(layers, w, gen):
@@ -41,13 +42,12 @@ def _fill(layers, w, gen):
         L["G"].copy_(t)   # rounded to nearest for a bf16 G
 
 
-@pytest.mark.parametrize("cfg,kw", CASES, ids=[f"cfg{c}-{next(iter(k.values()))}" for c, k in CASES])
-def test_rescale_norms_every_layer(cfg, kw):
-    w = W.CONFIGS[cfg]
+@pytest.mark.parametrize("w,kw", CASES, ids=[f"{w.name}-{next(iter(k.values()))}" for w, k in CASES])
+def test_rescale_norms_every_layer(w, kw):
     layers = H.allocate_layers(w.shapes, w.grad_dtype, **kw)
     plan = H.make_plan(layers)
     gen = torch.Generator(device="cuda")
-    gen.manual_seed(9000 + cfg)
+    gen.manual_seed(9000 + w.cid)
     p = Params(gamma=w.gamma, zeta=0.5, eps=100.0)
     worst_g = worst_r = 0.0
     for t in range(3):

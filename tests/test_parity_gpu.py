@@ -103,7 +103,7 @@ def test_update_factors_single_step(variant, norm_kind, eps):
 
 @pytest.mark.parametrize("eps", [math.inf, 4.0])
 def test_cfg1_free_running(eps):
-    w = W.CONFIGS[1]
+    w = W.SINGLE_64
     fr = FreeRun(w, Params(gamma=w.gamma, eps=eps), sample=[0], explicit=True)
     for t in range(w.steps):
         out = fr.step(precond_oracle=True)

@@ -123,7 +123,7 @@ def test_update_every_f_steps():
 def test_bert_large_means_from_16384_bf16_rows():
     """Full BERT-Large layer set with 16384 bf16 token rows per layer (14.5 GB of
     rows): means of sampled layers against the oracle, one full step."""
-    w = W.CONFIGS[3]
+    w = W.BERT_LARGE
     sample = [0, 4, 5]
     layers = H.allocate_layers(w.shapes, w.grad_dtype, stats=False, rows=w.rows, act_dtype="bf16")
     gen = torch.Generator(device="cuda")

@@ -6,19 +6,19 @@ import workloads as W
 
 
 def test_config_shapes():
-    assert W.CONFIGS[1].shapes == ((64, 64),)
-    assert W.CONFIGS[2].n_layers == 72
-    assert W.CONFIGS[3].n_layers == 144 and W.CONFIGS[3].grad_dtype == "bf16"
-    assert W.CONFIGS[4].shapes == ((8192, 8192),) and W.CONFIGS[4].gamma == 0.95
-    assert W.CONFIGS[5].n_layers == 192
+    assert W.SINGLE_64.shapes == ((64, 64),)
+    assert W.BERT_BASE.n_layers == 72
+    assert W.BERT_LARGE.n_layers == 144 and W.BERT_LARGE.grad_dtype == "bf16"
+    assert W.SINGLE_8192.shapes == ((8192, 8192),) and W.SINGLE_8192.gamma == 0.95
+    assert W.GPT2_XL.n_layers == 192
     # algorithmic sizes used for the roofline (factor elements, precondition flops)
-    assert W.CONFIGS[3].factor_elems == 1_056_964_608
-    assert abs(W.CONFIGS[3].precond_flops - 2.474e12) / 2.474e12 < 1e-3
-    assert abs(W.CONFIGS[5].precond_flops - 21.23e12) / 21.23e12 < 1e-3
+    assert W.BERT_LARGE.factor_elems == 1_056_964_608
+    assert abs(W.BERT_LARGE.precond_flops - 2.474e12) / 2.474e12 < 1e-3
+    assert abs(W.GPT2_XL.precond_flops - 21.23e12) / 21.23e12 < 1e-3
 
 
 def test_reproducible_and_independent():
-    w = W.CONFIGS[2]
+    w = W.BERT_BASE
     a1, g1 = W.rank1_vectors(w, 5, 3)
     a2, g2 = W.rank1_vectors(w, 5, 3)
     np.testing.assert_array_equal(a1, a2)
@@ -55,7 +55,7 @@ def test_bf16_rounding():
     torch = pytest.importorskip("torch")
     t = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
     np.testing.assert_array_equal(r, t)
-    G = W.gradient(W.CONFIGS[3], 0, 0)
+    G = W.gradient(W.BERT_LARGE, 0, 0)
     assert (G.view(np.uint32) & 0xFFFF == 0).all()
 
 
@@ -69,7 +69,7 @@ def test_perturbed_init_spd_symmetric():
 
 
 def test_token_rows_seeded_and_shaped():
-    w = W.CONFIGS[1]
+    w = W.SINGLE_64
     A, Go = W.token_rows(w, 0, 3)
     assert A.shape == (32, 64) and Go.shape == (32, 64) and A.dtype == np.float32
     A2, Go2 = W.token_rows(w, 0, 3)

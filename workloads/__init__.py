@@ -67,17 +67,18 @@ def _mk(cid, name, blocks, block_shapes, **kw):
                     blocks=blocks, block_shapes=tuple(block_shapes), **kw)
 
 
-CONFIGS = {
-    1: _mk(1, "single-64x64", 1, [(64, 64)], grad_dtype="fp32", gamma=0.9, steps=20, rows=32),
-    2: _mk(2, "bert-base-72", 12, [(768, 768)] * 4 + [(768, 3072), (3072, 768)],
-           grad_dtype="fp32", gamma=0.9, steps=50, rows=8192),
-    3: _mk(3, "bert-large-144", 24, [(1024, 1024)] * 4 + [(1024, 4096), (4096, 1024)],
-           grad_dtype="bf16", gamma=0.9, steps=50, rows=16384),
-    4: _mk(4, "single-8192x8192", 1, [(8192, 8192)], grad_dtype="fp32", gamma=0.95,
-           steps=20, rows=8192, init="perturbed"),
-    5: _mk(5, "gpt2-xl-192", 48, [(1600, 4800), (1600, 1600), (1600, 6400), (6400, 1600)],
-           grad_dtype="bf16", gamma=0.9, steps=50, rows=32768, act_dist="student_t4"),
-}
+SINGLE_64 = _mk(1, "single-64x64", 1, [(64, 64)], grad_dtype="fp32", gamma=0.9, steps=20, rows=32)
+BERT_BASE = _mk(2, "bert-base-72", 12, [(768, 768)] * 4 + [(768, 3072), (3072, 768)],
+                grad_dtype="fp32", gamma=0.9, steps=50, rows=8192)
+BERT_LARGE = _mk(3, "bert-large-144", 24, [(1024, 1024)] * 4 + [(1024, 4096), (4096, 1024)],
+                 grad_dtype="bf16", gamma=0.9, steps=50, rows=16384)
+SINGLE_8192 = _mk(4, "single-8192x8192", 1, [(8192, 8192)], grad_dtype="fp32", gamma=0.95,
+                  steps=20, rows=8192, init="perturbed")
+GPT2_XL = _mk(5, "gpt2-xl-192", 48, [(1600, 4800), (1600, 1600), (1600, 6400), (6400, 1600)],
+              grad_dtype="bf16", gamma=0.9, steps=50, rows=32768, act_dist="student_t4")
+
+# by workload number (bench.py --config N; the number also keys the seeded streams)
+WORKLOADS = {w.cid: w for w in (SINGLE_64, BERT_BASE, BERT_LARGE, SINGLE_8192, GPT2_XL)}
 
 
 def rng(cid: int, layer: int, step: int, kind: int) -> np.random.Generator:
