@@ -54,6 +54,17 @@ __device__ __forceinline__ void gst4_nt(float* p, const float4& v) {
     __builtin_nontemporal_store(w, (MKOR_GLOBAL mk_f4*)p);
 }
 
+__device__ __forceinline__ uint4 gld_u4_nt(const void* p) {
+    const mk_u4 v = __builtin_nontemporal_load((const MKOR_GLOBAL mk_u4*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void gst_u4_nt(void* p, const uint4& v) {
+    mk_u4 w;
+    w.x = v.x; w.y = v.y; w.z = v.z; w.w = v.w;
+    __builtin_nontemporal_store(w, (MKOR_GLOBAL mk_u4*)p);
+}
+
 // base (wave-uniform) + 32-bit byte offset: the form of the scalar-base
 // addressing mode, so per-thread addresses need one 32-bit register.
 __device__ __forceinline__ float4 gld4_off(const void* base, unsigned byte_off) {

@@ -174,7 +174,7 @@ __device__ __forceinline__ void pass_rows8h(const FactorDesc& f, const Pending& 
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
             if (!FULL && r >= nr) continue;
-            h[r] = gld_u4(P16 + (size_t)r * d + 8 * j);
+            h[r] = MKOR_SM_NT_HALF ? gld_u4_nt(P16 + (size_t)r * d + 8 * j) : gld_u4(P16 + (size_t)r * d + 8 * j);
         }
         float xv[8], wv[8];
         if constexpr (MV) {
@@ -202,7 +202,8 @@ __device__ __forceinline__ void pass_rows8h(const FactorDesc& f, const Pending& 
                         if ((row & 7) == e) p[e] = __fadd_rn(p[e], q.c2);
                 }
                 const uint4 hn = pack8(p);
-                gst_u4(P16 + (size_t)r * d + 8 * j, hn);
+                if (MKOR_SM_NT_HALF) gst_u4_nt(P16 + (size_t)r * d + 8 * j, hn);
+                else                 gst_u4(P16 + (size_t)r * d + 8 * j, hn);
                 unpack8(hn, p);   // the stored (rounded) values are the factor from now on
             }
             if constexpr (MV) {
