@@ -431,3 +431,105 @@ def test_entry_points_open_roctx_ranges(lib):
     import subprocess
     out = subprocess.run(["nm", "-D", "--undefined-only", M.LIB_PATH], capture_output=True, text=True).stdout
     assert "roctxRangePushA" in out and "roctxRangePop" in out
+
+
+# ------------------------------------------------------------------ property-based fuzz of validation
+
+from hypothesis import HealthCheck, given, settings, strategies as hst  # noqa: E402
+
+FUZZ_DIMS = [-1, 0, 1, 3, 37, 64, 100, 128, 192, 1024, M.MAX_DIM, M.MAX_DIM + 1]
+PTR_KEYS = ["Linv", "Rinv", "a", "g", "G", "dW", "stats", "A", "Gout"]
+
+
+def _mutate(L, other, kind, key):
+    if kind == "null" and key in PTR_KEYS:
+        L[key] = None
+    elif kind == "misalign" and key in PTR_KEYS and L.get(key):
+        L[key] += 4
+    elif kind == "alias_out":
+        L["dW"] = L["G"]
+    elif kind == "overlap_factors":
+        L["Rinv"] = L["Linv"] + 256
+    elif kind == "cross_layer" and other is not None:
+        L["dW"] = other["dW"]
+    elif kind == "bad_code":
+        L[key if key in ("grad_dtype", "factor_dtype", "act_dtype", "gemm_path", "second_order")
+          else "grad_dtype"] = 7
+
+
+def _valid_layer(fk, data):
+    """A layer that satisfies every documented constraint."""
+    d_in, d_out = (data.draw(hst.sampled_from([1, 3, 37, 64, 100, 128, 192, 1024])) for _ in range(2))
+    m64 = d_in % 64 == 0 and d_out % 64 == 0
+    so = data.draw(hst.sampled_from([0, 1, 1]))
+    rows = data.draw(hst.sampled_from([0, 0, 1, 128]))
+    fdt = data.draw(hst.sampled_from([0, 1])) if m64 else 0
+    rank = data.draw(hst.sampled_from([0, 1, 2, 4])) if (so and fdt == 0 and rows == 0) else 0
+    L = layer(fk, d_in, d_out, so=so, dt=data.draw(hst.sampled_from([0, 1])), stats=data.draw(hst.booleans()),
+              rows=rows, adt=data.draw(hst.sampled_from([0, 1])), fdt=fdt, rank=rank)
+    L["gemm_path"] = data.draw(hst.sampled_from([0, 1, 2] if m64 else [0, 1]))
+    return L
+
+
+def _random_layer(fk, data, prev):
+    """A layer with random, often out-of-range values and up to two mutations."""
+    d_in, d_out = data.draw(hst.sampled_from(FUZZ_DIMS)), data.draw(hst.sampled_from(FUZZ_DIMS))
+    rows = data.draw(hst.sampled_from([0, 0, 0, 1, 128]))
+    L = layer(fk, max(d_in, 1), max(d_out, 1), so=data.draw(hst.sampled_from([0, 1, 1, 1, 2])),
+              dt=data.draw(hst.sampled_from([0, 1])), stats=data.draw(hst.booleans()), rows=rows,
+              adt=data.draw(hst.sampled_from([0, 1])), fdt=data.draw(hst.sampled_from([0, 0, 1])),
+              rank=data.draw(hst.sampled_from([0, 0, 1, 2, 4, 5, -1])))
+    L["d_in"], L["d_out"] = d_in, d_out
+    L["gemm_path"] = data.draw(hst.sampled_from([0, 0, 1, 2, 3, -1]))
+    if data.draw(hst.booleans()):
+        L["rows"] = data.draw(hst.sampled_from([-1, 8, M.MAX_ROWS + 1]))
+    for _ in range(data.draw(hst.integers(1, 2))):
+        _mutate(L, prev,
+                data.draw(hst.sampled_from(["null", "misalign", "alias_out", "overlap_factors", "cross_layer",
+                                            "bad_code"])),
+                data.draw(hst.sampled_from(PTR_KEYS + ["gemm_path", "act_dtype", "factor_dtype"])))
+    return L
+
+
+@settings(max_examples=400, deadline=None, derandomize=True, suppress_health_check=list(HealthCheck))
+@given(data=hst.data())
+def test_validation_fuzz(lib, data):
+    """Random layer lists (two thirds of the layers valid by construction, the
+    others with out-of-range values, null or misaligned pointers, aliasing):
+    mkor_workspace_size returns a documented status (and the error text on
+    failure), the same size on a repeated call, a multiple of 256 B; plan
+    creation with one byte too little workspace is refused with
+    MKOR_WORKSPACE_TOO_SMALL before any HIP call."""
+    fk = Fake()
+    descs = []
+    for _ in range(data.draw(hst.integers(0, 4), label="n")):
+        ok = data.draw(hst.sampled_from([True, True, False]))
+        descs.append(_valid_layer(fk, data) if ok else _random_layer(fk, data, descs[-1] if descs else None))
+    st, size = ws_status(descs)
+    assert st in (M.MKOR_OK, M.MKOR_INVALID_ARG, M.MKOR_UNSUPPORTED), (st, M.last_error())
+    if st != M.MKOR_OK:
+        assert M.last_error()
+        return
+    assert ws_status(descs) == (st, size)
+    assert size % 256 == 0
+    if size > 0:
+        arr = B.make_layer_array(descs)
+        plan = ctypes.c_void_p(None)
+        ws = fk.alloc(size)
+        assert lib.mkor_plan_create(arr, len(descs), ctypes.c_void_p(ws), size - 1,
+                                    ctypes.byref(plan)) == M.MKOR_WORKSPACE_TOO_SMALL
+        assert not plan.value
+
+
+@settings(max_examples=300, deadline=None, derandomize=True, suppress_health_check=list(HealthCheck))
+@given(gamma=hst.floats(allow_nan=True, allow_infinity=True, width=32),
+       zeta=hst.floats(allow_nan=True, allow_infinity=True, width=32),
+       eps=hst.floats(allow_nan=True, allow_infinity=True, width=32),
+       norm_kind=hst.integers(-1, 2), variant=hst.integers(-1, 2))
+def test_params_fuzz(lib, gamma, zeta, eps, norm_kind, variant):
+    """mkor_params_check against the documented ranges: 0 < gamma < 1,
+    0 < zeta <= 1, eps >= 0 (or +inf), norm kind and variant 0 or 1."""
+    p = M.Params(gamma=gamma, zeta=zeta, eps=eps, norm_kind=norm_kind, variant=variant)
+    valid = (0 < gamma < 1 and 0 < zeta <= 1 and (eps >= 0 or eps == math.inf) and not math.isnan(eps)
+             and norm_kind in (0, 1) and variant in (0, 1))
+    assert M.params_check(p) == (M.MKOR_OK if valid else M.MKOR_INVALID_ARG), (gamma, zeta, eps, M.last_error())
