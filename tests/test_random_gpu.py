@@ -169,3 +169,109 @@ def test_random_plan(seed):
         tol = TOL_HALF_FREE if sp["half"] else TOL_FREE
         assert rel(Lg, Lo) <= tol and rel(Rg, Ro) <= tol, (seed, k, desc[k], rel(Lg, Lo), rel(Rg, Ro))
     print("plan", seed, "worst dW error", worst)
+
+
+def _f32(x):
+    return float(np.float32(x))   # the ABI takes fp32 hyper-parameters
+
+
+@pytest.mark.parametrize("seed", range(N_PLANS // 2))
+def test_random_plan_switch_and_optimizer(seed):
+    """Random plans as above with the backend optimizer fused (SGD or LAMB,
+    random hyper-parameters) and MKOR-H switches between the calls: a random
+    subset of the second-order layers runs the first-order branch for the
+    second call (a step or a precondition only), and another random subset for
+    the third.  The oracle follows each layer's branch; W, m (and v), and dW
+    when stored, are checked after every call."""
+    from oracle.optimizer import lamb_step, sgd_step
+    from paper_2306_01685_amd import OPT_LAMB, OPT_SGD, OptParams
+
+    rng = np.random.default_rng([2307, seed])
+    specs = [_spec(rng) for _ in range(int(rng.integers(1, 5)))]
+    lamb = bool(rng.random() < 0.5)
+    layers = [H.allocate_layers([(sp["d_in"], sp["d_out"])], sp["gdt"], second_order=[sp["so"]],
+                                factor_dtype="bf16" if sp["half"] else "fp32", rank=sp["rank"], rows=sp["rows"],
+                                act_dtype=sp["adt"], gemm_path=sp["path"], optimizer="lamb" if lamb else "sgd")[0]
+              for sp in specs]
+    state, opt = [], []
+    for k, (L, sp) in enumerate(zip(layers, specs)):
+        shape = (sp["d_in"], sp["d_out"])
+        W0 = (rng.standard_normal(shape) * 0.02).astype(np.float32)
+        m0 = (rng.standard_normal(shape) * 1e-4).astype(np.float32)
+        v0 = np.abs(rng.standard_normal(shape) * 1e-7).astype(np.float32)
+        L["W"].copy_(torch.from_numpy(W0))
+        L["opt_m"].copy_(torch.from_numpy(m0))
+        if lamb:
+            L["opt_v"].copy_(torch.from_numpy(v0))
+        opt.append([W0.astype(np.float64), m0.astype(np.float64), v0.astype(np.float64)])
+        if not sp["so"]:
+            state.append(None)
+            continue
+        Li, Ri = spd(3000 * seed + 2 * k, sp["d_in"], 0.3), spd(3000 * seed + 2 * k + 1, sp["d_out"], 0.3)
+        if sp["half"]:
+            Li, Ri = _bf16(Li), _bf16(Ri)
+        H.set_factors(L, Li, Ri)
+        state.append([Li.astype(np.float64), Ri.astype(np.float64)])
+    has_rank = any(sp["rank"] > 1 for sp in specs)
+    eps = [math.inf, 0.0, float(rng.uniform(1.2, 2.5))][int(rng.integers(0, 3))]
+    p = Params(gamma=float(rng.uniform(0.5, 0.99)), zeta=float(rng.uniform(0.1, 0.9)), eps=eps,
+               norm_kind=int(rng.integers(0, 2)), variant=0 if has_rank or rng.random() < 0.75 else 1)
+    op = oparams(p)
+    hp = dict(lr=float(rng.uniform(1e-4, 1e-2)), momentum=float(rng.uniform(0.5, 0.95)),
+              beta1=float(rng.uniform(0.8, 0.95)), beta2=float(rng.uniform(0.99, 0.9999)), eps=1e-6,
+              weight_decay=float(rng.choice([0.0, 0.01])))
+    plan = H.make_plan(layers)
+    print("plan", seed, "lamb" if lamb else "sgd", [(sp["d_in"], sp["d_out"], sp["so"], sp["half"], sp["path"],
+                                                     sp["rank"], sp["rows"], sp["gdt"]) for sp in specs], p, hp,
+          flush=True)
+    mode = [bool(sp["so"]) for sp in specs]
+    for t, update in enumerate((True, bool(rng.random() < 0.5), True)):
+        if t > 0:
+            mode = [bool(sp["so"]) and bool(rng.random() < 0.5) for sp in specs]
+            plan.set_second_order([int(m) for m in mode])
+        store = bool(rng.random() < 0.7)
+        o = OptParams(kind=OPT_LAMB if lamb else OPT_SGD, step=t + 1, store_dw=store, **hp)
+        xs = [_inputs(rng, sp) for sp in specs]
+        for L, sp, x in zip(layers, specs, xs):
+            _feed(L, sp, x, update)
+        (plan.step_opt if update else plan.precondition_opt)(p, o)
+        torch.cuda.synchronize()
+        for k, (L, sp, x) in enumerate(zip(layers, specs, xs)):
+            if mode[k]:
+                stt = H.get_stats(L)
+                flags = {"L": bool(stt["stab_L"]), "R": bool(stt["stab_R"])}
+                state[k], dW, _ = _oracle(sp, state[k], x, op, flags, update)
+                dtol = (TOL_HALF_STEP if sp["half"] else TOL_STEP) if t == 0 else (
+                    TOL_HALF_FREE if sp["half"] else TOL_FREE)
+            else:
+                dW, dtol = x["G"].astype(np.float64), 0.0
+            if store:
+                e = rel(H.get_dW(L), dW)
+                assert e <= dtol, (seed, t, k, "dW", e)
+            Wo, mo, vo = opt[k]
+            if lamb:
+                Wo, mo, vo, _ = lamb_step(Wo, mo, vo, dW, t + 1, _f32(hp["lr"]), _f32(hp["beta1"]),
+                                          _f32(hp["beta2"]), _f32(hp["eps"]), _f32(hp["weight_decay"]))
+            else:
+                Wo, mo = sgd_step(Wo, mo, dW, _f32(hp["lr"]), _f32(hp["momentum"]), _f32(hp["weight_decay"]))
+            opt[k] = [Wo, mo, vo]
+            # bars: the layer's dW bar (at least the one-step bar, for the rounding of the
+            # update itself); twice that for v, which accumulates g^2
+            wtol = max(dtol, TOL_STEP)
+            checks = [("W", L["W"], Wo, wtol), ("m", L["opt_m"], mo, wtol)]
+            if lamb:
+                checks.append(("v", L["opt_v"], vo, 2 * wtol))
+            for name, got, want, tol in checks:
+                e = rel(got.cpu().numpy(), want)
+                assert e <= tol, (seed, t, k, name, e)
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    for k, (L, sp) in enumerate(zip(layers, specs)):
+        if not sp["so"]:
+            continue
+        Lg, Rg = H.get_factors(L)
+        Lo, Ro = state[k]
+        if sp["half"]:
+            Lo, Ro = round_bf16(Lo), round_bf16(Ro)
+        tol = TOL_HALF_FREE if sp["half"] else TOL_FREE
+        assert rel(Lg, Lo) <= tol and rel(Rg, Ro) <= tol, (seed, k, rel(Lg, Lo), rel(Rg, Ro))
