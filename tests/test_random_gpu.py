@@ -44,7 +44,7 @@ def _spec(rng):
         path = "fp32" if path == "split" else path
         d_in, d_out = int(rng.integers(1, 301)), int(rng.integers(1, 301))
     rank = int(rng.integers(2, 4)) if (so and not half and rng.random() < 0.25) else 1
-    rows = int(rng.choice([1, 33, 200])) if (so and not half and rank == 1 and rng.random() < 0.25) else 0
+    rows = int(rng.choice([1, 33, 200])) if (so and rank == 1 and rng.random() < 0.25) else 0
     return dict(d_in=d_in, d_out=d_out, so=so, half=half, path=path, rank=rank, rows=rows,
                 gdt="bf16" if rng.random() < 0.5 else "fp32", adt="bf16" if rng.random() < 0.5 else "fp32")
 
