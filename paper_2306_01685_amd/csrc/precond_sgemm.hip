@@ -513,22 +513,24 @@ __device__ __forceinline__ float row_sums8(const float (&v)[8], int lane) {
 
 template <bool TWO>
 __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, const Pending& q, float* partials,
-                                           float* red) {
+                                           double* red) {
     constexpr int RB = 8;   // rows in flight per wave
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int K = L.K, J = L.J;
     const float* w2 = L.w + K;
-    // this lane's part of ||Q||^2: a short chain per row (K / 64 terms), the
-    // rows of a pass added as a tree, the passes chained.  One fp32 chain over
-    // all the block's rows (thousands of positive terms) drifts low by several
-    // 1e-6 relative, which the rescale would carry into every element of dW.
-    float sq = 0.f;
+    // this lane's part of ||Q||^2: the squares of one 16-byte chunk summed in
+    // fp32, the chunks accumulated in fp64, whatever K and the block's rows.
+    // A long fp32 chain of positive terms (thousands of them) drifts low by
+    // 1e-6 relative and more, which the rescale would carry into every
+    // element of dW.
+    double sq = 0.0;
     for (int r0 = wave * RB; r0 < b.rows; r0 += 4 * RB) {
         const int jb = b.rb * b.rows + r0;
         if (jb >= J) break;   // J is a multiple of 64: all RB rows in or all out
-        float dot[RB], dot2[RB], sqr[RB];
+        float dot[RB], dot2[RB];
+        double sqr[RB];
 #pragma unroll
-        for (int i = 0; i < RB; ++i) dot[i] = dot2[i] = sqr[i] = 0.f;
+        for (int i = 0; i < RB; ++i) { dot[i] = dot2[i] = 0.f; sqr[i] = 0.0; }
         if (L.qf32) {
             const float* row = static_cast<const float*>(L.Q) + (size_t)jb * K;
             for (int k = 4 * lane; k < K; k += 256) {
@@ -537,7 +539,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
                     const float4 v = gld4(row + (size_t)i * K + k);
-                    sqr[i] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, sqr[i]))));
+                    sqr[i] += (double)fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, v.w * v.w)));
                     dot[i] = fmaf(v.x, wv.x, fmaf(v.y, wv.y, fmaf(v.z, wv.z, fmaf(v.w, wv.w, dot[i]))));
                     if (TWO) dot2[i] = fmaf(v.x, wv2.x, fmaf(v.y, wv2.y, fmaf(v.z, wv2.z, fmaf(v.w, wv2.w, dot2[i]))));
                 }
@@ -560,13 +562,15 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
                 for (int i = 0; i < RB; ++i) {
                     const uint4 u = gld_u4(row + (size_t)i * K + k);
                     const unsigned h[4] = {u.x, u.y, u.z, u.w};
+                    float s8 = 0.f;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float v0 = __uint_as_float(h[e] << 16), v1 = __uint_as_float(h[e] & 0xffff0000u);
-                        sqr[i] = fmaf(v1, v1, fmaf(v0, v0, sqr[i]));
+                        s8 = fmaf(v1, v1, fmaf(v0, v0, s8));
                         dot[i] = fmaf(v1, wv[2 * e + 1], fmaf(v0, wv[2 * e], dot[i]));
                         if (TWO) dot2[i] = fmaf(v1, wv2[2 * e + 1], fmaf(v0, wv2[2 * e], dot2[i]));
                     }
+                    sqr[i] += (double)s8;
                 }
             }
         }
@@ -578,10 +582,11 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
             if ((lane & 7) == 0) gst(L.rq + J + jb + (lane >> 3), d2);
         }
     }
-    const float gsq = wave_sum(sq);
-    if (lane == 0) red[wave] = gsq;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
+    if (lane == 0) red[wave] = sq;
     __syncthreads();
-    if (t == 0) gst(partials + L.part0 + b.rb, (red[0] + red[1]) + (red[2] + red[3]));
+    if (t == 0) gst(partials + L.part0 + b.rb, (float)((red[0] + red[1]) + (red[2] + red[3])));
 }
 
 // Stage-1 Q rows ahead of the first split GEMM: (Q w)[j] for each pending
@@ -592,7 +597,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
 // deterministic.
 __global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ layers,
                                                   const QdBlock* __restrict__ blocks, float* __restrict__ partials) {
-    __shared__ float red[4];
+    __shared__ double red[4];
     const QdBlock b = blocks[blockIdx.x];
     const HgLayer L = layers[b.layer];
     if (!gld_i32(L.mode)) return;   // block-uniform

@@ -211,3 +211,84 @@ def test_single_8192_layer_20_steps():
     fired = fr.check_flags()
     print("8192 layer: sampled-row dW error", e, "stabiliser fired", fired)
     assert fired > 0
+
+
+def _identity_update_k(x, gamma):
+    """From P = I the oracle's update is (1/gamma)(I - k x x^T) with
+    k = (1 - gamma) / (gamma + (1 - gamma) x^T x) (the SM step with P_hat = I,
+    u = x, s = x^T x); returns k."""
+    x = np.asarray(x, np.float64)
+    return (1.0 - gamma) / (gamma + (1.0 - gamma) * float(x @ x))
+
+
+def test_max_dim_layer_one_step():
+    """The largest layer the ABI accepts, MKOR_MAX_DIM x MKOR_MAX_DIM (32768):
+    each fp32 factor is 4 GiB and the kernels form their largest offsets.  bf16
+    G, factors from the identity, one step on the default (split) path.  From
+    the identity the oracle's update has a closed form, checked against the
+    oracle itself at d = 64 first; then every element of both factors is
+    compared with it (1024 rows at a time), sampled rows of dW_hat through
+    Linv[i, :] G Rinv = (G[i, :] - kL a_i (a^T G)) Rinv, and the rescale
+    property ||dW|| = ||G||."""
+    import paper_2306_01685_amd as M
+
+    gamma = 0.9
+    p = Params(gamma=gamma, zeta=0.5, eps=100.0)
+    op = oparams(p)
+    x64 = np.random.default_rng(64).standard_normal(64) / 8.0
+    P1, st1 = O.update_factor(np.eye(64), x64, op)
+    k64 = _identity_update_k(x64, gamma)
+    assert not st1.stab
+    assert rel(P1, (np.eye(64) - k64 * np.outer(x64, x64)) / gamma) <= 1e-14
+
+    d = M.MAX_DIM
+    L = H.allocate_layers([(d, d)], "bf16")[0]
+    rng = np.random.default_rng(32768)
+    a = (rng.standard_normal(d) / math.sqrt(d)).astype(np.float32)
+    g = (rng.standard_normal(d) / math.sqrt(d)).astype(np.float32)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7)
+    tmp = torch.empty((d, d), dtype=torch.float32, device="cuda")
+    tmp.normal_(0.0, 1e-3, generator=gen)
+    L["G"].copy_(tmp)
+    del tmp
+    torch.cuda.empty_cache()
+    H.set_inputs(L, a, g)
+    plan = H.make_plan([L])
+    plan.step(p)
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    st = H.get_stats(L)
+    assert not st["stab_L"] and not st["stab_R"]
+
+    kL, kR = _identity_update_k(a, gamma), _identity_update_k(g, gamma)
+    a64, g64 = a.astype(np.float64), g.astype(np.float64)
+    worst_f = 0.0
+    aG = np.zeros(d)        # a^T G, accumulated over row blocks of G
+    nG2 = 0.0
+    CH = 1024
+    for r0 in range(0, d, CH):
+        r1 = r0 + CH
+        for key, x, k in (("Linv", a64, kL), ("Rinv", g64, kR)):
+            got = L[key][r0:r1].cpu().numpy().astype(np.float64)
+            want = -k * np.outer(x[r0:r1], x)
+            want[np.arange(CH), np.arange(r0, r1)] += 1.0
+            want /= gamma
+            e = rel(got, want)
+            worst_f = max(worst_f, e)
+            assert e <= TOL_STEP, (key, r0, e)
+        Gb = L["G"][r0:r1].float().cpu().numpy().astype(np.float64)
+        aG += a64[r0:r1] @ Gb
+        nG2 += float((Gb * Gb).sum())
+    nG = math.sqrt(nG2)
+    assert st["norm_G"] == pytest.approx(nG, rel=2e-7)
+    nW = float(torch.linalg.vector_norm(L["dW"], dtype=torch.float64))
+    assert nW == pytest.approx(nG, rel=2e-7)
+    rows = np.concatenate([[0, d - 1], np.random.default_rng(9).choice(d, size=14, replace=False)])
+    Grows = L["G"][torch.from_numpy(rows).cuda()].float().cpu().numpy().astype(np.float64)
+    v = (Grows - kL * np.outer(a64[rows], aG)) / gamma                   # rows of Linv G
+    ref = (v - kR * np.outer(v @ g64, g64)) / gamma                      # rows of Linv G Rinv
+    got = L["dW"][torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64) / st["scale"]
+    e = rel(got, ref)
+    assert e <= TOL_STEP, e
+    print("max-dim layer: worst factor block error", worst_f, "sampled dW_hat rows error", e)
