@@ -147,3 +147,47 @@ def test_bert_large_means_from_16384_bf16_rows():
         a, g = H.get_means(layers[i])
         _mean_check(a, A)
         _mean_check(g, Go)
+
+
+@pytest.mark.slow
+def test_max_rows_means_and_step():
+    """The largest token-row count the ABI accepts, MKOR_MAX_ROWS = 2^26 bf16
+    rows for each of A and Gout of a 64 x 64 layer (8 GiB per matrix, so row
+    offsets pass 2^32 bytes).  The means against the float64 column means of
+    the same stored rows (streamed back in chunks, at 2 fp32 ulps), and the step
+    they drive against the oracle."""
+    import paper_2306_01685_amd as M
+
+    n, d, CH = M.MAX_ROWS, 64, 1 << 22
+    L = H.allocate_layers([(d, d)], "fp32", rows=n, act_dtype="bf16")[0]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(26)
+    for key, std in (("A", 1.0), ("Gout", 1e-3)):
+        tmp = torch.empty((CH, d), dtype=torch.float32, device="cuda")
+        for r0 in range(0, n, CH):
+            tmp.normal_(0.0, std, generator=gen)
+            L[key][r0:r0 + CH].copy_(tmp)
+        del tmp
+    G = (np.random.default_rng(3).standard_normal((d, d)) * 1e-3).astype(np.float32)
+    H.set_inputs(L, G=G)
+    plan = H.make_plan([L])
+    p = Params()
+    plan.step(p)
+    torch.cuda.synchronize()
+    a, g = H.get_means(L)
+    means = {}
+    for key in ("A", "Gout"):
+        s = np.zeros(d)
+        for r0 in range(0, n, CH):
+            s += L[key][r0:r0 + CH].float().cpu().numpy().astype(np.float64).sum(axis=0)
+        means[key] = s / n
+    np.testing.assert_array_max_ulp(a, means["A"].astype(np.float32), maxulp=2)
+    np.testing.assert_array_max_ulp(g, means["Gout"].astype(np.float32), maxulp=2)
+    Lo, Ro, dW, _ = O.layer_step(np.eye(d), np.eye(d), means["A"], means["Gout"], G, oparams(p))
+    e = rel(H.get_dW(L), dW)
+    assert e <= TOL_STEP, e
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    Lg, Rg = H.get_factors(L)
+    assert rel(Lg, Lo) <= TOL_STEP and rel(Rg, Ro) <= TOL_STEP
+    print("max rows: dW error", e)
