@@ -118,6 +118,9 @@ def parse():
                          "power: run the step and single GEMM stages back to back, --power-seconds "
                          "each, while sampling board power and clocks with amd-smi")
     ap.add_argument("--power-seconds", type=float, default=6.0)
+    ap.add_argument("--no-power", action="store_true",
+                    help="skip the board power / clock sample taken while the dominant GEMM runs "
+                         "(roofline.power)")
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--factor-dtype", choices=["fp32", "bf16"], default="fp32",
                     help="storage type of the inverse factors of the timed run (bf16: the "
@@ -318,7 +321,43 @@ def stage_times(plan, params, stream, steps):
     return [a / steps for a in acc]
 
 
-def measure(w, args, factor_dtype, gemm_path="auto"):
+NOMINAL_GFX_MHZ = 2400.0   # MI355X peak engine clock, the clock the MFMA peaks are quoted at
+
+
+def clock_during(fn, seconds):
+    """Median board power (W) and graphics clock (MHz) from amd-smi (read-only,
+    a background thread) while fn runs back to back for `seconds`; the first
+    1.5 s are left out.  None if amd-smi gives nothing."""
+    import threading
+
+    import torch
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            t, v = time.time(), _smi_sample()
+            if v is not None:
+                samples.append((t, *v))
+            time.sleep(0.1)
+
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    torch.cuda.synchronize()
+    t0 = time.time()
+    while time.time() - t0 < seconds:
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=30)
+    xs = [x for x in samples if x[0] >= t0 + 1.5]
+    if not xs:
+        return None
+    return dict(board_w=statistics.median(x[1] for x in xs), gfx_mhz=statistics.median(x[2] for x in xs),
+                samples=len(xs))
+
+
+def measure(w, args, factor_dtype, gemm_path="auto", sample_power=False):
     """Times mkor_step over the workload with the given factor storage type
     (and, for fp32 factors, GEMM path).  Returns (ms_per_step, kernels,
     roofline, schedule)."""
@@ -462,6 +501,17 @@ def measure(w, args, factor_dtype, gemm_path="auto"):
                         traffic=None if traffic is None else traffic["total_bytes"],
                         per_launch=f"{k['alg_bytes']:.4e} B")
         roof["traffic_detail"] = traffic
+        if sample_power and roof["bound"] == "mfma" and not getattr(args, "no_power", False):
+            # the clock the dominant GEMM runs at: at the board's power limit it
+            # is below the nominal clock its peak assumes
+            stage = [1, 2, 4, 5, 6][dom]
+            pw = clock_during(lambda: plan.run_stage(params, stage), args.power_seconds)
+            if pw is not None:
+                peak_clk = roof["peak"] * pw["gfx_mhz"] / NOMINAL_GFX_MHZ
+                pw.update(nominal_mhz=NOMINAL_GFX_MHZ, peak_at_clock=peak_clk,
+                          frac_at_clock=roof["achieved"] / peak_clk,
+                          note="amd-smi while this kernel's stage runs back to back after the timed windows")
+            roof["power"] = pw
         # the SM update, the step's bandwidth-bound half: its roofline beside (its
         # traffic differs with the GEMM path: only the split path writes some
         # factors every other step)
@@ -713,7 +763,7 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     w = W.WORKLOADS[args.config]
-    ms_step, kernels, roof, schedule, extra = measure(w, args, args.factor_dtype, args.gemm_path)
+    ms_step, kernels, roof, schedule, extra = measure(w, args, args.factor_dtype, args.gemm_path, sample_power=True)
     value = w.n_layers / (ms_step / 1e3)
     fp32_path = None
     if (args.factor_dtype == "fp32" and not args.no_fp32_path and args.rank == 1

@@ -44,6 +44,11 @@ def test_bench_line_fields():
     assert roof["bound"] in ("hbm", "mfma", "alu")
     assert roof["frac"] == pytest.approx(roof["achieved"] / roof["peak"])
     assert 0 < roof["frac"] < 1
+    pw = roof.get("power")
+    if pw is not None:   # amd-smi present: the clock the dominant GEMM ran at
+        assert 0 < pw["gfx_mhz"] <= pw["nominal_mhz"] * 1.05 and pw["board_w"] > 0 and pw["samples"] > 0
+        assert pw["frac_at_clock"] == pytest.approx(roof["achieved"] / pw["peak_at_clock"])
+        assert pw["frac_at_clock"] >= roof["frac"] * 0.999
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["unit"] and cb["sample"]
     assert len(d["timing"]["windows_ms_per_step"]) == d["timing"]["repeats"]
