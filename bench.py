@@ -777,7 +777,7 @@ def main():
     if args.factor_dtype == "fp32" and not args.no_half and args.rank == 1:
         # the same workload with half-precision (bf16) factors, reported beside
         h_ms, h_k, h_roof, h_sched, _ = measure(w, argparse.Namespace(**{**vars(args), "no_stabilised": True}),
-                                                "bf16")
+                                                "bf16", sample_power=True)
         half = dict(value=w.n_layers / (h_ms / 1e3), unit="layer-updates/s", ms_per_step=h_ms,
                     dtype="bf16 factors, bf16 MFMA (fp32 accumulation)", roofline=h_roof,
                     schedule_f10=h_sched, kernels=h_k)
