@@ -20,7 +20,8 @@
 // factor as P:
 //   stage 1:  Y^T = R G^T     P = S_R (d_out x d_out, fp32), Q = G (d_in x
 //                             d_out, bf16 or fp32), C = Y^T in fp32 (d_out x
-//                             d_in), plus ||G||^2 partials;
+//                             d_in); its (Q w) and the ||G||^2 partials come
+//                             from the row pass ahead of it (qdot_kernel);
 //   stage 2:  dW_hat = L Y    P = S_L (d_in x d_in, fp32), Q = Y^T (fp32),
 //                             C = dW_hat in fp32, plus ||dW_hat||^2 partials.
 // Layers with a bf16 G and d_in > d_out take the other association, so that
