@@ -43,6 +43,15 @@ def relmax(a, b) -> float:
     return d if mb == 0.0 else d / mb
 
 
+def check_close(got, ref, tol, *ctx) -> float:
+    """Asserts both the relative Frobenius error and the element-wise one
+    (relmax) are within tol; returns the Frobenius error."""
+    e, m = rel(got, ref), relmax(got, ref)
+    assert e <= tol, (*ctx, "Frobenius", e)
+    assert m <= tol, (*ctx, "element-wise", m)
+    return e
+
+
 def spd(seed, d, spread=0.25):
     """Seeded symmetric positive-definite fp32 matrix, bitwise symmetric."""
     rng = np.random.default_rng(seed)

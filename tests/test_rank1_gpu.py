@@ -14,7 +14,7 @@ import torch
 import oracle as O
 import workloads as W
 from paper_2306_01685_amd import Params, harness as H
-from tests.parity import TOL_FREE, TOL_STEP, oparams, rel
+from tests.parity import TOL_FREE, TOL_STEP, check_close, oparams
 
 pytestmark = pytest.mark.gpu
 
@@ -76,8 +76,7 @@ def test_step_from_rows_free_running():
             fired += int(ost.L.stab) + int(ost.R.stab)
             assert bool(ost.L.stab) == bool(st["stab_L"]) and bool(ost.R.stab) == bool(st["stab_R"])
             state[i] = (Li, Ri)
-            tol = TOL_STEP if t == 0 else TOL_FREE
-            assert rel(H.get_dW(L), dW) <= tol, (i, t)
+            check_close(H.get_dW(L), dW, TOL_STEP if t == 0 else TOL_FREE, i, t)
             ga, gg = H.get_means(L)
             np.testing.assert_array_max_ulp(ga, a.astype(np.float32), maxulp=2)
             np.testing.assert_array_max_ulp(gg, g.astype(np.float32), maxulp=2)
@@ -85,7 +84,8 @@ def test_step_from_rows_free_running():
     torch.cuda.synchronize()
     for i, L in enumerate(layers):
         Lg, Rg = H.get_factors(L)
-        assert rel(Lg, state[i][0]) <= TOL_FREE and rel(Rg, state[i][1]) <= TOL_FREE
+        check_close(Lg, state[i][0], TOL_FREE, i, "L")
+        check_close(Rg, state[i][1], TOL_FREE, i, "R")
     assert fired > 0
 
 
@@ -116,7 +116,7 @@ def test_update_every_f_steps():
             a, g, G = ins[i]
             Li, Ri, dW, _ = O.layer_step(*state[i], a, g, G, op, update=update)
             state[i] = (Li, Ri)
-            assert rel(H.get_dW(L), dW) <= (TOL_STEP if t == 0 else TOL_FREE), (i, t)
+            check_close(H.get_dW(L), dW, TOL_STEP if t == 0 else TOL_FREE, i, t)
 
 
 @pytest.mark.slow
@@ -184,10 +184,10 @@ def test_max_rows_means_and_step():
     np.testing.assert_array_max_ulp(a, means["A"].astype(np.float32), maxulp=2)
     np.testing.assert_array_max_ulp(g, means["Gout"].astype(np.float32), maxulp=2)
     Lo, Ro, dW, _ = O.layer_step(np.eye(d), np.eye(d), means["A"], means["Gout"], G, oparams(p))
-    e = rel(H.get_dW(L), dW)
-    assert e <= TOL_STEP, e
+    e = check_close(H.get_dW(L), dW, TOL_STEP, "dW")
     plan.sync_factors()
     torch.cuda.synchronize()
     Lg, Rg = H.get_factors(L)
-    assert rel(Lg, Lo) <= TOL_STEP and rel(Rg, Ro) <= TOL_STEP
+    check_close(Lg, Lo, TOL_STEP, "L")
+    check_close(Rg, Ro, TOL_STEP, "R")
     print("max rows: dW error", e)

@@ -5,6 +5,9 @@ the fp32 MFMA path (MKOR_GEMM_FP32) on the same inputs.
 Bars: relative Frobenius error <= 1e-4 after one step from the same state (as
 for every path); the split's error is also held to the fp32 MFMA path's order
 (at most 3x it, or 2e-6), since it is meant as an fp32-accurate product.
+Without a pending term the split's dW is held to 2e-6 Frobenius and 4e-6
+element-wise (TOL_SPLIT_ELEM: the largest of some 10^5 element errors runs
+2-3x the Frobenius figure on these shapes).
 """
 import math
 
@@ -15,7 +18,7 @@ import torch
 import oracle as O
 import workloads as W
 from paper_2306_01685_amd import MkorError, Params, harness as H
-from tests.parity import TOL_STEP, oparams, rel, spd
+from tests.parity import TOL_STEP, check_close, oparams, rel, relmax, spd
 
 pytestmark = pytest.mark.gpu
 
@@ -23,6 +26,7 @@ pytestmark = pytest.mark.gpu
 # with d_in > d_out take the other association ((Linv G) Rinv, dW stored
 # transposed from the second GEMM)
 SHAPES = [(64, 64), (128, 192), (192, 320), (320, 64), (256, 512), (576, 320)]
+TOL_SPLIT_ELEM = 4e-6
 
 
 def _inputs(seed, d_in, d_out, grad_dtype, scale=1.0):
@@ -64,9 +68,11 @@ def test_split_single_step(grad_dtype, eps):
     for i, (Ls, Lf, (Li, Ri, a, g, G)) in enumerate(zip(split, fp32, host)):
         Lo, Ro, dW, st = O.layer_step(Li, Ri, a, g, G, op)
         es, ef = rel(H.get_dW(Ls), dW), rel(H.get_dW(Lf), dW)
-        print(SHAPES[i], grad_dtype, eps, "dW error split", es, "fp32 MFMA", ef)
-        assert es <= TOL_STEP, (i, es)
+        ms, mf = relmax(H.get_dW(Ls), dW), relmax(H.get_dW(Lf), dW)
+        print(SHAPES[i], grad_dtype, eps, "dW error split", es, ms, "fp32 MFMA", ef, mf)
+        assert es <= TOL_STEP and ms <= TOL_STEP, (i, es, ms)
         assert es <= max(3 * ef, 2e-6), (i, es, ef)
+        assert ms <= max(3 * mf, TOL_SPLIT_ELEM), (i, ms, mf)
         s = H.get_stats(Ls)
         assert s["norm_G"] == pytest.approx(st.norm_G, rel=1e-5)
         assert s["norm_dW_hat"] == pytest.approx(st.norm_dW_hat, rel=1e-5)
@@ -85,8 +91,9 @@ def test_split_precondition_only(grad_dtype):
         layers, host = _run("split", grad_dtype, 60, p, update=False)
         for i, (L, (Li, Ri, a, g, G)) in enumerate(zip(layers, host)):
             _, _, dW, _ = O.layer_step(Li, Ri, a, g, G, oparams(p), update=False)
-            e = rel(H.get_dW(L), dW)
-            assert e <= min(TOL_STEP, 2e-6), (i, rescale, e)
+            e, m = rel(H.get_dW(L), dW), relmax(H.get_dW(L), dW)
+            print(SHAPES[i], grad_dtype, rescale, "dW error", e, m)
+            assert e <= 2e-6 and m <= TOL_SPLIT_ELEM, (i, rescale, e, m)
 
 
 def test_split_small_and_large_magnitudes():
@@ -98,8 +105,9 @@ def test_split_small_and_large_magnitudes():
         layers, host = _run("split", "fp32", 90, p, update=False, fscale=fscale, gscale=gscale)
         for i, (L, (Li, Ri, a, g, G)) in enumerate(zip(layers, host)):
             ref = O.precondition(Li, G, Ri)
-            e = rel(H.get_dW(L), ref)
-            assert e <= 2e-6, (fscale, i, e)
+            e, m = rel(H.get_dW(L), ref), relmax(H.get_dW(L), ref)
+            print(SHAPES[i], fscale, "dW error", e, m)
+            assert e <= 2e-6 and m <= TOL_SPLIT_ELEM, (fscale, i, e, m)
 
 
 def test_split_after_sync_and_over_steps():
@@ -136,8 +144,7 @@ def test_split_after_sync_and_over_steps():
             plan.sync_factors()
         torch.cuda.synchronize()
         for i, L in enumerate(layers):
-            e = rel(H.get_dW(L), outs[i])
-            assert e <= TOL_STEP, (t, i, e)
+            check_close(H.get_dW(L), outs[i], TOL_STEP, t, i)
 
 
 def test_split_shape_rule():
