@@ -210,6 +210,37 @@ def torch_matmul_reference(w, reps=3):
             "note": "torch.matmul fp32, Linv @ G @ Rinv per layer, shapes timed one pair at a time"}
 
 
+def torch_matmul_bf16_reference(n=8192, settle_s=1.5, reps=200, sample_power=True, power_seconds=3.0):
+    """torch.matmul in bf16 (the vendor GEMM library) on one n x n x n
+    product, run back to back for settle_s before a timed window of reps so
+    that the clock has settled under load as it has in the bench's windows:
+    the bf16 matrix-core rate the library sustains on this part, a measured
+    ceiling for GEMMs that feed the bf16 MFMAs."""
+    import torch
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    t0 = time.time()
+    while time.time() - t0 < settle_s:
+        for _ in range(10):
+            torch.matmul(a, b)
+        torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        torch.matmul(a, b)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    pw = clock_during(lambda: torch.matmul(a, b), power_seconds) if sample_power else None
+    del a, b
+    torch.cuda.empty_cache()
+    return {"n": n, "ms": ms, "tflops": 2 * n ** 3 / (ms / 1e3) / 1e12,
+            "frac_bf16_peak": 2 * n ** 3 / (ms / 1e3) / 1e12 / BF16_MFMA_PEAK_TF, "power": pw,
+            "note": f"torch.matmul bf16, {n}^3, timed after {settle_s} s back to back"}
+
+
 def workload_desc(w, factor_dtype="fp32"):
     counts = {}
     for s in w.block_shapes:
@@ -495,6 +526,7 @@ def measure(w, args, factor_dtype, gemm_path="auto", sample_power=False):
                                       f"TFLOP/s bf16 MFMA peak / {k['bf16_mfma_terms']} bf16 products each")
                 roof["frac_of_fp32_mfma_peak"] = k["tflops"] / FP32_MFMA_PEAK_TF
                 roof["frac_of_bf16_peak"] = k["tflops"] / BF16_MFMA_PEAK_TF
+                roof["bf16_mfma_tflops"] = k["bf16_mfma_tflops"]
         else:
             roof = dict(kernel=name, bound="hbm", achieved=k["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
                         frac=k["gbs"] / HBM_PEAK_GBS,
@@ -788,7 +820,18 @@ def main():
     refs = None
     if not args.no_references:
         refs = dict(copy_kernel=copy_measure(args.copy_mib, args.steps, args.warmup),
-                    torch_matmul_fp32=torch_matmul_reference(w))
+                    torch_matmul_fp32=torch_matmul_reference(w),
+                    torch_matmul_bf16=torch_matmul_bf16_reference(sample_power=not args.no_power))
+        bf = roof.get("bf16_mfma_tflops")
+        if bf is not None:
+            # the dominant split GEMM's bf16 matrix-core rate beside the rate
+            # the library's own bf16 GEMM sustains on this part
+            lib = refs["torch_matmul_bf16"]["tflops"]
+            roof["vs_library_bf16"] = dict(kernel_bf16_mfma_tflops=bf, library_bf16_tflops=lib, ratio=bf / lib)
+        if half is not None and half["roofline"]["bound"] == "mfma":
+            hr, lib = half["roofline"], refs["torch_matmul_bf16"]["tflops"]
+            hr["vs_library_bf16"] = dict(kernel_bf16_mfma_tflops=hr["achieved"], library_bf16_tflops=lib,
+                                         ratio=hr["achieved"] / lib)
 
     out = {
         "metric": METRIC, "value": value, "unit": "layer-updates/s", "n_gpus": 1,
