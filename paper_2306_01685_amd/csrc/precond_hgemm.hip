@@ -59,6 +59,12 @@ typedef __attribute__((address_space(3))) mk_u4 lds_u4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf8;
 typedef __attribute__((address_space(3))) float lds_float;
 typedef __attribute__((address_space(3))) unsigned short lds_u16;
+typedef __attribute__((address_space(3))) mk_f4 lds_f4;
+
+__device__ __forceinline__ float4 lds4(const lds_float* p) {
+    const mk_f4 v = *(const lds_f4*)p;
+    return make_float4(v.x, v.y, v.z, v.w);
+}
 
 constexpr int BI = HG_BI, BJ = HG_BJ, NT = HG_THREADS;
 constexpr int WI = BI / 128, WJ = BJ / HG_TJ;   // wave grid
@@ -85,7 +91,7 @@ constexpr int RING = NS * STB;
 constexpr int CPITCH = BJ * 2, CCH = BJ / 8;
 static_assert(BI * CPITCH <= RING && (CCH & (CCH - 1)) == 0, "output staging fits in the ring");
 __device__ __forceinline__ int cst(int r, int cj) { return r * CPITCH + ((cj ^ (r & (CCH - 1))) << 4); }
-constexpr int SMEM = RING + NS * WSLOT + 4 * (BJ + NW);
+constexpr int SMEM = RING + NS * WSLOT + 4 * (BJ + NW + BI);   // ring, w slices, (Q w), block sums, w rows
 
 // Row r's chunk c sits in 16-byte slot c ^ f(r): for 64-byte rows f(r) =
 // (r >> 2) & 3, for 128-byte rows f(r) = (r & 7) ^ ((r >> 3) & 1).  Either way
@@ -155,6 +161,7 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     const bool want_gsq = STAGE == 1 && tile.tm == 0;   // ||G||^2: each Q row once
     lds_float* rvec = (lds_float*)(smem + RING + NS * WSLOT);
     lds_float* red = rvec + BJ;
+    lds_float* ewv = red + NW;   // w over the tile's rows, for the epilogue
     const unsigned lds0 = (unsigned)(size_t)smem;
 
     floatx16 acc[FI][FJ];
@@ -274,16 +281,22 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     if (PEND) {
         const float v = TPQ == 2 ? rdot + __shfl_xor(rdot, 1, 64) : rdot;
         if (rh == 0) rvec[rr] = v;
+        // w of the tile's rows into LDS ahead of the stores: a global load
+        // issued after stores shares the vector-memory counter with them, so
+        // waiting for its value would also wait for those stores (rows past
+        // the edge clamped; their outputs are never stored)
+        for (int r = t; r < BI; r += NT) ewv[r] = gld(L.w + min(i0 + r, I - 1));
     }
-    __syncthreads();   // rvec complete; the ring is free for the output staging
+    __syncthreads();   // rvec and w complete; the ring is free for the output staging
 
     const float c1 = PEND ? q.c1 : 1.f, c2 = PEND ? q.c2 : 0.f, sg = PEND ? q.sgn : 0.f;
     float csq = 0.f;
-    // One MFMA row block (x) at a time: first every load its output groups
-    // need (rows past the edge clamped, so the loads go out together without
-    // branches), then C[i][j] = c1 acc + c2 Q[j][i] + sgn w[i] (Q w)[j].  c2 is
-    // zero unless the stabiliser blended the factor (Alg. 1): Q[j][i] is only
-    // read when it counts (a branch on a value uniform over the tile).
+    // One MFMA row block (x) at a time: first the values its output groups
+    // need (w from LDS; Q[j][i] from global memory, rows past the edge
+    // clamped, so the loads go out together without branches), then
+    // C[i][j] = c1 acc + c2 Q[j][i] + sgn w[i] (Q w)[j].  c2 is zero unless
+    // the stabiliser blended the factor (Alg. 1): Q[j][i] is only read when
+    // it counts (a branch on a value uniform over the tile).
     const bool qterm = PEND && c2 != 0.f;
 #pragma unroll
     for (int x = 0; x < FI; ++x) {
@@ -292,8 +305,8 @@ __device__ void hgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         if (PEND) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
-                wv[g] = gld4(L.w + i);
+                const int il = wi * TI + x * 32 + 8 * g + 4 * lk, i = min(i0 + il, I - 4);
+                wv[g] = lds4(ewv + il);
 #pragma unroll
                 for (int y = 0; y < FJ; ++y) {
                     const int j = min(j0 + wj * TJ + y * 32 + li, J - 1);

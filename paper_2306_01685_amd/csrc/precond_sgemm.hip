@@ -101,7 +101,13 @@ template <int GV> struct Geo {
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 constexpr int RING = cmax(Geo<GV_F32>::RING, cmax(Geo<GV_H>::RING, Geo<GV_HW>::RING));   // 144 KB
 constexpr int BJMAX = SG_BJ > SG_BJ1H ? SG_BJ : SG_BJ1H;
-constexpr int SMEM = RING + 4 * (BJMAX + NW);
+constexpr int BIMAX = SG_BI > SG_BI1H ? SG_BI : SG_BI1H;
+// after the ring: (P w) or (Q w) of the second GEMM's rows, the block
+// reduction, and the epilogue's vectors (w over the tile's rows, or columns
+// when FQ, then the second term's; (Q w) over its columns, then the second
+// term's)
+constexpr int EW = BJMAX + NW, EQ = EW + 2 * (BIMAX > BJMAX ? BIMAX : BJMAX);
+constexpr int SMEM = RING + 4 * (EQ + 2 * BJMAX);
 
 __device__ __forceinline__ void dma16(unsigned lds, unsigned voff, const void* base) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base)
@@ -112,6 +118,12 @@ template <int ROWB>
 __device__ __forceinline__ int slot(int r, int c) {
     return ROWB == 32 ? r * 32 + ((c ^ ((r >> 3) & 1)) << 4)
                       : r * 64 + ((c ^ ((r >> 2) & 3) ^ ((r >> 1) & 1)) << 4);
+}
+
+typedef __attribute__((address_space(3))) mk_f4 lds_f4;
+__device__ __forceinline__ float4 lds4(const lds_float* p) {
+    const mk_f4 v = *(const lds_f4*)p;
+    return make_float4(v.x, v.y, v.z, v.w);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -170,6 +182,8 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     const int I = L.I, J = L.J, K = L.K;
     lds_float* rvec = (lds_float*)(smem + RING);
     lds_float* red = rvec + BJMAX;
+    lds_float* ew = rvec + EW;
+    lds_float* eq = rvec + EQ;
 
     floatx16 acc[FI][FJ];
 #pragma unroll
@@ -373,6 +387,31 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         const float v = rdot + __shfl_xor(rdot, 1, 64);
         if (sh == 0) rvec[sr] = v;
     }
+    // a lazy factor (the first GEMM's) may carry a second term: w2 = w + K,
+    // (Q w2) at rq + J, coefficient sgnb (q holds the composed c1, c2 and
+    // the first term's c1b sgn: see sgemm_kernel)
+    const bool two = STAGE == 1 && PEND && !FQ && q.has == 2;
+    // The epilogue's vectors go into LDS here, ahead of its stores: a global
+    // load issued after stores shares the vector-memory counter with them, so
+    // waiting for its value also waits for those stores, and loads between
+    // the output stores would serialise the tile's store drains.  Rows and
+    // columns past the edge are clamped (their outputs are never stored).
+    if constexpr (PEND) {
+        if constexpr (FQ) {
+            for (int c = t; c < BJ; c += NT) ew[c] = gld(L.w + min(j0 + c, J - 1));
+        } else {
+            for (int r = t; r < BI; r += NT) {
+                ew[r] = gld(L.w + min(i0 + r, I - 1));
+                if (two) ew[BI + r] = gld(L.w + K + min(i0 + r, I - 1));
+            }
+            if constexpr (STAGE == 1) {
+                for (int c = t; c < BJ; c += NT) {
+                    eq[c] = gld(L.rq + min(j0 + c, J - 1));
+                    if (two) eq[BJ + c] = gld(L.rq + J + min(j0 + c, J - 1));
+                }
+            }
+        }
+    }
     __syncthreads();
 
     const float c1 = PEND ? q.c1 : 1.f, sg = PEND ? q.sgn : 0.f;
@@ -382,10 +421,6 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
     // (rows past the edge clamped), then C[i][j] = c1 acc + sgn w[i] (Q w)[j]
     // (FQ: c1 acc + sgn w[j] (P w)[i]), c2 I having entered acc through the
     // staged factor, stored as 128-byte row segments.
-    // a lazy factor (the first GEMM's) may carry a second term: w2 = w + K,
-    // (Q w2) at rq + J, coefficient sgnb (q holds the composed c1, c2 and
-    // the first term's c1b sgn: see sgemm_kernel)
-    const bool two = STAGE == 1 && PEND && !FQ && q.has == 2;
     const float sg2 = two ? q.sgnb : 0.f;
 #pragma unroll
     for (int x = 0; x < FI; ++x) {
@@ -394,21 +429,21 @@ __device__ void sgemm_tile(const HgLayer& L, const GemmTile& tile, const Pending
         if (PEND) {
             if constexpr (FQ) {
 #pragma unroll
-                for (int y = 0; y < FJ; ++y) wcol[y] = gld(L.w + min(j0 + wj * TJ + y * 32 + li, J - 1));
+                for (int y = 0; y < FJ; ++y) wcol[y] = ew[wj * TJ + y * 32 + li];
             } else {
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    const int i = min(i0 + wi * TI + x * 32 + 8 * g + 4 * lk, I - 4);
-                    wv[g] = gld4(L.w + i);
-                    wv2[g] = two ? gld4(L.w + K + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+                    const int il = wi * TI + x * 32 + 8 * g + 4 * lk;
+                    wv[g] = lds4(ew + il);
+                    wv2[g] = two ? lds4(ew + BI + il) : make_float4(0.f, 0.f, 0.f, 0.f);
                 }
             }
         }
 #pragma unroll
         for (int y = 0; y < FJ; ++y) {
             const int jl = wj * TJ + y * 32 + li, j = j0 + jl;
-            const float rq = (PEND && !FQ) ? (STAGE == 1 ? gld(L.rq + min(j, J - 1)) : rvec[jl]) : 0.f;
-            const float rq2 = two ? gld(L.rq + J + min(j, J - 1)) : 0.f;
+            const float rq = (PEND && !FQ) ? (STAGE == 1 ? eq[jl] : rvec[jl]) : 0.f;
+            const float rq2 = two ? eq[BJ + jl] : 0.f;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int il = wi * TI + x * 32 + 8 * g + 4 * lk, i = i0 + il;
