@@ -286,6 +286,21 @@ int64_t dpart_count(const mkor_layer& L) {
 // bf16-factor layer whose gradient is fp32: the GEMMs read a bf16 copy
 bool needs_cvt(const mkor_layer& L) { return is_half(L) && L.grad_dtype == MKOR_DTYPE_F32; }
 
+// Rows per block of the column-mean partials for the whole plan: the largest
+// power of two in [MEAN_ROWS_MIN, MEAN_ROWS_MAX] that still gives at least
+// MEAN_MIN_BLOCKS blocks over every token-row matrix (else the minimum).
+int32_t mean_rows_per_block(const mkor_layer* layers, int32_t n) {
+    for (int32_t rpb = MEAN_ROWS_MAX; rpb > MEAN_ROWS_MIN; rpb /= 2) {
+        int64_t blocks = 0;
+        for (int32_t i = 0; i < n; ++i)
+            if (layers[i].rows > 0)
+                blocks += (int64_t)(ceil_div(layers[i].d_in, MEAN_COLS) + ceil_div(layers[i].d_out, MEAN_COLS)) *
+                          ceil_div(layers[i].rows, rpb);
+        if (blocks >= MEAN_MIN_BLOCKS) return rpb;
+    }
+    return MEAN_ROWS_MIN;
+}
+
 }  // namespace
 
 int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
@@ -313,10 +328,11 @@ int compute_layout(const mkor_layer* layers, int32_t n, Layout& Lo) {
         usum += L.d_in + L.d_out;
     }
     int64_t mitems = 0, mchunks = 0, mpart = 0, mmats = 0;
+    Lo.mean_rpb = mean_rows_per_block(layers, n);
     for (int32_t i = 0; i < n; ++i) {
         const mkor_layer& L = layers[i];
         if (L.rows <= 0) continue;
-        const int64_t nrb = ceil_div(L.rows, MEAN_ROWS);
+        const int64_t nrb = ceil_div(L.rows, Lo.mean_rpb);
         for (const int32_t d : {L.d_in, L.d_out}) {
             const int64_t nch = ceil_div(d, MEAN_COLS);
             mmats += 1;
@@ -493,7 +509,9 @@ void build_tables(const mkor_layer* layers, int32_t n, char* base, const Layout&
                 M.bf16 = L.act_dtype == MKOR_DTYPE_BF16;
                 M.vec = (M.cols % 8) == 0;
                 M.nchunk = ceil_div(M.cols, MEAN_COLS);
-                M.nrb = ceil_div(M.rows, MEAN_ROWS);
+                M.nrb = ceil_div(M.rows, lo.mean_rpb);
+                M.rpb = lo.mean_rpb;
+                M._pad = 0;
                 M.part0 = p0;
                 M.mode = mode_d + i;
                 p0 += (int64_t)M.nchunk * M.nrb * MEAN_COLS;

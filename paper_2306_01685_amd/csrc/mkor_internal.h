@@ -23,8 +23,15 @@ namespace mkor {
 
 // ---------------------------------------------------------------- rank-1 means
 // Column means of the rows x cols activation / output-gradient matrices.
-constexpr int MEAN_COLS = 512;      // columns per chunk: 8 per lane of one wave
-constexpr int MEAN_ROWS = 1024;     // rows per block of the partial sums
+#ifndef MKOR_MEAN_COLS
+#define MKOR_MEAN_COLS 512
+#endif
+constexpr int MEAN_COLS = MKOR_MEAN_COLS;   // columns per chunk, a multiple of 8 per lane of one wave
+// Rows per block of the partial sums: a power of two between MEAN_ROWS_MIN
+// and MEAN_ROWS_MAX, the largest that still gives the plan MEAN_MIN_BLOCKS
+// blocks (longer blocks stream better; enough of them fill the chip).
+constexpr int MEAN_ROWS_MIN = 512, MEAN_ROWS_MAX = 8192;
+constexpr int64_t MEAN_MIN_BLOCKS = 1024;
 constexpr int MEAN_THREADS = 256;   // 4 waves, each taking every 4th row of a block
 
 struct MeanMat {
@@ -34,7 +41,9 @@ struct MeanMat {
     int32_t     bf16;     // element type of X
     int32_t     vec;      // cols % 8 == 0: vector loads of 8 columns
     int32_t     nchunk;   // column chunks of MEAN_COLS
-    int32_t     nrb;      // row blocks of MEAN_ROWS
+    int32_t     nrb;      // row blocks of rpb rows
+    int32_t     rpb;      // rows per block (the plan's, see MEAN_ROWS_MIN)
+    int32_t     _pad;
     int64_t     part0;    // first partial (double) of this matrix
     const int32_t* mode;  // the layer's mode word (see LayerMode)
 };

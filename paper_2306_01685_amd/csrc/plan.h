@@ -55,6 +55,7 @@ struct Layout {
     int32_t nsecond = 0;
     int32_t nranked = 0;      // second-order layers with rank > 1
     int32_t nmeanmat = 0, nmeanitem = 0, nmeanchunk = 0;
+    int32_t mean_rpb = MEAN_ROWS_MIN;   // rows per block of the mean partials
     int64_t nmeanpart = 0;   // doubles
     std::vector<size_t> u_off, w_off, x_off;   // per factor / per layer offsets (bytes)
     std::vector<size_t> gh_off;                // per layer: bf16 copy of an fp32 G (bf16 factors)

@@ -5,13 +5,14 @@
 //
 // Two grouped launches over every such matrix of the plan:
 //
-//   colmean_partial_kernel  one workgroup per (matrix, 512-column chunk,
-//                           MEAN_ROWS-row block): each thread sums its 8
-//                           columns over the block's rows (one row per wave
-//                           and step, so a wave reads 1 KB (bf16) or 2 KB
-//                           (fp32) of a row at a time) in float64, the four
-//                           waves are combined in a fixed order, and the
-//                           block's partial sums are stored.
+//   colmean_partial_kernel  one workgroup per (matrix, MEAN_COLS-column
+//                           chunk, block of rpb rows): each thread sums its
+//                           MEAN_COLS / 64 contiguous columns over the block's
+//                           rows (one row per wave and step: with 512 columns
+//                           a wave reads 1 KB (bf16) or 2 KB (fp32) of a row
+//                           at a time) in float64, the four waves are combined
+//                           in a fixed order, and the block's partial sums are
+//                           stored.
 //   colmean_final_kernel    one thread per column: sums the row-block partials
 //                           in a fixed order and stores sum / rows as fp32.
 //
@@ -24,7 +25,7 @@
 namespace mkor {
 namespace {
 
-constexpr int MT = MEAN_THREADS;   // 4 waves
+constexpr int MT = MEAN_THREADS;
 constexpr int MW = MT / 64;
 
 __device__ __forceinline__ void acc_bf16x2(double& lo, double& hi, unsigned h) {
@@ -39,33 +40,41 @@ __global__ __launch_bounds__(MT) void colmean_partial_kernel(const MeanMat* __re
     const MeanMat m = mats[it.mat];
     if (!gld_i32(m.mode)) return;   // first-order layer: no means (block-uniform)
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    constexpr int CPT = MEAN_COLS / 64;                // columns per thread (8)
+    constexpr int CPT = MEAN_COLS / 64;                // columns per thread
+    static_assert(CPT % 8 == 0, "whole 16-byte bf16 loads per lane");
     const int c0 = it.chunk * MEAN_COLS + CPT * lane;  // this thread's columns
-    const int r0 = it.rb * MEAN_ROWS;
-    const int r1 = min(r0 + MEAN_ROWS, m.rows);
+    const int r0 = it.rb * m.rpb;
+    const int r1 = min(r0 + m.rpb, m.rows);
     double s[CPT];
 #pragma unroll
     for (int e = 0; e < CPT; ++e) s[e] = 0.0;
     if (m.vec && c0 + CPT - 1 < m.cols) {
+        // each row is read once: streaming (non-temporal) loads, 8 rows in
+        // flight per wave
         if (m.bf16) {
-            // 8 bf16 = 16 bytes per lane: a wave reads 1 KB of a row at a time
+            // 8 bf16 = 16 bytes per load: a wave reads MEAN_COLS * 2 bytes of a row at a time
             const unsigned short* X = static_cast<const unsigned short*>(m.X) + c0;
-#pragma unroll 4
+#pragma unroll 8
             for (int r = r0 + wave; r < r1; r += MW) {
-                const uint4 h = gld_u4(X + (size_t)r * m.cols);
-                acc_bf16x2(s[0], s[1], h.x);
-                acc_bf16x2(s[2], s[3], h.y);
-                acc_bf16x2(s[4], s[5], h.z);
-                acc_bf16x2(s[6], s[7], h.w);
+#pragma unroll
+                for (int l = 0; l < CPT / 8; ++l) {
+                    const uint4 h = gld_u4_nt(X + (size_t)r * m.cols + 8 * l);
+                    acc_bf16x2(s[8 * l + 0], s[8 * l + 1], h.x);
+                    acc_bf16x2(s[8 * l + 2], s[8 * l + 3], h.y);
+                    acc_bf16x2(s[8 * l + 4], s[8 * l + 5], h.z);
+                    acc_bf16x2(s[8 * l + 6], s[8 * l + 7], h.w);
+                }
             }
         } else {
             const float* X = static_cast<const float*>(m.X) + c0;
-#pragma unroll 4
+#pragma unroll 8
             for (int r = r0 + wave; r < r1; r += MW) {
-                const float4 v0 = gld4(X + (size_t)r * m.cols);
-                const float4 v1 = gld4(X + (size_t)r * m.cols + 4);
-                s[0] += (double)v0.x; s[1] += (double)v0.y; s[2] += (double)v0.z; s[3] += (double)v0.w;
-                s[4] += (double)v1.x; s[5] += (double)v1.y; s[6] += (double)v1.z; s[7] += (double)v1.w;
+#pragma unroll
+                for (int l = 0; l < CPT / 4; ++l) {
+                    const float4 v = gld4_nt(X + (size_t)r * m.cols + 4 * l);
+                    s[4 * l + 0] += (double)v.x; s[4 * l + 1] += (double)v.y;
+                    s[4 * l + 2] += (double)v.z; s[4 * l + 3] += (double)v.w;
+                }
             }
         }
     } else {
