@@ -549,7 +549,7 @@ __device__ __forceinline__ float row_sums8(const float (&v)[8], int lane) {
 
 template <bool TWO>
 __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, const Pending& q, float* partials,
-                                           double* red) {
+                                           double* red, float (*rqs)[QD_MAX_ROWS]) {
     constexpr int RB = 8;   // rows in flight per wave
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int K = L.K, J = L.J;
@@ -574,7 +574,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
                 const float4 wv2 = TWO ? gld4(w2 + k) : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
-                    const float4 v = gld4(row + (size_t)i * K + k);
+                    const float4 v = gld4_nt(row + (size_t)i * K + k);
                     sqr[i] += (double)fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, v.w * v.w)));
                     dot[i] = fmaf(v.x, wv.x, fmaf(v.y, wv.y, fmaf(v.z, wv.z, fmaf(v.w, wv.w, dot[i]))));
                     if (TWO) dot2[i] = fmaf(v.x, wv2.x, fmaf(v.y, wv2.y, fmaf(v.z, wv2.z, fmaf(v.w, wv2.w, dot2[i]))));
@@ -596,7 +596,7 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
                 }
 #pragma unroll
                 for (int i = 0; i < RB; ++i) {
-                    const uint4 u = gld_u4(row + (size_t)i * K + k);
+                    const uint4 u = gld_u4_nt(row + (size_t)i * K + k);
                     const unsigned h[4] = {u.x, u.y, u.z, u.w};
                     float s8 = 0.f;
 #pragma unroll
@@ -611,11 +611,13 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
             }
         }
         sq += ((sqr[0] + sqr[1]) + (sqr[2] + sqr[3])) + ((sqr[4] + sqr[5]) + (sqr[6] + sqr[7]));
+        // the row results wait in LDS: a store here would hold up the next
+        // rows' loads, which share the vector-memory counter with it
         const float d = row_sums8(dot, lane);
-        if ((lane & 7) == 0 && q.has) gst(L.rq + jb + (lane >> 3), d);
+        if ((lane & 7) == 0) rqs[0][r0 + (lane >> 3)] = d;
         if (TWO) {
             const float d2 = row_sums8(dot2, lane);
-            if ((lane & 7) == 0) gst(L.rq + J + jb + (lane >> 3), d2);
+            if ((lane & 7) == 0) rqs[1][r0 + (lane >> 3)] = d2;
         }
     }
 #pragma unroll
@@ -623,23 +625,29 @@ __device__ __forceinline__ void qdot_block(const HgLayer& L, const QdBlock& b, c
     if (lane == 0) red[wave] = sq;
     __syncthreads();
     if (t == 0) gst(partials + L.part0 + b.rb, (float)((red[0] + red[1]) + (red[2] + red[3])));
+    const int j0 = b.rb * b.rows, nr = min(b.rows, J - j0);
+    if (q.has)
+        for (int r = t; r < nr; r += 256) gst(L.rq + j0 + r, rqs[0][r]);
+    if (TWO)
+        for (int r = t; r < nr; r += 256) gst(L.rq + J + j0 + r, rqs[1][r]);
 }
 
 // Stage-1 Q rows ahead of the first split GEMM: (Q w)[j] for each pending
 // term of the factor (one, or two for a lazy factor) and the ||G||^2 partial
 // of the block of rows (Q is G, or G^T: the same elements).  Four
-// waves take 8 rows at a time (8 loads in flight per lane); lanes take
-// 16-byte chunks with a stride of 64 chunks, then fixed-order wave sums:
+// waves take 8 rows at a time (8 streaming loads in flight per lane); lanes
+// take 16-byte chunks with a stride of 64 chunks, then fixed-order wave sums:
 // deterministic.
 __global__ __launch_bounds__(256) void qdot_kernel(const HgLayer* __restrict__ layers,
                                                   const QdBlock* __restrict__ blocks, float* __restrict__ partials) {
     __shared__ double red[4];
+    __shared__ float rqs[2][QD_MAX_ROWS];
     const QdBlock b = blocks[blockIdx.x];
     const HgLayer L = layers[b.layer];
     if (!gld_i32(L.mode)) return;   // block-uniform
     const Pending q = *L.pend;
-    if (q.has == 2) qdot_block<true>(L, b, q, partials, red);
-    else            qdot_block<false>(L, b, q, partials, red);
+    if (q.has == 2) qdot_block<true>(L, b, q, partials, red, rqs);
+    else            qdot_block<false>(L, b, q, partials, red, rqs);
 }
 
 // G^T of bf16 gradients, 64 x 64 tiles through LDS (rows of 64 + 2 elements,
