@@ -58,6 +58,18 @@ def test_lamb_first_step_trust_ratio():
     assert np.allclose(m, 0.1 * g) and np.allclose(v, 0.001 * g * g)
 
 
+def test_lamb_weight_decay_inside_trust_ratio():
+    # LAMB adds the decay term to the adaptive step before the layer-wise
+    # trust ratio is taken.  t = 1, eps = 0: m_hat = g, v_hat = g^2, so with
+    # W = (2, 0), g = (-1, 1), wd = 0.5:  r = sign(g) + wd W = (0, 1),
+    # ||W|| = 2, ||r|| = 1, phi = 2, W' = W - lr phi r = (2, -2 lr)
+    W = np.array([2.0, 0.0])
+    g = np.array([-1.0, 1.0])
+    Wn, m, v, phi = lamb_step(W, np.zeros(2), np.zeros(2), g, 1, 0.25, 0.9, 0.999, 0.0, 0.5)
+    assert phi == 2.0
+    np.testing.assert_array_equal(Wn, np.array([2.0, -0.5]))
+
+
 def test_lamb_zero_norms():
     # W = 0: phi = 1 (the raw adaptive step)
     Wn, _, _, phi = lamb_step(np.zeros(3), np.zeros(3), np.zeros(3), np.ones(3), 1, 0.5, 0.9, 0.999, 0.0, 0.0)
