@@ -19,10 +19,14 @@ import numpy as np
 import pytest
 
 import oracle as O
+import oracle.half as HF
+import oracle.hybrid as HY
 import oracle.mkor_oracle as M
 import oracle.optimizer as OPT
 import oracle.rank as RK
+import tests.test_hybrid as THY
 import tests.test_oracle as T
+import tests.test_oracle_half as TH
 import tests.test_oracle_optimizer as TO
 import tests.test_oracle_rank as TR
 
@@ -349,6 +353,148 @@ OPT_MUTANTS = {
 }
 
 
+# ------------------------------------------- the half-precision oracle and its pins
+
+def _half_pins():
+    return [
+        ("round_vs_library_cast", TH.test_round_matches_library_cast),
+        ("round_hand_values", lambda: [TH.test_round_hand_values(x, w) for x, w in (
+            (1.0 + 2.0 ** -8, 1.0), (1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -6), (2.0 ** -133 * 1.5, 2.0 ** -132),
+            ((2.0 - 2.0 ** -8) * 2.0 ** 127, math.inf))]),
+        ("round_properties", TH.test_round_properties),
+        ("exact_case", TH.test_exact_case_equals_fp64_step),
+        ("intermediate_rounded", TH.test_intermediate_is_rounded),
+        ("gradient_rounded", TH.test_gradient_enters_rounded),
+        ("stored_state", TH.test_stored_state_and_update_from_it),
+        ("fresh_factor", TH.test_preconditioning_uses_fresh_factor),
+        ("lemma2", lambda: TH.test_lemma2_bound(64)),
+        ("close_to_fp64", TH.test_half_step_close_to_full_precision),
+    ]
+
+
+def _round(change):
+    def round_bf16(x):
+        x = np.asarray(x, dtype=np.float64)
+        out = np.empty_like(x)
+        fin = np.isfinite(x)
+        out[~fin] = x[~fin]
+        v = x[fin]
+        _m, k = np.frexp(np.abs(v))
+        e = np.maximum(k - 1, HF.BF16_EMIN)
+        q = np.ldexp(1.0, e - (HF.BF16_MANT - (2 if change == "seven_bits" else 1)))
+        if change == "truncate":
+            r = np.trunc(v / q) * q
+        elif change == "ties_away":
+            r = np.sign(v) * np.floor(np.abs(v) / q + 0.5) * q
+        else:
+            r = np.rint(v / q) * q
+        big = np.abs(r) >= 2.0 ** 128
+        r[big] = np.copysign(np.inf, r[big])
+        out[fin] = r
+        return out
+    return {"round_bf16": round_bf16}
+
+
+def _precond_half(change):
+    def precondition_half(PL, G_h, PR):
+        PL, G_h, PR = (np.asarray(v, np.float64) for v in (PL, G_h, PR))
+        if change == "other_intermediate":          # (PL G) rounded, then times PR
+            X = HF.round_bf16(PL @ G_h)
+            return X @ PR, X
+        Y = G_h @ PR
+        Y_h = Y if change == "y_unrounded" else HF.round_bf16(Y)
+        return PL @ Y_h, Y_h
+    return {"precondition_half": precondition_half}
+
+
+def _step_half(change):
+    def layer_step_half(PL, PR, a, g, G, p, stab_override=(None, None), update=True, precond=True):
+        st = O.LayerStats()
+        PL = np.asarray(PL, dtype=np.float64)
+        PR = np.asarray(PR, dtype=np.float64)
+        if update:
+            QL, QR = (PL, PR) if change == "update_from_unrounded" else (HF.round_bf16(PL), HF.round_bf16(PR))
+            PL, st.L = O.update_factor(QL, a, p, stab_override[0])
+            PR, st.R = O.update_factor(QR, g, p, stab_override[1])
+        dW = None
+        if precond:
+            G64 = np.asarray(G, np.float64)
+            G_h = G64 if change == "gradient_unrounded" else HF.round_bf16(G64)
+            PLp, PRp = (HF.round_bf16(PL), HF.round_bf16(PR)) if change == "rounded_factor" else (PL, PR)
+            with np.errstate(all="ignore"):
+                dW_hat, _ = HF.precondition_half(PLp, G_h, PRp)
+                Gn = G64 if change == "norm_of_unrounded_gradient" else G_h
+                if p.rescale:
+                    dW, st.norm_G, st.norm_dW_hat, st.scale = O.rescale(Gn, dW_hat)
+                else:
+                    dW = dW_hat
+                    st.norm_G = float(np.linalg.norm(Gn))
+                    st.norm_dW_hat = float(np.linalg.norm(dW_hat))
+                    st.scale = 1.0
+        return PL, PR, dW, st
+    return {"layer_step_half": layer_step_half}
+
+
+HALF_MUTANTS = {
+    "bf16_truncates": _round("truncate"),
+    "bf16_ties_away_from_zero": _round("ties_away"),
+    "bf16_seven_bit_significand": _round("seven_bits"),
+    "half_y_not_rounded": _precond_half("y_unrounded"),
+    "half_rounds_the_other_intermediate": _precond_half("other_intermediate"),
+    "half_update_from_unrounded_factor": _step_half("update_from_unrounded"),
+    "half_preconditions_with_rounded_factor": _step_half("rounded_factor"),
+    "half_gradient_not_rounded": _step_half("gradient_unrounded"),
+    "half_norm_of_unrounded_gradient": _step_half("norm_of_unrounded_gradient"),
+}
+
+
+# ------------------------------------------------ the MKOR-H rule and its pins
+
+def _hybrid_pins():
+    return [(n, getattr(THY, n)) for n in sorted(dir(THY)) if n.startswith("test_reference_")]
+
+
+def _hybrid(change):
+    def hybrid_decisions(losses, window, patience, warmup, threshold):
+        decisions, means = [], []
+        slow, decision, switched = 0, 1, None
+        for t in range(1, len(losses) + 1):
+            if t % window == 0:
+                mean = sum(float(x) for x in losses[t - window:t]) / window
+                k = len(means)
+                first = 0 if change == "counts_first_window" else 1
+                if k >= first and k >= (warmup + 1 if change == "warmup_off_by_one" else warmup) and means:
+                    prev = means[-1]
+                    if change == "rate_sign":
+                        rate = (mean - prev) / abs(prev) if prev != 0.0 else 0.0
+                    elif change == "rate_not_relative":
+                        rate = prev - mean
+                    else:
+                        rate = (prev - mean) / abs(prev) if prev != 0.0 else 0.0
+                    is_slow = rate <= threshold if change == "le" else rate < threshold
+                    if change == "patience_never_resets":
+                        slow = slow + 1 if is_slow else slow
+                    else:
+                        slow = slow + 1 if is_slow else 0
+                    need = patience + 1 if change == "patience_strict" else patience
+                    if decision == 1 and slow >= need:
+                        decision, switched = 0, t
+                means.append(mean)
+            decisions.append(decision)
+        return decisions, switched
+    return {"hybrid_decisions": hybrid_decisions}
+
+
+HYBRID_MUTANTS = {
+    "hybrid_rate_sign": _hybrid("rate_sign"),
+    "hybrid_rate_not_relative": _hybrid("rate_not_relative"),
+    "hybrid_le_threshold": _hybrid("le"),
+    "hybrid_patience_never_resets": _hybrid("patience_never_resets"),
+    "hybrid_patience_off_by_one": _hybrid("patience_strict"),
+    "hybrid_warmup_off_by_one": _hybrid("warmup_off_by_one"),
+}
+
+
 def _failing(pins):
     failed = []
     for name, pin in pins:
@@ -374,6 +520,8 @@ def test_unmutated_oracles_pass_every_pin():
     assert _failing_pins() == []
     assert _failing(_rank_pins()) == []
     assert _failing(_opt_pins()) == []
+    assert _failing(_half_pins()) == []
+    assert _failing(_hybrid_pins()) == []
 
 
 @pytest.mark.parametrize("mutant", sorted(MUTANTS))
@@ -393,3 +541,15 @@ def test_rank_pins_catch_planted_mistake(monkeypatch, mutant):
 def test_optimizer_pins_catch_planted_mistake(monkeypatch, mutant):
     _plant(monkeypatch, OPT_MUTANTS[mutant], OPT, TO)
     assert _failing(_opt_pins()), f"no optimizer pin catches the mutant {mutant}"
+
+
+@pytest.mark.parametrize("mutant", sorted(HALF_MUTANTS))
+def test_half_pins_catch_planted_mistake(monkeypatch, mutant):
+    _plant(monkeypatch, HALF_MUTANTS[mutant], HF, TH)
+    assert _failing(_half_pins()), f"no half-precision pin catches the mutant {mutant}"
+
+
+@pytest.mark.parametrize("mutant", sorted(HYBRID_MUTANTS))
+def test_hybrid_pins_catch_planted_mistake(monkeypatch, mutant):
+    _plant(monkeypatch, HYBRID_MUTANTS[mutant], HY, THY)
+    assert _failing(_hybrid_pins()), f"no MKOR-H pin catches the mutant {mutant}"
