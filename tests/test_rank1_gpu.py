@@ -149,6 +149,73 @@ def test_bert_large_means_from_16384_bf16_rows():
         _mean_check(g, Go)
 
 
+def _plan_rows_per_block(shapes, rows):
+    """The plan's rows per block of the mean partials: the largest power of
+    two in [512, 8192] that gives at least 1024 blocks of (matrix, 512-column
+    chunk, row block) over the plan, else 512."""
+    for rpb in (8192, 4096, 2048, 1024):
+        blocks = sum((-(-i // 512) + -(-o // 512)) * -(-rows // rpb) for i, o in shapes)
+        if blocks >= 1024:
+            return rpb
+    return 512
+
+
+# (layer count, shape, rows per layer) -> the plan's rows per block; the rows
+# are never a multiple of it, so every matrix ends in a short block
+INTERMEDIATE = [(8, (4096, 4096), 7500, 1024), (128, (512, 512), 10000, 2048), (96, (1024, 1024), 12000, 4096)]
+
+
+@pytest.mark.parametrize("n,shape,rows,rpb", INTERMEDIATE)
+def test_means_at_intermediate_row_blocks(n, shape, rows, rpb):
+    """Plans whose size puts the mean partials at 1024, 2048 and 4096 rows per
+    block (the small and the largest choices are covered above and at full
+    size): every matrix's means against its float64 column means, sampled
+    ones against the oracle, and their step against the oracle."""
+    shapes = [shape] * n
+    assert _plan_rows_per_block(shapes, rows) == rpb and rows % rpb
+    layers = H.allocate_layers(shapes, "fp32", stats=False, rows=rows, act_dtype="bf16")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(rows)
+    sample = [0, n // 2, n - 1]
+    rng = np.random.default_rng(rows)
+    host = {}
+    for i, L in enumerate(layers):
+        if i in sample:
+            A = W.round_to_bf16(rng.standard_normal((rows, shape[0])).astype(np.float32))
+            Go = W.round_to_bf16((rng.standard_normal((rows, shape[1])) * 1e-3).astype(np.float32))
+            G = (rng.standard_normal(shape) * 1e-3).astype(np.float32)
+            H.set_rows(L, A, Go)
+            H.set_inputs(L, G=G)
+            host[i] = (A, Go, G)
+        else:
+            for k in ("A", "Gout"):
+                tmp = torch.empty(L[k].shape, dtype=torch.float32, device="cuda")
+                tmp.normal_(0.0, 1.0, generator=gen)
+                L[k].copy_(tmp)
+                del tmp
+    plan = H.make_plan(layers)
+    p = Params(gamma=0.9, eps=math.inf)
+    plan.step(p)
+    torch.cuda.synchronize()
+    for i, L in enumerate(layers):
+        a, g = H.get_means(L)
+        for got, key in ((a, "A"), (g, "Gout")):
+            want = L[key].double().sum(dim=0).div(rows).float().cpu().numpy()
+            np.testing.assert_array_max_ulp(got, want, maxulp=2)
+    plan.sync_factors()
+    torch.cuda.synchronize()
+    op = oparams(p)
+    for i, (A, Go, G) in host.items():
+        a, g = H.get_means(layers[i])
+        _mean_check(a, A)
+        _mean_check(g, Go)
+        Lo, Ro, dW, _ = O.layer_step(np.eye(shape[0]), np.eye(shape[1]), O.rank1_means(A), O.rank1_means(Go), G, op)
+        check_close(H.get_dW(layers[i]), dW, TOL_STEP, i, "dW")
+        Lg, Rg = H.get_factors(layers[i])
+        check_close(Lg, Lo, TOL_STEP, i, "L")
+        check_close(Rg, Ro, TOL_STEP, i, "R")
+
+
 @pytest.mark.slow
 def test_max_rows_means_and_step():
     """The largest token-row count the ABI accepts, MKOR_MAX_ROWS = 2^26 bf16
