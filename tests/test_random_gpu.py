@@ -28,7 +28,7 @@ from tests.parity import TOL_FREE, TOL_HALF_FREE, TOL_HALF_STEP, TOL_STEP, near_
 
 pytestmark = pytest.mark.gpu
 
-N_PLANS = 40
+N_PLANS = 120
 M64 = [64, 128, 192, 256, 320]
 
 
