@@ -12,6 +12,7 @@ import pytest
 
 import paper_2306_01685_amd as M
 from paper_2306_01685_amd import binding as B
+from tests.test_rank1_gpu import INTERMEDIATE   # plans at 1024 / 2048 / 4096 rows per block
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -207,9 +208,24 @@ def test_workspace_grows_with_rows(lib):
     fk = Fake()
     base = ws_status([layer(fk, 1024, 4096)])[1]
     with_rows = ws_status([layer(fk, 1024, 4096, rows=16384, adt=1)])[1]
-    # float64 partial sums: (1024 + 4096) / 512 chunks x 16 row blocks x 512
-    assert with_rows - base >= 8 * (1024 + 4096) * 16
-    assert with_rows - base < 8 * (1024 + 4096) * 16 + (1 << 20)
+    # float64 partial sums: (1024 + 4096) / 512 chunks x 32 row blocks x 512 (one
+    # layer gives too few blocks for more than the smallest, 512 rows per block)
+    assert with_rows - base >= 8 * (1024 + 4096) * 32
+    assert with_rows - base < 8 * (1024 + 4096) * 32 + (1 << 20)
+
+
+@pytest.mark.parametrize("n,shape,rows,rpb", [(1, (1024, 4096), 16384, 512)] + INTERMEDIATE)
+def test_mean_rows_per_block_rule(lib, n, shape, rows, rpb):
+    """The plan's rows per block of the column-mean partials, seen through the
+    workspace size: the partials of the expected block size fit in what the
+    rows add, those of half that size (about twice as many) do not."""
+    fk = Fake()
+    base = ws_status([layer(fk, *shape) for _ in range(n)])[1]
+    extra = ws_status([layer(fk, *shape, rows=rows, adt=1) for _ in range(n)])[1] - base
+
+    def partials(r):
+        return 8 * 512 * n * (-(-shape[0] // 512) + -(-shape[1] // 512)) * -(-rows // r)
+    assert partials(rpb) <= extra < partials(rpb // 2)
 
 
 def test_first_order_layer_needs_no_factors(lib):
