@@ -23,10 +23,7 @@ namespace mkor {
 
 // ---------------------------------------------------------------- rank-1 means
 // Column means of the rows x cols activation / output-gradient matrices.
-#ifndef MKOR_MEAN_COLS
-#define MKOR_MEAN_COLS 512
-#endif
-constexpr int MEAN_COLS = MKOR_MEAN_COLS;   // columns per chunk, a multiple of 8 per lane of one wave
+constexpr int MEAN_COLS = 512;      // columns per chunk: 8 per lane of one wave
 // Rows per block of the partial sums: a power of two between MEAN_ROWS_MIN
 // and MEAN_ROWS_MAX, the largest that still gives the plan MEAN_MIN_BLOCKS
 // blocks (longer blocks stream better; enough of them fill the chip).
