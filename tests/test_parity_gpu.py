@@ -345,3 +345,45 @@ def test_plan_reuse_two_plans_same_buffers():
         Li, Ri, a, g, G = host[0]
         Lo, Ro, dW, _ = O.layer_step(Li, Ri, a, g, G, oparams(Params(eps=math.inf)))
         check_close(H.get_dW(layers[0]), dW, TOL_STEP)
+
+
+def test_layer_results_do_not_depend_on_the_plan():
+    """A layer's dW and factors are the same bits whether it is stepped alone
+    or among other layers (every reduction is per layer, in a fixed order;
+    tile scheduling and table positions change with the plan's contents):
+    three layers on the split path, the fp32 MFMA path and bf16 factors, each
+    alone and together with 20 filler layers, over three steps."""
+    spec = [((128, 192), "bf16", {}), ((37, 100), "fp32", {}), ((64, 64), "fp32", dict(factor_dtype="bf16"))]
+    rng = np.random.default_rng(31)
+    fill = [(int(rng.integers(1, 300)), int(rng.integers(1, 300))) for _ in range(20)]
+
+    def run(which, with_fill):
+        layers = []
+        for k in which:
+            shape, gdt, kw = spec[k]
+            L = H.allocate_layers([shape], gdt, **kw)[0]
+            Li, Ri = spd(70 + 2 * k, shape[0], 0.3), spd(71 + 2 * k, shape[1], 0.3)
+            if kw.get("factor_dtype") == "bf16":
+                Li, Ri = W.round_to_bf16(Li), W.round_to_bf16(Ri)
+            H.set_factors(L, Li, Ri)
+            layers.append((k, L))
+        extra = H.allocate_layers(fill, "fp32") if with_fill else []
+        plan = H.make_plan([L for _, L in layers[:1]] + extra + [L for _, L in layers[1:]])
+        p = Params(gamma=0.9, zeta=0.5, eps=2.0)
+        for t in range(3):
+            for k, L in layers:
+                a, g, G = _random_inputs(500 + 10 * t + k, L["d_in"], L["d_out"], spec[k][1])
+                H.set_inputs(L, a, g, G)
+            for j, E in enumerate(extra):
+                a, g, G = _random_inputs(900 + 50 * t + j, E["d_in"], E["d_out"], "fp32")
+                H.set_inputs(E, a, g, G)
+            plan.step(p)
+        plan.sync_factors()
+        torch.cuda.synchronize()
+        return {k: (L["dW"].clone(), L["Linv"].clone(), L["Rinv"].clone()) for k, L in layers}
+
+    together = run([0, 1, 2], True)
+    for k in range(3):
+        alone = run([k], False)[k]
+        for name, x, y in zip(("dW", "Linv", "Rinv"), alone, together[k]):
+            assert torch.equal(x, y), (k, name)
