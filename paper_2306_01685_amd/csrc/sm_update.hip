@@ -452,9 +452,18 @@ __device__ __forceinline__ void rank_rows(const FactorDesc& f, const Pending& q,
     }
 }
 
+// MV = 1: the read pass of a step (r products, Gram partials, norms);
+// MV = 0: the write of the pending rank-r term after the finalize.  Two
+// kernels, so that each gets the registers of its own path (the write pass
+// then holds four waves per SIMD, against two for one kernel with both
+// paths).  The plan writes a rank-r term in the stage that forms it, so the
+// read pass meets no pending term; should it meet one, the scalar path applies
+// and writes it before the products.
+template <int MV>
 __global__ __launch_bounds__(SM_THREADS) void sm_pass_rank_kernel(
     const FactorDesc* __restrict__ factors, const RowBlock* __restrict__ blocks,
-    float4* __restrict__ partials, float* __restrict__ gram, int nblocks, int maxabs, int matvec) {
+    float4* __restrict__ partials, float* __restrict__ gram, int nblocks, int maxabs) {
+    constexpr bool matvec = MV != 0;
     __shared__ float4 sred[SM_THREADS / 64];
     __shared__ float sgram[SM_THREADS / 64][GRAM];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -476,13 +485,19 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_rank_kernel(
 #pragma unroll
             for (int l = 0; l < MAXR; ++l) dot[r][l] = 0.f;
         }
+        // lane k < RR MAXR holds x_l[row] of the wave's row kr = k / MAXR and
+        // vector kl = k % MAXR (0 past the rows or the rank), loaded ahead of
+        // the stream so that the u stores and Gram partials below wait on no
+        // load
+        const int kr = lane / MAXR, kl = lane % MAXR;
+        const bool kin = lane < RR * MAXR && kr < nr && kl < rk;
+        const float xk = (matvec && kin) ? gld(f.x + (size_t)kl * f.d + rbase + kr) : 0.f;
         if (nr > 0) {
             const bool vec = (f.d & 3) == 0;
-            if (matvec) {
-                if (has) { if (vec) rank_rows<true, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-                           else     rank_rows<true, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm); }
-                else     { if (vec) rank_rows<false, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
-                           else     rank_rows<false, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm); }
+            if constexpr (matvec) {
+                if (has)      rank_rows<true, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+                else if (vec) rank_rows<false, true, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
+                else          rank_rows<false, true, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
             } else {
                 if (vec) rank_rows<true, false, true>(f, q, rbase, nr, lane, maxabs, dot, nrm);
                 else     rank_rows<true, false, false>(f, q, rbase, nr, lane, maxabs, dot, nrm);
@@ -495,38 +510,40 @@ __global__ __launch_bounds__(SM_THREADS) void sm_pass_rank_kernel(
             for (int l = 0; l < MAXR; ++l) dot[r][l] = wave_sum(dot[r][l]);
             nrm[r] = maxabs ? wave_nanmax(nrm[r]) : wave_sum(nrm[r]);
         }
-        if (lane == 0) {
-            float mx = 0.f, gxu[MAXR][MAXR], gxx[MAXR][MAXR];
+        // u_l[row] = dot[kr][kl], one store per lane
+        float dk = 0.f;
+#pragma unroll
+        for (int r = 0; r < RR; ++r)
 #pragma unroll
             for (int l = 0; l < MAXR; ++l)
+                if (lane == r * MAXR + l) dk = dot[r][l];
+        if (kin) gst(f.u + (size_t)kl * f.d + rbase + kr, dk);
+        // Gram entry e = lane < GRAM: e < MAXR^2 is sum_r x_l[r] (P x_m)[r],
+        // the rest sum_r x_l[r] x_m[r] ((l, m) = (e / MAXR, e % MAXR) of
+        // e mod MAXR^2), rows in order from 0, each term one fma
+        const int e = lane % (MAXR * MAXR), gl = e / MAXR, gm = e % MAXR;
+        const bool gxu_lane = lane < MAXR * MAXR;
+        float gacc = 0.f;
 #pragma unroll
-                for (int m = 0; m < MAXR; ++m) { gxu[l][m] = 0.f; gxx[l][m] = 0.f; }
-            for (int r = 0; r < nr; ++r) {
-                const int row = rbase + r;
-                float xr[MAXR];
+        for (int r = 0; r < RR; ++r) {
+            if (r >= nr) break;
+            const float xl = __shfl(xk, r * MAXR + gl, 64);
+            const float xm = __shfl(xk, r * MAXR + gm, 64);
+            float dm = 0.f;
 #pragma unroll
-                for (int l = 0; l < MAXR; ++l) {
-                    xr[l] = l < rk ? gld(f.x + (size_t)l * f.d + row) : 0.f;
-                    if (l < rk) gst(f.u + (size_t)l * f.d + row, dot[r][l]);
-                }
-                mx = nanmax(mx, nrm[r]);
-#pragma unroll
-                for (int l = 0; l < MAXR; ++l)
-#pragma unroll
-                    for (int m = 0; m < MAXR; ++m) {
-                        gxu[l][m] = fmaf(xr[l], dot[r][m], gxu[l][m]);
-                        gxx[l][m] = fmaf(xr[l], xr[m], gxx[l][m]);
-                    }
-            }
-            sred[wave] = make_float4(mx, 0.f, 0.f, 0.f);
-#pragma unroll
-            for (int l = 0; l < MAXR; ++l)
-#pragma unroll
-                for (int m = 0; m < MAXR; ++m) {
-                    sgram[wave][l * MAXR + m] = gxu[l][m];
-                    sgram[wave][MAXR * MAXR + l * MAXR + m] = gxx[l][m];
-                }
+            for (int m = 0; m < MAXR; ++m)
+                if (gm == m) dm = dot[r][m];
+            gacc = fmaf(xl, gxu_lane ? dm : xm, gacc);
         }
+        if (lane < GRAM) sgram[wave][lane] = gacc;
+        if (lane == 0) {
+            float mx = 0.f;
+#pragma unroll
+            for (int r = 0; r < RR; ++r)
+                if (r < nr) mx = nanmax(mx, nrm[r]);
+            sred[wave] = make_float4(mx, 0.f, 0.f, 0.f);
+        }
+        static_assert(RR * MAXR <= 64 && GRAM == 2 * MAXR * MAXR && GRAM <= 64, "one lane per x value and Gram entry");
         __syncthreads();
         if (threadIdx.x == 0) {
             float4 acc = sred[0];
@@ -764,8 +781,12 @@ hipError_t launch_sm_pass(const FactorDesc* factors, const RowBlock* blocks, int
                        partials, nblocks, maxabs, matvec ? 1 : 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !ranked) return e;
-    hipLaunchKernelGGL(sm_pass_rank_kernel, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
-                       partials, gram, nblocks, maxabs, matvec ? 1 : 0);
+    if (matvec)
+        hipLaunchKernelGGL(sm_pass_rank_kernel<1>, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
+                           partials, gram, nblocks, maxabs);
+    else
+        hipLaunchKernelGGL(sm_pass_rank_kernel<0>, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
+                           partials, gram, nblocks, maxabs);
     return hipGetLastError();
 }
 
@@ -773,8 +794,8 @@ hipError_t launch_sm_apply_rank(const FactorDesc* factors, const RowBlock* block
                                 int32_t nfactors, hipStream_t stream) {
     if (nblocks <= 0 || nfactors <= 0) return hipSuccess;
     const int32_t grid = (SM_GRID > 0 && nblocks > SM_GRID) ? SM_GRID : nblocks;
-    hipLaunchKernelGGL(sm_pass_rank_kernel, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
-                       (float4*)nullptr, (float*)nullptr, nblocks, 0, 0);
+    hipLaunchKernelGGL(sm_pass_rank_kernel<0>, dim3(grid), dim3(SM_THREADS), 0, stream, factors, blocks,
+                       (float4*)nullptr, (float*)nullptr, nblocks, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(sm_reset_kernel, dim3((nfactors + 255) / 256), dim3(256), 0, stream, factors,
